@@ -1,0 +1,194 @@
+"""Pins for the oracle's rounding and layer functions (CPU only).
+
+Each layer function is checked against something other than itself: torch's
+float64 CPU operators (a different implementation of the textbook
+definitions, in NCHW layout), pure-Python loops on tiny inputs, and
+hand-computed cases."""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle as O
+from oracle.layers import phi
+import workloads as W
+from workloads.graph import Node, Model, CONV2D, DENSE, ADD, GAP, INPUT
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------- bf16 RNE
+
+def test_rne_bf16_matches_torch_conversion():
+    rng = np.random.default_rng(0)
+    x = np.concatenate([
+        rng.standard_normal(100000).astype(np.float32) * 10.0 ** rng.integers(-30, 30, 100000),
+        np.array([0.0, -0.0, np.inf, -np.inf, 3.4e38, -3.4e38, 1e-40, -1e-40], np.float32),
+    ]).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
+    got = O.rne_bf16(x)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
+def test_rne_bf16_ties_to_even():
+    # low halves exactly 0x8000 are ties: round to the even kept pattern
+    u = np.array([0x3F808000, 0x3F818000, 0x3F807FFF, 0x3F808001, 0x7F7F8000], np.uint32)
+    got = O.rne_bf16(u.view(np.float32)).view(np.uint32)
+    assert list(got) == [0x3F800000, 0x3F820000, 0x3F800000, 0x3F810000, 0x7F800000]
+    assert np.isnan(O.rne_bf16(np.array([np.nan], np.float32)))[0]
+
+
+# ---------------------------------------------------------------- helpers
+
+def _model(nodes, dtype="f32", weights=None, biases=None):
+    n = len(nodes)
+    return O.OracleModel(Model("t", dtype, nodes, weights or [None] * n, biases or [None] * n))
+
+
+def _conv_node(hwc, cout, k, s, p, relu, pool):
+    h, w, c = hwc
+    ho = (h + 2 * p - k) // s + 1
+    wo = (w + 2 * p - k) // s + 1
+    if pool:
+        ho, wo = ho // 2, wo // 2
+    return Node(CONV2D, (0,), c, cout, k, k, s, p, relu, pool, 0, (ho, wo, cout))
+
+
+# ---------------------------------------------------------------- conv
+
+@pytest.mark.parametrize("hwc,cout,k,s,p,relu,pool", [
+    ((9, 9, 3), 5, 3, 1, 1, True, 0),
+    ((12, 12, 6), 16, 5, 1, 0, True, 2),
+    ((11, 10, 4), 8, 3, 2, 1, True, 0),
+    ((8, 8, 4), 8, 1, 2, 0, False, 0),
+    ((13, 13, 2), 3, 5, 1, 0, False, 2),
+])
+def test_conv_matches_torch_float64(hwc, cout, k, s, p, relu, pool):
+    rng = np.random.default_rng(1)
+    node = _conv_node(hwc, cout, k, s, p, relu, pool)
+    Wt = rng.standard_normal((cout, k, k, hwc[2])).astype(np.float32)
+    b = rng.standard_normal(cout).astype(np.float32)
+    m = _model([Node(INPUT, (), out_hwc=hwc), node], weights=[None, Wt], biases=[None, b])
+    x = rng.standard_normal((3,) + hwc).astype(np.float32)
+    got = phi(m, 1, [x])
+    xt = torch.from_numpy(x.astype(np.float64)).permute(0, 3, 1, 2)
+    wt = torch.from_numpy(Wt.astype(np.float64)).permute(0, 3, 1, 2)
+    ref = F.conv2d(xt, wt, torch.from_numpy(b.astype(np.float64)), stride=s, padding=p)
+    ref = ref.float()
+    if relu:
+        ref = torch.relu(ref)
+    if pool:
+        ref = F.max_pool2d(ref, 2)
+    ref = ref.permute(0, 2, 3, 1).numpy()
+    assert got.shape == ref.shape == (3,) + node.out_hwc
+    # torch adds the bias in float64 too: results agree to float32 rounding
+    np.testing.assert_allclose(got, ref, rtol=1e-6, atol=1e-6)
+
+
+def test_conv_brute_force_loops():
+    rng = np.random.default_rng(2)
+    hwc, cout, k, s, p = (5, 4, 2), 3, 3, 2, 1
+    node = _conv_node(hwc, cout, k, s, p, False, 0)
+    Wt = rng.standard_normal((cout, k, k, 2)).astype(np.float32)
+    b = rng.standard_normal(cout).astype(np.float32)
+    m = _model([Node(INPUT, (), out_hwc=hwc), node], weights=[None, Wt], biases=[None, b])
+    x = rng.standard_normal((1,) + hwc).astype(np.float32)
+    got = phi(m, 1, [x])
+    ho, wo, _ = node.out_hwc
+    for i in range(ho):
+        for j in range(wo):
+            for o in range(cout):
+                acc = 0.0
+                for dy in range(k):
+                    for dx in range(k):
+                        y, xx = i * s + dy - p, j * s + dx - p
+                        if 0 <= y < hwc[0] and 0 <= xx < hwc[1]:
+                            for c in range(2):
+                                acc += float(x[0, y, xx, c]) * float(Wt[o, dy, dx, c])
+                assert got[0, i, j, o] == np.float32(acc + float(b[o]))
+
+
+# ---------------------------------------------------------------- dense / flatten order
+
+def test_dense_reads_hwc_flatten_order():
+    rng = np.random.default_rng(3)
+    hwc = (2, 3, 4)
+    node = Node(DENSE, (0,), 24, 5, relu=True, out_hwc=(1, 1, 5))
+    Wt = rng.standard_normal((5, 24)).astype(np.float32)
+    b = rng.standard_normal(5).astype(np.float32)
+    m = _model([Node(INPUT, (), out_hwc=hwc), node], weights=[None, Wt], biases=[None, b])
+    x = rng.standard_normal((2,) + hwc).astype(np.float32)
+    got = phi(m, 1, [x]).reshape(2, 5)
+    for n in range(2):
+        for o in range(5):
+            acc = sum(float(x[n, h, w, c]) * float(Wt[o, (h * 3 + w) * 4 + c])
+                      for h in range(2) for w in range(3) for c in range(4))
+            assert got[n, o] == max(np.float32(acc + float(b[o])), np.float32(0))
+    ref = torch.relu(F.linear(torch.from_numpy(x.reshape(2, -1).astype(np.float64)),
+                              torch.from_numpy(Wt.astype(np.float64)),
+                              torch.from_numpy(b.astype(np.float64))).float()).numpy()
+    np.testing.assert_allclose(got, ref, rtol=1e-6)
+
+
+# ---------------------------------------------------------------- add / gap
+
+def test_add_option_a_shortcut_hand_example():
+    a = np.zeros((1, 2, 2, 4), np.float32)
+    a[0, :, :, :] = np.arange(16, dtype=np.float32).reshape(2, 2, 4) - 8
+    s = np.zeros((1, 4, 4, 2), np.float32)
+    s[0, :, :, 0] = np.arange(16).reshape(4, 4)
+    s[0, :, :, 1] = 100 + np.arange(16).reshape(4, 4)
+    node = Node(ADD, (1, 2), 2, 4, relu=True, shortcut=1, out_hwc=(2, 2, 4))
+    m = _model([Node(INPUT, (), out_hwc=(4, 4, 2))] * 3 + [node])
+    got = phi(m, 3, [a, s])[0]
+    # subsample rows/cols 0 and 2; one zero channel before, one after
+    for i in range(2):
+        for j in range(2):
+            sub = [0.0, s[0, 2 * i, 2 * j, 0], s[0, 2 * i, 2 * j, 1], 0.0]
+            for c in range(4):
+                assert got[i, j, c] == max(a[0, i, j, c] + np.float32(sub[c]), 0)
+
+
+def test_gap_matches_torch_mean_and_bf16_rounding():
+    rng = np.random.default_rng(4)
+    x = O.rne_bf16(rng.standard_normal((3, 8, 8, 5)).astype(np.float32))
+    node = Node(GAP, (0,), 5, 5, out_hwc=(1, 1, 5))
+    out = Node(DENSE, (1,), 5, 2, out_hwc=(1, 1, 2))
+    m = _model([Node(INPUT, (), out_hwc=(8, 8, 5)), node, out], dtype="bf16")
+    got = phi(m, 1, [x]).reshape(3, 5)
+    ref = torch.from_numpy(x.astype(np.float64)).mean(dim=(1, 2)).float().to(torch.bfloat16).float()
+    assert np.array_equal(got, ref.numpy())
+
+
+# ---------------------------------------------------------------- rounding points
+
+def test_bf16_rounding_points_every_node_but_logits():
+    m = W.tiny_resnet("bf16")
+    om = O.OracleModel(m)
+    x = W.make_inputs(m, 4, "normal")
+    acts = O.forward_all(om, x, accumulate="ordered")
+    for v, a in acts.items():
+        if v == om.out:
+            continue
+        assert np.array_equal(O.rne_bf16(a), a), f"node {v} not bf16-representable"
+    logits = acts[om.out]
+    assert not np.array_equal(O.rne_bf16(logits), logits)   # fp32 logits keep low bits
+
+
+# ---------------------------------------------------------------- Table 1 pins the model builders
+
+def test_table1_parameter_counts():
+    with open(os.path.join(GOLDEN, "table1_param_counts.json")) as f:
+        rows = json.load(f)["models"]
+    for r in rows:
+        m = W.make_model(r["graph"], "f32", 0.01, tuple(r["in_hwc"]), r["classes"])
+        assert m.n_params() == r["params"], r["row"]
+        # the oracle's layer functions produce the shapes the builder declares
+        om = O.OracleModel(m)
+        x = W.make_inputs(m, 2, "uniform")
+        acts = O.forward_all(om, x)
+        for v, n in enumerate(m.nodes):
+            assert acts[v].shape[1:] == tuple(n.out_hwc), (r["row"], v)
