@@ -1,0 +1,45 @@
+// Device helpers shared by the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+#include "kernels.hpp"
+
+namespace mure {
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef uint16_t bf16_t;   // bfloat16 bit pattern
+
+__device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// float -> bfloat16, round to nearest, ties to even (NaN stays NaN).
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+template <typename T> __device__ __forceinline__ float to_f(T v);
+template <> __device__ __forceinline__ float to_f<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f<bf16_t>(bf16_t v) { return bf2f(v); }
+
+template <typename T> __device__ __forceinline__ T from_f(float v);
+template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16_t from_f<bf16_t>(float v) { return f2bf(v); }
+
+// index of a tensor row for chunk row r (slot-major, nx inputs per slot)
+__device__ __forceinline__ int64_t row_index(int mode, int64_t r, int nx, int x0) {
+  return mode == MODE_BUF ? r : (int64_t)x0 + (r % nx);
+}
+
+// store a node output element (the network output is kept in float32)
+template <typename T>
+__device__ __forceinline__ void store_out(void* out, int out_f32, int64_t i, float v) {
+  if (out_f32) reinterpret_cast<float*>(out)[i] = v;
+  else reinterpret_cast<T*>(out)[i] = from_f<T>(v);
+}
+
+}  // namespace mure

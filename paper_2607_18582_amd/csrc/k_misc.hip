@@ -1,0 +1,277 @@
+// Element-wise layers, the channel-patch (delta) kernel at the first mutated
+// layer, the kill reduction, labels, scoring and copy-on-write mutation.
+#include "dev.hpp"
+
+namespace mure {
+
+// ---------------------------------------------------------------- ADD
+// out = ReLU?(float(a) + float(s')) with s' = s, or for option A
+// s'[y][x][c] = s[2y][2x][c - before] inside the copied channel range, else 0.
+template <typename T>
+__global__ void add_kernel(AddArgs a) {
+  const int64_t per = (int64_t)a.H * a.W * a.C;
+  const int64_t total = a.rows * per;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / per;
+    const int64_t e = i % per;
+    const int c = (int)(e % a.C);
+    const int64_t pix = e / a.C;
+    const T* ap = reinterpret_cast<const T*>(a.a.p) + row_index(a.a.mode, r, a.nx, a.x0) * a.a.row_elems;
+    const T* sp = reinterpret_cast<const T*>(a.s.p) + row_index(a.s.mode, r, a.nx, a.x0) * a.s.row_elems;
+    float sv;
+    if (a.shortcut == 0) {
+      sv = to_f<T>(sp[e]);
+    } else {
+      const int y = (int)(pix / a.W), x = (int)(pix % a.W);
+      const int cs = c - (a.C - a.Cs) / 2;
+      sv = (cs >= 0 && cs < a.Cs) ? to_f<T>(sp[((int64_t)(2 * y) * a.Ws + 2 * x) * a.Cs + cs]) : 0.f;
+    }
+    float v = to_f<T>(ap[e]) + sv;
+    if (a.relu) v = fmaxf(v, 0.f);
+    store_out<T>(a.out, a.out_f32, row_index(a.out_mode, r, a.nx, a.x0) * per + e, v);
+  }
+}
+
+// ---------------------------------------------------------------- GAP
+// sum over the H*W pixels in order (float32), times 1/(H*W), then rounding.
+template <typename T>
+__global__ void gap_kernel(GapArgs a) {
+  const int64_t total = a.rows * a.C;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / a.C;
+    const int c = (int)(i % a.C);
+    const T* ip = reinterpret_cast<const T*>(a.in.p) + row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems;
+    float s = 0.f;
+    for (int p = 0; p < a.P; ++p) s += to_f<T>(ip[(int64_t)p * a.C + c]);
+    store_out<T>(a.out, a.out_f32, row_index(a.out_mode, r, a.nx, a.x0) * a.C + c, s * (1.0f / (float)a.P));
+  }
+}
+
+// ---------------------------------------------------------------- channel patch
+// Node mmi of an effect-block / switch mutant: the original's output with
+// channel c taken from original channel chmap[c] (-1: zero).  Bitwise copy.
+template <typename E>
+__global__ void patch_kernel(PatchArgs a) {
+  const int64_t per = (int64_t)a.P * a.C;
+  const int64_t total = (int64_t)a.nslots * a.nx * per;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t rr = i / per;               // row within this launch
+    const int64_t e = i % per;
+    const int c = (int)(e % a.C);
+    const int sl = (int)(rr / a.nx);
+    const int xi = (int)(rr % a.nx);
+    const int src = a.chmap[(int64_t)(a.chmap_slot0 + sl) * a.C + c];
+    const E* cp = reinterpret_cast<const E*>(a.cache) + ((int64_t)a.x0 + xi) * per;
+    E v = src < 0 ? E(0) : cp[e - c + src];
+    reinterpret_cast<E*>(a.out)[((int64_t)(a.slot0 + sl) * a.nx + xi) * per + e] = v;
+  }
+}
+
+// ---------------------------------------------------------------- kill reduction
+// One thread per (slot, input); a wavefront covers 64 consecutive inputs of
+// one slot, i.e. exactly one 64-bit kill word (x0 is a multiple of 64).
+__global__ __launch_bounds__(256) void kill_kernel(KillArgs a) {
+  const int sl = a.slot0 + (int)blockIdx.y;
+  const int xi = (int)blockIdx.x * 256 + (int)threadIdx.x;
+  const bool valid = xi < a.nx;
+  bool kill = false;
+  if (valid) {
+    const float* z = a.logits + ((int64_t)sl * a.nx + xi) * a.C;
+    float best = z[0];
+    int arg = 0, bad = !isfinite(best);
+    if (bad) best = -INFINITY;
+    for (int c = 1; c < a.C; ++c) {
+      const float v = z[c];
+      if (!isfinite(v)) { ++bad; continue; }
+      if (v > best) { best = v; arg = c; }
+    }
+    if (bad) atomicAdd(a.nonfinite, (unsigned long long)bad);
+    const int x = a.x0 + xi;
+    kill = a.orig_ok[x] && arg != a.label[x];
+    if (a.logits_out)
+      for (int c = 0; c < a.C; ++c) a.logits_out[(int64_t)x * a.C + c] = z[c];
+  }
+  const unsigned long long word = __ballot(kill);
+  const int wave_first = (int)blockIdx.x * 256 + ((int)threadIdx.x & ~63);
+  if ((threadIdx.x & 63) == 0 && wave_first < a.nx && a.kill_words) {
+    const int64_t m = a.slot_mutant[sl];
+    a.kill_words[m * a.nwords + (a.x0 + wave_first) / 64] = word;
+  }
+}
+
+// ---------------------------------------------------------------- labels
+__global__ void labels_kernel(LabelArgs a) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= a.N) return;
+  const float* z = a.logits + x * a.C;
+  float best = -INFINITY;
+  int arg = 0, bad = 0;
+  for (int c = 0; c < a.C; ++c) {
+    const float v = z[c];
+    if (!isfinite(v)) { ++bad; continue; }
+    if (v > best) { best = v; arg = c; }
+  }
+  if (bad) atomicAdd(a.nonfinite, (unsigned long long)bad);
+  const int lab = a.given ? a.given[x] : arg;
+  a.label[x] = lab;
+  a.ok[x] = (uint8_t)(arg == lab);
+  atomicOr(&a.class_mask[lab >> 6], 1ull << (lab & 63));
+}
+
+// ---------------------------------------------------------------- score
+// Per mutant: kills = popcount of its words; killingLabels mask = OR of
+// 1 << label(x) over killed x.  Integer only: order-independent.
+__global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
+  __shared__ unsigned long long mask[8];
+  __shared__ unsigned long long count;
+  const int64_t m = blockIdx.x;
+  if (threadIdx.x < 8) mask[threadIdx.x] = 0;
+  if (threadIdx.x == 0) count = 0;
+  __syncthreads();
+  unsigned long long cnt = 0;
+  for (int64_t w = threadIdx.x; w < a.nwords; w += blockDim.x) {
+    unsigned long long bits = a.kill_words[m * a.nwords + w];
+    cnt += __popcll(bits);
+    while (bits) {
+      const int b = __ffsll((long long)bits) - 1;
+      bits &= bits - 1;
+      const int lab = a.label[w * 64 + b];
+      atomicOr(&mask[lab >> 6], 1ull << (lab & 63));
+    }
+  }
+  atomicAdd(&count, cnt);
+  __syncthreads();
+  if (threadIdx.x == 0) a.kills[m] = (int64_t)count;
+  if (threadIdx.x < a.mask_words) a.masks[m * a.mask_words + threadIdx.x] = mask[threadIdx.x];
+}
+
+// ---------------------------------------------------------------- copy-on-write mutation
+// One block per (mutant, layer) copy: copy the original parameters, then
+// apply that mutant's records on this layer in order.
+template <typename T>
+__global__ __launch_bounds__(256) void cow_kernel(const CowArgs* args, const DevRecord* recs,
+                                                  const float* noise) {
+  const CowArgs c = args[blockIdx.x];
+  const T* ws = reinterpret_cast<const T*>(c.w_src);
+  T* wd = reinterpret_cast<T*>(c.w_dst);
+  const int64_t n = (int64_t)c.c_out * c.fan_in;
+  for (int64_t i = threadIdx.x; i < n; i += blockDim.x) wd[i] = ws[i];
+  for (int i = threadIdx.x; i < c.c_out; i += blockDim.x) c.b_dst[i] = c.b_src[i];
+  __syncthreads();
+  for (int ri = c.rec0; ri < c.rec1; ++ri) {
+    const DevRecord r = recs[ri];
+    T* row = wd + (int64_t)r.neuron * c.fan_in;
+    if (r.op == 0) {                      // Gaussian fuzz: float32 add, then round
+      const float* eps = noise + r.noise_off;
+      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x)
+        row[k] = from_f<T>(to_f<T>(row[k]) + eps[k]);
+    } else if (r.op == 1) {               // effect block
+      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) row[k] = T(0);
+      if (threadIdx.x == 0) c.b_dst[r.neuron] = 0.f;
+    } else if (r.op == 2) {               // activation inverse (exact sign flip)
+      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) {
+        if constexpr (sizeof(T) == 2) row[k] = (T)(row[k] ^ 0x8000u);
+        else row[k] = -row[k];
+      }
+      if (threadIdx.x == 0) c.b_dst[r.neuron] = -c.b_dst[r.neuron];
+    } else {                              // neuron switch
+      T* other = wd + (int64_t)r.partner * c.fan_in;
+      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) {
+        const T t = row[k]; row[k] = other[k]; other[k] = t;
+      }
+      if (threadIdx.x == 0) {
+        const float t = c.b_dst[r.neuron]; c.b_dst[r.neuron] = c.b_dst[r.partner]; c.b_dst[r.partner] = t;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------- row copy (FLATTEN)
+template <typename E>
+__global__ void copy_rows_kernel(TensorArg src, E* dst, int64_t rows, int nx, int x0) {
+  const int64_t total = rows * src.row_elems;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / src.row_elems, e = i % src.row_elems;
+    dst[i] = reinterpret_cast<const E*>(src.p)[row_index(src.mode, r, nx, x0) * src.row_elems + e];
+  }
+}
+
+// ---------------------------------------------------------------- launchers
+static unsigned grid_for(int64_t total, int block = 256) {
+  int64_t g = (total + block - 1) / block;
+  if (g > 65536LL * 8) g = 65536LL * 8;
+  return (unsigned)(g < 1 ? 1 : g);
+}
+
+hipError_t launch_add(const AddArgs& a, int dtype, hipStream_t s) {
+  const int64_t total = a.rows * a.H * a.W * a.C;
+  if (total == 0) return hipSuccess;
+  if (dtype == 0) hipLaunchKernelGGL(add_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(add_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gap(const GapArgs& a, int dtype, hipStream_t s) {
+  const int64_t total = a.rows * a.C;
+  if (total == 0) return hipSuccess;
+  if (dtype == 0) hipLaunchKernelGGL(gap_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(gap_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_patch(const PatchArgs& a, hipStream_t s) {
+  const int64_t total = (int64_t)a.nslots * a.nx * a.P * a.C;
+  if (total == 0) return hipSuccess;
+  if (a.esize == 4) hipLaunchKernelGGL(patch_kernel<uint32_t>, dim3(grid_for(total)), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(patch_kernel<uint16_t>, dim3(grid_for(total)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_kill(const KillArgs& a, hipStream_t s) {
+  if (a.nslots <= 0 || a.nx <= 0) return hipSuccess;
+  dim3 grid((unsigned)((a.nx + 255) / 256), (unsigned)a.nslots);
+  hipLaunchKernelGGL(kill_kernel, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_labels(const LabelArgs& a, hipStream_t s) {
+  if (a.N == 0) return hipSuccess;
+  hipLaunchKernelGGL(labels_kernel, dim3((unsigned)((a.N + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_score(const ScoreArgs& a, int n_mutants, hipStream_t s) {
+  if (n_mutants == 0) return hipSuccess;
+  hipLaunchKernelGGL(score_kernel, dim3((unsigned)n_mutants), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_cow(const CowArgs* d_args, int n_copies, const DevRecord* d_recs,
+                      const float* d_noise, int dtype, hipStream_t s) {
+  if (n_copies == 0) return hipSuccess;
+  if (dtype == 0)
+    hipLaunchKernelGGL(cow_kernel<float>, dim3((unsigned)n_copies), dim3(256), 0, s, d_args, d_recs, d_noise);
+  else
+    hipLaunchKernelGGL(cow_kernel<bf16_t>, dim3((unsigned)n_copies), dim3(256), 0, s, d_args, d_recs, d_noise);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_rows(const TensorArg& src, void* dst, int64_t rows, int nx, int x0,
+                            int esize, hipStream_t s) {
+  const int64_t total = rows * src.row_elems;
+  if (total == 0) return hipSuccess;
+  if (esize == 4)
+    hipLaunchKernelGGL(copy_rows_kernel<uint32_t>, dim3(grid_for(total)), dim3(256), 0, s, src,
+                       reinterpret_cast<uint32_t*>(dst), rows, nx, x0);
+  else
+    hipLaunchKernelGGL(copy_rows_kernel<uint16_t>, dim3(grid_for(total)), dim3(256), 0, s, src,
+                       reinterpret_cast<uint16_t*>(dst), rows, nx, x0);
+  return hipGetLastError();
+}
+
+}  // namespace mure

@@ -1,0 +1,127 @@
+// Kernel argument blocks and host-side launchers of the gfx950 kernels.
+//
+// Activation tensors are addressed by "row": a row is one (mutant slot,
+// input) pair of the current chunk, r = slot * nx + xi with xi in [0, nx).
+// A tensor is either a chunk buffer (row r lives at index r) or a prefix-cache
+// tensor holding the original model's activation for every input (row r
+// reads index x0 + xi, shared by all mutant slots).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace mure {
+
+enum { MODE_BUF = 0, MODE_CACHE = 1 };
+
+struct TensorArg {
+  const void* p = nullptr;
+  int mode = MODE_BUF;
+  int64_t row_elems = 0;   // elements per row
+};
+
+// CONV2D / DENSE (a DENSE layer is a 1x1 convolution over a 1x1xC_in input).
+struct ConvArgs {
+  TensorArg in;
+  void* out = nullptr;
+  int out_mode = MODE_BUF;
+  int64_t out_row = 0;
+  int out_f32 = 0;                       // 1: store float32 (network output)
+  const void* const* wtab = nullptr;     // [slots] weights [C_out][kh][kw][C_in]
+  const float* const* btab = nullptr;    // [slots] bias [C_out]
+  int slot0 = 0;                         // first slot of this launch (rows start at slot0*nx)
+  int nx = 0, x0 = 0;
+  int H = 0, W = 0, C = 0;               // input geometry
+  int Hc = 0, Wc = 0;                    // convolution output before pooling
+  int Hp = 0, Wp = 0;                    // stored output
+  int Cout = 0, kh = 1, kw = 1, stride = 1, pad = 0, relu = 0, pool = 0;
+  int K = 0;                             // kh*kw*C
+  int P = 0;                             // GEMM rows per input
+};
+
+struct AddArgs {
+  TensorArg a, s;
+  void* out = nullptr;
+  int out_mode = MODE_BUF, out_f32 = 0;
+  int nx = 0, x0 = 0;
+  int64_t rows = 0;
+  int H = 0, W = 0, C = 0;               // output (= in[0]) geometry
+  int Hs = 0, Ws = 0, Cs = 0;            // in[1] geometry
+  int shortcut = 0, relu = 0;
+};
+
+struct GapArgs {
+  TensorArg in;
+  void* out = nullptr;
+  int out_mode = MODE_BUF, out_f32 = 0;
+  int nx = 0, x0 = 0;
+  int64_t rows = 0;
+  int P = 0, C = 0;
+};
+
+struct PatchArgs {                       // channel patch of node mmi for NEB/NS mutants
+  const void* cache = nullptr;           // original output of mmi, all inputs
+  void* out = nullptr;                   // chunk buffer
+  const int32_t* chmap = nullptr;        // [patch slots][C]: source channel or -1
+  int slot0 = 0;                         // first slot of this launch
+  int chmap_slot0 = 0;                   // chmap row of slot0
+  int nx = 0, x0 = 0, nslots = 0;
+  int P = 0, C = 0, esize = 2;
+};
+
+struct KillArgs {
+  const float* logits = nullptr;         // chunk buffer [rows][C]
+  int C = 0, nx = 0, x0 = 0, nslots = 0, slot0 = 0;
+  const int32_t* slot_mutant = nullptr;  // global mutant id of each slot of the group
+  const int32_t* label = nullptr;        // [N]
+  const uint8_t* orig_ok = nullptr;      // [N] argmax original == label
+  uint64_t* kill_words = nullptr;        // [M][nwords]
+  int64_t nwords = 0;
+  unsigned long long* nonfinite = nullptr;
+  float* logits_out = nullptr;           // optional [N][C] copy (single-slot runs)
+};
+
+struct LabelArgs {
+  const float* logits = nullptr;         // [N][C]
+  int64_t N = 0;
+  int C = 0;
+  const int32_t* given = nullptr;        // optional [N]
+  int32_t* label = nullptr;
+  uint8_t* ok = nullptr;
+  unsigned long long* class_mask = nullptr;   // [ceil(C/64)]
+  unsigned long long* nonfinite = nullptr;
+};
+
+struct ScoreArgs {
+  const uint64_t* kill_words = nullptr;
+  int64_t nwords = 0;
+  int64_t N = 0;
+  const int32_t* label = nullptr;
+  int mask_words = 0;
+  int64_t* kills = nullptr;                   // [M]
+  unsigned long long* masks = nullptr;        // [M][mask_words]
+};
+
+struct CowArgs {                           // one copy-on-write parameter copy
+  const void* w_src; void* w_dst;
+  const float* b_src; float* b_dst;
+  int c_out; int64_t fan_in;
+  int rec0, rec1;                          // records [rec0, rec1) in the device record table
+};
+
+struct DevRecord { int op, neuron, partner, pad; int64_t noise_off; };
+
+// launchers (return the launch status)
+hipError_t launch_conv(const ConvArgs& a, int nslots, int dtype, hipStream_t s);
+hipError_t launch_add(const AddArgs& a, int dtype, hipStream_t s);
+hipError_t launch_gap(const GapArgs& a, int dtype, hipStream_t s);
+hipError_t launch_patch(const PatchArgs& a, hipStream_t s);
+hipError_t launch_kill(const KillArgs& a, hipStream_t s);
+hipError_t launch_labels(const LabelArgs& a, hipStream_t s);
+hipError_t launch_score(const ScoreArgs& a, int n_mutants, hipStream_t s);
+hipError_t launch_cow(const CowArgs* d_args, int n_copies, const DevRecord* d_recs,
+                      const float* d_noise, int dtype, hipStream_t s);
+hipError_t launch_copy_rows(const TensorArg& src, void* dst, int64_t rows, int nx, int x0,
+                            int esize, hipStream_t s);
+
+}  // namespace mure

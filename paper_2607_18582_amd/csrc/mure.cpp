@@ -1,0 +1,815 @@
+// C ABI of the library: context, state machine, device memory, and the
+// executor that runs the original model (filling the prefix cache) and every
+// mutant's suffix over chunks of (mutant slots x inputs).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "../../include/mure.h"
+#include "kernels.hpp"
+#include "plan.hpp"
+
+using namespace mure;
+
+namespace {
+
+thread_local std::string g_create_error;
+
+struct DevBuf {
+  void* p = nullptr;
+  size_t bytes = 0;
+  DevBuf() = default;
+  DevBuf(const DevBuf&) = delete;
+  DevBuf& operator=(const DevBuf&) = delete;
+  ~DevBuf() { release(); }
+  void release() {
+    if (p) (void)hipFree(p);
+    p = nullptr;
+    bytes = 0;
+  }
+  hipError_t alloc(size_t n) {
+    release();
+    if (n == 0) return hipSuccess;
+    hipError_t e = hipMalloc(&p, n);
+    if (e == hipSuccess) bytes = n;
+    else p = nullptr;
+    return e;
+  }
+  template <typename T> T* as() const { return reinterpret_cast<T*>(p); }
+};
+
+// Liveness-based placement of per-row activation buffers: offsets in bytes
+// per row; a buffer is reused once every reader of its previous owner ran.
+struct Placement {
+  std::map<int, int64_t> offset;   // node -> byte offset per row
+  int64_t peak = 0;                // bytes per row
+};
+
+Placement place_buffers(const Graph& g, const std::vector<int>& nodes, const std::set<int>& external) {
+  // nodes: executed in this order; external: nodes whose output lives elsewhere
+  std::map<int, int> last_use;
+  for (int v : nodes) {
+    for (int k = 0; k < g.nodes[v].n_in; ++k) last_use[g.nodes[v].in[k]] = v;
+  }
+  struct Blk { int64_t off, size; int owner; };
+  std::vector<Blk> blocks;
+  Placement pl;
+  const int out = g.out();
+  for (int v : nodes) {
+    // free blocks whose owner is no longer needed by v or later nodes
+    for (Blk& b : blocks) {
+      if (b.owner < 0) continue;
+      auto it = last_use.find(b.owner);
+      const int lu = (b.owner == out) ? 1 << 30 : (it == last_use.end() ? -1 : it->second);
+      if (lu < v) b.owner = -1;
+    }
+    if (external.count(v)) continue;
+    const int64_t need = (g.act_bytes(v) + 255) / 256 * 256;
+    int best = -1;
+    for (size_t i = 0; i < blocks.size(); ++i)
+      if (blocks[i].owner < 0 && blocks[i].size >= need && (best < 0 || blocks[i].size < blocks[best].size))
+        best = (int)i;
+    if (best < 0) {
+      blocks.push_back({pl.peak, need, v});
+      pl.peak += need;
+      best = (int)blocks.size() - 1;
+    } else {
+      blocks[best].owner = v;
+    }
+    pl.offset[v] = blocks[best].off;
+  }
+  return pl;
+}
+
+}  // namespace
+
+struct mure_ctx {
+  int device = -1;
+  bool plan_only = false;
+  hipStream_t stream = nullptr;
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  std::string err;
+  int state = 0;   // 0 created, 1 model loaded, 2 mutants applied, 3 original run
+  Graph g;
+  bool have_graph = false;
+  std::vector<std::unique_ptr<DevBuf>> d_w, d_b;     // original parameters per node
+  // mutants
+  Plan plan;
+  std::vector<Record> recs;
+  DevBuf d_cow;                                       // copy-on-write parameters
+  DevBuf d_tables;                                    // pointer tables
+  struct GroupTabs {
+    std::map<int, int64_t> w, b;                      // node -> offset (in pointers) into d_tables
+    int64_t slot_mutant = 0;                          // offset (int32) into d_slots
+    int64_t chmap = 0;                                // offset (int32) into d_chmap
+  };
+  std::vector<GroupTabs> gtabs;
+  std::map<int, int64_t> orig_w, orig_b;              // node -> offset of 1-entry original tables
+  DevBuf d_slots, d_chmap;
+  // prefix cache and original results
+  int64_t N = 0;
+  std::map<int, std::unique_ptr<DevBuf>> cache;
+  DevBuf d_logits, d_label, d_ok, d_classmask, d_nonfinite;
+  int64_t n_labels = 0;
+  // run_mutants scratch
+  DevBuf d_ws, d_kill, d_kills, d_masks;
+  // options
+  int64_t max_ws_mb = 16384;
+  int64_t chunk_inputs = 0;
+  int64_t fused = 1;
+  mure_stats stats{};
+
+  mure_status fail(mure_status s, const std::string& m) {
+    err = m;
+    return s;
+  }
+  mure_status dev_fail(hipError_t e, const char* what) {
+    err = std::string(what) + ": " + hipGetErrorString(e);
+    return e == hipErrorOutOfMemory ? MURE_E_NOMEM : MURE_E_DEVICE;
+  }
+};
+
+#define HIPTRY(expr)                                  \
+  do {                                                \
+    hipError_t e_ = (expr);                           \
+    if (e_ != hipSuccess) return ctx->dev_fail(e_, #expr); \
+  } while (0)
+
+namespace {
+
+int64_t esize_of(const Graph& g, int v) { return (v == g.out() || g.dtype == DT_F32) ? 4 : 2; }
+
+// Tensor reference of node p for the executor.
+struct Where {
+  const void* p;
+  int mode;
+};
+
+// Launch node v over rows of slots [slot0, slot0 + nslots) of a chunk with
+// nx inputs starting at x0.
+mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void* out, int out_mode,
+                      const void* const* wtab, const float* const* btab, int slot0, int nslots,
+                      int nx, int x0, int64_t chunk_rows) {
+  const Graph& g = ctx->g;
+  const Node& n = g.nodes[v];
+  const int out_f32 = v == g.out() ? 1 : 0;
+  hipError_t e = hipSuccess;
+  if (n.kind == K_CONV || n.kind == K_DENSE) {
+    ConvArgs a;
+    a.in.p = ins[0].p;
+    a.in.mode = ins[0].mode;
+    a.in.row_elems = (int64_t)n.inH * n.inW * n.inC;
+    a.out = out;
+    a.out_mode = out_mode;
+    a.out_row = n.out_elems();
+    a.out_f32 = out_f32;
+    a.wtab = wtab;
+    a.btab = btab;
+    a.slot0 = slot0;
+    a.nx = nx;
+    a.x0 = x0;
+    if (n.kind == K_CONV) {
+      a.H = n.inH; a.W = n.inW; a.C = n.inC;
+      a.Hc = n.Hc; a.Wc = n.Wc; a.Hp = n.H; a.Wp = n.W;
+      a.kh = n.kh; a.kw = n.kw; a.stride = n.stride; a.pad = n.pad; a.pool = n.maxpool ? 1 : 0;
+    } else {
+      a.H = 1; a.W = 1; a.C = n.c_in;
+      a.Hc = a.Wc = a.Hp = a.Wp = 1;
+      a.kh = a.kw = a.stride = 1; a.pad = 0; a.pool = 0;
+    }
+    a.Cout = n.c_out;
+    a.relu = n.relu;
+    a.K = a.kh * a.kw * a.C;
+    a.P = a.pool ? 4 * a.Hp * a.Wp : a.Hc * a.Wc;
+    e = launch_conv(a, nslots, g.dtype, ctx->stream);
+  } else if (n.kind == K_ADD) {
+    const Node& s = g.nodes[n.in[1]];
+    AddArgs a;
+    a.a.p = ins[0].p; a.a.mode = ins[0].mode; a.a.row_elems = n.out_elems();
+    a.s.p = ins[1].p; a.s.mode = ins[1].mode; a.s.row_elems = s.out_elems();
+    a.out = out; a.out_mode = out_mode; a.out_f32 = out_f32;
+    a.nx = nx; a.x0 = x0; a.rows = chunk_rows;
+    a.H = n.H; a.W = n.W; a.C = n.C; a.Hs = s.H; a.Ws = s.W; a.Cs = s.C;
+    a.shortcut = n.shortcut; a.relu = n.relu;
+    e = launch_add(a, g.dtype, ctx->stream);
+  } else if (n.kind == K_GAP) {
+    GapArgs a;
+    a.in.p = ins[0].p; a.in.mode = ins[0].mode; a.in.row_elems = (int64_t)n.inH * n.inW * n.inC;
+    a.out = out; a.out_mode = out_mode; a.out_f32 = out_f32;
+    a.nx = nx; a.x0 = x0; a.rows = chunk_rows; a.P = n.inH * n.inW; a.C = n.C;
+    e = launch_gap(a, g.dtype, ctx->stream);
+  } else if (n.kind == K_FLATTEN) {
+    if (out_mode != MODE_BUF) return ctx->fail(MURE_E_UNSUPPORTED, "a cached FLATTEN node");
+    TensorArg src;
+    src.p = ins[0].p; src.mode = ins[0].mode; src.row_elems = n.out_elems();
+    e = launch_copy_rows(src, out, chunk_rows, nx, x0, (int)esize_of(g, n.in[0]), ctx->stream);
+  } else {
+    return ctx->fail(MURE_E_INVALID, "node without a layer function");
+  }
+  if (e != hipSuccess) return ctx->dev_fail(e, "kernel launch");
+  ctx->stats.launches++;
+  return MURE_OK;
+}
+
+void reset_cache(mure_ctx* ctx) {
+  ctx->cache.clear();
+  ctx->d_logits.release();
+  ctx->d_label.release();
+  ctx->d_ok.release();
+  ctx->N = 0;
+}
+
+}  // namespace
+
+// =========================================================================
+extern "C" {
+
+int32_t mure_version(void) { return MURE_VERSION; }
+
+mure_status mure_create(mure_ctx** out, int32_t device, void* hip_stream) {
+  if (!out) {
+    g_create_error = "out is NULL";
+    return MURE_E_INVALID;
+  }
+  *out = nullptr;
+  std::unique_ptr<mure_ctx> ctx(new mure_ctx());
+  if (device < 0) {
+    if (device != -1) { g_create_error = "device must be >= 0, or -1 for a planning-only context"; return MURE_E_INVALID; }
+    ctx->plan_only = true;
+  } else {
+    int count = 0;
+    hipError_t e = hipGetDeviceCount(&count);
+    if (e != hipSuccess) { g_create_error = std::string("hipGetDeviceCount: ") + hipGetErrorString(e); return MURE_E_DEVICE; }
+    if (device >= count) { g_create_error = "no such device"; return MURE_E_INVALID; }
+    e = hipSetDevice(device);
+    if (e != hipSuccess) { g_create_error = std::string("hipSetDevice: ") + hipGetErrorString(e); return MURE_E_DEVICE; }
+    ctx->device = device;
+    ctx->stream = reinterpret_cast<hipStream_t>(hip_stream);
+    if (hipEventCreate(&ctx->ev0) != hipSuccess || hipEventCreate(&ctx->ev1) != hipSuccess) {
+      g_create_error = "hipEventCreate failed";
+      return MURE_E_DEVICE;
+    }
+  }
+  *out = ctx.release();
+  return MURE_OK;
+}
+
+void mure_destroy(mure_ctx* ctx) {
+  if (!ctx) return;
+  if (!ctx->plan_only) {
+    (void)hipSetDevice(ctx->device);
+    (void)hipStreamSynchronize(ctx->stream);
+    if (ctx->ev0) (void)hipEventDestroy(ctx->ev0);
+    if (ctx->ev1) (void)hipEventDestroy(ctx->ev1);
+  }
+  delete ctx;
+}
+
+const char* mure_last_error(const mure_ctx* ctx) {
+  if (!ctx) return g_create_error.c_str();
+  return ctx->err.c_str();
+}
+
+mure_status mure_set_option(mure_ctx* ctx, const char* name, int64_t value) {
+  if (!ctx || !name) return MURE_E_INVALID;
+  const std::string n(name);
+  if (n == "max_workspace_mb") {
+    if (value < 1) return ctx->fail(MURE_E_INVALID, "max_workspace_mb must be >= 1");
+    ctx->max_ws_mb = value;
+  } else if (n == "chunk_inputs") {
+    if (value < 0 || value % 64) return ctx->fail(MURE_E_INVALID, "chunk_inputs must be 0 or a multiple of 64");
+    ctx->chunk_inputs = value;
+  } else if (n == "fused_paths") {
+    if (value != 0 && value != 1) return ctx->fail(MURE_E_INVALID, "fused_paths must be 0 or 1");
+    ctx->fused = value;
+  } else {
+    return ctx->fail(MURE_E_INVALID, "unknown option " + n);
+  }
+  return MURE_OK;
+}
+
+mure_status mure_load_model(mure_ctx* ctx, const mure_layer* layers, int32_t n_layers,
+                            const int32_t in_hwc[3], int32_t dtype, const void* const* weights,
+                            const float* const* biases) {
+  if (!ctx) return MURE_E_INVALID;
+  if (!layers || !in_hwc || n_layers < 2) return ctx->fail(MURE_E_INVALID, "layers/in_hwc missing or fewer than 2 nodes");
+  Graph g;
+  g.nodes.resize(n_layers);
+  for (int i = 0; i < n_layers; ++i) {
+    const mure_layer& L = layers[i];
+    Node& v = g.nodes[i];
+    v.kind = L.kind; v.n_in = L.n_in; v.in[0] = L.in[0]; v.in[1] = L.in[1];
+    v.c_in = L.c_in; v.c_out = L.c_out; v.kh = L.kh; v.kw = L.kw; v.stride = L.stride; v.pad = L.pad;
+    v.relu = L.relu; v.maxpool = L.maxpool; v.shortcut = L.shortcut;
+    if (v.kind == K_ADD || v.kind == K_GAP || v.kind == K_FLATTEN || v.kind == K_INPUT) {
+      if (v.kh > 1 || v.kw > 1) return ctx->fail(MURE_E_INVALID, "geometry given for a node without weights");
+    }
+  }
+  std::string m = build_graph(g, in_hwc[0], in_hwc[1], in_hwc[2], dtype);
+  if (!m.empty()) return ctx->fail(MURE_E_INVALID, m);
+  for (int i = 0; i < n_layers; ++i) {
+    const bool need = g.nodes[i].weighted();
+    const bool hw = weights && weights[i], hb = biases && biases[i];
+    if (need && (!hw || !hb)) return ctx->fail(MURE_E_INVALID, "node " + std::to_string(i) + ": weights and bias required");
+    if (!need && (hw || hb)) return ctx->fail(MURE_E_INVALID, "node " + std::to_string(i) + ": has no parameters");
+  }
+  std::vector<std::unique_ptr<DevBuf>> dw(n_layers), db(n_layers);
+  if (!ctx->plan_only) {
+    HIPTRY(hipSetDevice(ctx->device));
+    const int64_t es = dtype == DT_F32 ? 4 : 2;
+    for (int i = 0; i < n_layers; ++i) {
+      dw[i].reset(new DevBuf());
+      db[i].reset(new DevBuf());
+      if (!g.nodes[i].weighted()) continue;
+      const size_t wb = (size_t)g.nodes[i].n_weights() * es, bb = (size_t)g.nodes[i].c_out * 4;
+      HIPTRY(dw[i]->alloc(wb));
+      HIPTRY(db[i]->alloc(bb));
+      HIPTRY(hipMemcpy(dw[i]->p, weights[i], wb, hipMemcpyHostToDevice));
+      HIPTRY(hipMemcpy(db[i]->p, biases[i], bb, hipMemcpyHostToDevice));
+    }
+  }
+  ctx->g = std::move(g);
+  ctx->have_graph = true;
+  ctx->d_w = std::move(dw);
+  ctx->d_b = std::move(db);
+  ctx->plan = Plan();
+  ctx->recs.clear();
+  ctx->d_cow.release();
+  ctx->d_tables.release();
+  reset_cache(ctx);
+  ctx->stats = mure_stats{};
+  ctx->state = 1;
+  return MURE_OK;
+}
+
+mure_status mure_apply_mutants(mure_ctx* ctx, int32_t n_mutants, const mure_record* records,
+                               int64_t n_records) {
+  if (!ctx) return MURE_E_INVALID;
+  if (ctx->state < 1) return ctx->fail(MURE_E_STATE, "load_model first");
+  if (n_mutants < 0 || n_records < 0 || (n_records > 0 && !records))
+    return ctx->fail(MURE_E_INVALID, "bad mutant/record counts");
+  const Graph& g = ctx->g;
+  std::vector<Record> recs(n_records);
+  std::vector<float> noise;
+  for (int64_t r = 0; r < n_records; ++r) {
+    const mure_record& x = records[r];
+    Record& y = recs[r];
+    y.mutant = x.mutant; y.op = x.op; y.layer = x.layer; y.neuron = x.neuron; y.partner = x.partner;
+    y.noise_off = 0; y.noise_len = 0;
+    if (x.op == OP_GF) {
+      if (!x.noise || x.noise_len <= 0)
+        return ctx->fail(MURE_E_INVALID, "record " + std::to_string(r) + ": Gaussian fuzz needs noise");
+      y.noise_off = (int64_t)noise.size();
+      y.noise_len = x.noise_len;
+      if (x.layer >= 0 && x.layer < (int)g.nodes.size() && x.noise_len == g.nodes[x.layer].fan_in)
+        noise.insert(noise.end(), x.noise, x.noise + x.noise_len);
+    }
+  }
+  Plan plan;
+  std::string m = build_plan(g, n_mutants, recs, plan);
+  if (!m.empty()) return ctx->fail(MURE_E_INVALID, m);
+
+  if (!ctx->plan_only) {
+    HIPTRY(hipSetDevice(ctx->device));
+    HIPTRY(hipEventRecord(ctx->ev0, ctx->stream));
+    const int64_t es = g.dtype == DT_F32 ? 4 : 2;
+    // copy-on-write pool: weights (256-byte aligned) then biases
+    std::vector<int64_t> woff(plan.cows.size()), boff(plan.cows.size());
+    int64_t pos = 0;
+    for (size_t c = 0; c < plan.cows.size(); ++c) {
+      woff[c] = pos;
+      pos += (g.nodes[plan.cows[c].layer].n_weights() * es + 255) / 256 * 256;
+    }
+    for (size_t c = 0; c < plan.cows.size(); ++c) {
+      boff[c] = pos;
+      pos += ((int64_t)g.nodes[plan.cows[c].layer].c_out * 4 + 255) / 256 * 256;
+    }
+    auto cow = std::make_unique<DevBuf>();
+    HIPTRY(cow->alloc((size_t)std::max<int64_t>(pos, 256)));
+    char* base = cow->as<char>();
+    std::map<std::pair<int, int>, size_t> cow_index;
+    std::vector<CowArgs> cargs(plan.cows.size());
+    std::vector<DevRecord> drecs;
+    for (size_t c = 0; c < plan.cows.size(); ++c) {
+      const CowCopy& cc = plan.cows[c];
+      CowArgs& a = cargs[c];
+      a.w_src = ctx->d_w[cc.layer]->p;
+      a.w_dst = base + woff[c];
+      a.b_src = ctx->d_b[cc.layer]->as<float>();
+      a.b_dst = reinterpret_cast<float*>(base + boff[c]);
+      a.c_out = g.nodes[cc.layer].c_out;
+      a.fan_in = g.nodes[cc.layer].fan_in;
+      a.rec0 = (int)drecs.size();
+      for (int r : cc.records) {
+        DevRecord d;
+        d.op = recs[r].op; d.neuron = recs[r].neuron; d.partner = recs[r].partner; d.pad = 0;
+        d.noise_off = recs[r].noise_off;
+        drecs.push_back(d);
+      }
+      a.rec1 = (int)drecs.size();
+      cow_index[{cc.mutant, cc.layer}] = c;
+    }
+    // pointer tables: per group, per weighted node >= mmi, one pointer per slot;
+    // plus 1-entry tables of the original parameters (run_original)
+    std::vector<const void*> tabs;
+    std::vector<mure_ctx::GroupTabs> gtabs(plan.groups.size());
+    std::vector<int32_t> slots, chmaps;
+    std::map<int, int64_t> ow, ob;
+    for (int v = 0; v < (int)g.nodes.size(); ++v) {
+      if (!g.nodes[v].weighted()) continue;
+      ow[v] = (int64_t)tabs.size(); tabs.push_back(ctx->d_w[v]->p);
+      ob[v] = (int64_t)tabs.size(); tabs.push_back(ctx->d_b[v]->p);
+    }
+    for (size_t gi = 0; gi < plan.groups.size(); ++gi) {
+      const Group& gr = plan.groups[gi];
+      mure_ctx::GroupTabs& gt = gtabs[gi];
+      for (int v = gr.mmi; v < (int)g.nodes.size(); ++v) {
+        if (!g.nodes[v].weighted()) continue;
+        gt.w[v] = (int64_t)tabs.size();
+        for (int mu : gr.mutants) {
+          auto it = cow_index.find({mu, v});
+          tabs.push_back(it == cow_index.end() ? ctx->d_w[v]->p : cargs[it->second].w_dst);
+        }
+        gt.b[v] = (int64_t)tabs.size();
+        for (int mu : gr.mutants) {
+          auto it = cow_index.find({mu, v});
+          tabs.push_back(it == cow_index.end() ? ctx->d_b[v]->p : (const void*)cargs[it->second].b_dst);
+        }
+      }
+      gt.slot_mutant = (int64_t)slots.size();
+      for (int mu : gr.mutants) slots.push_back(mu);
+      gt.chmap = (int64_t)chmaps.size();
+      for (size_t s = gr.n_recompute; s < gr.mutants.size(); ++s) {
+        const std::vector<int>& cm = plan.mutants[gr.mutants[s]].chmap;
+        chmaps.insert(chmaps.end(), cm.begin(), cm.end());
+      }
+    }
+    auto dtab = std::make_unique<DevBuf>(), dslots = std::make_unique<DevBuf>(), dch = std::make_unique<DevBuf>();
+    HIPTRY(dtab->alloc(std::max<size_t>(tabs.size() * sizeof(void*), 8)));
+    HIPTRY(dslots->alloc(std::max<size_t>(slots.size() * 4, 4)));
+    HIPTRY(dch->alloc(std::max<size_t>(chmaps.size() * 4, 4)));
+    if (!tabs.empty()) HIPTRY(hipMemcpy(dtab->p, tabs.data(), tabs.size() * sizeof(void*), hipMemcpyHostToDevice));
+    if (!slots.empty()) HIPTRY(hipMemcpy(dslots->p, slots.data(), slots.size() * 4, hipMemcpyHostToDevice));
+    if (!chmaps.empty()) HIPTRY(hipMemcpy(dch->p, chmaps.data(), chmaps.size() * 4, hipMemcpyHostToDevice));
+    if (!cargs.empty()) {
+      DevBuf dargs, dr, dn;
+      HIPTRY(dargs.alloc(cargs.size() * sizeof(CowArgs)));
+      HIPTRY(dr.alloc(std::max<size_t>(drecs.size() * sizeof(DevRecord), 8)));
+      HIPTRY(dn.alloc(std::max<size_t>(noise.size() * 4, 4)));
+      HIPTRY(hipMemcpy(dargs.p, cargs.data(), cargs.size() * sizeof(CowArgs), hipMemcpyHostToDevice));
+      if (!drecs.empty()) HIPTRY(hipMemcpy(dr.p, drecs.data(), drecs.size() * sizeof(DevRecord), hipMemcpyHostToDevice));
+      if (!noise.empty()) HIPTRY(hipMemcpy(dn.p, noise.data(), noise.size() * 4, hipMemcpyHostToDevice));
+      HIPTRY(launch_cow(dargs.as<CowArgs>(), (int)cargs.size(), dr.as<DevRecord>(), dn.as<float>(), g.dtype, ctx->stream));
+      HIPTRY(hipStreamSynchronize(ctx->stream));
+    }
+    HIPTRY(hipEventRecord(ctx->ev1, ctx->stream));
+    HIPTRY(hipEventSynchronize(ctx->ev1));
+    float ms = 0.f;
+    (void)hipEventElapsedTime(&ms, ctx->ev0, ctx->ev1);
+    ctx->stats.ms_apply = ms;
+    // commit
+    ctx->d_cow.release();
+    std::swap(ctx->d_cow.p, cow->p); std::swap(ctx->d_cow.bytes, cow->bytes);
+    ctx->d_tables.release();
+    std::swap(ctx->d_tables.p, dtab->p); std::swap(ctx->d_tables.bytes, dtab->bytes);
+    ctx->d_slots.release();
+    std::swap(ctx->d_slots.p, dslots->p); std::swap(ctx->d_slots.bytes, dslots->bytes);
+    ctx->d_chmap.release();
+    std::swap(ctx->d_chmap.p, dch->p); std::swap(ctx->d_chmap.bytes, dch->bytes);
+    ctx->gtabs = std::move(gtabs);
+    ctx->orig_w = std::move(ow);
+    ctx->orig_b = std::move(ob);
+  }
+  ctx->plan = std::move(plan);
+  ctx->recs = std::move(recs);
+  reset_cache(ctx);
+  ctx->stats.n_groups = (int64_t)ctx->plan.groups.size();
+  ctx->stats.n_identity_mutants = ctx->plan.n_identity;
+  ctx->state = 2;
+  return MURE_OK;
+}
+
+
+// -------------------------------------------------------------------------
+// run_original: the original model once over X; fills the prefix cache.
+mure_status mure_run_original(mure_ctx* ctx, const void* inputs_dev, int64_t n_inputs,
+                              const int32_t* labels) {
+  if (!ctx) return MURE_E_INVALID;
+  if (ctx->plan_only) return ctx->fail(MURE_E_UNSUPPORTED, "planning-only context");
+  if (ctx->state < 2) return ctx->fail(MURE_E_STATE, "apply_mutants must run before run_original");
+  if (!inputs_dev || n_inputs < 1 || n_inputs > (int64_t)1 << 30)
+    return ctx->fail(MURE_E_INVALID, "inputs missing or n_inputs out of range");
+  const Graph& g = ctx->g;
+  const int C = g.classes();
+  const int L = g.out();
+  if (labels)
+    for (int64_t i = 0; i < n_inputs; ++i)
+      if (labels[i] < 0 || labels[i] >= C) return ctx->fail(MURE_E_INVALID, "label out of range");
+  HIPTRY(hipSetDevice(ctx->device));
+  reset_cache(ctx);
+  ctx->state = 2;
+  const int64_t n = n_inputs;
+  std::set<int> cached(ctx->plan.cache_nodes.begin(), ctx->plan.cache_nodes.end());
+  int64_t cache_bytes = 0;
+  for (int v : cached) {
+    if (v == L) continue;                               // the logits buffer serves the output
+    auto b = std::make_unique<DevBuf>();
+    HIPTRY(b->alloc((size_t)(n * g.act_bytes(v))));
+    cache_bytes += (int64_t)b->bytes;
+    ctx->cache[v] = std::move(b);
+  }
+  HIPTRY(ctx->d_logits.alloc((size_t)(n * C * 4)));
+  HIPTRY(ctx->d_label.alloc((size_t)(n * 4)));
+  HIPTRY(ctx->d_ok.alloc((size_t)n));
+  HIPTRY(ctx->d_classmask.alloc(64));
+  HIPTRY(ctx->d_nonfinite.alloc(8));
+  cache_bytes += n * C * 4;
+  DevBuf d_given;
+  if (labels) {
+    HIPTRY(d_given.alloc((size_t)(n * 4)));
+    HIPTRY(hipMemcpy(d_given.p, labels, (size_t)(n * 4), hipMemcpyHostToDevice));
+  }
+  std::vector<int> nodes;
+  for (int v = 1; v <= L; ++v) nodes.push_back(v);
+  std::set<int> external(cached);
+  external.insert(L);
+  Placement pl = place_buffers(g, nodes, external);
+  const int64_t budget = ctx->max_ws_mb << 20;
+  int64_t nx = n;
+  if (ctx->chunk_inputs) nx = std::min<int64_t>(nx, ctx->chunk_inputs);
+  if (pl.peak * nx > budget) nx = std::max<int64_t>(64, budget / std::max<int64_t>(pl.peak, 1) / 64 * 64);
+  if (nx > n) nx = n;
+  if (pl.peak * nx > (int64_t)ctx->d_ws.bytes) HIPTRY(ctx->d_ws.alloc((size_t)(pl.peak * nx)));
+  char* ws = ctx->d_ws.as<char>();
+
+  HIPTRY(hipEventRecord(ctx->ev0, ctx->stream));
+  HIPTRY(hipMemsetAsync(ctx->d_classmask.p, 0, 64, ctx->stream));
+  HIPTRY(hipMemsetAsync(ctx->d_nonfinite.p, 0, 8, ctx->stream));
+  if (cached.count(0))
+    HIPTRY(hipMemcpyAsync(ctx->cache[0]->p, inputs_dev, (size_t)(n * g.act_bytes(0)),
+                          hipMemcpyDeviceToDevice, ctx->stream));
+  const void* const* tabs = ctx->d_tables.as<const void*>();
+  ctx->stats.launches = 0;
+  for (int64_t x0 = 0; x0 < n; x0 += nx) {
+    const int cnt = (int)std::min<int64_t>(nx, n - x0);
+    auto where = [&](int p) -> Where {
+      if (p == 0) return {cached.count(0) ? ctx->cache[0]->p : inputs_dev, MODE_CACHE};
+      if (p == L) return {ctx->d_logits.p, MODE_CACHE};
+      if (cached.count(p)) return {ctx->cache[p]->p, MODE_CACHE};
+      return {ws + pl.offset.at(p) * nx, MODE_BUF};
+    };
+    for (int v = 1; v <= L; ++v) {
+      const Node& nd = g.nodes[v];
+      std::vector<Where> ins;
+      for (int k = 0; k < nd.n_in; ++k) ins.push_back(where(nd.in[k]));
+      Where o = where(v);
+      const void* const* wt = nd.weighted() ? tabs + ctx->orig_w.at(v) : nullptr;
+      const float* const* bt = nd.weighted() ? reinterpret_cast<const float* const*>(tabs + ctx->orig_b.at(v)) : nullptr;
+      mure_status st = exec_node(ctx, v, ins, const_cast<void*>(o.p), o.mode, wt, bt, 0, 1, cnt, (int)x0, cnt);
+      if (st != MURE_OK) return st;
+    }
+  }
+  LabelArgs la;
+  la.logits = ctx->d_logits.as<float>();
+  la.N = n;
+  la.C = C;
+  la.given = labels ? d_given.as<int32_t>() : nullptr;
+  la.label = ctx->d_label.as<int32_t>();
+  la.ok = ctx->d_ok.as<uint8_t>();
+  la.class_mask = ctx->d_classmask.as<unsigned long long>();
+  la.nonfinite = ctx->d_nonfinite.as<unsigned long long>();
+  HIPTRY(launch_labels(la, ctx->stream));
+  HIPTRY(hipEventRecord(ctx->ev1, ctx->stream));
+  HIPTRY(hipEventSynchronize(ctx->ev1));
+  float ms = 0.f;
+  HIPTRY(hipEventElapsedTime(&ms, ctx->ev0, ctx->ev1));
+  unsigned long long mask[8];
+  HIPTRY(hipMemcpy(mask, ctx->d_classmask.p, 64, hipMemcpyDeviceToHost));
+  ctx->n_labels = 0;
+  for (int i = 0; i < 8; ++i) ctx->n_labels += __builtin_popcountll(mask[i]);
+  ctx->N = n;
+  ctx->stats.ms_run_original = ms;
+  ctx->stats.macs_original = g.full_macs() * n;
+  ctx->stats.cache_bytes = cache_bytes;
+  ctx->state = 3;
+  return MURE_OK;
+}
+
+// -------------------------------------------------------------------------
+// The suffix of group gi for its slots [s_begin, s_end), over all inputs.
+static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint64_t* kill_words,
+                             float* logits_out) {
+  const Graph& g = ctx->g;
+  const Group& gr = ctx->plan.groups[gi];
+  const mure_ctx::GroupTabs& gt = ctx->gtabs[gi];
+  const int L = g.out(), mmi = gr.mmi;
+  const int64_t N = ctx->N;
+  std::vector<int> nodes;
+  for (int v = mmi; v <= L; ++v) nodes.push_back(v);
+  Placement pl = place_buffers(g, nodes, {});
+  const int64_t budget = ctx->max_ws_mb << 20;
+  int64_t nx = N;
+  if (ctx->chunk_inputs) nx = std::min<int64_t>(nx, ctx->chunk_inputs);
+  if (pl.peak * nx > budget) nx = std::max<int64_t>(64, budget / pl.peak / 64 * 64);
+  if (nx > N) nx = N;
+  int64_t spc = std::max<int64_t>(1, budget / (pl.peak * nx));
+  spc = std::min<int64_t>(spc, std::min<int64_t>(65535, s_end - s_begin));
+  spc = std::min<int64_t>(spc, std::max<int64_t>(1, ((int64_t)1 << 31) / nx / 64));
+  const int64_t cap_rows = spc * nx;
+  if (pl.peak * cap_rows > (int64_t)ctx->d_ws.bytes) HIPTRY(ctx->d_ws.alloc((size_t)(pl.peak * cap_rows)));
+  ctx->stats.workspace_bytes = std::max<int64_t>(ctx->stats.workspace_bytes, (int64_t)ctx->d_ws.bytes);
+  char* ws = ctx->d_ws.as<char>();
+  const void* const* tabs = ctx->d_tables.as<const void*>();
+  const int32_t* slot_mut = ctx->d_slots.as<int32_t>() + gt.slot_mutant;
+  const Node& nm = g.nodes[mmi];
+  const void* mmi_cache = mmi == L ? ctx->d_logits.p : (ctx->cache.count(mmi) ? ctx->cache[mmi]->p : nullptr);
+  for (int cs0 = s_begin; cs0 < s_end; cs0 += (int)spc) {
+    const int cs1 = (int)std::min<int64_t>(s_end, cs0 + spc);
+    const int ns = cs1 - cs0;
+    for (int64_t x0 = 0; x0 < N; x0 += nx) {
+      const int cnt = (int)std::min<int64_t>(nx, N - x0);
+      const int64_t rows = (int64_t)ns * cnt;
+      auto where = [&](int p) -> Where {
+        if (p < mmi) {
+          if (p == 0 && !ctx->cache.count(0)) return {nullptr, MODE_CACHE};
+          return {ctx->cache.at(p)->p, MODE_CACHE};
+        }
+        return {ws + pl.offset.at(p) * cap_rows, MODE_BUF};
+      };
+      // node mmi: recompute (fuzz / inverse) slots, then channel-patch slots
+      {
+        std::vector<Where> ins;
+        for (int k = 0; k < nm.n_in; ++k) ins.push_back(where(nm.in[k]));
+        void* out = const_cast<void*>(where(mmi).p);
+        const int rec_end = std::min(cs1, gr.n_recompute);
+        if (cs0 < rec_end) {
+          mure_status st = exec_node(ctx, mmi, ins, out, MODE_BUF, tabs + gt.w.at(mmi) + cs0,
+                                     reinterpret_cast<const float* const*>(tabs + gt.b.at(mmi) + cs0),
+                                     0, rec_end - cs0, cnt, (int)x0, rows);
+          if (st != MURE_OK) return st;
+        }
+        const int pa = std::max(cs0, gr.n_recompute);
+        if (pa < cs1) {
+          PatchArgs a;
+          a.cache = mmi_cache;
+          a.out = out;
+          a.chmap = ctx->d_chmap.as<int32_t>() + gt.chmap;
+          a.slot0 = pa - cs0;
+          a.chmap_slot0 = pa - gr.n_recompute;
+          a.nx = cnt; a.x0 = (int)x0; a.nslots = cs1 - pa;
+          a.P = nm.H * nm.W; a.C = nm.C; a.esize = (int)esize_of(g, mmi);
+          HIPTRY(launch_patch(a, ctx->stream));
+          ctx->stats.launches++;
+        }
+      }
+      for (int v = mmi + 1; v <= L; ++v) {
+        const Node& nd = g.nodes[v];
+        std::vector<Where> ins;
+        for (int k = 0; k < nd.n_in; ++k) ins.push_back(where(nd.in[k]));
+        const void* const* wt = nd.weighted() ? tabs + gt.w.at(v) + cs0 : nullptr;
+        const float* const* bt = nd.weighted() ? reinterpret_cast<const float* const*>(tabs + gt.b.at(v) + cs0) : nullptr;
+        mure_status st = exec_node(ctx, v, ins, const_cast<void*>(where(v).p), MODE_BUF, wt, bt, 0, ns, cnt, (int)x0, rows);
+        if (st != MURE_OK) return st;
+      }
+      KillArgs ka;
+      ka.logits = reinterpret_cast<const float*>(where(L).p);
+      ka.C = g.classes();
+      ka.nx = cnt; ka.x0 = (int)x0; ka.nslots = ns; ka.slot0 = 0;
+      ka.slot_mutant = slot_mut + cs0;
+      ka.label = ctx->d_label.as<int32_t>();
+      ka.orig_ok = ctx->d_ok.as<uint8_t>();
+      ka.kill_words = kill_words;
+      ka.nwords = (N + 63) / 64;
+      ka.nonfinite = ctx->d_nonfinite.as<unsigned long long>();
+      ka.logits_out = logits_out;
+      HIPTRY(launch_kill(ka, ctx->stream));
+      ctx->stats.launches++;
+    }
+  }
+  return MURE_OK;
+}
+
+mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* kills_host, mure_score* score) {
+  if (!ctx) return MURE_E_INVALID;
+  if (ctx->plan_only) return ctx->fail(MURE_E_UNSUPPORTED, "planning-only context");
+  if (ctx->state != 3) return ctx->fail(MURE_E_STATE, "run_original must run after the last apply_mutants");
+  HIPTRY(hipSetDevice(ctx->device));
+  const int64_t M = ctx->plan.n_mutants, N = ctx->N, nwords = (N + 63) / 64;
+  const int C = ctx->g.classes();
+  const int mw = (C + 63) / 64;
+  uint64_t* kw = kill_bits_dev;
+  if (!kw) {
+    if ((size_t)(M * nwords * 8) > ctx->d_kill.bytes) HIPTRY(ctx->d_kill.alloc((size_t)std::max<int64_t>(M * nwords * 8, 8)));
+    kw = ctx->d_kill.as<uint64_t>();
+  }
+  if ((size_t)(M * 8) > ctx->d_kills.bytes) HIPTRY(ctx->d_kills.alloc((size_t)std::max<int64_t>(M * 8, 8)));
+  if ((size_t)(M * mw * 8) > ctx->d_masks.bytes) HIPTRY(ctx->d_masks.alloc((size_t)std::max<int64_t>(M * mw * 8, 8)));
+  ctx->stats.launches = 0;
+  HIPTRY(hipEventRecord(ctx->ev0, ctx->stream));
+  HIPTRY(hipMemsetAsync(ctx->d_nonfinite.p, 0, 8, ctx->stream));
+  if (M > 0) HIPTRY(hipMemsetAsync(kw, 0, (size_t)(M * nwords * 8), ctx->stream));
+  for (int gi = 0; gi < (int)ctx->plan.groups.size(); ++gi) {
+    mure_status st = run_group(ctx, gi, 0, (int)ctx->plan.groups[gi].mutants.size(), kw, nullptr);
+    if (st != MURE_OK) return st;
+  }
+  ScoreArgs sa;
+  sa.kill_words = kw;
+  sa.nwords = nwords;
+  sa.N = N;
+  sa.label = ctx->d_label.as<int32_t>();
+  sa.mask_words = mw;
+  sa.kills = ctx->d_kills.as<int64_t>();
+  sa.masks = ctx->d_masks.as<unsigned long long>();
+  HIPTRY(launch_score(sa, (int)M, ctx->stream));
+  HIPTRY(hipEventRecord(ctx->ev1, ctx->stream));
+  HIPTRY(hipEventSynchronize(ctx->ev1));
+  float ms = 0.f;
+  HIPTRY(hipEventElapsedTime(&ms, ctx->ev0, ctx->ev1));
+  std::vector<int64_t> kills(M);
+  std::vector<unsigned long long> masks(M * mw);
+  unsigned long long nonfinite = 0;
+  if (M > 0) {
+    HIPTRY(hipMemcpy(kills.data(), ctx->d_kills.p, (size_t)(M * 8), hipMemcpyDeviceToHost));
+    HIPTRY(hipMemcpy(masks.data(), ctx->d_masks.p, (size_t)(M * mw * 8), hipMemcpyDeviceToHost));
+  }
+  HIPTRY(hipMemcpy(&nonfinite, ctx->d_nonfinite.p, 8, hipMemcpyDeviceToHost));
+  int64_t num = 0, killed = 0;
+  for (int64_t m = 0; m < M; ++m) {
+    for (int w = 0; w < mw; ++w) num += __builtin_popcountll(masks[m * mw + w]);
+    killed += kills[m] > 0;
+  }
+  if (kills_host && M > 0) std::memcpy(kills_host, kills.data(), (size_t)(M * 8));
+  if (score) {
+    score->ms_num = num;
+    score->ms_den = M * ctx->n_labels;
+    score->ms = score->ms_den ? (double)num / (double)score->ms_den : 0.0;
+    score->killed_mutants = killed;
+    score->n_mutants = M;
+    score->n_labels = ctx->n_labels;
+    score->n_inputs = N;
+    score->nonfinite_logits = (int64_t)nonfinite;
+  }
+  ctx->stats.ms_run_mutants = ms;
+  ctx->stats.macs_vanilla = ctx->plan.macs_vanilla * N;
+  ctx->stats.macs_memoized = ctx->plan.macs_memoized * N;
+  ctx->stats.macs_algorithmic = ctx->plan.macs_algorithmic * N;
+  ctx->stats.macs_executed = ctx->plan.macs_executed * N;
+  return MURE_OK;
+}
+
+mure_status mure_get_logits(mure_ctx* ctx, int32_t mutant_id, float* out_dev) {
+  if (!ctx) return MURE_E_INVALID;
+  if (ctx->plan_only) return ctx->fail(MURE_E_UNSUPPORTED, "planning-only context");
+  if (ctx->state != 3) return ctx->fail(MURE_E_STATE, "run_original must run first");
+  if (!out_dev) return ctx->fail(MURE_E_INVALID, "out_dev is NULL");
+  if (mutant_id < -1 || mutant_id >= ctx->plan.n_mutants) return ctx->fail(MURE_E_INVALID, "mutant id out of range");
+  HIPTRY(hipSetDevice(ctx->device));
+  const int64_t bytes = ctx->N * ctx->g.classes() * 4;
+  if (mutant_id == -1 || ctx->plan.mutants[mutant_id].mmi < 0) {
+    HIPTRY(hipMemcpyAsync(out_dev, ctx->d_logits.p, (size_t)bytes, hipMemcpyDeviceToDevice, ctx->stream));
+  } else {
+    const MutantPlan& mp = ctx->plan.mutants[mutant_id];
+    mure_status st = run_group(ctx, mp.group, mp.slot, mp.slot + 1, nullptr, out_dev);
+    if (st != MURE_OK) return st;
+  }
+  HIPTRY(hipStreamSynchronize(ctx->stream));
+  return MURE_OK;
+}
+
+mure_status mure_mutant_plan(const mure_ctx* ctx, int32_t mutant_id, int32_t* mmi, int32_t* group,
+                             int32_t* k_nodes, int32_t max_k, int32_t* n_k) {
+  if (!ctx) return MURE_E_INVALID;
+  if (ctx->state < 2) return const_cast<mure_ctx*>(ctx)->fail(MURE_E_STATE, "apply_mutants first");
+  if (mutant_id < 0 || mutant_id >= ctx->plan.n_mutants)
+    return const_cast<mure_ctx*>(ctx)->fail(MURE_E_INVALID, "mutant id out of range");
+  const MutantPlan& mp = ctx->plan.mutants[mutant_id];
+  if (mmi) *mmi = mp.mmi;
+  if (group) *group = mp.group;
+  if (n_k) *n_k = (int32_t)mp.K.size();
+  if (k_nodes)
+    for (int i = 0; i < (int)mp.K.size() && i < max_k; ++i) k_nodes[i] = mp.K[i];
+  return MURE_OK;
+}
+
+mure_status mure_get_stats(const mure_ctx* ctx, mure_stats* out) {
+  if (!ctx || !out) return MURE_E_INVALID;
+  *out = ctx->stats;
+  out->n_groups = (int64_t)ctx->plan.groups.size();
+  out->n_identity_mutants = ctx->plan.n_identity;
+  if (ctx->N == 0) {   // before run_original: per-input ledger
+    out->macs_vanilla = ctx->plan.macs_vanilla;
+    out->macs_memoized = ctx->plan.macs_memoized;
+    out->macs_algorithmic = ctx->plan.macs_algorithmic;
+    out->macs_executed = ctx->plan.macs_executed;
+  }
+  return MURE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,98 @@
+// Host planner for memoized mutation testing (no HIP dependency).
+//
+// Graph validation and shape inference, the dependence graph (Algorithm 2,
+// given explicitly by the node descriptors), each mutant's mutated layers,
+// earliest mutated layer mmi and memoization boundary K (Algorithm 1;
+// Section 4), the clustering of mutants (grouped by mmi, which determines K),
+// the prefix-cache set, the per-mutant channel patches at mmi, and the MAC
+// ledger of Section 5.2 (Lemma 4).
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+namespace mure {
+
+enum Kind { K_INPUT = 0, K_DENSE = 1, K_CONV = 2, K_ADD = 3, K_GAP = 4, K_FLATTEN = 5 };
+enum Op { OP_GF = 0, OP_NEB = 1, OP_NAI = 2, OP_NS = 3 };
+enum DType { DT_F32 = 0, DT_BF16 = 1 };
+
+struct Node {
+  int kind = 0, n_in = 0, in[2] = {-1, -1};
+  int c_in = 0, c_out = 0, kh = 1, kw = 1, stride = 1, pad = 0;
+  int relu = 0, maxpool = 0, shortcut = 0;
+  // derived
+  int H = 0, W = 0, C = 0;        // output shape (after pool)
+  int Hc = 0, Wc = 0;             // convolution output before pooling
+  int inH = 0, inW = 0, inC = 0;  // shape of in[0]
+  int64_t fan_in = 0;             // weights per neuron
+  int64_t macs = 0;               // multiply-accumulates per input
+  bool weighted() const { return kind == K_DENSE || kind == K_CONV; }
+  int64_t out_elems() const { return (int64_t)H * W * C; }
+  int64_t n_weights() const { return weighted() ? (int64_t)c_out * fan_in : 0; }
+};
+
+struct Graph {
+  int dtype = DT_F32;
+  std::vector<Node> nodes;
+  int out() const { return (int)nodes.size() - 1; }
+  int classes() const { return nodes.back().C; }
+  int64_t full_macs() const;
+  // bytes per input of node v's activation as stored (the output node is float32)
+  int64_t act_bytes(int v) const;
+};
+
+// Validates `nodes` (topological order, shapes, kind-specific fields) and
+// fills the derived fields.  Returns "" on success, else a message.
+std::string build_graph(Graph& g, int in_h, int in_w, int in_c, int dtype);
+
+struct Record {
+  int mutant, op, layer, neuron, partner;
+  int64_t noise_off, noise_len;   // into the concatenated noise array
+};
+
+struct MutantPlan {
+  int mmi = -1;                 // -1: identity mutant (no records)
+  int group = -1;
+  int slot = -1;                // position inside its group
+  std::vector<int> layers;      // mu(M'), ascending
+  std::vector<int> K;           // memoization boundary, ascending
+  bool recompute = false;       // a fuzz/inverse record at mmi: recompute node mmi
+  std::vector<int> chmap;       // !recompute: output channel c of mmi <- original channel
+                                // chmap[c] (-1 = zero); size c_out(mmi)
+  int64_t touched = 0;          // channels of mmi changed by fuzz/inverse records
+};
+
+// Copy-on-write parameter copy of one (mutant, layer).
+struct CowCopy {
+  int mutant, layer;
+  std::vector<int> records;     // indices into the record array, in order
+};
+
+struct Group {
+  int mmi = -1;
+  std::vector<int> K;
+  std::vector<int> mutants;     // global ids; recompute mutants first
+  int n_recompute = 0;
+};
+
+struct Plan {
+  int n_mutants = 0;
+  std::vector<MutantPlan> mutants;
+  std::vector<Group> groups;
+  std::vector<CowCopy> cows;
+  std::vector<int> cache_nodes;  // nodes whose original activations are cached
+  int64_t n_identity = 0;
+  // ledger, per input
+  int64_t macs_vanilla = 0, macs_memoized = 0, macs_algorithmic = 0, macs_executed = 0;
+};
+
+// Memoization boundary K of a first mutated layer (Algorithm 1 / Section 4).
+std::vector<int> boundary(const Graph& g, int mmi);
+
+// Validates records and builds the plan.  Returns "" or a message.
+std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>& recs,
+                       Plan& plan);
+
+}  // namespace mure

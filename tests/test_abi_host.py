@@ -1,0 +1,134 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, and
+its planner (planning-only contexts, no GPU) agrees with the oracle's
+independent reading of Algorithm 1 (first mutated layer, boundary K,
+clusters) and with the Lemma 4 ledger; invalid calls are rejected."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from paper_2607_18582_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    with open(os.path.join(ROOT, "include", "mure.h")) as f:
+        src = f.read()
+    return sorted(set(re.findall(r"\b(mure_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.load_library()
+    declared = _declared_functions()
+    assert set(declared) == set(B.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert lib.mure_version() == 1
+
+
+def _plan_ctx(model):
+    m = B.Mure(device=-1)
+    m.load_model(model.nodes, model.in_hwc, model.dtype, model.weights, model.biases)
+    return m
+
+
+@pytest.mark.parametrize("cfg", ["cfg1", "cfg2", "cfg3", "cfg4", "cfg5"])
+def test_planner_matches_oracle_boundaries_and_ledger(cfg):
+    wl = W.make_workload(cfg, n_inputs=1, n_mutants=60)
+    m = _plan_ctx(wl.model)
+    m.apply(wl.mutants)
+    om = O.OracleModel(wl.model)
+    dg = O.get_dep_graph(om)
+    groups = {}
+    for mid in range(wl.mutants.n_mutants):
+        mmi, grp, K = m.mutant_plan(mid)
+        mu = sorted(set(wl.mutants.layer[wl.mutants.records_of(mid)].tolist()))
+        assert mmi == mu[0]
+        assert K == sorted(O.boundary(dg, mmi, len(om.nodes)))
+        groups.setdefault(grp, set()).add(mmi)
+    assert all(len(v) == 1 for v in groups.values())           # one mmi per cluster
+    st = m.stats()
+    assert st["n_groups"] == len(groups)
+    cc = O.cluster_costs(om, wl.mutants)
+    assert st["macs_vanilla"] == sum(c["vanilla"] for c in cc)
+    assert st["macs_memoized"] == sum(c["memoized"] for c in cc)
+    assert st["macs_vanilla"] - st["macs_memoized"] == sum((c["size"] - 1) * c["cost_prefix"] for c in cc)
+    assert st["macs_executed"] <= st["macs_memoized"]
+    m.close()
+
+
+def test_identity_mutants_have_no_plan():
+    wl = W.make_workload("cfg1", n_inputs=1, n_mutants=3)
+    m = _plan_ctx(wl.model)
+    mu = wl.mutants
+    m.apply_mutants(5, mu.mutant_id, mu.op, mu.layer, mu.neuron, mu.partner, mu.noise)
+    assert m.mutant_plan(4)[0] == -1 and m.mutant_plan(3)[0] == -1
+    assert m.stats()["n_identity_mutants"] == 2
+
+
+def test_invalid_calls_are_rejected_atomically():
+    wl = W.make_workload("cfg2", n_inputs=1, n_mutants=4)
+    m = B.Mure(device=-1)
+    mu = wl.mutants
+    with pytest.raises(B.MureError) as e:                       # before load_model
+        m.apply(mu)
+    assert e.value.status == B.MURE_E_STATE
+    model = wl.model
+    m.load_model(model.nodes, model.in_hwc, model.dtype, model.weights, model.biases)
+    m.apply(mu)
+    before = [m.mutant_plan(i) for i in range(4)]
+    bad_cases = [
+        dict(layer=[0]),                     # the input has no neurons
+        dict(neuron=[99]),                   # neuron out of range
+        dict(op=[7]),                        # unknown operator
+        dict(mutant_id=[9]),                 # mutant out of range
+    ]
+    for case in bad_cases:
+        args = dict(mutant_id=[0], op=[1], layer=[1], neuron=[0], partner=[-1], noise=[None])
+        args.update(case)
+        with pytest.raises(B.MureError) as e:
+            m.apply_mutants(4, **args)
+        assert e.value.status == B.MURE_E_INVALID
+    with pytest.raises(B.MureError):         # switch partner equal to the neuron
+        m.apply_mutants(4, [0], [3], [1], [2], [2], [None])
+    with pytest.raises(B.MureError):         # fuzz noise of the wrong length
+        m.apply_mutants(4, [0], [0], [1], [2], [-1], [np.zeros(3, np.float32)])
+    assert [m.mutant_plan(i) for i in range(4)] == before     # nothing applied
+    with pytest.raises(B.MureError) as e:
+        m.set_option("chunk_inputs", 100)
+    assert e.value.status == B.MURE_E_INVALID
+
+
+def test_planning_context_refuses_device_work():
+    import ctypes as C
+    wl = W.make_workload("cfg1", n_inputs=1, n_mutants=2)
+    m = _plan_ctx(wl.model)
+    m.apply(wl.mutants)
+    st = m.lib.mure_run_original(m.ctx, C.c_void_p(1), 1, None)
+    assert st == B.MURE_E_UNSUPPORTED
+    st = m.lib.mure_run_mutants(m.ctx, None, None, None)
+    assert st == B.MURE_E_UNSUPPORTED
+
+
+def test_model_validation():
+    model = W.tiny_resnet()
+    m = B.Mure(device=-1)
+    nodes = [n for n in model.nodes]
+    import copy
+    bad = copy.deepcopy(nodes)
+    bad[2].inputs = (5,)                     # reads a later node
+    with pytest.raises(B.MureError):
+        m.load_model(bad, model.in_hwc, "f32", model.weights, model.biases)
+    bad = copy.deepcopy(nodes)
+    bad[1].c_in = 3                          # wrong channel count
+    with pytest.raises(B.MureError):
+        m.load_model(bad, model.in_hwc, "f32", model.weights, model.biases)
+    w = list(model.weights)
+    w[1] = None                              # missing weights
+    with pytest.raises(B.MureError):
+        m.load_model(nodes, model.in_hwc, "f32", w, model.biases)
+    m.load_model(nodes, model.in_hwc, "f32", model.weights, model.biases)

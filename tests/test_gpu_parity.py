@@ -1,0 +1,130 @@
+"""GPU parity: the library's kill bits, score and logits against the CPU oracle
+(vanilla mutation testing) on the same seeded inputs.
+
+Bar: kill bits identical outside the ambiguous pairs (oracle margin of the
+original or the mutant below 1e-3), mutation score identical whenever no
+ambiguous pair disagrees, logits within 1e-4*S (fp32) / 2e-2*S (bf16) where
+S is the largest |logit| of the original."""
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from harness import (log, run_gpu, oracle_run, compare, compare_logits, sample_mutants,
+                     gpu_context, device_inputs, unpack_words)
+
+pytestmark = pytest.mark.gpu
+
+
+def _parity(wl, n_sample_logits=8, tau=1e-3, labels=None, **opts):
+    log(f"[parity] {wl.name} N={wl.n_inputs} M={wl.mutants.n_mutants}")
+    m, words, kills, score = run_gpu(wl, labels=labels, **opts)
+    ids = sample_mutants(m, wl)[:max(n_sample_logits, 1) * 4]
+    res = oracle_run(wl, labels=labels, keep_logits=ids)
+    out = compare(res, words, kills, score, wl, tau, m=m)
+    worst = compare_logits(m, res, ids, wl.model.dtype)
+    log(f"  {out} logit err/S {worst:.2e} MS {score['ms_num']}/{score['ms_den']}")
+    return m, res, words
+
+
+def test_cfg1_full():
+    _parity(W.make_workload("cfg1"))
+
+
+def test_cfg2_ragged_inputs():
+    _parity(W.make_workload("cfg2", n_inputs=1000, n_mutants=60))
+
+
+def test_cfg3_small_each_ratio():
+    for ri in range(3):
+        _parity(W.make_workload("cfg3", n_inputs=70, n_mutants=10, ratio_index=ri))
+
+
+def test_cfg4_small():
+    _parity(W.make_workload("cfg4", n_inputs=66, n_mutants=24))
+
+
+def test_cfg5_small():
+    _parity(W.make_workload("cfg5", n_inputs=12, n_mutants=4))
+
+
+def test_ground_truth_labels_path():
+    wl = W.make_workload("cfg2", n_inputs=300, n_mutants=30)
+    labels = np.random.default_rng(9).integers(0, 10, wl.n_inputs).astype(np.int32)
+    _parity(wl, labels=labels)
+
+
+def test_chunking_does_not_change_results():
+    wl = W.make_workload("cfg2", n_inputs=700, n_mutants=40)
+    _, w0, k0, s0 = run_gpu(wl)
+    _, w1, k1, s1 = run_gpu(wl, chunk_inputs=128, max_workspace_mb=1)
+    assert np.array_equal(w0, w1) and np.array_equal(k0, k1) and s0 == s1
+
+
+def test_repeat_is_deterministic():
+    wl = W.make_workload("cfg4", n_inputs=64, n_mutants=12)
+    m = gpu_context(wl)
+    m.run_original(device_inputs(wl))
+    a = m.run_mutants()
+    b = m.run_mutants()
+    assert np.array_equal(a[0].cpu().numpy(), b[0].cpu().numpy()) and a[2] == b[2]
+    z1 = m.get_logits(3).cpu().numpy()
+    z2 = m.get_logits(3).cpu().numpy()
+    assert np.array_equal(z1, z2)
+
+
+@pytest.mark.parametrize("cfg", ["cfg2", "cfg4"])
+def test_identity_mutants_bit_exact(cfg):
+    """Zero-noise fuzz at every layer and a mutant without records reproduce
+    the original's logits bit for bit and are never killed."""
+    base = W.make_workload(cfg, n_inputs=130, n_mutants=1)
+    md = base.model
+    layers = md.weighted_nodes()
+    recs = [(i, W.GF, l, i % md.nodes[l].c_out, -1, np.zeros(md.nodes[l].fan_in, np.float32))
+            for i, l in enumerate(layers)]
+    n = len(recs)
+    a = lambda k: np.array([r[k] for r in recs], np.int32)
+    muts = W.Mutants(n + 1, a(0), a(1), a(2), a(3), a(4), [r[5] for r in recs])
+    wl = W.Workload(cfg + "_identity", md, base.inputs, muts)
+    m, words, kills, score = run_gpu(wl)
+    assert not words.any() and score["ms_num"] == 0
+    z = m.get_logits(-1).cpu().numpy()
+    for mid in range(n + 1):
+        assert np.array_equal(m.get_logits(mid).cpu().numpy(), z), mid
+
+
+def test_output_layer_closed_forms_on_gpu():
+    """On the output layer a switch swaps two logits, an inverse negates one
+    and a block zeroes one -- exactly, relative to the GPU's own original."""
+    base = W.make_workload("cfg3", n_inputs=64, n_mutants=1, ratio_index=0)
+    md = base.model
+    out = len(md.nodes) - 1
+    muts = W.Mutants(3, np.array([0, 1, 2], np.int32), np.array([W.NS, W.NAI, W.NEB], np.int32),
+                     np.array([out] * 3, np.int32), np.array([0, 1, 2], np.int32),
+                     np.array([3, -1, -1], np.int32), [None, None, None])
+    m, words, kills, score = run_gpu(W.Workload("closed", md, base.inputs, muts))
+    z = m.get_logits(-1).cpu().numpy()
+    sw = z.copy(); sw[:, [0, 3]] = z[:, [3, 0]]
+    assert np.array_equal(m.get_logits(0).cpu().numpy(), sw)
+    ng = z.copy(); ng[:, 1] = -z[:, 1]
+    assert np.array_equal(m.get_logits(1).cpu().numpy(), ng)
+    zr = z.copy(); zr[:, 2] = 0
+    assert np.array_equal(m.get_logits(2).cpu().numpy(), zr)
+    pred = z.argmax(1)
+    for k, zz in enumerate((sw, ng, zr)):
+        assert np.array_equal(unpack_words(words, 64)[k], zz.argmax(1) != pred)
+
+
+def test_state_machine_errors():
+    from paper_2607_18582_amd import MureError, MURE_E_STATE
+    wl = W.make_workload("cfg1", n_inputs=64, n_mutants=4)
+    m = gpu_context(wl)
+    with pytest.raises(MureError) as e:
+        m.run_mutants()
+    assert e.value.status == MURE_E_STATE
+    m.run_original(device_inputs(wl))
+    m.run_mutants()
+    m.apply(wl.mutants)                      # invalidates the cache
+    with pytest.raises(MureError) as e:
+        m.run_mutants()
+    assert e.value.status == MURE_E_STATE
