@@ -1,0 +1,154 @@
+"""Throughput of memoized mutation testing on one MI355X.
+
+One step = the whole hot path over one batch: load the model (a1), apply the
+mutants (a2: clusters, copy-on-write layers), run the original once and fill
+the prefix cache (a3), run every mutant's suffix (a4 delta at the first
+mutated layer, a5 layers after it) and reduce to kill bits and the mutation
+score (a6).  Inputs are resident in device memory before the timed region.
+
+value = (mutants x inputs) / step time: (mutant, input) evaluations per
+second of the whole job.  The line also carries the suffix-only rate
+(run_mutants alone), the implicit-GEMM kernel's achieved rate against the
+MFMA peak of its dtype (per-launch HIP events on the library's stream), and
+the CPU oracle timed on a bounded sample.
+
+    python bench.py [--steps K] [--warmup W] [--config cfg2] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workloads as W  # noqa: E402
+
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}    # MI355X dense MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def cpu_baseline(wl, n_mut: int, n_in: int):
+    """The oracle (vanilla: every mutant from the raw input), as it stands,
+    on a bounded sample of the workload, timed on this host's cores."""
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max(int(p.get("num_threads", 1)) for p in threadpool_info()) if threadpool_info() else 1
+    except Exception:
+        threads = os.cpu_count() or 1
+    sub = W.Workload(wl.name, wl.model, wl.inputs[:n_in], wl.mutants.subset(n_mut))
+    om = O.OracleModel(wl.model)
+    t = time.perf_counter()
+    O.run_vanilla(om, sub.inputs, sub.mutants, chunk=256)
+    dt = time.perf_counter() - t
+    return {"value": n_mut * n_in / dt, "unit": "evals/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {n_mut} mutants x first {n_in} inputs of {wl.name} "
+                      f"(vanilla, float64 accumulation), {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="cfg2")
+    ap.add_argument("--ratio-index", type=int, default=1)
+    ap.add_argument("--inputs", type=int, default=None)
+    ap.add_argument("--mutants", type=int, default=None)
+    ap.add_argument("--oracle-mutants", type=int, default=24)
+    ap.add_argument("--oracle-inputs", type=int, default=6000)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--fused", type=int, default=1)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(the inputs would shard across GPUs with one small all-gather of the "
+              "per-mutant label masks at the end)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_18582_amd import Mure
+
+    wl = W.make_workload(args.config, n_inputs=args.inputs, n_mutants=args.mutants,
+                         ratio_index=args.ratio_index)
+    md = wl.model
+    M, N = wl.mutants.n_mutants, wl.n_inputs
+    dev = torch.device("cuda:0")
+    x = wl.inputs
+    xt = torch.from_numpy(x.view(np.int16).copy() if x.dtype == np.uint16 else x).to(dev)
+    kill = torch.empty((M, (N + 63) // 64), dtype=torch.int64, device=dev)
+    m = Mure(device=0)
+    m.set_option("kernel_timing", 1)
+    m.set_option("fused_paths", args.fused)
+
+    def step():
+        m.load_model(md.nodes, md.in_hwc, md.dtype, md.weights, md.biases)
+        m.apply(wl.mutants)
+        m.run_original(xt)
+        return m.run_mutants(kill)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    stats = []
+    for _ in range(args.steps):
+        _, kills, score = step()
+        stats.append(m.stats())
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / args.steps
+
+    ms_mut = float(np.median([s["ms_run_mutants"] for s in stats]))
+    ms_gemm = float(np.mean([s["ms_gemm"] for s in stats]))
+    launches = stats[-1]["gemm_launches"]
+    alg_flops = 2.0 * stats[-1]["gemm_macs_algorithmic"]
+    exe_flops = 2.0 * stats[-1]["gemm_macs_executed"]
+    achieved = alg_flops / (ms_gemm * 1e-3) / 1e12 if ms_gemm > 0 else 0.0
+    peak = PEAK_TFLOPS[md.dtype]
+    st = stats[-1]
+    line = {
+        "metric": "mutant-input suffix evals/sec + MFMA/HBM roofline fraction, 1 MI355X",
+        "value": M * N / dt,
+        "unit": "evals/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": dt * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": md.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {wl.description}", "n_inputs": N, "n_mutants": M,
+                   "parallelism": "single GPU"},
+        "suffix_evals_per_s": M * N / (ms_mut * 1e-3),
+        "ms_run_mutants": ms_mut,
+        "ms_run_original": float(np.median([s["ms_run_original"] for s in stats])),
+        "ms_apply": float(np.median([s["ms_apply"] for s in stats])),
+        "mutation_score": [score["ms_num"], score["ms_den"]],
+        "roofline": {"bound": "mfma", "kernel": "conv_mfma_kernel (CONV2D/DENSE implicit GEMM)",
+                     "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None,
+                     "launches": launches, "avg_launch_ms": ms_gemm / max(launches, 1),
+                     "alg_flops_per_launch": alg_flops / max(launches, 1),
+                     "executed_flops_per_launch": exe_flops / max(launches, 1),
+                     "share_of_run_mutants": ms_gemm / ms_mut if ms_mut else None},
+        "work": {"macs_algorithmic": st["macs_algorithmic"], "macs_executed": st["macs_executed"],
+                 "macs_vanilla": st["macs_vanilla"], "macs_memoized": st["macs_memoized"],
+                 "groups": st["n_groups"], "cache_bytes": st["cache_bytes"],
+                 "launches_run_mutants": st["launches"]},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl, args.oracle_mutants, min(args.oracle_inputs, N))
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -138,6 +138,12 @@ typedef struct {
   int64_t workspace_bytes;       /* per-chunk activation buffers */
   int64_t launches;              /* kernel launches in the last run_mutants */
   double ms_apply, ms_run_original, ms_run_mutants;   /* device time, milliseconds */
+  /* With option "kernel_timing" = 1: the CONV2D/DENSE (implicit-GEMM)
+   * launches of the last run_mutants, timed one by one with HIP events on the
+   * context's stream; MACs are algorithmic (as macs_algorithmic) and executed. */
+  int64_t gemm_launches;
+  double ms_gemm;
+  int64_t gemm_macs_algorithmic, gemm_macs_executed;
 } mure_stats;
 
 /* Version of this interface (MURE_VERSION). */
@@ -223,6 +229,8 @@ mure_status mure_get_stats(const mure_ctx* ctx, mure_stats* out);
  *   "chunk_inputs"      inputs per chunk, multiple of 64 (0 = automatic)
  *   "fused_paths"       1 (default) use fused kernels where a graph allows, 0
  *                       force the layer-by-layer engine
+ *   "kernel_timing"     1: time each implicit-GEMM launch of run_mutants (see
+ *                       mure_stats); 0 (default) off
  * Errors: MURE_E_INVALID for an unknown name or value. */
 mure_status mure_set_option(mure_ctx* ctx, const char* name, int64_t value);
 

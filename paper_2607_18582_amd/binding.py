@@ -55,7 +55,9 @@ class mure_stats(C.Structure):
                 ("macs_executed", C.c_int64), ("cache_bytes", C.c_int64),
                 ("workspace_bytes", C.c_int64), ("launches", C.c_int64),
                 ("ms_apply", C.c_double), ("ms_run_original", C.c_double),
-                ("ms_run_mutants", C.c_double)]
+                ("ms_run_mutants", C.c_double), ("gemm_launches", C.c_int64),
+                ("ms_gemm", C.c_double), ("gemm_macs_algorithmic", C.c_int64),
+                ("gemm_macs_executed", C.c_int64)]
 
 
 class MureError(RuntimeError):

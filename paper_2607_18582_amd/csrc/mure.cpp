@@ -124,6 +124,9 @@ struct mure_ctx {
   int64_t max_ws_mb = 16384;
   int64_t chunk_inputs = 0;
   int64_t fused = 1;
+  int64_t kernel_timing = 0;
+  std::vector<hipEvent_t> tevents;                    // pairs around timed launches
+  size_t tevents_used = 0;
   mure_stats stats{};
 
   mure_status fail(mure_status s, const std::string& m) {
@@ -156,7 +159,7 @@ struct Where {
 // nx inputs starting at x0.
 mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void* out, int out_mode,
                       const void* const* wtab, const float* const* btab, int slot0, int nslots,
-                      int nx, int x0, int64_t chunk_rows) {
+                      int nx, int x0, int64_t chunk_rows, int64_t alg_macs = 0, bool timed = false) {
   const Graph& g = ctx->g;
   const Node& n = g.nodes[v];
   const int out_f32 = v == g.out() ? 1 : 0;
@@ -188,7 +191,26 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
     a.relu = n.relu;
     a.K = a.kh * a.kw * a.C;
     a.P = a.pool ? 4 * a.Hp * a.Wp : a.Hc * a.Wc;
+    timed = timed && ctx->kernel_timing;
+    if (timed) {
+      while (ctx->tevents.size() < ctx->tevents_used + 2) {
+        hipEvent_t ev;
+        hipError_t ee = hipEventCreate(&ev);
+        if (ee != hipSuccess) return ctx->dev_fail(ee, "hipEventCreate");
+        ctx->tevents.push_back(ev);
+      }
+      hipError_t ee = hipEventRecord(ctx->tevents[ctx->tevents_used], ctx->stream);
+      if (ee != hipSuccess) return ctx->dev_fail(ee, "hipEventRecord");
+    }
     e = launch_conv(a, nslots, g.dtype, ctx->stream);
+    if (timed && e == hipSuccess) {
+      hipError_t ee = hipEventRecord(ctx->tevents[ctx->tevents_used + 1], ctx->stream);
+      if (ee != hipSuccess) return ctx->dev_fail(ee, "hipEventRecord");
+      ctx->tevents_used += 2;
+      ctx->stats.gemm_launches++;
+      ctx->stats.gemm_macs_algorithmic += alg_macs;
+      ctx->stats.gemm_macs_executed += (int64_t)nslots * nx * n.macs;
+    }
   } else if (n.kind == K_ADD) {
     const Node& s = g.nodes[n.in[1]];
     AddArgs a;
@@ -268,6 +290,7 @@ void mure_destroy(mure_ctx* ctx) {
     (void)hipStreamSynchronize(ctx->stream);
     if (ctx->ev0) (void)hipEventDestroy(ctx->ev0);
     if (ctx->ev1) (void)hipEventDestroy(ctx->ev1);
+    for (hipEvent_t e : ctx->tevents) (void)hipEventDestroy(e);
   }
   delete ctx;
 }
@@ -289,6 +312,9 @@ mure_status mure_set_option(mure_ctx* ctx, const char* name, int64_t value) {
   } else if (n == "fused_paths") {
     if (value != 0 && value != 1) return ctx->fail(MURE_E_INVALID, "fused_paths must be 0 or 1");
     ctx->fused = value;
+  } else if (n == "kernel_timing") {
+    if (value != 0 && value != 1) return ctx->fail(MURE_E_INVALID, "kernel_timing must be 0 or 1");
+    ctx->kernel_timing = value;
   } else {
     return ctx->fail(MURE_E_INVALID, "unknown option " + n);
   }
@@ -650,9 +676,12 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
         void* out = const_cast<void*>(where(mmi).p);
         const int rec_end = std::min(cs1, gr.n_recompute);
         if (cs0 < rec_end) {
+          int64_t touched = 0;
+          for (int sl = cs0; sl < rec_end; ++sl) touched += ctx->plan.mutants[gr.mutants[sl]].touched;
+          const int64_t alg = touched * (nm.macs / nm.c_out) * cnt;
           mure_status st = exec_node(ctx, mmi, ins, out, MODE_BUF, tabs + gt.w.at(mmi) + cs0,
                                      reinterpret_cast<const float* const*>(tabs + gt.b.at(mmi) + cs0),
-                                     0, rec_end - cs0, cnt, (int)x0, rows);
+                                     0, rec_end - cs0, cnt, (int)x0, rows, alg, true);
           if (st != MURE_OK) return st;
         }
         const int pa = std::max(cs0, gr.n_recompute);
@@ -675,7 +704,8 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
         for (int k = 0; k < nd.n_in; ++k) ins.push_back(where(nd.in[k]));
         const void* const* wt = nd.weighted() ? tabs + gt.w.at(v) + cs0 : nullptr;
         const float* const* bt = nd.weighted() ? reinterpret_cast<const float* const*>(tabs + gt.b.at(v) + cs0) : nullptr;
-        mure_status st = exec_node(ctx, v, ins, const_cast<void*>(where(v).p), MODE_BUF, wt, bt, 0, ns, cnt, (int)x0, rows);
+        mure_status st = exec_node(ctx, v, ins, const_cast<void*>(where(v).p), MODE_BUF, wt, bt, 0, ns, cnt,
+                                   (int)x0, rows, rows * nd.macs, true);
         if (st != MURE_OK) return st;
       }
       KillArgs ka;
@@ -712,6 +742,11 @@ mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* ki
   if ((size_t)(M * 8) > ctx->d_kills.bytes) HIPTRY(ctx->d_kills.alloc((size_t)std::max<int64_t>(M * 8, 8)));
   if ((size_t)(M * mw * 8) > ctx->d_masks.bytes) HIPTRY(ctx->d_masks.alloc((size_t)std::max<int64_t>(M * mw * 8, 8)));
   ctx->stats.launches = 0;
+  ctx->stats.gemm_launches = 0;
+  ctx->stats.ms_gemm = 0;
+  ctx->stats.gemm_macs_algorithmic = 0;
+  ctx->stats.gemm_macs_executed = 0;
+  ctx->tevents_used = 0;
   HIPTRY(hipEventRecord(ctx->ev0, ctx->stream));
   HIPTRY(hipMemsetAsync(ctx->d_nonfinite.p, 0, 8, ctx->stream));
   if (M > 0) HIPTRY(hipMemsetAsync(kw, 0, (size_t)(M * nwords * 8), ctx->stream));
@@ -732,6 +767,12 @@ mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* ki
   HIPTRY(hipEventSynchronize(ctx->ev1));
   float ms = 0.f;
   HIPTRY(hipEventElapsedTime(&ms, ctx->ev0, ctx->ev1));
+  for (size_t i = 0; i + 1 < ctx->tevents_used; i += 2) {
+    float t = 0.f;
+    HIPTRY(hipEventElapsedTime(&t, ctx->tevents[i], ctx->tevents[i + 1]));
+    ctx->stats.ms_gemm += t;
+  }
+  ctx->tevents_used = 0;
   std::vector<int64_t> kills(M);
   std::vector<unsigned long long> masks(M * mw);
   unsigned long long nonfinite = 0;
