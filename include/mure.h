@@ -144,6 +144,12 @@ typedef struct {
   int64_t gemm_launches;
   double ms_gemm;
   int64_t gemm_macs_algorithmic, gemm_macs_executed;
+  /* The same, split by kernel: [0] dense GEMM, [1] vector-ALU convolution
+   * (few output channels), [2] LDS-resident convolution, [3] im2col implicit
+   * GEMM. */
+  int64_t kernel_launches[4];
+  double kernel_ms[4];
+  int64_t kernel_macs_algorithmic[4];
 } mure_stats;
 
 /* Version of this interface (MURE_VERSION). */

@@ -57,7 +57,8 @@ class mure_stats(C.Structure):
                 ("ms_apply", C.c_double), ("ms_run_original", C.c_double),
                 ("ms_run_mutants", C.c_double), ("gemm_launches", C.c_int64),
                 ("ms_gemm", C.c_double), ("gemm_macs_algorithmic", C.c_int64),
-                ("gemm_macs_executed", C.c_int64)]
+                ("gemm_macs_executed", C.c_int64), ("kernel_launches", C.c_int64 * 4),
+                ("kernel_ms", C.c_double * 4), ("kernel_macs_algorithmic", C.c_int64 * 4)]
 
 
 class MureError(RuntimeError):
@@ -174,20 +175,27 @@ class Mure:
         self._check(self.lib.mure_load_model(self.ctx, arr, n, hwc, dt, wp, bp))
         self.classes = int(nodes[-1].out_hwc[2]) if hasattr(nodes[-1], "out_hwc") else 0
 
+    RECORD_DTYPE = np.dtype([("mutant", "<i4"), ("op", "<i4"), ("layer", "<i4"), ("neuron", "<i4"),
+                             ("partner", "<i4"), ("reserved", "<i4"), ("noise", "<u8"),
+                             ("noise_len", "<i8")])
+
     def apply_mutants(self, n_mutants: int, mutant_id, op, layer, neuron, partner, noise):
         R = len(mutant_id)
-        recs = (mure_record * max(R, 1))()
-        keep = []
-        for r in range(R):
-            x = recs[r]
-            x.mutant, x.op, x.layer = int(mutant_id[r]), int(op[r]), int(layer[r])
-            x.neuron, x.partner, x.reserved = int(neuron[r]), int(partner[r]), 0
-            if noise[r] is not None:
-                e = np.ascontiguousarray(noise[r], dtype=np.float32)
-                keep.append(e)
-                x.noise = e.ctypes.data_as(C.POINTER(C.c_float))
-                x.noise_len = e.size
-        self._check(self.lib.mure_apply_mutants(self.ctx, int(n_mutants), recs, R))
+        recs = np.zeros(max(R, 1), dtype=self.RECORD_DTYPE)
+        recs["mutant"][:R] = mutant_id
+        recs["op"][:R] = op
+        recs["layer"][:R] = layer
+        recs["neuron"][:R] = neuron
+        recs["partner"][:R] = partner
+        lens = np.array([0 if e is None else len(e) for e in noise], np.int64)
+        pool = np.concatenate([np.asarray(e, np.float32) for e in noise if e is not None] or
+                              [np.zeros(1, np.float32)])
+        offs = np.concatenate([[0], np.cumsum(lens)[:-1]]) if R else np.zeros(0, np.int64)
+        recs["noise"][:R] = np.where(lens > 0, pool.ctypes.data + 4 * offs, 0)
+        recs["noise_len"][:R] = lens
+        assert self.RECORD_DTYPE.itemsize == C.sizeof(mure_record)
+        ptr = recs.ctypes.data_as(C.POINTER(mure_record))
+        self._check(self.lib.mure_apply_mutants(self.ctx, int(n_mutants), ptr, R))
         self.n_mutants = int(n_mutants)
 
     def apply(self, mutants):
@@ -241,7 +249,11 @@ class Mure:
     def stats(self) -> Dict[str, float]:
         s = mure_stats()
         self._check(self.lib.mure_get_stats(self.ctx, C.byref(s)))
-        return {k: getattr(s, k) for k, _ in mure_stats._fields_}
+        out = {}
+        for k, _ in mure_stats._fields_:
+            v = getattr(s, k)
+            out[k] = list(v) if isinstance(v, C.Array) else v
+        return out
 
     def set_option(self, name: str, value: int):
         self._check(self.lib.mure_set_option(self.ctx, name.encode(), int(value)))

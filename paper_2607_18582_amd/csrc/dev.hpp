@@ -42,4 +42,25 @@ __device__ __forceinline__ void store_out(void* out, int out_f32, int64_t i, flo
   else reinterpret_cast<T*>(out)[i] = from_f<T>(v);
 }
 
+// q / d and q % d for 0 <= q < 2^22 and 0 < d, through a float reciprocal
+// (inv = 1.0f / d) and one correction step -- cheaper than integer division.
+__device__ __forceinline__ void fast_divmod(int q, int d, float inv, int& quo, int& rem) {
+  int t = __float2int_rz((float)q * inv);
+  int r = q - t * d;
+  if (r < 0) { --t; r += d; } else if (r >= d) { ++t; r -= d; }
+  quo = t;
+  rem = r;
+}
+
+// element (row r = slot*nx + xi, pixel, channel c) of a virtual input
+template <typename T>
+__device__ __forceinline__ T virtual_elem(const VirtualIn& v, const int32_t* chrow, int64_t r,
+                                          int xi, int x0, int pixel, int c) {
+  const int src = chrow[c];
+  if (src >= 0)
+    return reinterpret_cast<const T*>(v.cache)[((int64_t)x0 + xi) * v.HW * v.C + (int64_t)pixel * v.C + src];
+  if (src == -1) return T(0);
+  return reinterpret_cast<const T*>(v.delta)[(r * v.HW + pixel) * v.T + (-2 - src)];
+}
+
 }  // namespace mure

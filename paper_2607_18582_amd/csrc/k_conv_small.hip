@@ -1,0 +1,390 @@
+// Convolutions with small images or few output channels.
+//
+// conv_lds_kernel (fp32): the zero-padded input images a block needs and the
+// weight matrix of its output channels live in LDS, so the k loop runs without
+// barriers; A operands are read straight from the image through a per-k
+// offset table (k = (dy, dx, c_in), c_in fastest, steps of 4 -- the same
+// reduction order as the im2col kernel).  A block keeps its weights and walks
+// several 256-row pieces of its slot.  Its input may be "virtual": the first
+// mutated node's output seen through the mutant's channel map and compact
+// delta rows, so that output is never materialised per mutant.
+//
+// conv_valu_kernel: C_out below one MFMA tile.  A block stages a few input
+// images and the weights in LDS; each thread owns one stored output position
+// and accumulates every (pool-window pixel, channel) output as a fused
+// multiply-add chain over k in increasing order.  A list of channels per slot
+// restricts the work to the channels a fuzz or inverse record changed (the
+// delta at the first mutated layer); each output's chain is the same whichever
+// channels are computed, so the delta is bit-identical to the full layer.
+#include "dev.hpp"
+#include "plan.hpp"
+
+namespace mure {
+
+template <int BN>
+__global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap, int kpad, int iters) {
+  extern __shared__ __attribute__((aligned(16))) float smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int slot = a.slot0 + (int)blockIdx.y;
+  const int n0 = (int)blockIdx.z * BN;
+  const int64_t Mslot = (int64_t)a.nx * a.P;
+  const int Hp2 = a.H + 2 * a.pad, Wp2 = a.W + 2 * a.pad;
+  const int img = Hp2 * Wp2 * a.C;
+  const bool virt = a.vin.chmap != nullptr;
+  float* imgs = smem;
+  float* Ws = imgs + (int64_t)nimg_cap * img;
+  int* koff = reinterpret_cast<int*>(Ws + BN * kpad);
+  int* chrow = koff + kpad;
+  const float* __restrict__ X = reinterpret_cast<const float*>(a.in.p);
+  const float* __restrict__ Wt = reinterpret_cast<const float*>(a.wtab[slot]);
+  const float* __restrict__ bias = a.btab[slot];
+
+  for (int e = tid; e < BN * kpad; e += 256) {
+    const int n = e / kpad, k = e % kpad;
+    Ws[e] = (n0 + n < a.Cout && k < a.K) ? Wt[(int64_t)(n0 + n) * a.K + k] : 0.f;
+  }
+  for (int k = tid; k < kpad; k += 256) {
+    int o = 0;
+    if (k < a.K) {
+      const int ci = k % a.C, t = k / a.C;
+      o = ((t / a.kw) * Wp2 + (t % a.kw)) * a.C + ci;
+    }
+    koff[k] = o;
+  }
+  __shared__ int nchg;                   // channels the mutant's map changes
+  __shared__ int chg[64];
+  if (virt) {
+    for (int c = tid; c < a.C; c += 256) chrow[c] = a.vin.chmap[(int64_t)slot * a.C + c];
+    __syncthreads();
+    if (tid == 0) {
+      int n = 0;
+      for (int c = 0; c < a.C && n < 64; ++c)
+        if (chrow[c] != c) chg[n++] = c;
+      nchg = n;
+    }
+  }
+  constexpr int TN = BN / 16;
+  float bv[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int n = n0 + j * 16 + (lane & 15);
+    bv[j] = n < a.Cout ? bias[n] : 0.f;
+  }
+
+  for (int it = 0; it < iters; ++it) {
+    const int64_t m0 = ((int64_t)blockIdx.x * iters + it) * 256;
+    if (m0 >= Mslot) break;
+    const int xi_first = (int)(m0 / a.P);
+    const int xi_last = (int)min((int64_t)a.nx - 1, (m0 + 255) / a.P);
+    const int nimg = xi_last - xi_first + 1;
+    __syncthreads();                               // previous piece done with imgs
+    if (virt && a.pad == 0 && (img & 3) == 0 && a.C <= 64) {
+      // the cached original images, then the channels the mutant changes
+      const float4* src = reinterpret_cast<const float4*>(
+          reinterpret_cast<const float*>(a.vin.cache) + ((int64_t)a.x0 + xi_first) * img);
+      float4* dst = reinterpret_cast<float4*>(imgs);
+      for (int e = tid; e < nimg * img / 4; e += 256) dst[e] = src[e];
+      const int nc = nchg;
+      if (nc > 0) {
+        __syncthreads();
+        const int HW = a.H * a.W;
+        for (int e = tid; e < nimg * HW * nc; e += 256) {
+          const int j = e % nc, t = e / nc;
+          const int pix = t % HW, ii = t / HW;
+          const int c = chg[j];
+          const int xi = xi_first + ii;
+          imgs[(ii * HW + pix) * a.C + c] =
+              virtual_elem<float>(a.vin, chrow, (int64_t)slot * a.nx + xi, xi, a.x0, pix, c);
+        }
+      }
+    } else if (!virt && a.pad == 0 && (img & 3) == 0 && a.in.row_elems == img) {
+      // contiguous rows: straight 16-byte copies
+      const int64_t ri = row_index(a.in.mode, (int64_t)slot * a.nx + xi_first, a.nx, a.x0);
+      const float4* src = reinterpret_cast<const float4*>(X + ri * a.in.row_elems);
+      float4* dst = reinterpret_cast<float4*>(imgs);
+      const int nv = nimg * img / 4;
+      if (a.in.mode == MODE_BUF || ri + nimg <= (int64_t)a.x0 + a.nx) {
+        for (int e = tid; e < nv; e += 256) dst[e] = src[e];
+      } else {
+        for (int e = tid; e < nimg * img; e += 256) {
+          const int ii = e / img;
+          imgs[e] = X[row_index(a.in.mode, (int64_t)slot * a.nx + xi_first + ii, a.nx, a.x0) * a.in.row_elems + e % img];
+        }
+      }
+    } else {
+      for (int e = tid; e < nimg * img; e += 256) {
+        const int ii = e / img, rem = e % img;
+        const int c = rem % a.C, pix = rem / a.C;
+        const int iy = pix / Wp2 - a.pad, ix = pix % Wp2 - a.pad;
+        float v = 0.f;
+        if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W) {
+          const int xi = xi_first + ii;
+          const int64_t r = (int64_t)slot * a.nx + xi;
+          if (virt) {
+            v = virtual_elem<float>(a.vin, chrow, r, xi, a.x0, iy * a.W + ix, c);
+          } else {
+            v = X[row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems + ((int64_t)iy * a.W + ix) * a.C + c];
+          }
+        }
+        imgs[e] = v;
+      }
+    }
+    __syncthreads();
+
+    const int64_t mw = m0 + wave * 64;
+    int base[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t m = mw + i * 16 + (lane & 15);
+      int b = 0;
+      if (m < Mslot) {
+        const int xi = (int)(m / a.P), p = (int)(m % a.P);
+        int oy, ox;
+        if (a.pool) {
+          const int q = p >> 2, sub = p & 3;
+          oy = 2 * (q / a.Wp) + (sub >> 1);
+          ox = 2 * (q % a.Wp) + (sub & 1);
+        } else {
+          oy = p / a.Wc;
+          ox = p % a.Wc;
+        }
+        b = (xi - xi_first) * img + (oy * a.stride * Wp2 + ox * a.stride) * a.C;
+      }
+      base[i] = b;
+    }
+    v4f acc[4][TN];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int ks = 0; ks < kpad; ks += 4) {
+      const int k = ks + (lane >> 4);
+      const int ko = koff[k];
+      float bw[TN], av[4];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bw[j] = Ws[(j * 16 + (lane & 15)) * kpad + k];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) av[i] = imgs[base[i] + ko];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bw[j], acc[i][j], 0, 0, 0);
+    }
+
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + j * 16 + (lane & 15);
+      if (n >= a.Cout) continue;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t mb = mw + i * 16 + (lane >> 4) * 4;
+        if (mb >= Mslot) continue;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[e] = acc[i][j][e] + bv[j];
+          if (a.relu) v[e] = fmaxf(v[e], 0.f);
+        }
+        if (a.pool) {
+          const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+          const int xo = (int)(mb / a.P);
+          const int q = (int)(mb % a.P) >> 2;
+          const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xo, a.nx, a.x0);
+          store_out<float>(a.out, a.out_f32, ro * a.out_row + (int64_t)q * a.Cout + n, mx);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int64_t mm = mb + e;
+            if (mm >= Mslot) break;
+            const int xo = (int)(mm / a.P);
+            const int pp = (int)(mm % a.P);
+            const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xo, a.nx, a.x0);
+            store_out<float>(a.out, a.out_f32, ro * a.out_row + (int64_t)pp * a.Cout + n, v[e]);
+          }
+        }
+      }
+    }
+  }
+}
+
+hipError_t launch_conv_lds(const ConvArgs& a, int nslots, hipStream_t s) {
+  if (nslots <= 0 || a.nx <= 0) return hipSuccess;
+  if (a.Cout > 64) return hipErrorInvalidValue;
+  const int bn = conv_lds_bn(a.Cout);
+  const int kpad = (a.K + 3) / 4 * 4;
+  const int cap = conv_lds_nimg_cap(a.P);
+  const size_t lds = (size_t)conv_lds_bytes(a.H, a.W, a.C, a.pad, a.P, a.Cout, a.K);
+  if (lds > 64 * 1024) return hipErrorInvalidValue;
+  const int64_t Mslot = (int64_t)a.nx * a.P;
+  const int64_t pieces = (Mslot + 255) / 256;
+  // about 2048 blocks in flight, at most 8 pieces per block
+  int iters = (int)std::max<int64_t>(1, std::min<int64_t>(8, pieces * nslots / 2048));
+  dim3 grid((unsigned)((pieces + iters - 1) / iters), (unsigned)nslots, (unsigned)((a.Cout + bn - 1) / bn));
+  switch (bn) {
+    case 16: hipLaunchKernelGGL((conv_lds_kernel<16>), grid, dim3(256), lds, s, a, cap, kpad, iters); break;
+    case 32: hipLaunchKernelGGL((conv_lds_kernel<32>), grid, dim3(256), lds, s, a, cap, kpad, iters); break;
+    default: hipLaunchKernelGGL((conv_lds_kernel<64>), grid, dim3(256), lds, s, a, cap, kpad, iters); break;
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- VALU conv
+// SPEC = 1: 5x5 kernel, one input channel, stride 1, 2x2 pooling (LeNet's
+// first layer): the 6x6 input patch of a pooling window sits in registers.
+template <typename T, int SPEC>
+__global__ __launch_bounds__(256) void conv_valu_kernel(ValuArgs a, int R) {
+  extern __shared__ __attribute__((aligned(16))) float vsm[];
+  const int tid = threadIdx.x;
+  const int sl = a.slot0 + (int)blockIdx.y;
+  const int xi0 = (int)blockIdx.x * R;
+  const int nr = min(R, a.nx - xi0);
+  const int Q = a.Hp * a.Wp;
+  const int Hp2 = a.H + 2 * a.pad, Wp2 = a.W + 2 * a.pad;
+  const int img = Hp2 * Wp2 * a.C;
+  int c_beg = 0, c_end = a.Cout;
+  if (a.ch_off) { c_beg = a.ch_off[sl]; c_end = a.ch_off[sl + 1]; }
+  const int nall = c_end - c_beg;
+  if (nall <= 0 || nr <= 0) return;
+  float* imgs = vsm;
+  float* Wl = imgs + (int64_t)R * img;                 // [nall][K]
+  const T* __restrict__ Wt = reinterpret_cast<const T*>(a.wtab[sl]);
+  const float* __restrict__ bias = a.btab[sl];
+  for (int e = tid; e < nall * a.K; e += 256) {
+    const int u = e / a.K, k = e - u * a.K;
+    const int c = a.ch_list ? a.ch_list[c_beg + u] : c_beg + u;
+    Wl[e] = to_f<T>(Wt[(int64_t)c * a.K + k]);
+  }
+  const T* __restrict__ X = reinterpret_cast<const T*>(a.in.p);
+  if (a.pad == 0 && a.in.row_elems == img) {
+    // rows of one launch are consecutive in both tensor modes
+    const T* src = X + row_index(a.in.mode, (int64_t)sl * a.nx + xi0, a.nx, a.x0) * a.in.row_elems;
+    for (int e = tid; e < nr * img; e += 256) imgs[e] = to_f<T>(src[e]);
+  } else {
+    for (int e = tid; e < nr * img; e += 256) {
+      const int ii = e / img, rem = e - ii * img;
+      const int c = rem % a.C, pix = rem / a.C;
+      const int iy = pix / Wp2 - a.pad, ix = pix % Wp2 - a.pad;
+      float v = 0.f;
+      if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W) {
+        const int64_t ri = row_index(a.in.mode, (int64_t)sl * a.nx + xi0 + ii, a.nx, a.x0);
+        v = to_f<T>(X[ri * a.in.row_elems + ((int64_t)iy * a.W + ix) * a.C + c]);
+      }
+      imgs[e] = v;
+    }
+  }
+  __syncthreads();
+  const int npix = a.pool ? 4 : 1;
+  const float invWp = 1.0f / (float)a.Wp;
+  int rr = tid / Q, q = tid - (tid / Q) * Q;
+  for (int p = tid; p < nr * Q; p += 256) {
+    const float* im = imgs + (int64_t)rr * img;
+    int qy, qx;
+    fast_divmod(q, a.Wp, invWp, qy, qx);
+    const int64_t r = (int64_t)sl * a.nx + xi0 + rr;
+    const int64_t ro = row_index(a.out_mode, r, a.nx, a.x0);
+    if constexpr (SPEC == 1) {
+      float pt[6][6];
+      const float* p0 = im + (2 * qy) * Wp2 + 2 * qx;
+#pragma unroll
+      for (int y = 0; y < 6; ++y)
+#pragma unroll
+        for (int x = 0; x < 6; ++x) pt[y][x] = p0[y * Wp2 + x];
+      for (int u = 0; u < nall; ++u) {
+        const float* wu = Wl + u * 25;
+        float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+        for (int dy = 0; dy < 5; ++dy)
+#pragma unroll
+          for (int dx = 0; dx < 5; ++dx) {
+            const float w = wu[dy * 5 + dx];
+            a0 = fmaf(pt[dy][dx], w, a0);
+            a1 = fmaf(pt[dy][dx + 1], w, a1);
+            a2 = fmaf(pt[dy + 1][dx], w, a2);
+            a3 = fmaf(pt[dy + 1][dx + 1], w, a3);
+          }
+        const int c = a.ch_list ? a.ch_list[c_beg + u] : c_beg + u;
+        const float bv = bias[c];
+        float v0 = a0 + bv, v1 = a1 + bv, v2 = a2 + bv, v3 = a3 + bv;
+        if (a.relu) { v0 = fmaxf(v0, 0.f); v1 = fmaxf(v1, 0.f); v2 = fmaxf(v2, 0.f); v3 = fmaxf(v3, 0.f); }
+        const float v = fmaxf(fmaxf(v0, v1), fmaxf(v2, v3));
+        if (a.delta_T > 0) store_out<T>(a.out, 0, ro * a.out_row + (int64_t)q * a.delta_T + u, v);
+        else store_out<T>(a.out, a.out_f32, ro * a.out_row + (int64_t)q * a.Cout + c, v);
+      }
+    } else {
+      int off[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        int oy, ox;
+        if (a.pool) { oy = 2 * qy + (j >> 1); ox = 2 * qx + (j & 1); }
+        else { oy = qy; ox = qx; }
+        off[j] = (oy * a.stride * Wp2 + ox * a.stride) * a.C;
+      }
+      for (int ub = 0; ub < nall; ub += 8) {
+        const int nch = min(8, nall - ub);
+        float acc[4][8];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int u = 0; u < 8; ++u) acc[j][u] = 0.f;
+        int k = 0;
+        for (int dy = 0; dy < a.kh; ++dy)
+          for (int dx = 0; dx < a.kw; ++dx) {
+            const int tap = (dy * Wp2 + dx) * a.C;
+            for (int ci = 0; ci < a.C; ++ci, ++k) {
+              float xv[4];
+#pragma unroll
+              for (int j = 0; j < 4; ++j) xv[j] = j < npix ? im[off[j] + tap + ci] : 0.f;
+#pragma unroll
+              for (int u = 0; u < 8; ++u) {
+                if (u >= nch) break;
+                const float w = Wl[(ub + u) * a.K + k];
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                  if (j < npix) acc[j][u] = fmaf(xv[j], w, acc[j][u]);
+              }
+            }
+          }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (u >= nch) break;
+          const int c = a.ch_list ? a.ch_list[c_beg + ub + u] : c_beg + ub + u;
+          const float bv = bias[c];
+          float v = acc[0][u] + bv;
+          if (a.relu) v = fmaxf(v, 0.f);
+          for (int j = 1; j < npix; ++j) {
+            float w2 = acc[j][u] + bv;
+            if (a.relu) w2 = fmaxf(w2, 0.f);
+            v = fmaxf(v, w2);
+          }
+          if (a.delta_T > 0)
+            store_out<T>(a.out, 0, ro * a.out_row + (int64_t)q * a.delta_T + ub + u, v);
+          else
+            store_out<T>(a.out, a.out_f32, ro * a.out_row + (int64_t)q * a.Cout + c, v);
+        }
+      }
+    }
+    q += 256;
+    while (q >= Q) { q -= Q; ++rr; }
+  }
+}
+
+hipError_t launch_valu(const ValuArgs& a, int dtype, hipStream_t s) {
+  if (a.nslots <= 0 || a.nx <= 0) return hipSuccess;
+  const int Q = a.Hp * a.Wp;
+  const int R = valu_rows(Q);
+  const size_t lds = (size_t)valu_lds_bytes(a.H, a.W, a.C, a.pad, Q, a.Cout, a.K);
+  if (lds > 64 * 1024) return hipErrorInvalidValue;
+  dim3 grid((unsigned)((a.nx + R - 1) / R), (unsigned)a.nslots);
+  const bool spec = a.kh == 5 && a.kw == 5 && a.C == 1 && a.stride == 1 && a.pool;
+  if (dtype == 0) {
+    if (spec) hipLaunchKernelGGL((conv_valu_kernel<float, 1>), grid, dim3(256), lds, s, a, R);
+    else hipLaunchKernelGGL((conv_valu_kernel<float, 0>), grid, dim3(256), lds, s, a, R);
+  } else {
+    if (spec) hipLaunchKernelGGL((conv_valu_kernel<bf16_t, 1>), grid, dim3(256), lds, s, a, R);
+    else hipLaunchKernelGGL((conv_valu_kernel<bf16_t, 0>), grid, dim3(256), lds, s, a, R);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mure

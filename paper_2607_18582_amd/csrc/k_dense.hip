@@ -1,0 +1,216 @@
+// DENSE layers as a GEMM on MFMA (gfx950), optionally fused with the kill
+// reduction of the network output.
+//
+// Rows are (mutant slot, input) pairs; a block owns 64 consecutive inputs of
+// one slot and BN output units, so with the kill fused one wavefront turns the
+// block's 64 rows into one 64-bit kill word.  The reduction over k runs in
+// increasing steps of the MFMA's depth (4 for fp32, 32 for bf16), the same
+// order as every other kernel computing the node.
+#include <climits>
+
+#include "dev.hpp"
+
+namespace mure {
+
+template <typename T> struct DenseCfg;
+template <> struct DenseCfg<float> { static constexpr int BK = 32, VEC = 4, PAD = 4; };
+template <> struct DenseCfg<bf16_t> { static constexpr int BK = 64, VEC = 8, PAD = 8; };
+
+template <int VEC, typename T> struct VecOf;
+template <> struct VecOf<4, float> { typedef float4 type; };
+template <> struct VecOf<8, bf16_t> { typedef uint4 type; };
+
+// VIRT: the input is the first mutated node's output seen through the
+// mutant's channel map: a per-block table maps each k of the flattened row to
+// the cached original, zero, or a compact delta entry.
+template <typename T, int BN, int WAVES_M, bool VIRT>
+__global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
+  constexpr int BM = 64;
+  constexpr int BK = DenseCfg<T>::BK, VEC = DenseCfg<T>::VEC, LD = BK + DenseCfg<T>::PAD;
+  constexpr int WAVES_N = 4 / WAVES_M;
+  constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+  constexpr int TM = WM / 16, TN = WN / 16;
+  constexpr int LSN = BN <= 64 ? BM * (BN + 1) : 1;
+  typedef typename VecOf<VEC, T>::type vec_t;
+  __shared__ __attribute__((aligned(16))) T As[BM * LD];
+  __shared__ __attribute__((aligned(16))) T Bs[BN * LD];
+  __shared__ float Ls[LSN];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+  const int slot = a.slot0 + (int)blockIdx.y;
+  const int m0 = (int)blockIdx.x * BM;
+  const int n0 = (int)blockIdx.z * BN;
+  const T* __restrict__ Wt = reinterpret_cast<const T*>(a.wtab[slot]);
+  const T* __restrict__ X = reinterpret_cast<const T*>(a.in.p);
+
+  v4f acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  constexpr int KMAP = VIRT ? 4096 : 1;
+  __shared__ int kmap[KMAP];
+  if constexpr (VIRT) {
+    const int32_t* chrow = a.vin.chmap + (int64_t)slot * a.vin.C;
+    for (int k = tid; k < a.K; k += 256) {
+      const int pix = k / a.vin.C, c = k - pix * a.vin.C;
+      const int src = chrow[c];
+      kmap[k] = src >= 0 ? pix * a.vin.C + src
+              : src == -1 ? INT_MIN : -1 - (pix * a.vin.T + (-2 - src));
+    }
+    __syncthreads();
+  }
+  for (int kc = 0; kc < a.K; kc += BK) {
+    constexpr int AV = BM * BK / VEC;
+#pragma unroll
+    for (int i = tid; i < AV; i += 256) {
+      const int row = i / (BK / VEC), kv = i % (BK / VEC);
+      const int k = kc + kv * VEC;
+      if constexpr (VIRT) {
+        const int xi = m0 + row;
+        const T* crow = reinterpret_cast<const T*>(a.vin.cache) + ((int64_t)a.x0 + xi) * a.K;
+        const T* drow = reinterpret_cast<const T*>(a.vin.delta) + ((int64_t)slot * a.nx + xi) * a.vin.T;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          T v = T(0);
+          if (xi < a.nx && k + e < a.K) {
+            const int code = kmap[k + e];
+            if (code >= 0) v = crow[code];
+            else if (code != INT_MIN) v = drow[-1 - code];
+          }
+          As[row * LD + kv * VEC + e] = v;
+        }
+        continue;
+      }
+      vec_t v{};
+      if (m0 + row < a.nx && k < a.K) {
+        const int64_t ri = row_index(a.in.mode, (int64_t)slot * a.nx + m0 + row, a.nx, a.x0);
+        v = *reinterpret_cast<const vec_t*>(X + ri * a.K + k);
+      }
+      *reinterpret_cast<vec_t*>(&As[row * LD + kv * VEC]) = v;
+    }
+    constexpr int BV = BN * BK / VEC;
+    for (int i = tid; i < BV; i += 256) {
+      const int row = i / (BK / VEC), kv = i % (BK / VEC);
+      const int k = kc + kv * VEC;
+      vec_t v{};
+      if (n0 + row < a.Cout && k < a.K) v = *reinterpret_cast<const vec_t*>(Wt + (int64_t)(n0 + row) * a.K + k);
+      *reinterpret_cast<vec_t*>(&Bs[row * LD + kv * VEC]) = v;
+    }
+    __syncthreads();
+    if constexpr (sizeof(T) == 4) {
+#pragma unroll
+      for (int ks = 0; ks < BK / 4; ++ks) {
+        float av[TM], bv[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) av[i] = As[(wm * WM + i * 16 + (lane & 15)) * LD + ks * 4 + (lane >> 4)];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) bv[j] = Bs[(wn * WN + j * 16 + (lane & 15)) * LD + ks * 4 + (lane >> 4)];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < BK / 32; ++ks) {
+        v8bf av[TM], bv[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          av[i] = *reinterpret_cast<const v8bf*>(&As[(wm * WM + i * 16 + (lane & 15)) * LD + ks * 32 + (lane >> 4) * 8]);
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          bv[j] = *reinterpret_cast<const v8bf*>(&Bs[(wn * WN + j * 16 + (lane & 15)) * LD + ks * 32 + (lane >> 4) * 8]);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+
+  const float* __restrict__ bias = a.btab[slot];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int nl = wn * WN + j * 16 + (lane & 15);
+    const int n = n0 + nl;
+    const float bv = n < a.Cout ? bias[n] : 0.f;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int rl = wm * WM + i * 16 + (lane >> 4) * 4 + e;
+        float v = acc[i][j][e] + bv;
+        if (a.relu) v = fmaxf(v, 0.f);
+        if (a.write_out && n < a.Cout && m0 + rl < a.nx) {
+          const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + m0 + rl, a.nx, a.x0);
+          store_out<T>(a.out, a.out_f32, ro * a.Cout + n, v);
+        }
+        if constexpr (LSN > 1) {
+          if (a.do_kill) Ls[rl * (BN + 1) + nl] = v;
+        }
+      }
+    }
+  }
+  if constexpr (LSN > 1) {
+    if (!a.do_kill) return;
+    __syncthreads();
+    if (wave != 0) return;
+    const int xi = m0 + lane;
+    const bool valid = xi < a.nx;
+    bool kill = false;
+    if (valid) {
+      const float* z = &Ls[lane * (BN + 1)];
+      float best = -INFINITY;
+      int arg = 0, bad = 0;
+      for (int c = 0; c < a.Cout; ++c) {
+        const float v = z[c];
+        if (!isfinite(v)) { ++bad; continue; }
+        if (v > best) { best = v; arg = c; }
+      }
+      if (bad) atomicAdd(a.nonfinite, (unsigned long long)bad);
+      const int x = a.x0 + xi;
+      kill = a.orig_ok[x] && arg != a.label[x];
+      if (a.logits_out)
+        for (int c = 0; c < a.Cout; ++c) a.logits_out[(int64_t)x * a.Cout + c] = z[c];
+    }
+    const unsigned long long word = __ballot(kill);
+    if (lane == 0 && a.kill_words && m0 < a.nx)
+      a.kill_words[(int64_t)a.slot_mutant[slot] * a.nwords + (a.x0 + m0) / 64] = word;
+  }
+}
+
+template <typename T, bool VIRT>
+static hipError_t dense_dispatch(const DenseArgs& a, dim3 grid, int bn, hipStream_t s) {
+  switch (bn) {
+    case 16: hipLaunchKernelGGL((dense_kernel<T, 16, 4, VIRT>), grid, dim3(256), 0, s, a); break;
+    case 32: hipLaunchKernelGGL((dense_kernel<T, 32, 4, VIRT>), grid, dim3(256), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((dense_kernel<T, 64, 2, VIRT>), grid, dim3(256), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((dense_kernel<T, 128, 2, VIRT>), grid, dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((dense_kernel<T, 256, 1, VIRT>), grid, dim3(256), 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+int dense_bn(int cout) {
+  return cout <= 16 ? 16 : cout <= 32 ? 32 : cout <= 64 ? 64 : cout <= 128 ? 128 : 256;
+}
+
+hipError_t launch_dense(const DenseArgs& a, int nslots, int dtype, hipStream_t s) {
+  if (nslots <= 0 || a.nx <= 0) return hipSuccess;
+  const int bn = dense_bn(a.Cout);
+  dim3 grid((unsigned)((a.nx + 63) / 64), (unsigned)nslots, (unsigned)((a.Cout + bn - 1) / bn));
+  if (a.do_kill && (grid.z != 1 || bn > 64)) return hipErrorInvalidValue;
+  if (a.vin.chmap) {
+    if (a.K > 4096) return hipErrorInvalidValue;
+    return dtype == 0 ? dense_dispatch<float, true>(a, grid, bn, s) : dense_dispatch<bf16_t, true>(a, grid, bn, s);
+  }
+  return dtype == 0 ? dense_dispatch<float, false>(a, grid, bn, s) : dense_dispatch<bf16_t, false>(a, grid, bn, s);
+}
+
+}  // namespace mure

@@ -20,9 +20,23 @@ struct TensorArg {
   int64_t row_elems = 0;   // elements per row
 };
 
+// A consumer's view of the first mutated node's output without materialising
+// it per mutant: element (slot, input x, pixel, channel c) is
+//   chmap[slot][c] >= 0   the original's channel chmap[slot][c] (prefix cache),
+//   chmap[slot][c] == -1  zero (effect block),
+//   chmap[slot][c] <= -2  recomputed channel t = -2 - chmap[slot][c], read from
+//                         the compact delta rows delta[r][pixel][t] (r = chunk row).
+struct VirtualIn {
+  const void* cache = nullptr;           // [N][H][W][C]
+  const int32_t* chmap = nullptr;        // [chunk slots][C]; nullptr: not virtual
+  const void* delta = nullptr;           // [chunk rows][H*W][T]
+  int C = 0, HW = 0, T = 0;
+};
+
 // CONV2D / DENSE (a DENSE layer is a 1x1 convolution over a 1x1xC_in input).
 struct ConvArgs {
   TensorArg in;
+  VirtualIn vin;                         // used instead of `in` when vin.chmap != nullptr
   void* out = nullptr;
   int out_mode = MODE_BUF;
   int64_t out_row = 0;
@@ -37,6 +51,47 @@ struct ConvArgs {
   int Cout = 0, kh = 1, kw = 1, stride = 1, pad = 0, relu = 0, pool = 0;
   int K = 0;                             // kh*kw*C
   int P = 0;                             // GEMM rows per input
+};
+
+// DENSE on MFMA: out[r][n] = sum_k in[r][k] * W[n][k] + b[n] (k in increasing
+// steps), optional ReLU; optionally fused with the kill reduction when one
+// block column covers every class.
+struct DenseArgs {
+  TensorArg in;                          // row_elems = K
+  VirtualIn vin;                         // used instead of `in` when vin.chmap != nullptr
+  void* out = nullptr;
+  int out_mode = MODE_BUF, out_f32 = 0, write_out = 1;
+  const void* const* wtab = nullptr;
+  const float* const* btab = nullptr;
+  int slot0 = 0, nx = 0, x0 = 0, K = 0, Cout = 0, relu = 0;
+  // fused kill
+  int do_kill = 0;
+  const int32_t* slot_mutant = nullptr;
+  const int32_t* label = nullptr;
+  const uint8_t* orig_ok = nullptr;
+  uint64_t* kill_words = nullptr;
+  int64_t nwords = 0;
+  unsigned long long* nonfinite = nullptr;
+  float* logits_out = nullptr;
+};
+
+// CONV2D with tiny C_out on the vector ALU, one output position per thread.
+// ch_off/ch_list (optional) restrict each slot to a list of output channels:
+// slot sl computes channels ch_list[ch_off[sl] .. ch_off[sl+1]).
+struct ValuArgs {
+  TensorArg in;
+  void* out = nullptr;
+  int out_mode = MODE_BUF, out_f32 = 0;
+  int64_t out_row = 0;
+  const void* const* wtab = nullptr;
+  const float* const* btab = nullptr;
+  int slot0 = 0, nslots = 0, nx = 0, x0 = 0;
+  int H = 0, W = 0, C = 0, Hp = 0, Wp = 0;
+  int Cout = 0, kh = 1, kw = 1, stride = 1, pad = 0, relu = 0, pool = 0, K = 0;
+  const int32_t* ch_off = nullptr;
+  const int32_t* ch_list = nullptr;
+  int delta_T = 0;                       // > 0: write channel t of the list to the compact
+                                         // delta row out[r][q][t] (out_row = Hp*Wp*delta_T)
 };
 
 struct AddArgs {
@@ -113,6 +168,9 @@ struct DevRecord { int op, neuron, partner, pad; int64_t noise_off; };
 
 // launchers (return the launch status)
 hipError_t launch_conv(const ConvArgs& a, int nslots, int dtype, hipStream_t s);
+hipError_t launch_conv_lds(const ConvArgs& a, int nslots, hipStream_t s);
+hipError_t launch_dense(const DenseArgs& a, int nslots, int dtype, hipStream_t s);
+hipError_t launch_valu(const ValuArgs& a, int dtype, hipStream_t s);
 hipError_t launch_add(const AddArgs& a, int dtype, hipStream_t s);
 hipError_t launch_gap(const GapArgs& a, int dtype, hipStream_t s);
 hipError_t launch_patch(const PatchArgs& a, hipStream_t s);

@@ -42,6 +42,12 @@ struct DevBuf {
     else p = nullptr;
     return e;
   }
+  // grow-only: keep the allocation when it is large enough (no free/malloc
+  // churn between calls)
+  hipError_t ensure(size_t n) {
+    if (n <= bytes && p) return hipSuccess;
+    return alloc(n < 256 ? 256 : n);
+  }
   template <typename T> T* as() const { return reinterpret_cast<T*>(p); }
 };
 
@@ -108,11 +114,15 @@ struct mure_ctx {
   struct GroupTabs {
     std::map<int, int64_t> w, b;                      // node -> offset (in pointers) into d_tables
     int64_t slot_mutant = 0;                          // offset (int32) into d_slots
-    int64_t chmap = 0;                                // offset (int32) into d_chmap
+    int64_t chmap = 0;                                // offset (int32) into d_chmap: [slots][C]
+    int64_t choff = 0;                                // offset (int32) into d_slots: touched-list
+                                                      // offsets of the recompute slots (+1)
+    int64_t vchmap = 0;                               // offset (int32) into d_chmap: virtual maps
   };
   std::vector<GroupTabs> gtabs;
   std::map<int, int64_t> orig_w, orig_b;              // node -> offset of 1-entry original tables
   DevBuf d_slots, d_chmap;
+  DevBuf d_cargs, d_drecs, d_noise, d_given;          // upload staging
   // prefix cache and original results
   int64_t N = 0;
   std::map<int, std::unique_ptr<DevBuf>> cache;
@@ -126,6 +136,7 @@ struct mure_ctx {
   int64_t fused = 1;
   int64_t kernel_timing = 0;
   std::vector<hipEvent_t> tevents;                    // pairs around timed launches
+  std::vector<int> tevent_family;                     // kernel family of each timed pair
   size_t tevents_used = 0;
   mure_stats stats{};
 
@@ -155,61 +166,120 @@ struct Where {
   int mode;
 };
 
+// Extra arguments of a weighted-node launch.
+struct Extra {
+  const int32_t* ch_off = nullptr;    // per-slot channel lists (VALU delta at mmi)
+  const int32_t* ch_list = nullptr;
+  int delta_T = 0;                    // write compact delta rows of delta_T channels
+  const VirtualIn* vin = nullptr;     // read the first mutated node's output virtually
+  const KillArgs* kill = nullptr;     // fuse the kill reduction when possible
+  bool* kill_fused = nullptr;
+};
+
+mure_status timing_begin(mure_ctx* ctx) {
+  while (ctx->tevents.size() < ctx->tevents_used + 2) {
+    hipEvent_t ev;
+    hipError_t ee = hipEventCreate(&ev);
+    if (ee != hipSuccess) return ctx->dev_fail(ee, "hipEventCreate");
+    ctx->tevents.push_back(ev);
+  }
+  hipError_t ee = hipEventRecord(ctx->tevents[ctx->tevents_used], ctx->stream);
+  if (ee != hipSuccess) return ctx->dev_fail(ee, "hipEventRecord");
+  return MURE_OK;
+}
+
 // Launch node v over rows of slots [slot0, slot0 + nslots) of a chunk with
 // nx inputs starting at x0.
 mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void* out, int out_mode,
                       const void* const* wtab, const float* const* btab, int slot0, int nslots,
-                      int nx, int x0, int64_t chunk_rows, int64_t alg_macs = 0, bool timed = false) {
+                      int nx, int x0, int64_t chunk_rows, int64_t alg_macs = 0, bool timed = false,
+                      const Extra& ex = Extra()) {
   const Graph& g = ctx->g;
   const Node& n = g.nodes[v];
   const int out_f32 = v == g.out() ? 1 : 0;
   hipError_t e = hipSuccess;
   if (n.kind == K_CONV || n.kind == K_DENSE) {
-    ConvArgs a;
-    a.in.p = ins[0].p;
-    a.in.mode = ins[0].mode;
-    a.in.row_elems = (int64_t)n.inH * n.inW * n.inC;
-    a.out = out;
-    a.out_mode = out_mode;
-    a.out_row = n.out_elems();
-    a.out_f32 = out_f32;
-    a.wtab = wtab;
-    a.btab = btab;
-    a.slot0 = slot0;
-    a.nx = nx;
-    a.x0 = x0;
-    if (n.kind == K_CONV) {
-      a.H = n.inH; a.W = n.inW; a.C = n.inC;
-      a.Hc = n.Hc; a.Wc = n.Wc; a.Hp = n.H; a.Wp = n.W;
-      a.kh = n.kh; a.kw = n.kw; a.stride = n.stride; a.pad = n.pad; a.pool = n.maxpool ? 1 : 0;
-    } else {
-      a.H = 1; a.W = 1; a.C = n.c_in;
-      a.Hc = a.Wc = a.Hp = a.Wp = 1;
-      a.kh = a.kw = a.stride = 1; a.pad = 0; a.pool = 0;
-    }
-    a.Cout = n.c_out;
-    a.relu = n.relu;
-    a.K = a.kh * a.kw * a.C;
-    a.P = a.pool ? 4 * a.Hp * a.Wp : a.Hc * a.Wc;
+    const int fam = node_family(g, v);
     timed = timed && ctx->kernel_timing;
     if (timed) {
-      while (ctx->tevents.size() < ctx->tevents_used + 2) {
-        hipEvent_t ev;
-        hipError_t ee = hipEventCreate(&ev);
-        if (ee != hipSuccess) return ctx->dev_fail(ee, "hipEventCreate");
-        ctx->tevents.push_back(ev);
-      }
-      hipError_t ee = hipEventRecord(ctx->tevents[ctx->tevents_used], ctx->stream);
-      if (ee != hipSuccess) return ctx->dev_fail(ee, "hipEventRecord");
+      mure_status st = timing_begin(ctx);
+      if (st != MURE_OK) return st;
     }
-    e = launch_conv(a, nslots, g.dtype, ctx->stream);
+    int64_t exec_macs = (int64_t)nslots * nx * n.macs;
+    if (fam == FAM_DENSE) {
+      DenseArgs a;
+      a.in.p = ins[0].p; a.in.mode = ins[0].mode; a.in.row_elems = n.c_in;
+      a.out = out; a.out_mode = out_mode; a.out_f32 = out_f32;
+      a.wtab = wtab; a.btab = btab;
+      a.slot0 = slot0; a.nx = nx; a.x0 = x0; a.K = n.c_in; a.Cout = n.c_out; a.relu = n.relu;
+      if (ex.vin) a.vin = *ex.vin;
+      if (ex.kill && n.c_out <= 64 && out_mode == MODE_BUF) {
+        const KillArgs& k = *ex.kill;
+        a.do_kill = 1;
+        a.write_out = 0;
+        a.slot_mutant = k.slot_mutant; a.label = k.label; a.orig_ok = k.orig_ok;
+        a.kill_words = k.kill_words; a.nwords = k.nwords; a.nonfinite = k.nonfinite;
+        a.logits_out = k.logits_out;
+        if (ex.kill_fused) *ex.kill_fused = true;
+      }
+      e = launch_dense(a, nslots, g.dtype, ctx->stream);
+    } else if (fam == FAM_VALU) {
+      ValuArgs a;
+      a.in.p = ins[0].p; a.in.mode = ins[0].mode; a.in.row_elems = (int64_t)n.inH * n.inW * n.inC;
+      a.out = out; a.out_mode = out_mode; a.out_f32 = out_f32; a.out_row = n.out_elems();
+      a.wtab = wtab; a.btab = btab;
+      a.slot0 = slot0; a.nslots = nslots; a.nx = nx; a.x0 = x0;
+      a.H = n.inH; a.W = n.inW; a.C = n.inC; a.Hp = n.H; a.Wp = n.W;
+      a.Cout = n.c_out; a.kh = n.kh; a.kw = n.kw; a.stride = n.stride; a.pad = n.pad;
+      a.relu = n.relu; a.pool = n.maxpool ? 1 : 0; a.K = (int)n.fan_in;
+      a.ch_off = ex.ch_off; a.ch_list = ex.ch_list;
+      if (ex.delta_T > 0) { a.delta_T = ex.delta_T; a.out_row = (int64_t)n.H * n.W * ex.delta_T; }
+      if (ex.vin) return ctx->fail(MURE_E_INVALID, "internal: virtual input to a VALU convolution");
+      if (ex.ch_off) exec_macs = alg_macs;
+      e = launch_valu(a, g.dtype, ctx->stream);
+    } else {
+      ConvArgs a;
+      a.in.p = ins[0].p;
+      a.in.mode = ins[0].mode;
+      a.in.row_elems = (int64_t)n.inH * n.inW * n.inC;
+      a.out = out;
+      a.out_mode = out_mode;
+      a.out_row = n.out_elems();
+      a.out_f32 = out_f32;
+      a.wtab = wtab;
+      a.btab = btab;
+      a.slot0 = slot0;
+      a.nx = nx;
+      a.x0 = x0;
+      if (n.kind == K_CONV) {
+        a.H = n.inH; a.W = n.inW; a.C = n.inC;
+        a.Hc = n.Hc; a.Wc = n.Wc; a.Hp = n.H; a.Wp = n.W;
+        a.kh = n.kh; a.kw = n.kw; a.stride = n.stride; a.pad = n.pad; a.pool = n.maxpool ? 1 : 0;
+      } else {
+        a.H = 1; a.W = 1; a.C = n.c_in;
+        a.Hc = a.Wc = a.Hp = a.Wp = 1;
+        a.kh = a.kw = a.stride = 1; a.pad = 0; a.pool = 0;
+      }
+      a.Cout = n.c_out;
+      a.relu = n.relu;
+      a.K = a.kh * a.kw * a.C;
+      a.P = a.pool ? 4 * a.Hp * a.Wp : a.Hc * a.Wc;
+      if (ex.vin) {
+        if (fam != FAM_LDS) return ctx->fail(MURE_E_INVALID, "internal: virtual input to an im2col convolution");
+        a.vin = *ex.vin;
+      }
+      e = fam == FAM_LDS ? launch_conv_lds(a, nslots, ctx->stream) : launch_conv(a, nslots, g.dtype, ctx->stream);
+    }
     if (timed && e == hipSuccess) {
       hipError_t ee = hipEventRecord(ctx->tevents[ctx->tevents_used + 1], ctx->stream);
       if (ee != hipSuccess) return ctx->dev_fail(ee, "hipEventRecord");
       ctx->tevents_used += 2;
+      ctx->tevent_family.push_back(fam);
       ctx->stats.gemm_launches++;
       ctx->stats.gemm_macs_algorithmic += alg_macs;
-      ctx->stats.gemm_macs_executed += (int64_t)nslots * nx * n.macs;
+      ctx->stats.gemm_macs_executed += exec_macs;
+      ctx->stats.kernel_launches[fam]++;
+      ctx->stats.kernel_macs_algorithmic[fam] += alg_macs;
     }
   } else if (n.kind == K_ADD) {
     const Node& s = g.nodes[n.in[1]];
@@ -240,13 +310,8 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
   return MURE_OK;
 }
 
-void reset_cache(mure_ctx* ctx) {
-  ctx->cache.clear();
-  ctx->d_logits.release();
-  ctx->d_label.release();
-  ctx->d_ok.release();
-  ctx->N = 0;
-}
+// Invalidate the prefix cache; its device buffers stay allocated for reuse.
+void reset_cache(mure_ctx* ctx) { ctx->N = 0; }
 
 }  // namespace
 
@@ -346,29 +411,30 @@ mure_status mure_load_model(mure_ctx* ctx, const mure_layer* layers, int32_t n_l
     if (need && (!hw || !hb)) return ctx->fail(MURE_E_INVALID, "node " + std::to_string(i) + ": weights and bias required");
     if (!need && (hw || hb)) return ctx->fail(MURE_E_INVALID, "node " + std::to_string(i) + ": has no parameters");
   }
-  std::vector<std::unique_ptr<DevBuf>> dw(n_layers), db(n_layers);
   if (!ctx->plan_only) {
     HIPTRY(hipSetDevice(ctx->device));
+    // from here on a device failure leaves the context without a model
+    ctx->state = 0;
+    ctx->have_graph = false;
     const int64_t es = dtype == DT_F32 ? 4 : 2;
+    while ((int)ctx->d_w.size() < n_layers) {
+      ctx->d_w.emplace_back(new DevBuf());
+      ctx->d_b.emplace_back(new DevBuf());
+    }
     for (int i = 0; i < n_layers; ++i) {
-      dw[i].reset(new DevBuf());
-      db[i].reset(new DevBuf());
       if (!g.nodes[i].weighted()) continue;
       const size_t wb = (size_t)g.nodes[i].n_weights() * es, bb = (size_t)g.nodes[i].c_out * 4;
-      HIPTRY(dw[i]->alloc(wb));
-      HIPTRY(db[i]->alloc(bb));
-      HIPTRY(hipMemcpy(dw[i]->p, weights[i], wb, hipMemcpyHostToDevice));
-      HIPTRY(hipMemcpy(db[i]->p, biases[i], bb, hipMemcpyHostToDevice));
+      HIPTRY(ctx->d_w[i]->ensure(wb));
+      HIPTRY(ctx->d_b[i]->ensure(bb));
+      HIPTRY(hipMemcpyAsync(ctx->d_w[i]->p, weights[i], wb, hipMemcpyHostToDevice, ctx->stream));
+      HIPTRY(hipMemcpyAsync(ctx->d_b[i]->p, biases[i], bb, hipMemcpyHostToDevice, ctx->stream));
     }
+    HIPTRY(hipStreamSynchronize(ctx->stream));
   }
   ctx->g = std::move(g);
   ctx->have_graph = true;
-  ctx->d_w = std::move(dw);
-  ctx->d_b = std::move(db);
   ctx->plan = Plan();
   ctx->recs.clear();
-  ctx->d_cow.release();
-  ctx->d_tables.release();
   reset_cache(ctx);
   ctx->stats = mure_stats{};
   ctx->state = 1;
@@ -417,9 +483,11 @@ mure_status mure_apply_mutants(mure_ctx* ctx, int32_t n_mutants, const mure_reco
       boff[c] = pos;
       pos += ((int64_t)g.nodes[plan.cows[c].layer].c_out * 4 + 255) / 256 * 256;
     }
-    auto cow = std::make_unique<DevBuf>();
-    HIPTRY(cow->alloc((size_t)std::max<int64_t>(pos, 256)));
-    char* base = cow->as<char>();
+    // from here on a device failure leaves the context without mutants
+    ctx->state = 1;
+    ctx->plan = Plan();
+    HIPTRY(ctx->d_cow.ensure((size_t)std::max<int64_t>(pos, 256)));
+    char* base = ctx->d_cow.as<char>();
     std::map<std::pair<int, int>, size_t> cow_index;
     std::vector<CowArgs> cargs(plan.cows.size());
     std::vector<DevRecord> drecs;
@@ -472,43 +540,57 @@ mure_status mure_apply_mutants(mure_ctx* ctx, int32_t n_mutants, const mure_reco
       gt.slot_mutant = (int64_t)slots.size();
       for (int mu : gr.mutants) slots.push_back(mu);
       gt.chmap = (int64_t)chmaps.size();
-      for (size_t s = gr.n_recompute; s < gr.mutants.size(); ++s) {
+      for (size_t s = 0; s < gr.mutants.size(); ++s) {
         const std::vector<int>& cm = plan.mutants[gr.mutants[s]].chmap;
         chmaps.insert(chmaps.end(), cm.begin(), cm.end());
       }
+      gt.vchmap = (int64_t)chmaps.size();
+      chmaps.insert(chmaps.end(), gr.vchmap.begin(), gr.vchmap.end());
     }
-    auto dtab = std::make_unique<DevBuf>(), dslots = std::make_unique<DevBuf>(), dch = std::make_unique<DevBuf>();
-    HIPTRY(dtab->alloc(std::max<size_t>(tabs.size() * sizeof(void*), 8)));
-    HIPTRY(dslots->alloc(std::max<size_t>(slots.size() * 4, 4)));
-    HIPTRY(dch->alloc(std::max<size_t>(chmaps.size() * 4, 4)));
-    if (!tabs.empty()) HIPTRY(hipMemcpy(dtab->p, tabs.data(), tabs.size() * sizeof(void*), hipMemcpyHostToDevice));
-    if (!slots.empty()) HIPTRY(hipMemcpy(dslots->p, slots.data(), slots.size() * 4, hipMemcpyHostToDevice));
-    if (!chmaps.empty()) HIPTRY(hipMemcpy(dch->p, chmaps.data(), chmaps.size() * 4, hipMemcpyHostToDevice));
+    // touched-channel lists of the recompute mutants (CSR, absolute offsets
+    // into the list stored after every group's offsets)
+    {
+      std::vector<int32_t> offs, list;
+      std::vector<int64_t> where(plan.groups.size());
+      for (size_t gi = 0; gi < plan.groups.size(); ++gi) {
+        const Group& gr = plan.groups[gi];
+        where[gi] = (int64_t)offs.size();
+        for (int s = 0; s < gr.n_recompute; ++s) {
+          offs.push_back((int32_t)list.size());
+          const std::vector<int>& tl = plan.mutants[gr.mutants[s]].touched_list;
+          list.insert(list.end(), tl.begin(), tl.end());
+        }
+        offs.push_back((int32_t)list.size());
+      }
+      const int64_t base = (int64_t)slots.size();
+      for (size_t gi = 0; gi < plan.groups.size(); ++gi) gtabs[gi].choff = base + where[gi];
+      const int64_t list_base = base + (int64_t)offs.size();
+      for (int32_t& o : offs) o += (int32_t)list_base;
+      slots.insert(slots.end(), offs.begin(), offs.end());
+      slots.insert(slots.end(), list.begin(), list.end());
+    }
+    HIPTRY(ctx->d_tables.ensure(tabs.size() * sizeof(void*)));
+    HIPTRY(ctx->d_slots.ensure(slots.size() * 4));
+    HIPTRY(ctx->d_chmap.ensure(chmaps.size() * 4));
+    hipStream_t st = ctx->stream;
+    if (!tabs.empty()) HIPTRY(hipMemcpyAsync(ctx->d_tables.p, tabs.data(), tabs.size() * sizeof(void*), hipMemcpyHostToDevice, st));
+    if (!slots.empty()) HIPTRY(hipMemcpyAsync(ctx->d_slots.p, slots.data(), slots.size() * 4, hipMemcpyHostToDevice, st));
+    if (!chmaps.empty()) HIPTRY(hipMemcpyAsync(ctx->d_chmap.p, chmaps.data(), chmaps.size() * 4, hipMemcpyHostToDevice, st));
     if (!cargs.empty()) {
-      DevBuf dargs, dr, dn;
-      HIPTRY(dargs.alloc(cargs.size() * sizeof(CowArgs)));
-      HIPTRY(dr.alloc(std::max<size_t>(drecs.size() * sizeof(DevRecord), 8)));
-      HIPTRY(dn.alloc(std::max<size_t>(noise.size() * 4, 4)));
-      HIPTRY(hipMemcpy(dargs.p, cargs.data(), cargs.size() * sizeof(CowArgs), hipMemcpyHostToDevice));
-      if (!drecs.empty()) HIPTRY(hipMemcpy(dr.p, drecs.data(), drecs.size() * sizeof(DevRecord), hipMemcpyHostToDevice));
-      if (!noise.empty()) HIPTRY(hipMemcpy(dn.p, noise.data(), noise.size() * 4, hipMemcpyHostToDevice));
-      HIPTRY(launch_cow(dargs.as<CowArgs>(), (int)cargs.size(), dr.as<DevRecord>(), dn.as<float>(), g.dtype, ctx->stream));
-      HIPTRY(hipStreamSynchronize(ctx->stream));
+      HIPTRY(ctx->d_cargs.ensure(cargs.size() * sizeof(CowArgs)));
+      HIPTRY(ctx->d_drecs.ensure(drecs.size() * sizeof(DevRecord)));
+      HIPTRY(ctx->d_noise.ensure(noise.size() * 4));
+      HIPTRY(hipMemcpyAsync(ctx->d_cargs.p, cargs.data(), cargs.size() * sizeof(CowArgs), hipMemcpyHostToDevice, st));
+      if (!drecs.empty()) HIPTRY(hipMemcpyAsync(ctx->d_drecs.p, drecs.data(), drecs.size() * sizeof(DevRecord), hipMemcpyHostToDevice, st));
+      if (!noise.empty()) HIPTRY(hipMemcpyAsync(ctx->d_noise.p, noise.data(), noise.size() * 4, hipMemcpyHostToDevice, st));
+      HIPTRY(launch_cow(ctx->d_cargs.as<CowArgs>(), (int)cargs.size(), ctx->d_drecs.as<DevRecord>(),
+                        ctx->d_noise.as<float>(), g.dtype, st));
     }
     HIPTRY(hipEventRecord(ctx->ev1, ctx->stream));
     HIPTRY(hipEventSynchronize(ctx->ev1));
     float ms = 0.f;
     (void)hipEventElapsedTime(&ms, ctx->ev0, ctx->ev1);
     ctx->stats.ms_apply = ms;
-    // commit
-    ctx->d_cow.release();
-    std::swap(ctx->d_cow.p, cow->p); std::swap(ctx->d_cow.bytes, cow->bytes);
-    ctx->d_tables.release();
-    std::swap(ctx->d_tables.p, dtab->p); std::swap(ctx->d_tables.bytes, dtab->bytes);
-    ctx->d_slots.release();
-    std::swap(ctx->d_slots.p, dslots->p); std::swap(ctx->d_slots.bytes, dslots->bytes);
-    ctx->d_chmap.release();
-    std::swap(ctx->d_chmap.p, dch->p); std::swap(ctx->d_chmap.bytes, dch->bytes);
     ctx->gtabs = std::move(gtabs);
     ctx->orig_w = std::move(ow);
     ctx->orig_b = std::move(ob);
@@ -544,23 +626,25 @@ mure_status mure_run_original(mure_ctx* ctx, const void* inputs_dev, int64_t n_i
   const int64_t n = n_inputs;
   std::set<int> cached(ctx->plan.cache_nodes.begin(), ctx->plan.cache_nodes.end());
   int64_t cache_bytes = 0;
+  for (auto it = ctx->cache.begin(); it != ctx->cache.end();)     // drop tensors no longer cached
+    it = cached.count(it->first) ? std::next(it) : ctx->cache.erase(it);
   for (int v : cached) {
     if (v == L) continue;                               // the logits buffer serves the output
-    auto b = std::make_unique<DevBuf>();
-    HIPTRY(b->alloc((size_t)(n * g.act_bytes(v))));
-    cache_bytes += (int64_t)b->bytes;
-    ctx->cache[v] = std::move(b);
+    auto& b = ctx->cache[v];
+    if (!b) b.reset(new DevBuf());
+    HIPTRY(b->ensure((size_t)(n * g.act_bytes(v))));
+    cache_bytes += n * g.act_bytes(v);
   }
-  HIPTRY(ctx->d_logits.alloc((size_t)(n * C * 4)));
-  HIPTRY(ctx->d_label.alloc((size_t)(n * 4)));
-  HIPTRY(ctx->d_ok.alloc((size_t)n));
-  HIPTRY(ctx->d_classmask.alloc(64));
-  HIPTRY(ctx->d_nonfinite.alloc(8));
+  HIPTRY(ctx->d_logits.ensure((size_t)(n * C * 4)));
+  HIPTRY(ctx->d_label.ensure((size_t)(n * 4)));
+  HIPTRY(ctx->d_ok.ensure((size_t)n));
+  HIPTRY(ctx->d_classmask.ensure(64));
+  HIPTRY(ctx->d_nonfinite.ensure(8));
   cache_bytes += n * C * 4;
-  DevBuf d_given;
+  DevBuf& d_given = ctx->d_given;
   if (labels) {
-    HIPTRY(d_given.alloc((size_t)(n * 4)));
-    HIPTRY(hipMemcpy(d_given.p, labels, (size_t)(n * 4), hipMemcpyHostToDevice));
+    HIPTRY(d_given.ensure((size_t)(n * 4)));
+    HIPTRY(hipMemcpyAsync(d_given.p, labels, (size_t)(n * 4), hipMemcpyHostToDevice, ctx->stream));
   }
   std::vector<int> nodes;
   for (int v = 1; v <= L; ++v) nodes.push_back(v);
@@ -572,7 +656,7 @@ mure_status mure_run_original(mure_ctx* ctx, const void* inputs_dev, int64_t n_i
   if (ctx->chunk_inputs) nx = std::min<int64_t>(nx, ctx->chunk_inputs);
   if (pl.peak * nx > budget) nx = std::max<int64_t>(64, budget / std::max<int64_t>(pl.peak, 1) / 64 * 64);
   if (nx > n) nx = n;
-  if (pl.peak * nx > (int64_t)ctx->d_ws.bytes) HIPTRY(ctx->d_ws.alloc((size_t)(pl.peak * nx)));
+  HIPTRY(ctx->d_ws.ensure((size_t)(pl.peak * nx)));
   char* ws = ctx->d_ws.as<char>();
 
   HIPTRY(hipEventRecord(ctx->ev0, ctx->stream));
@@ -649,7 +733,7 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
   spc = std::min<int64_t>(spc, std::min<int64_t>(65535, s_end - s_begin));
   spc = std::min<int64_t>(spc, std::max<int64_t>(1, ((int64_t)1 << 31) / nx / 64));
   const int64_t cap_rows = spc * nx;
-  if (pl.peak * cap_rows > (int64_t)ctx->d_ws.bytes) HIPTRY(ctx->d_ws.alloc((size_t)(pl.peak * cap_rows)));
+  HIPTRY(ctx->d_ws.ensure((size_t)(pl.peak * cap_rows)));
   ctx->stats.workspace_bytes = std::max<int64_t>(ctx->stats.workspace_bytes, (int64_t)ctx->d_ws.bytes);
   char* ws = ctx->d_ws.as<char>();
   const void* const* tabs = ctx->d_tables.as<const void*>();
@@ -669,47 +753,7 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
         }
         return {ws + pl.offset.at(p) * cap_rows, MODE_BUF};
       };
-      // node mmi: recompute (fuzz / inverse) slots, then channel-patch slots
-      {
-        std::vector<Where> ins;
-        for (int k = 0; k < nm.n_in; ++k) ins.push_back(where(nm.in[k]));
-        void* out = const_cast<void*>(where(mmi).p);
-        const int rec_end = std::min(cs1, gr.n_recompute);
-        if (cs0 < rec_end) {
-          int64_t touched = 0;
-          for (int sl = cs0; sl < rec_end; ++sl) touched += ctx->plan.mutants[gr.mutants[sl]].touched;
-          const int64_t alg = touched * (nm.macs / nm.c_out) * cnt;
-          mure_status st = exec_node(ctx, mmi, ins, out, MODE_BUF, tabs + gt.w.at(mmi) + cs0,
-                                     reinterpret_cast<const float* const*>(tabs + gt.b.at(mmi) + cs0),
-                                     0, rec_end - cs0, cnt, (int)x0, rows, alg, true);
-          if (st != MURE_OK) return st;
-        }
-        const int pa = std::max(cs0, gr.n_recompute);
-        if (pa < cs1) {
-          PatchArgs a;
-          a.cache = mmi_cache;
-          a.out = out;
-          a.chmap = ctx->d_chmap.as<int32_t>() + gt.chmap;
-          a.slot0 = pa - cs0;
-          a.chmap_slot0 = pa - gr.n_recompute;
-          a.nx = cnt; a.x0 = (int)x0; a.nslots = cs1 - pa;
-          a.P = nm.H * nm.W; a.C = nm.C; a.esize = (int)esize_of(g, mmi);
-          HIPTRY(launch_patch(a, ctx->stream));
-          ctx->stats.launches++;
-        }
-      }
-      for (int v = mmi + 1; v <= L; ++v) {
-        const Node& nd = g.nodes[v];
-        std::vector<Where> ins;
-        for (int k = 0; k < nd.n_in; ++k) ins.push_back(where(nd.in[k]));
-        const void* const* wt = nd.weighted() ? tabs + gt.w.at(v) + cs0 : nullptr;
-        const float* const* bt = nd.weighted() ? reinterpret_cast<const float* const*>(tabs + gt.b.at(v) + cs0) : nullptr;
-        mure_status st = exec_node(ctx, v, ins, const_cast<void*>(where(v).p), MODE_BUF, wt, bt, 0, ns, cnt,
-                                   (int)x0, rows, rows * nd.macs, true);
-        if (st != MURE_OK) return st;
-      }
       KillArgs ka;
-      ka.logits = reinterpret_cast<const float*>(where(L).p);
       ka.C = g.classes();
       ka.nx = cnt; ka.x0 = (int)x0; ka.nslots = ns; ka.slot0 = 0;
       ka.slot_mutant = slot_mut + cs0;
@@ -719,6 +763,97 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
       ka.nwords = (N + 63) / 64;
       ka.nonfinite = ctx->d_nonfinite.as<unsigned long long>();
       ka.logits_out = logits_out;
+      bool fused = false;
+      // node mmi.  Delta groups: every slot starts from the cached output
+      // (patched for effect-block / switch mutants), then the touched channels
+      // of the fuzz / inverse mutants are recomputed.  Otherwise the fuzz /
+      // inverse mutants recompute the whole node and the others are patched.
+      {
+        std::vector<Where> ins;
+        for (int k = 0; k < nm.n_in; ++k) ins.push_back(where(nm.in[k]));
+        void* out = const_cast<void*>(where(mmi).p);
+        const int rec_end = std::min(cs1, gr.n_recompute);
+        const int pa = gr.virt ? cs1 : gr.delta ? cs0 : std::max(cs0, gr.n_recompute);
+        if (pa < cs1) {
+          PatchArgs a;
+          a.cache = mmi_cache;
+          a.out = out;
+          a.chmap = ctx->d_chmap.as<int32_t>() + gt.chmap;
+          a.slot0 = pa - cs0;
+          a.chmap_slot0 = pa;
+          a.nx = cnt; a.x0 = (int)x0; a.nslots = cs1 - pa;
+          a.P = nm.H * nm.W; a.C = nm.C; a.esize = (int)esize_of(g, mmi);
+          HIPTRY(launch_patch(a, ctx->stream));
+          ctx->stats.launches++;
+        }
+        if (cs0 < rec_end) {
+          int64_t touched = 0, tl = 0;
+          for (int sl = cs0; sl < rec_end; ++sl) {
+            touched += ctx->plan.mutants[gr.mutants[sl]].touched;
+            tl += (int64_t)ctx->plan.mutants[gr.mutants[sl]].touched_list.size();
+          }
+          const int64_t per_ch = nm.macs / nm.c_out;
+          Extra ex;
+          if (gr.delta) {
+            ex.ch_off = ctx->d_slots.as<int32_t>() + gt.choff + cs0;
+            ex.ch_list = ctx->d_slots.as<int32_t>();
+            if (gr.virt) ex.delta_T = gr.T;
+          }
+          // the kill fuses into the output layer only when every slot of the
+          // chunk is recomputed here (patched slots need the kill kernel, which
+          // reads the logits buffer)
+          if (mmi == L && pa >= cs1) { ex.kill = &ka; ex.kill_fused = &fused; }
+          mure_status st = exec_node(ctx, mmi, ins, out, MODE_BUF, tabs + gt.w.at(mmi) + cs0,
+                                     reinterpret_cast<const float* const*>(tabs + gt.b.at(mmi) + cs0),
+                                     0, rec_end - cs0, cnt, (int)x0, rows, touched * per_ch * cnt, true, ex);
+          if (st != MURE_OK) return st;
+          (void)tl;
+        }
+      }
+      VirtualIn vin;
+      if (gr.virt) {
+        vin.cache = mmi_cache;
+        vin.chmap = ctx->d_chmap.as<int32_t>() + gt.vchmap + (int64_t)cs0 * nm.C;
+        vin.delta = where(mmi).p;
+        vin.C = nm.C;
+        vin.HW = nm.H * nm.W;
+        vin.T = gr.T;
+      }
+      for (int v = mmi + 1; v <= L; ++v) {
+        const Node& nd = g.nodes[v];
+        std::vector<Where> ins;
+        for (int k = 0; k < nd.n_in; ++k) ins.push_back(where(nd.in[k]));
+        const void* const* wt = nd.weighted() ? tabs + gt.w.at(v) + cs0 : nullptr;
+        const float* const* bt = nd.weighted() ? reinterpret_cast<const float* const*>(tabs + gt.b.at(v) + cs0) : nullptr;
+        Extra ex;
+        if (v == L) { ex.kill = &ka; ex.kill_fused = &fused; }
+        if (gr.virt && nd.n_in == 1 && nd.in[0] == mmi) {
+          // the consumer of mmi: delta groups read every slot virtually; in
+          // whole-node groups the recomputed slots read their own output rows
+          // and only the patched slots read the cache through their maps
+          const int rec_ns = gr.delta ? 0 : std::max(0, std::min(cs1, gr.n_recompute) - cs0);
+          if (rec_ns > 0) {
+            Extra ex1 = ex;
+            mure_status st = exec_node(ctx, v, ins, const_cast<void*>(where(v).p), MODE_BUF, wt, bt, 0, rec_ns,
+                                       cnt, (int)x0, (int64_t)rec_ns * cnt, (int64_t)rec_ns * cnt * nd.macs, true, ex1);
+            if (st != MURE_OK) return st;
+          }
+          if (rec_ns < ns) {
+            ex.vin = &vin;
+            mure_status st = exec_node(ctx, v, ins, const_cast<void*>(where(v).p), MODE_BUF, wt, bt, rec_ns,
+                                       ns - rec_ns, cnt, (int)x0, (int64_t)(ns - rec_ns) * cnt,
+                                       (int64_t)(ns - rec_ns) * cnt * nd.macs, true, ex);
+            if (st != MURE_OK) return st;
+          }
+          continue;
+        }
+        mure_status st = exec_node(ctx, v, ins, const_cast<void*>(where(v).p), MODE_BUF, wt, bt, 0, ns, cnt,
+                                   (int)x0, rows, rows * nd.macs, true, ex);
+        if (st != MURE_OK) return st;
+      }
+      if (fused) continue;
+
+      ka.logits = reinterpret_cast<const float*>(where(L).p);
       HIPTRY(launch_kill(ka, ctx->stream));
       ctx->stats.launches++;
     }
@@ -746,7 +881,13 @@ mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* ki
   ctx->stats.ms_gemm = 0;
   ctx->stats.gemm_macs_algorithmic = 0;
   ctx->stats.gemm_macs_executed = 0;
+  for (int f = 0; f < 4; ++f) {
+    ctx->stats.kernel_launches[f] = 0;
+    ctx->stats.kernel_ms[f] = 0;
+    ctx->stats.kernel_macs_algorithmic[f] = 0;
+  }
   ctx->tevents_used = 0;
+  ctx->tevent_family.clear();
   HIPTRY(hipEventRecord(ctx->ev0, ctx->stream));
   HIPTRY(hipMemsetAsync(ctx->d_nonfinite.p, 0, 8, ctx->stream));
   if (M > 0) HIPTRY(hipMemsetAsync(kw, 0, (size_t)(M * nwords * 8), ctx->stream));
@@ -771,8 +912,10 @@ mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* ki
     float t = 0.f;
     HIPTRY(hipEventElapsedTime(&t, ctx->tevents[i], ctx->tevents[i + 1]));
     ctx->stats.ms_gemm += t;
+    ctx->stats.kernel_ms[ctx->tevent_family[i / 2]] += t;
   }
   ctx->tevents_used = 0;
+  ctx->tevent_family.clear();
   std::vector<int64_t> kills(M);
   std::vector<unsigned long long> masks(M * mw);
   unsigned long long nonfinite = 0;

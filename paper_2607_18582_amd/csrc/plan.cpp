@@ -121,6 +121,22 @@ std::string build_graph(Graph& g, int in_h, int in_w, int in_c, int dtype) {
   return "";
 }
 
+int node_family(const Graph& g, int v) {
+  const Node& n = g.nodes[v];
+  if (n.kind == K_DENSE) {
+    const int vec = g.dtype == DT_F32 ? 4 : 8;       // 16-byte rows
+    return (n.c_in % vec == 0 && n.c_out <= 256) ? FAM_DENSE : FAM_GEMM;
+  }
+  if (n.kind != K_CONV) return -1;
+  const int P = n.maxpool ? 4 * n.H * n.W : n.Hc * n.Wc;
+  if (n.c_out < 16 && valu_lds_bytes(n.inH, n.inW, n.inC, n.pad, n.H * n.W, n.c_out, n.fan_in) <= 48 * 1024)
+    return FAM_VALU;
+  if (g.dtype == DT_F32 && n.c_out <= 64 &&
+      conv_lds_bytes(n.inH, n.inW, n.inC, n.pad, P, n.c_out, n.fan_in) <= 48 * 1024)
+    return FAM_LDS;
+  return FAM_GEMM;
+}
+
 std::vector<int> boundary(const Graph& g, int mmi) {
   std::set<int> K;
   for (int j = mmi; j < (int)g.nodes.size(); ++j)
@@ -172,18 +188,26 @@ std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>&
         fuzzed.insert(recs[r].neuron);
       }
     mp.touched = (int64_t)fuzzed.size();
+    const int C = g.nodes[mp.mmi].c_out;
+    mp.chmap.resize(C);
+    for (int c = 0; c < C; ++c) mp.chmap[c] = c;
     if (!mp.recompute) {
       // effect-block / switch records only: every CONV2D/DENSE epilogue here is
       // per channel (bias, ReLU, pool), so the mutated node's output is the
       // original's with channels zeroed or exchanged.
-      const int C = g.nodes[mp.mmi].c_out;
-      mp.chmap.resize(C);
-      for (int c = 0; c < C; ++c) mp.chmap[c] = c;
       for (int r : rs) {
         if (recs[r].layer != mp.mmi) continue;
         if (recs[r].op == OP_NEB) mp.chmap[recs[r].neuron] = -1;
         else std::swap(mp.chmap[recs[r].neuron], mp.chmap[recs[r].partner]);
       }
+    } else {
+      std::set<int> tl;
+      for (int r : rs) {
+        if (recs[r].layer != mp.mmi) continue;
+        tl.insert(recs[r].neuron);
+        if (recs[r].op == OP_NS) tl.insert(recs[r].partner);
+      }
+      mp.touched_list.assign(tl.begin(), tl.end());
     }
     for (int l : mp.layers) {
       CowCopy cc;
@@ -204,8 +228,41 @@ std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>&
     for (int m : kv.second) if (p.mutants[m].recompute) gr.mutants.push_back(m);
     gr.n_recompute = (int)gr.mutants.size();
     for (int m : kv.second) if (!p.mutants[m].recompute) gr.mutants.push_back(m);
+    gr.delta = gr.n_recompute > 0 && node_family(g, gr.mmi) == FAM_VALU;
+    // virtual mmi output: every consumer is an LDS convolution or a dense layer
+    gr.virt = gr.mmi != g.out();
+    for (int v = gr.mmi + 1; v < n && gr.virt; ++v)
+      for (int k = 0; k < g.nodes[v].n_in; ++k)
+        if (g.nodes[v].in[k] == gr.mmi) {
+          const int f = node_family(g, v);
+          if (!(f == FAM_LDS || (f == FAM_DENSE && g.nodes[v].c_in <= 4096))) gr.virt = false;
+        }
+    if (gr.virt) {
+      const int C = g.nodes[gr.mmi].c_out;
+      gr.T = 0;
+      if (gr.n_recompute > 0) {
+        if (gr.delta) {
+          for (int s = 0; s < gr.n_recompute; ++s)
+            gr.T = std::max(gr.T, (int)p.mutants[gr.mutants[s]].touched_list.size());
+        } else {
+          gr.T = C;
+        }
+      }
+      gr.vchmap.resize(gr.mutants.size() * C);
+      for (size_t s = 0; s < gr.mutants.size(); ++s) {
+        const MutantPlan& mp = p.mutants[gr.mutants[s]];
+        int* row = &gr.vchmap[s * C];
+        for (int c = 0; c < C; ++c) row[c] = mp.chmap[c];
+        if ((int)s < gr.n_recompute) {
+          if (gr.delta)
+            for (size_t t = 0; t < mp.touched_list.size(); ++t) row[mp.touched_list[t]] = -2 - (int)t;
+          else
+            for (int c = 0; c < C; ++c) row[c] = -2 - c;
+        }
+      }
+    }
     for (int k : gr.K) cache.insert(k);
-    if (gr.n_recompute < (int)gr.mutants.size()) cache.insert(gr.mmi);
+    if (gr.n_recompute < (int)gr.mutants.size() || gr.delta || gr.virt) cache.insert(gr.mmi);
     const int gi = (int)p.groups.size();
     for (size_t s = 0; s < gr.mutants.size(); ++s) {
       p.mutants[gr.mutants[s]].group = gi;
@@ -218,7 +275,9 @@ std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>&
       const MutantPlan& mp = p.mutants[m];
       p.macs_vanilla += full;
       p.macs_algorithmic += mp.touched * (l.macs / l.c_out) + after;
-      p.macs_executed += (mp.recompute ? l.macs : 0) + after;
+      const int64_t at_mmi = !mp.recompute ? 0
+                             : gr.delta ? (int64_t)mp.touched_list.size() * (l.macs / l.c_out) : l.macs;
+      p.macs_executed += at_mmi + after;
     }
     p.groups.push_back(std::move(gr));
   }

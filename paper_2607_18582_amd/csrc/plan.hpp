@@ -52,6 +52,33 @@ struct Record {
   int64_t noise_off, noise_len;   // into the concatenated noise array
 };
 
+// Kernel family of a CONV2D/DENSE node -- a pure function of its shape, so
+// every launch that computes a node (original forward, recompute at mmi,
+// suffix) uses the same accumulation order.
+enum Family {
+  FAM_DENSE = 0,   // dense GEMM on MFMA
+  FAM_VALU = 1,    // tiny C_out: per-output fused multiply-add chains (vector ALU)
+  FAM_LDS = 2,     // fp32 conv whose padded input image and weights fit in LDS
+  FAM_GEMM = 3     // implicit GEMM with an im2col gather
+};
+int node_family(const Graph& g, int v);
+
+// Launch geometry shared by the planner (family choice) and the kernels.
+// VALU convolution: rows per block and LDS bytes (zero-padded fp32 images of
+// those rows + the fp32 weights of every output channel).
+inline int valu_rows(int Q) { int r = (1024 + Q - 1) / Q; return r < 1 ? 1 : (r > 8 ? 8 : r); }
+inline int64_t valu_lds_bytes(int inH, int inW, int inC, int pad, int Q, int c_out, int64_t K) {
+  return (int64_t)valu_rows(Q) * (inH + 2 * pad) * (inW + 2 * pad) * inC * 4 + (int64_t)c_out * K * 4;
+}
+// LDS convolution: images a block may touch for 256 GEMM rows of P per input.
+inline int conv_lds_nimg_cap(int P) { return P >= 256 ? 2 : (256 + P - 1) / P + 1; }
+inline int conv_lds_bn(int c_out) { return c_out <= 16 ? 16 : c_out <= 32 ? 32 : 64; }
+inline int64_t conv_lds_bytes(int inH, int inW, int inC, int pad, int P, int c_out, int64_t K) {
+  const int64_t kpad = (K + 3) / 4 * 4;
+  return ((int64_t)conv_lds_nimg_cap(P) * (inH + 2 * pad) * (inW + 2 * pad) * inC +
+          (int64_t)conv_lds_bn(c_out) * kpad) * 4 + kpad * 4 + (int64_t)inC * 4;
+}
+
 struct MutantPlan {
   int mmi = -1;                 // -1: identity mutant (no records)
   int group = -1;
@@ -59,9 +86,11 @@ struct MutantPlan {
   std::vector<int> layers;      // mu(M'), ascending
   std::vector<int> K;           // memoization boundary, ascending
   bool recompute = false;       // a fuzz/inverse record at mmi: recompute node mmi
-  std::vector<int> chmap;       // !recompute: output channel c of mmi <- original channel
-                                // chmap[c] (-1 = zero); size c_out(mmi)
+  std::vector<int> chmap;       // output channel c of mmi <- original channel chmap[c]
+                                // (-1 = zero); identity for recompute mutants; size c_out(mmi)
   int64_t touched = 0;          // channels of mmi changed by fuzz/inverse records
+  std::vector<int> touched_list;  // recompute mutants: every channel of mmi any record
+                                  // changes (fuzz/inverse neurons, blocked, switched), ascending
 };
 
 // Copy-on-write parameter copy of one (mutant, layer).
@@ -75,6 +104,12 @@ struct Group {
   std::vector<int> K;
   std::vector<int> mutants;     // global ids; recompute mutants first
   int n_recompute = 0;
+  bool delta = false;           // recompute only the touched channels of mmi (VALU family)
+  bool virt = false;            // consumers read mmi's output through per-slot channel maps
+                                // (cache + compact delta rows); mmi is never materialised
+  int T = 0;                    // channels per delta row (virt): max touched list (delta)
+                                // or C_out (whole-node recompute)
+  std::vector<int> vchmap;      // virt: [slot][C_out] channel map (-2-t = delta channel t)
 };
 
 struct Plan {
