@@ -34,8 +34,11 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}    # MI355X dense MFMA
 KERNELS = ["dense_kernel (DENSE layers, MFMA GEMM)",
            "conv_valu_kernel (CONV2D with few output channels, vector ALU)",
            "conv_lds_kernel (CONV2D, LDS-resident images, MFMA)",
-           "conv_mfma_kernel (CONV2D, im2col implicit GEMM, MFMA)"]
+           "conv_mfma_kernel (CONV2D, im2col implicit GEMM with scalar gathers, MFMA)",
+           "conv_big_kernel (bf16 CONV2D, tiled implicit GEMM, MFMA)"]
 PEAK_HBM_GBS = 8000.0
+ORACLE_SAMPLE = {"cfg1": (100, 500), "cfg2": (24, 6000), "cfg3": (3, 64), "cfg4": (8, 256),
+                 "cfg5": (2, 16)}
 
 
 def cpu_baseline(wl, n_mut: int, n_in: int):
@@ -66,8 +69,8 @@ def main():
     ap.add_argument("--ratio-index", type=int, default=1)
     ap.add_argument("--inputs", type=int, default=None)
     ap.add_argument("--mutants", type=int, default=None)
-    ap.add_argument("--oracle-mutants", type=int, default=24)
-    ap.add_argument("--oracle-inputs", type=int, default=6000)
+    ap.add_argument("--oracle-mutants", type=int, default=None)
+    ap.add_argument("--oracle-inputs", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--fused", type=int, default=1)
     args = ap.parse_args()
@@ -155,7 +158,11 @@ def main():
                  "launches_run_mutants": st["launches"]},
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(wl, args.oracle_mutants, min(args.oracle_inputs, N))
+        # about 10 s of oracle work on the host cores
+        om, oi = ORACLE_SAMPLE[args.config]
+        om = args.oracle_mutants or om
+        oi = args.oracle_inputs or oi
+        line["cpu_baseline"] = cpu_baseline(wl, min(om, M), min(oi, N))
     print(json.dumps(line), flush=True)
 
 

@@ -146,10 +146,10 @@ typedef struct {
   int64_t gemm_macs_algorithmic, gemm_macs_executed;
   /* The same, split by kernel: [0] dense GEMM, [1] vector-ALU convolution
    * (few output channels), [2] LDS-resident convolution, [3] im2col implicit
-   * GEMM. */
-  int64_t kernel_launches[4];
-  double kernel_ms[4];
-  int64_t kernel_macs_algorithmic[4];
+   * GEMM with scalar gathers, [4] tiled bf16 implicit GEMM. */
+  int64_t kernel_launches[5];
+  double kernel_ms[5];
+  int64_t kernel_macs_algorithmic[5];
 } mure_stats;
 
 /* Version of this interface (MURE_VERSION). */

@@ -57,8 +57,8 @@ class mure_stats(C.Structure):
                 ("ms_apply", C.c_double), ("ms_run_original", C.c_double),
                 ("ms_run_mutants", C.c_double), ("gemm_launches", C.c_int64),
                 ("ms_gemm", C.c_double), ("gemm_macs_algorithmic", C.c_int64),
-                ("gemm_macs_executed", C.c_int64), ("kernel_launches", C.c_int64 * 4),
-                ("kernel_ms", C.c_double * 4), ("kernel_macs_algorithmic", C.c_int64 * 4)]
+                ("gemm_macs_executed", C.c_int64), ("kernel_launches", C.c_int64 * 5),
+                ("kernel_ms", C.c_double * 5), ("kernel_macs_algorithmic", C.c_int64 * 5)]
 
 
 class MureError(RuntimeError):

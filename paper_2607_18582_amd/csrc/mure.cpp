@@ -268,7 +268,9 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
         if (fam != FAM_LDS) return ctx->fail(MURE_E_INVALID, "internal: virtual input to an im2col convolution");
         a.vin = *ex.vin;
       }
-      e = fam == FAM_LDS ? launch_conv_lds(a, nslots, ctx->stream) : launch_conv(a, nslots, g.dtype, ctx->stream);
+      e = fam == FAM_LDS ? launch_conv_lds(a, nslots, ctx->stream)
+        : fam == FAM_BIG ? launch_conv_big(a, nslots, ctx->stream)
+        : launch_conv(a, nslots, g.dtype, ctx->stream);
     }
     if (timed && e == hipSuccess) {
       hipError_t ee = hipEventRecord(ctx->tevents[ctx->tevents_used + 1], ctx->stream);
@@ -881,7 +883,7 @@ mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* ki
   ctx->stats.ms_gemm = 0;
   ctx->stats.gemm_macs_algorithmic = 0;
   ctx->stats.gemm_macs_executed = 0;
-  for (int f = 0; f < 4; ++f) {
+  for (int f = 0; f < N_FAMILIES; ++f) {
     ctx->stats.kernel_launches[f] = 0;
     ctx->stats.kernel_ms[f] = 0;
     ctx->stats.kernel_macs_algorithmic[f] = 0;

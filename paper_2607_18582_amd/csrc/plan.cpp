@@ -134,6 +134,9 @@ int node_family(const Graph& g, int v) {
   if (g.dtype == DT_F32 && n.c_out <= 64 &&
       conv_lds_bytes(n.inH, n.inW, n.inC, n.pad, P, n.c_out, n.fan_in) <= 48 * 1024)
     return FAM_LDS;
+  if (g.dtype == DT_BF16 && n.inC % 8 == 0 && n.kh <= 15 && n.kw <= 15 && n.fan_in <= 8192 &&
+      P % 4 == 0 && ((int64_t)n.kh * n.inW + n.kw) * n.inC < (1 << 24))
+    return FAM_BIG;
   return FAM_GEMM;
 }
 

@@ -59,8 +59,10 @@ enum Family {
   FAM_DENSE = 0,   // dense GEMM on MFMA
   FAM_VALU = 1,    // tiny C_out: per-output fused multiply-add chains (vector ALU)
   FAM_LDS = 2,     // fp32 conv whose padded input image and weights fit in LDS
-  FAM_GEMM = 3     // implicit GEMM with an im2col gather
+  FAM_GEMM = 3,    // implicit GEMM with a scalar im2col gather (any shape)
+  FAM_BIG = 4      // bf16 tiled implicit GEMM with 16-byte gathers (C_in % 8 == 0)
 };
+constexpr int N_FAMILIES = 5;
 int node_family(const Graph& g, int v);
 
 // Launch geometry shared by the planner (family choice) and the kernels.
