@@ -78,6 +78,13 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it first (python -m paper_2607_18582_amd.build)")
+    # One HIP runtime per process: torch ships its own libamdhip64, and the
+    # streams and device memory it hands to the library belong to that
+    # runtime.  Loading torch first makes libmure bind to the same runtime.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = C.CDLL(path)
     P = C.c_void_p
     sig = {
