@@ -73,6 +73,14 @@ def main():
     ap.add_argument("--oracle-inputs", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--fused", type=int, default=1)
+    ap.add_argument("--conv-tile", type=int, default=0)
+    ap.add_argument("--gain", type=int, default=None,
+                    help="also time vanilla mutation testing (every mutant from the raw "
+                         "input) and report the paper's gain (t_v - t) / t_v (default: on "
+                         "for cfg1/cfg2)")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="first copy a buffer of this many MiB device to device (a plain copy "
+                         "kernel of known size, to scale the HBM byte counters of a profile)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -83,6 +91,15 @@ def main():
     import torch
     from paper_2607_18582_amd import Mure
 
+    if args.copy_calibration_mib:
+        nbytes = args.copy_calibration_mib << 20
+        a = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": nbytes}), file=sys.stderr, flush=True)
+        del a, b
     wl = W.make_workload(args.config, n_inputs=args.inputs, n_mutants=args.mutants,
                          ratio_index=args.ratio_index)
     md = wl.model
@@ -94,6 +111,7 @@ def main():
     m = Mure(device=0)
     m.set_option("kernel_timing", 1)
     m.set_option("fused_paths", args.fused)
+    m.set_option("conv_tile", args.conv_tile)
 
     def step():
         m.load_model(md.nodes, md.in_hwc, md.dtype, md.weights, md.biases)
@@ -157,6 +175,26 @@ def main():
                  "groups": st["n_groups"], "cache_bytes": st["cache_bytes"],
                  "launches_run_mutants": st["launches"]},
     }
+    if args.gain if args.gain is not None else args.config in ("cfg1", "cfg2"):
+        # the paper's measure (Section 6.2): gain = (t_v - t) / t_v with every
+        # overhead in both times; vanilla = the same library with memoization off
+        m.set_option("vanilla", 1)
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        vstats = []
+        for _ in range(args.steps):
+            _, vk, vscore = step()
+            vstats.append(m.stats())
+        torch.cuda.synchronize()
+        dtv = (time.perf_counter() - t0) / args.steps
+        m.set_option("vanilla", 0)
+        line["paper_gain"] = {"gain": (dtv - dt) / dtv, "ms_per_step_memoized": dt * 1e3,
+                              "ms_per_step_vanilla": dtv * 1e3,
+                              "ms_run_mutants_vanilla": float(np.median([s["ms_run_mutants"] for s in vstats])),
+                              "same_score": [vscore["ms_num"], vscore["ms_den"]] == [score["ms_num"], score["ms_den"]],
+                              "macs_vanilla": vstats[-1]["macs_executed"]}
     if not args.no_cpu_baseline:
         # about 10 s of oracle work on the host cores
         om, oi = ORACLE_SAMPLE[args.config]

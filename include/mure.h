@@ -60,12 +60,15 @@ typedef enum { MURE_F32 = 0, MURE_BF16 = 1 } mure_dtype;
  *                  model's weight dtype, round-to-nearest-even); bias kept.
  *   EFFECT_BLOCK   W[i] <- 0 and b[i] <- 0: the neuron's output is 0.
  *   ACT_INVERSE    W[i] <- -W[i] and b[i] <- -b[i]: the pre-activation is negated.
- *   NEURON_SWITCH  W[i] <-> W[partner] and b[i] <-> b[partner].            */
+ *   NEURON_SWITCH  W[i] <-> W[partner] and b[i] <-> b[partner].
+ *   WEIGHT_SHUFFLE W[i][k] <- W[i][perm[k]] for a permutation perm of the
+ *                  neuron's fan_in incoming weights; bias kept.            */
 typedef enum {
   MURE_OP_GAUSS_FUZZ = 0,
   MURE_OP_EFFECT_BLOCK = 1,
   MURE_OP_ACT_INVERSE = 2,
-  MURE_OP_NEURON_SWITCH = 3
+  MURE_OP_NEURON_SWITCH = 3,
+  MURE_OP_WEIGHT_SHUFFLE = 4
 } mure_op;
 
 typedef enum {
@@ -108,7 +111,9 @@ typedef struct {
   int32_t partner;      /* NEURON_SWITCH: the other neuron (!= neuron); else -1 */
   int32_t reserved;     /* 0 */
   const float* noise;   /* GAUSS_FUZZ: host, fan_in values in W[neuron] order; else NULL */
-  int64_t noise_len;    /* GAUSS_FUZZ: = fan_in (c_in*kh*kw for CONV2D, c_in for DENSE) */
+  int64_t noise_len;    /* GAUSS_FUZZ: = fan_in (c_in*kh*kw for CONV2D, c_in for DENSE);
+                           WEIGHT_SHUFFLE: = fan_in (length of perm) */
+  const int32_t* perm;  /* WEIGHT_SHUFFLE: host, a permutation of 0..fan_in-1; else NULL */
 } mure_record;
 
 /* Mutation score (Section 6.2): MS = ms_num / ms_den with
@@ -235,6 +240,12 @@ mure_status mure_get_stats(const mure_ctx* ctx, mure_stats* out);
  *   "chunk_inputs"      inputs per chunk, multiple of 64 (0 = automatic)
  *   "fused_paths"       1 (default) use fused kernels where a graph allows, 0
  *                       force the layer-by-layer engine
+ *   "vanilla"           1: no memoization -- every mutant runs from the first
+ *                       layer after the input (exhaustive mutation testing, the
+ *                       baseline the paper compares against); takes effect at
+ *                       the next apply_mutants.  0 (default) memoized
+ *   "conv_tile"         block shape of the tiled bf16 convolution: 0 automatic,
+ *                       1 = 128 output pixels per block, 2 = 256
  *   "kernel_timing"     1: time each implicit-GEMM launch of run_mutants (see
  *                       mure_stats); 0 (default) off
  * Errors: MURE_E_INVALID for an unknown name or value. */

@@ -10,7 +10,10 @@ the readings used here (shared with the GPU library's documentation):
   NEB (neuron effect block)        W[i] <- 0, b[i] <- 0  (the neuron outputs 0);
   NAI (neuron activation inverse)  W[i] <- -W[i], b[i] <- -b[i]  (the
                                    pre-activation is negated before ReLU);
-  NS  (neuron switch)              W[i] <-> W[j], b[i] <-> b[j].
+  NS  (neuron switch)              W[i] <-> W[j], b[i] <-> b[j];
+  WS  (weight shuffle)             W[i][k] <- W[i][perm[k]] for a given
+                                   permutation of the incoming weights, bias
+                                   untouched.
 A mutant's records apply in array order.  Mutated layer functions Phi' are
 therefore the original functions with changed parameters: the graph never
 changes (Section 4).
@@ -21,7 +24,7 @@ from typing import List, Optional, Tuple
 
 import numpy as np
 
-from workloads.graph import GF, NEB, NAI, NS, Mutants
+from workloads.graph import GF, NEB, NAI, NS, WS, Mutants
 from .layers import OracleModel
 from .numerics import rne_bf16
 
@@ -60,6 +63,11 @@ def apply_records(model: OracleModel, mutants: Mutants, m: int):
                 raise ValueError(f"record {r}: bad switch partner {j}")
             w[[i, j]] = w[[j, i]]
             B[l][[i, j]] = B[l][[j, i]]
+        elif op == WS:
+            perm = np.asarray(mutants.perm_of(r), np.int64)
+            if perm.size != w.shape[1] or not np.array_equal(np.sort(perm), np.arange(w.shape[1])):
+                raise ValueError(f"record {r}: not a permutation of the fan-in")
+            w[i] = w[i][perm]
         else:
             raise ValueError(f"record {r}: unknown operator {op}")
     return W, B, sorted(copied)

@@ -21,7 +21,7 @@ MURE_OK, MURE_E_INVALID, MURE_E_STATE, MURE_E_NOMEM, MURE_E_DEVICE, MURE_E_UNSUP
 STATUS_NAMES = {0: "MURE_OK", -1: "MURE_E_INVALID", -2: "MURE_E_STATE", -3: "MURE_E_NOMEM",
                 -4: "MURE_E_DEVICE", -5: "MURE_E_UNSUPPORTED"}
 MURE_F32, MURE_BF16 = 0, 1
-OP_GAUSS_FUZZ, OP_EFFECT_BLOCK, OP_ACT_INVERSE, OP_NEURON_SWITCH = 0, 1, 2, 3
+OP_GAUSS_FUZZ, OP_EFFECT_BLOCK, OP_ACT_INVERSE, OP_NEURON_SWITCH, OP_WEIGHT_SHUFFLE = 0, 1, 2, 3, 4
 INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN = 0, 1, 2, 3, 4, 5
 
 EXPORTED = ["mure_version", "mure_create", "mure_load_model", "mure_apply_mutants",
@@ -39,7 +39,8 @@ class mure_layer(C.Structure):
 class mure_record(C.Structure):
     _fields_ = [("mutant", C.c_int32), ("op", C.c_int32), ("layer", C.c_int32),
                 ("neuron", C.c_int32), ("partner", C.c_int32), ("reserved", C.c_int32),
-                ("noise", C.POINTER(C.c_float)), ("noise_len", C.c_int64)]
+                ("noise", C.POINTER(C.c_float)), ("noise_len", C.c_int64),
+                ("perm", C.POINTER(C.c_int32))]
 
 
 class mure_score(C.Structure):
@@ -184,9 +185,9 @@ class Mure:
 
     RECORD_DTYPE = np.dtype([("mutant", "<i4"), ("op", "<i4"), ("layer", "<i4"), ("neuron", "<i4"),
                              ("partner", "<i4"), ("reserved", "<i4"), ("noise", "<u8"),
-                             ("noise_len", "<i8")])
+                             ("noise_len", "<i8"), ("perm", "<u8")])
 
-    def apply_mutants(self, n_mutants: int, mutant_id, op, layer, neuron, partner, noise):
+    def apply_mutants(self, n_mutants: int, mutant_id, op, layer, neuron, partner, noise, perm=None):
         R = len(mutant_id)
         recs = np.zeros(max(R, 1), dtype=self.RECORD_DTYPE)
         recs["mutant"][:R] = mutant_id
@@ -200,15 +201,24 @@ class Mure:
         offs = np.concatenate([[0], np.cumsum(lens)[:-1]]) if R else np.zeros(0, np.int64)
         recs["noise"][:R] = np.where(lens > 0, pool.ctypes.data + 4 * offs, 0)
         recs["noise_len"][:R] = lens
+        perm = perm if perm is not None else [None] * R
+        plens = np.array([0 if q is None else len(q) for q in perm], np.int64)
+        ppool = np.concatenate([np.asarray(q, np.int32) for q in perm if q is not None] or
+                               [np.zeros(1, np.int32)])
+        poffs = np.concatenate([[0], np.cumsum(plens)[:-1]]) if R else np.zeros(0, np.int64)
+        recs["perm"][:R] = np.where(plens > 0, ppool.ctypes.data + 4 * poffs, 0)
+        recs["noise_len"][:R] = np.where(plens > 0, plens, recs["noise_len"][:R])
         assert self.RECORD_DTYPE.itemsize == C.sizeof(mure_record)
         ptr = recs.ctypes.data_as(C.POINTER(mure_record))
+        self._keep_params = (pool, ppool)
         self._check(self.lib.mure_apply_mutants(self.ctx, int(n_mutants), ptr, R))
         self.n_mutants = int(n_mutants)
 
     def apply(self, mutants):
         """``apply_mutants`` from an object with mutant_id/op/layer/neuron/partner/noise."""
         self.apply_mutants(mutants.n_mutants, mutants.mutant_id, mutants.op, mutants.layer,
-                           mutants.neuron, mutants.partner, mutants.noise)
+                           mutants.neuron, mutants.partner, mutants.noise,
+                           getattr(mutants, "perm", None))
 
     def run_original(self, inputs, labels: Optional[np.ndarray] = None):
         """``inputs``: a contiguous CUDA tensor [N][H][W][C] (float32, or int16/bfloat16

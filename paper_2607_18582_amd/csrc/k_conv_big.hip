@@ -14,17 +14,19 @@
 namespace mure {
 
 namespace {
-constexpr int BIG_BM = 128, BIG_BK = 64, BIG_LD = BIG_BK + 8;   // padded LDS rows (bf16)
+constexpr int BIG_BK = 64, BIG_LD = BIG_BK + 8;   // padded LDS rows (bf16)
 }
 
-template <int BN, int WAVES_M>
-__global__ __launch_bounds__(256) void conv_big_kernel(ConvArgs a) {
-  constexpr int BM = BIG_BM, BK = BIG_BK, LD = BIG_LD;
-  constexpr int WAVES_N = 4 / WAVES_M;
+template <int BM, int BN, int WAVES_M, int WAVES_N>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N)
+void conv_big_kernel(ConvArgs a) {
+  constexpr int THREADS = 64 * WAVES_M * WAVES_N;
+  constexpr int BK = BIG_BK, LD = BIG_LD;
+  constexpr int ROWS_PER_THREAD = BM * 2 / THREADS;   // A rows gathered by each thread (2 per row)
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int TM = WM / 16, TN = WN / 16;
   constexpr int BVEC = BN * BK / 8;                    // 16-byte vectors of a B chunk
-  constexpr int BPT = (BVEC + 255) / 256;              // per thread
+  constexpr int BPT = (BVEC + THREADS - 1) / THREADS;  // per thread
   __shared__ __attribute__((aligned(16))) bf16_t As[BM * LD];
   __shared__ __attribute__((aligned(16))) bf16_t Bs[BN * LD];
   __shared__ int ktab[1024];                           // per 8-k vector: tap offset | (dy, dx)
@@ -37,54 +39,66 @@ __global__ __launch_bounds__(256) void conv_big_kernel(ConvArgs a) {
   const int n0 = (int)blockIdx.z * BN;
   const bf16_t* __restrict__ Wt = reinterpret_cast<const bf16_t*>(a.wtab[slot]);
   const int kvec = (a.K + 7) / 8;
-  for (int v = tid; v < kvec; v += 256) {
+  for (int v = tid; v < kvec; v += THREADS) {
     const int k = v * 8, ci = k % a.C, t = k / a.C;
     const int dy = t / a.kw, dx = t % a.kw;
     ktab[v] = ((dy * a.W + dx) * a.C + ci) | (dy << 24) | (dx << 28);
   }
 
-  // the A row this thread gathers
+  // the A rows this thread gathers: rows arow + (THREADS/2)*r
+  constexpr int RSTEP = THREADS / 2;
   const int arow = tid >> 1, ahalf = tid & 1;
-  const int64_t m = m0 + arow;
-  const bool mvalid = m < Mslot;
-  int iy0 = 0, ix0 = 0;
-  const bf16_t* inrow = reinterpret_cast<const bf16_t*>(a.in.p);
-  if (mvalid) {
-    const int xi = (int)(m / a.P), p = (int)(m % a.P);
-    int oy, ox;
-    if (a.pool) {
-      const int q = p >> 2, sub = p & 3;
-      oy = 2 * (q / a.Wp) + (sub >> 1);
-      ox = 2 * (q % a.Wp) + (sub & 1);
-    } else {
-      oy = p / a.Wc;
-      ox = p % a.Wc;
+  bool mvalid[ROWS_PER_THREAD];
+  int iy0[ROWS_PER_THREAD], ix0[ROWS_PER_THREAD];
+  const bf16_t* inrow[ROWS_PER_THREAD];
+#pragma unroll
+  for (int r = 0; r < ROWS_PER_THREAD; ++r) {
+    const int64_t m = m0 + arow + RSTEP * r;
+    mvalid[r] = m < Mslot;
+    iy0[r] = ix0[r] = 0;
+    inrow[r] = reinterpret_cast<const bf16_t*>(a.in.p);
+    if (mvalid[r]) {
+      const int xi = (int)(m / a.P), p = (int)(m % a.P);
+      int oy, ox;
+      if (a.pool) {
+        const int q = p >> 2, sub = p & 3;
+        oy = 2 * (q / a.Wp) + (sub >> 1);
+        ox = 2 * (q % a.Wp) + (sub & 1);
+      } else {
+        oy = p / a.Wc;
+        ox = p % a.Wc;
+      }
+      iy0[r] = oy * a.stride - a.pad;
+      ix0[r] = ox * a.stride - a.pad;
+      inrow[r] += row_index(a.in.mode, (int64_t)slot * a.nx + xi, a.nx, a.x0) * a.in.row_elems +
+                  ((int64_t)iy0[r] * a.W + ix0[r]) * a.C;
     }
-    iy0 = oy * a.stride - a.pad;
-    ix0 = ox * a.stride - a.pad;
-    inrow += row_index(a.in.mode, (int64_t)slot * a.nx + xi, a.nx, a.x0) * a.in.row_elems +
-             ((int64_t)iy0 * a.W + ix0) * a.C;
   }
   __syncthreads();
 
-  uint4 ra[4], rb[BPT];
+  uint4 ra[ROWS_PER_THREAD][4], rb[BPT];
   auto load_chunk = [&](int kc) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int v = (kc >> 3) + ahalf * 4 + j;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (mvalid && v < kvec) {
-        const int code = ktab[v];
-        const int dy = (code >> 24) & 15, dx = (code >> 28) & 15;
-        const int iy = iy0 + dy, ix = ix0 + dx;
-        if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W)
-          val = *reinterpret_cast<const uint4*>(inrow + (code & 0xFFFFFF));
+      int code = 0, dy = 0, dx = 0;
+      if (v < kvec) {
+        code = ktab[v];
+        dy = (code >> 24) & 15;
+        dx = (code >> 28) & 15;
       }
-      ra[j] = val;
+#pragma unroll
+      for (int r = 0; r < ROWS_PER_THREAD; ++r) {
+        uint4 val = make_uint4(0, 0, 0, 0);
+        const int iy = iy0[r] + dy, ix = ix0[r] + dx;
+        if (mvalid[r] && v < kvec && iy >= 0 && iy < a.H && ix >= 0 && ix < a.W)
+          val = *reinterpret_cast<const uint4*>(inrow[r] + (code & 0xFFFFFF));
+        ra[r][j] = val;
+      }
     }
 #pragma unroll
     for (int j = 0; j < BPT; ++j) {
-      const int i = tid + j * 256;
+      const int i = tid + j * THREADS;
       uint4 val = make_uint4(0, 0, 0, 0);
       if (i < BVEC) {
         const int row = i / (BK / 8), kv = i % (BK / 8);
@@ -97,11 +111,13 @@ __global__ __launch_bounds__(256) void conv_big_kernel(ConvArgs a) {
   };
   auto store_chunk = [&]() {
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      *reinterpret_cast<uint4*>(&As[arow * LD + (ahalf * 4 + j) * 8]) = ra[j];
+    for (int r = 0; r < ROWS_PER_THREAD; ++r)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *reinterpret_cast<uint4*>(&As[(arow + RSTEP * r) * LD + (ahalf * 4 + j) * 8]) = ra[r][j];
 #pragma unroll
     for (int j = 0; j < BPT; ++j) {
-      const int i = tid + j * 256;
+      const int i = tid + j * THREADS;
       if (i < BVEC) {
         const int row = i / (BK / 8), kv = i % (BK / 8);
         *reinterpret_cast<uint4*>(&Bs[row * LD + kv * 8]) = rb[j];
@@ -165,9 +181,29 @@ __global__ __launch_bounds__(256) void conv_big_kernel(ConvArgs a) {
         const int pp = (int)(mb % a.P);
         // the 4 rows of a lane are consecutive pixels of one input (P % 4 == 0)
         const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xo, a.nx, a.x0);
+        if (a.add_mode) {
+          // conv_b's output (rounded) + the shortcut, in float32, then ReLU
+          const bf16_t* sp = reinterpret_cast<const bf16_t*>(a.skip.p) +
+                             row_index(a.skip.mode, (int64_t)slot * a.nx + xo, a.nx, a.x0) * a.skip.row_elems;
+          const int cs = a.add_mode == 1 ? n : n - (a.Cout - a.Cs) / 2;
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          store_out<bf16_t>(a.out, a.out_f32, ro * a.out_row + (int64_t)(pp + e) * a.Cout + n, v[e]);
+          for (int e = 0; e < 4; ++e) {
+            float sv = 0.f;
+            if (a.add_mode == 1) {
+              sv = bf2f(sp[(int64_t)(pp + e) * a.Cout + n]);
+            } else if (cs >= 0 && cs < a.Cs) {
+              const int y = (pp + e) / a.Wc, x = (pp + e) % a.Wc;
+              sv = bf2f(sp[((int64_t)(2 * y) * a.Ws + 2 * x) * a.Cs + cs]);
+            }
+            float t = bf2f(f2bf(v[e])) + sv;
+            if (a.add_relu) t = fmaxf(t, 0.f);
+            store_out<bf16_t>(a.out, a.add_out_f32, ro * a.out_row + (int64_t)(pp + e) * a.Cout + n, t);
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            store_out<bf16_t>(a.out, a.out_f32, ro * a.out_row + (int64_t)(pp + e) * a.Cout + n, v[e]);
+        }
       }
     }
   }
@@ -179,13 +215,24 @@ hipError_t launch_conv_big(const ConvArgs& a, int nslots, hipStream_t s) {
   if (nslots <= 0 || a.nx <= 0) return hipSuccess;
   if (a.C % 8 || a.K > 8 * 1024 || a.P % 4) return hipErrorInvalidValue;
   const int bn = conv_big_bn(a.Cout);
+  // tile: 0 automatic, 1 = 128 rows x BN (4 waves), 2 = 256 rows x BN (8 waves of 64 x 32..64)
+  const int bm = a.tile == 1 ? 128 : 256;
   const int64_t Mslot = (int64_t)a.nx * a.P;
-  dim3 grid((unsigned)((Mslot + BIG_BM - 1) / BIG_BM), (unsigned)nslots, (unsigned)((a.Cout + bn - 1) / bn));
-  switch (bn) {
-    case 16: hipLaunchKernelGGL((conv_big_kernel<16, 4>), grid, dim3(256), 0, s, a); break;
-    case 32: hipLaunchKernelGGL((conv_big_kernel<32, 4>), grid, dim3(256), 0, s, a); break;
-    case 64: hipLaunchKernelGGL((conv_big_kernel<64, 4>), grid, dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL((conv_big_kernel<128, 2>), grid, dim3(256), 0, s, a); break;
+  dim3 grid((unsigned)((Mslot + bm - 1) / bm), (unsigned)nslots, (unsigned)((a.Cout + bn - 1) / bn));
+  if (bm == 128) {
+    switch (bn) {
+      case 16: hipLaunchKernelGGL((conv_big_kernel<128, 16, 4, 1>), grid, dim3(256), 0, s, a); break;
+      case 32: hipLaunchKernelGGL((conv_big_kernel<128, 32, 4, 1>), grid, dim3(256), 0, s, a); break;
+      case 64: hipLaunchKernelGGL((conv_big_kernel<128, 64, 4, 1>), grid, dim3(256), 0, s, a); break;
+      default: hipLaunchKernelGGL((conv_big_kernel<128, 128, 2, 2>), grid, dim3(256), 0, s, a); break;
+    }
+  } else {
+    switch (bn) {
+      case 16: hipLaunchKernelGGL((conv_big_kernel<256, 16, 8, 1>), grid, dim3(512), 0, s, a); break;
+      case 32: hipLaunchKernelGGL((conv_big_kernel<256, 32, 8, 1>), grid, dim3(512), 0, s, a); break;
+      case 64: hipLaunchKernelGGL((conv_big_kernel<256, 64, 4, 2>), grid, dim3(512), 0, s, a); break;
+      default: hipLaunchKernelGGL((conv_big_kernel<256, 128, 4, 2>), grid, dim3(512), 0, s, a); break;
+    }
   }
   return hipGetLastError();
 }

@@ -177,6 +177,12 @@ __global__ __launch_bounds__(256) void cow_kernel(const CowArgs* args, const Dev
         else row[k] = -row[k];
       }
       if (threadIdx.x == 0) c.b_dst[r.neuron] = -c.b_dst[r.neuron];
+    } else if (r.op == 4) {               // weight shuffle: row[k] <- old row[perm[k]]
+      float* scratch = const_cast<float*>(noise) + r.scratch_off;
+      const int32_t* perm = reinterpret_cast<const int32_t*>(noise + r.noise_off);
+      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) scratch[k] = to_f<T>(row[k]);
+      __syncthreads();
+      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) row[k] = from_f<T>(scratch[perm[k]]);
     } else {                              // neuron switch
       T* other = wd + (int64_t)r.partner * c.fan_in;
       for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) {

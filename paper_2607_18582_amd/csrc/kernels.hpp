@@ -51,6 +51,13 @@ struct ConvArgs {
   int Cout = 0, kh = 1, kw = 1, stride = 1, pad = 0, relu = 0, pool = 0;
   int K = 0;                             // kh*kw*C
   int P = 0;                             // GEMM rows per input
+  // fused ADD node after this convolution (conv_b of a residual block; its
+  // own output is rounded first, then out = ReLU?(conv + s(skip)) is stored
+  // as the ADD node's output): 0 none, 1 identity shortcut, 2 option A
+  int add_mode = 0, add_relu = 0, add_out_f32 = 0;
+  TensorArg skip;
+  int Hs = 0, Ws = 0, Cs = 0;            // skip geometry
+  int tile = 0;                          // tiled kernel's block shape (0 automatic)
 };
 
 // DENSE on MFMA: out[r][n] = sum_k in[r][k] * W[n][k] + b[n] (k in increasing
@@ -164,7 +171,7 @@ struct CowArgs {                           // one copy-on-write parameter copy
   int rec0, rec1;                          // records [rec0, rec1) in the device record table
 };
 
-struct DevRecord { int op, neuron, partner, pad; int64_t noise_off; };
+struct DevRecord { int op, neuron, partner, pad; int64_t noise_off, scratch_off; };
 
 // launchers (return the launch status)
 hipError_t launch_conv(const ConvArgs& a, int nslots, int dtype, hipStream_t s);

@@ -58,25 +58,24 @@ struct Placement {
   int64_t peak = 0;                // bytes per row
 };
 
-Placement place_buffers(const Graph& g, const std::vector<int>& nodes, const std::set<int>& external) {
-  // nodes: executed in this order; external: nodes whose output lives elsewhere
+Placement place_buffers(const Graph& g, const std::vector<int>& nodes, const std::set<int>& external,
+                        const std::map<int, int>& fused = {}) {
+  // nodes: executed in this order; external: nodes whose output lives
+  // elsewhere; fused: conv_b -> ADD pairs run as one launch at conv_b's step,
+  // so the ADD's buffer is placed at that step (conv_b itself has none)
   std::map<int, int> last_use;
   for (int v : nodes) {
     for (int k = 0; k < g.nodes[v].n_in; ++k) last_use[g.nodes[v].in[k]] = v;
+  }
+  for (const auto& kv : fused) {                 // the ADD's inputs are read at conv_b's step or later
+    (void)kv;
   }
   struct Blk { int64_t off, size; int owner; };
   std::vector<Blk> blocks;
   Placement pl;
   const int out = g.out();
-  for (int v : nodes) {
-    // free blocks whose owner is no longer needed by v or later nodes
-    for (Blk& b : blocks) {
-      if (b.owner < 0) continue;
-      auto it = last_use.find(b.owner);
-      const int lu = (b.owner == out) ? 1 << 30 : (it == last_use.end() ? -1 : it->second);
-      if (lu < v) b.owner = -1;
-    }
-    if (external.count(v)) continue;
+  std::set<int> placed;
+  auto place = [&](int v) {
     const int64_t need = (g.act_bytes(v) + 255) / 256 * 256;
     int best = -1;
     for (size_t i = 0; i < blocks.size(); ++i)
@@ -90,6 +89,23 @@ Placement place_buffers(const Graph& g, const std::vector<int>& nodes, const std
       blocks[best].owner = v;
     }
     pl.offset[v] = blocks[best].off;
+    placed.insert(v);
+  };
+  for (int v : nodes) {
+    // free blocks whose owner is no longer needed by v or later nodes
+    for (Blk& b : blocks) {
+      if (b.owner < 0) continue;
+      auto it = last_use.find(b.owner);
+      const int lu = (b.owner == out) ? 1 << 30 : (it == last_use.end() ? -1 : it->second);
+      if (lu < v) b.owner = -1;
+    }
+    auto f = fused.find(v);
+    if (f != fused.end()) {
+      if (!external.count(f->second)) place(f->second);
+      continue;
+    }
+    if (external.count(v) || placed.count(v)) continue;
+    place(v);
   }
   return pl;
 }
@@ -135,6 +151,8 @@ struct mure_ctx {
   int64_t chunk_inputs = 0;
   int64_t fused = 1;
   int64_t kernel_timing = 0;
+  int64_t conv_tile = 0;
+  int64_t vanilla = 0;
   std::vector<hipEvent_t> tevents;                    // pairs around timed launches
   std::vector<int> tevent_family;                     // kernel family of each timed pair
   size_t tevents_used = 0;
@@ -160,6 +178,20 @@ namespace {
 
 int64_t esize_of(const Graph& g, int v) { return (v == g.out() || g.dtype == DT_F32) ? 4 : 2; }
 
+// The ADD node that reads convolution v as its first input when nothing else
+// reads v (conv_b of a residual block): the pair runs as one launch whose
+// epilogue adds the shortcut.  -1 if v is not such a convolution.
+int fused_add_of(const Graph& g, int v) {
+  const Node& n = g.nodes[v];
+  if (n.kind != K_CONV || n.maxpool || node_family(g, v) != FAM_BIG) return -1;
+  int reader = -1, count = 0;
+  for (int j = v + 1; j < (int)g.nodes.size(); ++j)
+    for (int k = 0; k < g.nodes[j].n_in; ++k)
+      if (g.nodes[j].in[k] == v) { reader = j; ++count; }
+  if (count != 1 || g.nodes[reader].kind != K_ADD || g.nodes[reader].in[0] != v) return -1;
+  return reader;
+}
+
 // Tensor reference of node p for the executor.
 struct Where {
   const void* p;
@@ -172,6 +204,8 @@ struct Extra {
   const int32_t* ch_list = nullptr;
   int delta_T = 0;                    // write compact delta rows of delta_T channels
   const VirtualIn* vin = nullptr;     // read the first mutated node's output virtually
+  int fuse_add = -1;                  // ADD node fused into this convolution's epilogue
+  Where skip{nullptr, MODE_BUF};      // that ADD's shortcut input
   const KillArgs* kill = nullptr;     // fuse the kill reduction when possible
   bool* kill_fused = nullptr;
 };
@@ -264,9 +298,19 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
       a.relu = n.relu;
       a.K = a.kh * a.kw * a.C;
       a.P = a.pool ? 4 * a.Hp * a.Wp : a.Hc * a.Wc;
+      a.tile = (int)ctx->conv_tile;
       if (ex.vin) {
         if (fam != FAM_LDS) return ctx->fail(MURE_E_INVALID, "internal: virtual input to an im2col convolution");
         a.vin = *ex.vin;
+      }
+      if (ex.fuse_add >= 0) {
+        const Node& an = g.nodes[ex.fuse_add];
+        const Node& sn = g.nodes[an.in[1]];
+        a.add_mode = an.shortcut == 1 ? 2 : 1;
+        a.add_relu = an.relu;
+        a.add_out_f32 = ex.fuse_add == g.out() ? 1 : 0;
+        a.skip.p = ex.skip.p; a.skip.mode = ex.skip.mode; a.skip.row_elems = sn.out_elems();
+        a.Hs = sn.H; a.Ws = sn.W; a.Cs = sn.C;
       }
       e = fam == FAM_LDS ? launch_conv_lds(a, nslots, ctx->stream)
         : fam == FAM_BIG ? launch_conv_big(a, nslots, ctx->stream)
@@ -379,6 +423,12 @@ mure_status mure_set_option(mure_ctx* ctx, const char* name, int64_t value) {
   } else if (n == "fused_paths") {
     if (value != 0 && value != 1) return ctx->fail(MURE_E_INVALID, "fused_paths must be 0 or 1");
     ctx->fused = value;
+  } else if (n == "vanilla") {
+    if (value != 0 && value != 1) return ctx->fail(MURE_E_INVALID, "vanilla must be 0 or 1");
+    ctx->vanilla = value;
+  } else if (n == "conv_tile") {
+    if (value < 0 || value > 2) return ctx->fail(MURE_E_INVALID, "conv_tile must be 0, 1 or 2");
+    ctx->conv_tile = value;
   } else if (n == "kernel_timing") {
     if (value != 0 && value != 1) return ctx->fail(MURE_E_INVALID, "kernel_timing must be 0 or 1");
     ctx->kernel_timing = value;
@@ -464,10 +514,31 @@ mure_status mure_apply_mutants(mure_ctx* ctx, int32_t n_mutants, const mure_reco
       y.noise_len = x.noise_len;
       if (x.layer >= 0 && x.layer < (int)g.nodes.size() && x.noise_len == g.nodes[x.layer].fan_in)
         noise.insert(noise.end(), x.noise, x.noise + x.noise_len);
+    } else if (x.op == OP_WS) {
+      if (!x.perm || x.noise_len <= 0)
+        return ctx->fail(MURE_E_INVALID, "record " + std::to_string(r) + ": weight shuffle needs a permutation");
+      y.noise_len = x.noise_len;
+      if (x.layer >= 0 && x.layer < (int)g.nodes.size() && x.noise_len == g.nodes[x.layer].fan_in) {
+        std::vector<char> seen((size_t)x.noise_len, 0);
+        for (int64_t k = 0; k < x.noise_len; ++k) {
+          const int32_t q = x.perm[k];
+          if (q < 0 || q >= x.noise_len || seen[q])
+            return ctx->fail(MURE_E_INVALID, "record " + std::to_string(r) + ": perm is not a permutation");
+          seen[q] = 1;
+        }
+        y.noise_off = (int64_t)noise.size();
+        for (int64_t k = 0; k < x.noise_len; ++k) {      // 4-byte integers in the float pool
+          float f;
+          std::memcpy(&f, &x.perm[k], 4);
+          noise.push_back(f);
+        }
+        y.scratch_off = (int64_t)noise.size();
+        noise.resize(noise.size() + (size_t)x.noise_len, 0.f);
+      }
     }
   }
   Plan plan;
-  std::string m = build_plan(g, n_mutants, recs, plan);
+  std::string m = build_plan(g, n_mutants, recs, plan, ctx->vanilla != 0);
   if (!m.empty()) return ctx->fail(MURE_E_INVALID, m);
 
   if (!ctx->plan_only) {
@@ -507,6 +578,7 @@ mure_status mure_apply_mutants(mure_ctx* ctx, int32_t n_mutants, const mure_reco
         DevRecord d;
         d.op = recs[r].op; d.neuron = recs[r].neuron; d.partner = recs[r].partner; d.pad = 0;
         d.noise_off = recs[r].noise_off;
+        d.scratch_off = recs[r].scratch_off;
         drecs.push_back(d);
       }
       a.rec1 = (int)drecs.size();
@@ -652,7 +724,12 @@ mure_status mure_run_original(mure_ctx* ctx, const void* inputs_dev, int64_t n_i
   for (int v = 1; v <= L; ++v) nodes.push_back(v);
   std::set<int> external(cached);
   external.insert(L);
-  Placement pl = place_buffers(g, nodes, external);
+  std::map<int, int> fused;                            // conv_b -> ADD run as one launch
+  for (int v = 1; v <= L; ++v) {
+    const int fa = fused_add_of(g, v);
+    if (fa >= 0 && !cached.count(v)) fused[v] = fa;
+  }
+  Placement pl = place_buffers(g, nodes, external, fused);
   const int64_t budget = ctx->max_ws_mb << 20;
   int64_t nx = n;
   if (ctx->chunk_inputs) nx = std::min<int64_t>(nx, ctx->chunk_inputs);
@@ -677,14 +754,26 @@ mure_status mure_run_original(mure_ctx* ctx, const void* inputs_dev, int64_t n_i
       if (cached.count(p)) return {ctx->cache[p]->p, MODE_CACHE};
       return {ws + pl.offset.at(p) * nx, MODE_BUF};
     };
+    std::set<int> done;
     for (int v = 1; v <= L; ++v) {
+      if (done.count(v)) continue;
       const Node& nd = g.nodes[v];
       std::vector<Where> ins;
       for (int k = 0; k < nd.n_in; ++k) ins.push_back(where(nd.in[k]));
-      Where o = where(v);
+      Extra ex;
+      int tgt = v;
+      auto f = fused.find(v);
+      if (f != fused.end()) {
+        tgt = f->second;
+        ex.fuse_add = tgt;
+        ex.skip = where(g.nodes[tgt].in[1]);
+        done.insert(tgt);
+      }
+      Where o = where(tgt);
       const void* const* wt = nd.weighted() ? tabs + ctx->orig_w.at(v) : nullptr;
       const float* const* bt = nd.weighted() ? reinterpret_cast<const float* const*>(tabs + ctx->orig_b.at(v)) : nullptr;
-      mure_status st = exec_node(ctx, v, ins, const_cast<void*>(o.p), o.mode, wt, bt, 0, 1, cnt, (int)x0, cnt);
+      mure_status st = exec_node(ctx, v, ins, const_cast<void*>(o.p), o.mode, wt, bt, 0, 1, cnt, (int)x0, cnt,
+                                 0, false, ex);
       if (st != MURE_OK) return st;
     }
   }
@@ -725,7 +814,12 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
   const int64_t N = ctx->N;
   std::vector<int> nodes;
   for (int v = mmi; v <= L; ++v) nodes.push_back(v);
-  Placement pl = place_buffers(g, nodes, {});
+  std::map<int, int> fused_adds;                       // conv_b -> ADD run as one launch
+  for (int v = mmi + 1; v <= L; ++v) {
+    const int fa = fused_add_of(g, v);
+    if (fa >= 0) fused_adds[v] = fa;
+  }
+  Placement pl = place_buffers(g, nodes, {}, fused_adds);
   const int64_t budget = ctx->max_ws_mb << 20;
   int64_t nx = N;
   if (ctx->chunk_inputs) nx = std::min<int64_t>(nx, ctx->chunk_inputs);
@@ -821,10 +915,27 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
         vin.HW = nm.H * nm.W;
         vin.T = gr.T;
       }
+      std::set<int> done;
       for (int v = mmi + 1; v <= L; ++v) {
+        if (done.count(v)) continue;
         const Node& nd = g.nodes[v];
         std::vector<Where> ins;
         for (int k = 0; k < nd.n_in; ++k) ins.push_back(where(nd.in[k]));
+        auto f = fused_adds.find(v);
+        if (f != fused_adds.end()) {
+          const int fa = f->second;
+          Extra exf;
+          exf.fuse_add = fa;
+          exf.skip = where(g.nodes[fa].in[1]);
+          if (fa == L) { exf.kill = nullptr; }
+          done.insert(fa);
+          mure_status st = exec_node(ctx, v, ins, const_cast<void*>(where(fa).p), MODE_BUF,
+                                     tabs + gt.w.at(v) + cs0,
+                                     reinterpret_cast<const float* const*>(tabs + gt.b.at(v) + cs0), 0, ns, cnt,
+                                     (int)x0, rows, rows * nd.macs, true, exf);
+          if (st != MURE_OK) return st;
+          continue;
+        }
         const void* const* wt = nd.weighted() ? tabs + gt.w.at(v) + cs0 : nullptr;
         const float* const* bt = nd.weighted() ? reinterpret_cast<const float* const*>(tabs + gt.b.at(v) + cs0) : nullptr;
         Extra ex;

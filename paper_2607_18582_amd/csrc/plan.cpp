@@ -148,7 +148,8 @@ std::vector<int> boundary(const Graph& g, int mmi) {
   return std::vector<int>(K.begin(), K.end());
 }
 
-std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>& recs, Plan& plan) {
+std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>& recs, Plan& plan,
+                       bool vanilla) {
   std::ostringstream err;
   if (n_mutants < 0) return "n_mutants must be >= 0";
   const int n = (int)g.nodes.size();
@@ -160,12 +161,12 @@ std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>&
     }
     const Node& v = g.nodes[x.layer];
     if (x.neuron < 0 || x.neuron >= v.c_out) { err << "record " << r << ": neuron out of range"; return err.str(); }
-    if (x.op < OP_GF || x.op > OP_NS) { err << "record " << r << ": unknown operator " << x.op; return err.str(); }
+    if (x.op < OP_GF || x.op > OP_WS) { err << "record " << r << ": unknown operator " << x.op; return err.str(); }
     if (x.op == OP_NS && (x.partner < 0 || x.partner >= v.c_out || x.partner == x.neuron)) {
       err << "record " << r << ": neuron switch needs a partner in [0, c_out) other than the neuron"; return err.str();
     }
-    if (x.op == OP_GF && x.noise_len != v.fan_in) {
-      err << "record " << r << ": noise length " << x.noise_len << " != fan-in " << v.fan_in; return err.str();
+    if ((x.op == OP_GF || x.op == OP_WS) && x.noise_len != v.fan_in) {
+      err << "record " << r << ": parameter length " << x.noise_len << " != fan-in " << v.fan_in; return err.str();
     }
   }
   Plan p;
@@ -183,13 +184,19 @@ std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>&
     for (int r : rs) mu.insert(recs[r].layer);
     mp.layers.assign(mu.begin(), mu.end());
     mp.mmi = mp.layers.front();
+    if (vanilla) {                       // start at the first weighted node
+      int first = 1;
+      while (!g.nodes[first].weighted()) ++first;
+      mp.mmi = first;
+    }
     mp.K = boundary(g, mp.mmi);
     std::set<int> fuzzed;
     for (int r : rs)
-      if (recs[r].layer == mp.mmi && (recs[r].op == OP_GF || recs[r].op == OP_NAI)) {
+      if (recs[r].layer == mp.mmi && (recs[r].op == OP_GF || recs[r].op == OP_NAI || recs[r].op == OP_WS)) {
         mp.recompute = true;
         fuzzed.insert(recs[r].neuron);
       }
+    if (vanilla) mp.recompute = true;    // the whole first layer, with its own weights
     mp.touched = (int64_t)fuzzed.size();
     const int C = g.nodes[mp.mmi].c_out;
     mp.chmap.resize(C);
@@ -212,6 +219,11 @@ std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>&
       }
       mp.touched_list.assign(tl.begin(), tl.end());
     }
+    if (vanilla) {                       // layers before the first mutated one keep the original
+      mp.chmap.assign(g.nodes[mp.mmi].c_out, 0);
+      for (int c = 0; c < (int)mp.chmap.size(); ++c) mp.chmap[c] = c;
+      mp.touched_list.clear();
+    }
     for (int l : mp.layers) {
       CowCopy cc;
       cc.mutant = m; cc.layer = l;
@@ -231,7 +243,7 @@ std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>&
     for (int m : kv.second) if (p.mutants[m].recompute) gr.mutants.push_back(m);
     gr.n_recompute = (int)gr.mutants.size();
     for (int m : kv.second) if (!p.mutants[m].recompute) gr.mutants.push_back(m);
-    gr.delta = gr.n_recompute > 0 && node_family(g, gr.mmi) == FAM_VALU;
+    gr.delta = !vanilla && gr.n_recompute > 0 && node_family(g, gr.mmi) == FAM_VALU;
     // virtual mmi output: every consumer is an LDS convolution or a dense layer
     gr.virt = gr.mmi != g.out();
     for (int v = gr.mmi + 1; v < n && gr.virt; ++v)

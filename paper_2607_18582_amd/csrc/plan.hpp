@@ -15,7 +15,7 @@
 namespace mure {
 
 enum Kind { K_INPUT = 0, K_DENSE = 1, K_CONV = 2, K_ADD = 3, K_GAP = 4, K_FLATTEN = 5 };
-enum Op { OP_GF = 0, OP_NEB = 1, OP_NAI = 2, OP_NS = 3 };
+enum Op { OP_GF = 0, OP_NEB = 1, OP_NAI = 2, OP_NS = 3, OP_WS = 4 };
 enum DType { DT_F32 = 0, DT_BF16 = 1 };
 
 struct Node {
@@ -49,7 +49,9 @@ std::string build_graph(Graph& g, int in_h, int in_w, int in_c, int dtype);
 
 struct Record {
   int mutant, op, layer, neuron, partner;
-  int64_t noise_off, noise_len;   // into the concatenated noise array
+  int64_t noise_off, noise_len;   // into the concatenated parameter array (noise or
+                                  // permutation, 4 bytes per entry)
+  int64_t scratch_off = 0;        // weight shuffle: row scratch in the same array
 };
 
 // Kernel family of a CONV2D/DENSE node -- a pure function of its shape, so
@@ -129,7 +131,9 @@ struct Plan {
 std::vector<int> boundary(const Graph& g, int mmi);
 
 // Validates records and builds the plan.  Returns "" or a message.
+// vanilla: no memoization -- every mutant runs from the first layer after
+// the input (exhaustive mutation testing, the paper's baseline).
 std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>& recs,
-                       Plan& plan);
+                       Plan& plan, bool vanilla = false);
 
 }  // namespace mure

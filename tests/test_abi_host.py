@@ -61,6 +61,17 @@ def test_planner_matches_oracle_boundaries_and_ledger(cfg):
     m.close()
 
 
+def test_vanilla_mode_starts_every_mutant_at_the_first_layer():
+    wl = W.make_workload("cfg4", n_inputs=1, n_mutants=40)
+    m = _plan_ctx(wl.model)
+    m.set_option("vanilla", 1)
+    m.apply(wl.mutants)
+    assert {m.mutant_plan(i)[0] for i in range(40)} == {1}
+    st = m.stats()
+    assert st["n_groups"] == 1
+    assert st["macs_memoized"] == st["macs_vanilla"]
+
+
 def test_identity_mutants_have_no_plan():
     wl = W.make_workload("cfg1", n_inputs=1, n_mutants=3)
     m = _plan_ctx(wl.model)
@@ -97,7 +108,13 @@ def test_invalid_calls_are_rejected_atomically():
         m.apply_mutants(4, [0], [3], [1], [2], [2], [None])
     with pytest.raises(B.MureError):         # fuzz noise of the wrong length
         m.apply_mutants(4, [0], [0], [1], [2], [-1], [np.zeros(3, np.float32)])
+    with pytest.raises(B.MureError):         # weight shuffle with a repeated index
+        m.apply_mutants(4, [0], [4], [1], [2], [-1], [None], [np.zeros(25, np.int32)])
+    with pytest.raises(B.MureError):         # weight shuffle of the wrong length
+        m.apply_mutants(4, [0], [4], [1], [2], [-1], [None], [np.arange(5, dtype=np.int32)])
     assert [m.mutant_plan(i) for i in range(4)] == before     # nothing applied
+    m.apply_mutants(4, [0], [4], [1], [2], [-1], [None], [np.arange(25, dtype=np.int32)[::-1].copy()])
+    assert m.mutant_plan(0)[0] == 1
     with pytest.raises(B.MureError) as e:
         m.set_option("chunk_inputs", 100)
     assert e.value.status == B.MURE_E_INVALID

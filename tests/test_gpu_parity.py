@@ -128,3 +128,23 @@ def test_state_machine_errors():
     with pytest.raises(MureError) as e:
         m.run_mutants()
     assert e.value.status == MURE_E_STATE
+
+
+def test_weight_shuffle_operator():
+    """The paper's fourth mutator (weight shuffle) against the oracle."""
+    for cfg, ni, nm in (("cfg2", 300, 40), ("cfg4", 66, 20)):
+        _parity(W.make_workload(cfg, n_inputs=ni, n_mutants=nm,
+                                ops=(W.GF, W.NEB, W.NAI, W.NS, W.WS)))
+
+
+@pytest.mark.parametrize("cfg", ["cfg2", "cfg3", "cfg4"])
+def test_vanilla_mode_equals_memoized_bit_for_bit(cfg):
+    """Theorem 1 on the GPU: running every mutant from the raw input gives
+    exactly the memoized result -- kill bits, score and logits, bit for bit."""
+    wl = W.make_workload(cfg, n_inputs=130, n_mutants=30, ops=(W.GF, W.NEB, W.NAI, W.NS, W.WS))
+    m1, w1, k1, s1 = run_gpu(wl)
+    m2, w2, k2, s2 = run_gpu(wl, vanilla=1)
+    assert np.array_equal(w1, w2) and np.array_equal(k1, k2) and s1 == s2
+    for mid in sample_mutants(m1, wl):
+        assert np.array_equal(m1.get_logits(mid).cpu().numpy(), m2.get_logits(mid).cpu().numpy()), mid
+    assert m2.stats()["n_groups"] == 1

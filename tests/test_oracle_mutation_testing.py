@@ -24,17 +24,18 @@ import oracle as O
 from oracle.memoized import mutated_layers
 from oracle.vanilla import predicted
 import workloads as W
-from workloads.graph import Mutants, GF, NEB, NAI, NS
+from workloads.graph import Mutants, GF, NEB, NAI, NS, WS
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
 def _mutants(records, n_mutants=None):
-    """records: list of (mutant, op, layer, neuron, partner, noise)."""
+    """records: list of (mutant, op, layer, neuron, partner, noise[, perm])."""
     if n_mutants is None:
         n_mutants = 1 + max(r[0] for r in records) if records else 0
     a = lambda k: np.array([r[k] for r in records], np.int32)
-    return Mutants(n_mutants, a(0), a(1), a(2), a(3), a(4), [r[5] for r in records])
+    return Mutants(n_mutants, a(0), a(1), a(2), a(3), a(4), [r[5] for r in records],
+                   [r[6] if len(r) > 6 else None for r in records])
 
 
 # ---------------------------------------------------------------- operators
@@ -59,6 +60,27 @@ def test_operators_on_a_dense_layer_by_hand():
     assert Bs[l][0] == b0[4] and Bs[l][4] == b0[0]
     # the original is untouched
     assert np.array_equal(om.weights[l], w0) and np.array_equal(om.biases[l], b0)
+
+
+def test_weight_shuffle_by_hand():
+    om = O.OracleModel(W.tiny_mlp())
+    w0 = om.weights[1].copy()
+    perm = np.array([5, 0, 4, 1, 3, 2], np.int32)
+    Wm, Bm, _ = O.apply_records(om, _mutants([(0, WS, 1, 2, -1, None, perm)]), 0)
+    assert [Wm[1][2][k] for k in range(6)] == [w0[2][p] for p in perm]
+    assert np.array_equal(np.delete(Wm[1], 2, 0), np.delete(w0, 2, 0))
+    assert np.array_equal(Bm[1], om.biases[1])
+    with pytest.raises(ValueError):                     # not a permutation
+        O.apply_records(om, _mutants([(0, WS, 1, 2, -1, None, np.zeros(6, np.int32))]), 0)
+    # the identity permutation is an identity mutation; a permutation followed
+    # by its inverse too
+    x = W.make_inputs(W.tiny_mlp(), 8, "uniform")
+    inv = np.argsort(perm).astype(np.int32)
+    muts = _mutants([(0, WS, 1, 2, -1, None, np.arange(6, dtype=np.int32)),
+                     (1, WS, 1, 2, -1, None, perm), (1, WS, 1, 2, -1, None, inv)])
+    van = O.run_vanilla(om, x, muts, keep_logits=[0, 1], accumulate="ordered")
+    assert np.array_equal(van.mutant_logits[0], van.logits)
+    assert np.array_equal(van.mutant_logits[1], van.logits)
 
 
 def test_switch_chain_applies_in_record_order():
@@ -159,12 +181,13 @@ def _all_single_mutants(m: W.Model, seed=0):
     for l in m.weighted_nodes():
         node = m.nodes[l]
         for i in range(node.c_out):
-            for op in (GF, NEB, NAI, NS):
+            for op in (GF, NEB, NAI, NS, WS):
                 part = -1
                 if op == NS:
                     part = (i + 1 + int(rng.integers(node.c_out - 1))) % node.c_out
                 eps = (rng.standard_normal(node.fan_in) * 0.1).astype(np.float32) if op == GF else None
-                recs.append((mid, op, l, i, part, eps))
+                perm = rng.permutation(node.fan_in).astype(np.int32) if op == WS else None
+                recs.append((mid, op, l, i, part, eps, perm))
                 mid += 1
     # a few multi-neuron mutants across layers
     wn = m.weighted_nodes()

@@ -7,14 +7,14 @@ application, no kill or score logic), so both the CPU oracle and the GPU path
 can consume it without sharing code.
 """
 from .graph import (INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, KIND_NAMES,
-                    GF, NEB, NAI, NS, OP_NAMES, Node, Model, Mutants, Workload)
+                    GF, NEB, NAI, NS, WS, OP_NAMES, Node, Model, Mutants, Workload)
 from .configs import (CONFIGS, make_workload, make_model, make_inputs,
                       make_mutants, neuron_layers, tiny_mlp, tiny_resnet,
                       tiny_lenet, bf16_bits_to_f32)
 
 __all__ = [
     "INPUT", "DENSE", "CONV2D", "ADD", "GAP", "FLATTEN", "KIND_NAMES",
-    "GF", "NEB", "NAI", "NS", "OP_NAMES", "Node", "Model", "Mutants", "Workload",
+    "GF", "NEB", "NAI", "NS", "WS", "OP_NAMES", "Node", "Model", "Mutants", "Workload",
     "CONFIGS", "make_workload", "make_model", "make_inputs", "make_mutants",
     "neuron_layers", "tiny_mlp", "tiny_resnet", "tiny_lenet", "bf16_bits_to_f32",
 ]

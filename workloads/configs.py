@@ -28,7 +28,7 @@ from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
-from .graph import (INPUT, DENSE, CONV2D, ADD, GAP, GF, NEB, NAI, NS, Node,
+from .graph import (INPUT, DENSE, CONV2D, ADD, GAP, GF, NEB, NAI, NS, WS, Node,
                     Model, Mutants, Workload)
 
 
@@ -216,7 +216,7 @@ def make_mutants(model: Model, n_mutants: int, k: int, mode: str,
     pool_layer = np.concatenate([np.full(model.nodes[l].c_out, l, np.int64) for l in cands])
     pool_neuron = np.concatenate([np.arange(model.nodes[l].c_out, dtype=np.int64) for l in cands])
     sigma = {l: 0.1 * _layer_std(model, l) for l in cands}
-    mid, opl, lay, neu, par, noise = [], [], [], [], [], []
+    mid, opl, lay, neu, par, noise, perms = [], [], [], [], [], [], []
     for m in range(n_mutants):
         op = int(ops[int(rng.integers(len(ops)))])
         if mode == "layer_first":
@@ -239,10 +239,13 @@ def make_mutants(model: Model, n_mutants: int, k: int, mode: str,
             eps = None
             if op == GF:
                 eps = (rng.standard_normal(model.nodes[l].fan_in) * sigma[l]).astype(np.float32)
+            perm = None
+            if op == WS:
+                perm = rng.permutation(model.nodes[l].fan_in).astype(np.int32)
             mid.append(m); opl.append(op); lay.append(l); neu.append(i); par.append(j)
-            noise.append(eps)
+            noise.append(eps); perms.append(perm)
     a = lambda v: np.asarray(v, np.int32)
-    return Mutants(n_mutants, a(mid), a(opl), a(lay), a(neu), a(par), noise)
+    return Mutants(n_mutants, a(mid), a(opl), a(lay), a(neu), a(par), noise, perms)
 
 
 def _k(ratio: float, n_neurons: int) -> int:
@@ -293,9 +296,10 @@ def _candidates(graph: str, model: Model) -> List[int]:
 
 
 def make_workload(cfg: str, n_inputs: Optional[int] = None, n_mutants: Optional[int] = None,
-                  ratio_index: int = 1) -> Workload:
+                  ratio_index: int = 1, ops: Sequence[int] = (GF, NEB, NAI, NS)) -> Workload:
     """Build workload ``cfg`` ("cfg1".."cfg5"); ``n_inputs``/``n_mutants``
-    truncate it (prefix-stable); ``ratio_index`` picks cfg3's ratio."""
+    truncate it (prefix-stable); ``ratio_index`` picks cfg3's ratio; ``ops``
+    the operators drawn (the paper's fourth, weight shuffle, is WS)."""
     c = CONFIGS[cfg]
     model = make_model(c["graph"], c["dtype"], c["bias_std"])
     cands = _candidates(c["graph"], model)
@@ -310,7 +314,7 @@ def make_workload(cfg: str, n_inputs: Optional[int] = None, n_mutants: Optional[
     ni = c["n_inputs"] if n_inputs is None else n_inputs
     nm = c["n_mutants"] if n_mutants is None else n_mutants
     x = make_inputs(model, ni, c["dist"])
-    muts = make_mutants(model, nm, k, c["mode"], cands, variant=variant)
+    muts = make_mutants(model, nm, k, c["mode"], cands, variant=variant, ops=ops)
     name = cfg if "ratios" not in c else f"{cfg}_r{ratio:g}"
     return Workload(name, model, x, muts, c["desc"])
 

@@ -16,10 +16,11 @@ arrays; bf16 models hold uint16 arrays of bfloat16 bit patterns.  Biases are
 float32 ``[C_out]``.
 
 Mutation records (one per mutated neuron, Section 3.1 and Section 4):
-``op`` in {GF, NEB, NAI, NS}; ``layer`` is a DENSE/CONV2D node index;
+``op`` in {GF, NEB, NAI, NS, WS}; ``layer`` is a DENSE/CONV2D node index;
 ``neuron`` an output channel (a neuron of a conv layer is one filter, Section
 2.1); ``partner`` the other neuron of a switch; GF records carry their noise,
-``fan_in`` float32 values in the row order of ``W[neuron]``.
+``fan_in`` float32 values in the row order of ``W[neuron]``; WS records a
+permutation of ``0..fan_in-1``.
 """
 from __future__ import annotations
 
@@ -33,9 +34,9 @@ KIND_NAMES = {INPUT: "input", DENSE: "dense", CONV2D: "conv2d", ADD: "add",
               GAP: "gap", FLATTEN: "flatten"}
 
 # mutation operators (Section 3.1): Gaussian fuzzing, neuron effect block,
-# neuron activation inverse, neuron switch
-GF, NEB, NAI, NS = 0, 1, 2, 3
-OP_NAMES = {GF: "GF", NEB: "NEB", NAI: "NAI", NS: "NS"}
+# neuron activation inverse, neuron switch, weight shuffle
+GF, NEB, NAI, NS, WS = 0, 1, 2, 3, 4
+OP_NAMES = {GF: "GF", NEB: "NEB", NAI: "NAI", NS: "NS", WS: "WS"}
 
 
 @dataclass
@@ -95,7 +96,11 @@ class Mutants:
     layer: np.ndarray               # int32 [R]
     neuron: np.ndarray              # int32 [R]
     partner: np.ndarray             # int32 [R], -1 unless NS
-    noise: List[Optional[np.ndarray]] = field(default_factory=list)  # per record
+    noise: List[Optional[np.ndarray]] = field(default_factory=list)  # per record (GF)
+    perm: List[Optional[np.ndarray]] = field(default_factory=list)   # per record (WS)
+
+    def perm_of(self, r: int):
+        return self.perm[r] if self.perm else None
 
     @property
     def n_records(self) -> int:
@@ -109,7 +114,8 @@ class Mutants:
         keep = np.nonzero(self.mutant_id < n)[0]
         return Mutants(n, self.mutant_id[keep].copy(), self.op[keep].copy(),
                        self.layer[keep].copy(), self.neuron[keep].copy(),
-                       self.partner[keep].copy(), [self.noise[i] for i in keep])
+                       self.partner[keep].copy(), [self.noise[i] for i in keep],
+                       [self.perm_of(i) for i in keep])
 
     def select(self, ids) -> "Mutants":
         """Mutants ``ids`` renumbered 0..len(ids)-1, records in their order."""
@@ -122,7 +128,7 @@ class Mutants:
         mid = np.array([n for n, _ in rows], dtype=np.int32)
         return Mutants(len(ids), mid, self.op[idx].copy(), self.layer[idx].copy(),
                        self.neuron[idx].copy(), self.partner[idx].copy(),
-                       [self.noise[i] for i in idx])
+                       [self.noise[i] for i in idx], [self.perm_of(i) for i in idx])
 
 
 @dataclass
