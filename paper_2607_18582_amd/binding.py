@@ -201,7 +201,8 @@ class Mure:
         offs = np.concatenate([[0], np.cumsum(lens)[:-1]]) if R else np.zeros(0, np.int64)
         recs["noise"][:R] = np.where(lens > 0, pool.ctypes.data + 4 * offs, 0)
         recs["noise_len"][:R] = lens
-        perm = perm if perm is not None else [None] * R
+        if perm is None or len(perm) == 0:
+            perm = [None] * R
         plens = np.array([0 if q is None else len(q) for q in perm], np.int64)
         ppool = np.concatenate([np.asarray(q, np.int32) for q in perm if q is not None] or
                                [np.zeros(1, np.int32)])

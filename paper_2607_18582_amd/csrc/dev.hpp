@@ -10,6 +10,7 @@ namespace mure {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));   // 16 raw bytes in registers
 typedef uint16_t bf16_t;   // bfloat16 bit pattern
 
 __device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
@@ -50,6 +51,17 @@ __device__ __forceinline__ void fast_divmod(int q, int d, float inv, int& quo, i
   if (r < 0) { --t; r += d; } else if (r >= d) { ++t; r -= d; }
   quo = t;
   rem = r;
+}
+
+// n / d and n % d through the multiply-high divider of DivU32
+__device__ __forceinline__ uint32_t divu(const DivU32& v, uint32_t n) {
+  const uint32_t t = __umulhi(v.mul, n);
+  return (t + ((n - t) >> v.sh1)) >> v.sh2;
+}
+__device__ __forceinline__ void divmodu(const DivU32& v, uint32_t n, int& quo, int& rem) {
+  const uint32_t q = divu(v, n);
+  quo = (int)q;
+  rem = (int)(n - q * v.d);
 }
 
 // element (row r = slot*nx + xi, pixel, channel c) of a virtual input

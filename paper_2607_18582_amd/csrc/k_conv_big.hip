@@ -17,7 +17,14 @@ namespace {
 constexpr int BIG_BK = 64, BIG_LD = BIG_BK + 8;   // padded LDS rows (bf16)
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N>
+// Zero bytes that out-of-image taps and rows past the end read instead of the
+// input, so every gather is an unconditional 16-byte load.
+static __device__ __attribute__((aligned(16))) v4u g_zero_page[16] = {};
+
+// TAP64: C_in % 64 == 0, so every 64-wide k chunk lies inside one filter tap
+// and each thread's 4 vectors are 64 contiguous bytes of one input pixel (one
+// bounds check, one address per chunk).
+template <int BM, int BN, int WAVES_M, int WAVES_N, bool TAP64>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N)
 void conv_big_kernel(ConvArgs a) {
   constexpr int THREADS = 64 * WAVES_M * WAVES_N;
@@ -34,77 +41,96 @@ void conv_big_kernel(ConvArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WAVES_M, wn = wave / WAVES_M;
   const int slot = a.slot0 + (int)blockIdx.y;
-  const int64_t Mslot = (int64_t)a.nx * a.P;
-  const int64_t m0 = (int64_t)blockIdx.x * BM;
+  const int Mslot = a.nx * a.P;                        // < 2^31 (checked by the launcher)
+  const int m0 = (int)blockIdx.x * BM;
   const int n0 = (int)blockIdx.z * BN;
   const bf16_t* __restrict__ Wt = reinterpret_cast<const bf16_t*>(a.wtab[slot]);
+  const bf16_t* const zp = reinterpret_cast<const bf16_t*>(g_zero_page);
   const int kvec = (a.K + 7) / 8;
-  for (int v = tid; v < kvec; v += THREADS) {
-    const int k = v * 8, ci = k % a.C, t = k / a.C;
-    const int dy = t / a.kw, dx = t % a.kw;
-    ktab[v] = ((dy * a.W + dx) * a.C + ci) | (dy << 24) | (dx << 28);
+  if constexpr (!TAP64) {
+    for (int v = tid; v < kvec; v += THREADS) {
+      const int k = v * 8, ci = k % a.C, t = k / a.C;
+      const int dy = t / a.kw, dx = t % a.kw;
+      ktab[v] = ((dy * a.W + dx) * a.C + ci) | (dy << 24) | (dx << 28);
+    }
   }
 
-  // the A rows this thread gathers: rows arow + (THREADS/2)*r
+  // the A rows this thread gathers: rows arow + RSTEP*r, k half ahalf (a wave
+  // covers 64 consecutive rows of one half, so its 16-byte LDS stores hit
+  // distinct banks)
   constexpr int RSTEP = THREADS / 2;
-  const int arow = tid >> 1, ahalf = tid & 1;
+  const int arow = tid % RSTEP, ahalf = tid / RSTEP;
   bool mvalid[ROWS_PER_THREAD];
   int iy0[ROWS_PER_THREAD], ix0[ROWS_PER_THREAD];
   const bf16_t* inrow[ROWS_PER_THREAD];
 #pragma unroll
   for (int r = 0; r < ROWS_PER_THREAD; ++r) {
-    const int64_t m = m0 + arow + RSTEP * r;
+    const int m = m0 + arow + RSTEP * r;
     mvalid[r] = m < Mslot;
-    iy0[r] = ix0[r] = 0;
-    inrow[r] = reinterpret_cast<const bf16_t*>(a.in.p);
+    iy0[r] = ix0[r] = -(1 << 20);                    // rows past the end: every tap out of the image
+    inrow[r] = zp;
     if (mvalid[r]) {
-      const int xi = (int)(m / a.P), p = (int)(m % a.P);
-      int oy, ox;
+      int xi, p, oy, ox;
+      divmodu(a.dP, (uint32_t)m, xi, p);
       if (a.pool) {
-        const int q = p >> 2, sub = p & 3;
-        oy = 2 * (q / a.Wp) + (sub >> 1);
-        ox = 2 * (q % a.Wp) + (sub & 1);
+        int qy, qx;
+        divmodu(a.dWp, (uint32_t)(p >> 2), qy, qx);
+        oy = 2 * qy + ((p >> 1) & 1);
+        ox = 2 * qx + (p & 1);
       } else {
-        oy = p / a.Wc;
-        ox = p % a.Wc;
+        divmodu(a.dWc, (uint32_t)p, oy, ox);
       }
       iy0[r] = oy * a.stride - a.pad;
       ix0[r] = ox * a.stride - a.pad;
-      inrow[r] += row_index(a.in.mode, (int64_t)slot * a.nx + xi, a.nx, a.x0) * a.in.row_elems +
-                  ((int64_t)iy0[r] * a.W + ix0[r]) * a.C;
+      inrow[r] = reinterpret_cast<const bf16_t*>(a.in.p) +
+                 row_index(a.in.mode, (int64_t)slot * a.nx + xi, a.nx, a.x0) * a.in.row_elems +
+                 ((int64_t)iy0[r] * a.W + ix0[r]) * a.C;
     }
   }
   __syncthreads();
 
-  uint4 ra[ROWS_PER_THREAD][4], rb[BPT];
+  v4u ra[ROWS_PER_THREAD][4], rb[BPT];
   auto load_chunk = [&](int kc) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int v = (kc >> 3) + ahalf * 4 + j;
-      int code = 0, dy = 0, dx = 0;
-      if (v < kvec) {
-        code = ktab[v];
-        dy = (code >> 24) & 15;
-        dx = (code >> 28) & 15;
-      }
+    if constexpr (TAP64) {
+      // chunk kc: tap t = kc / C (uniform), channels ci0 .. ci0 + 63
+      const int t = kc / a.C, ci0 = kc - t * a.C;
+      const int dy = t / a.kw, dx = t - dy * a.kw;
+      const int off = (dy * a.W + dx) * a.C + ci0 + ahalf * 32;
 #pragma unroll
       for (int r = 0; r < ROWS_PER_THREAD; ++r) {
-        uint4 val = make_uint4(0, 0, 0, 0);
         const int iy = iy0[r] + dy, ix = ix0[r] + dx;
-        if (mvalid[r] && v < kvec && iy >= 0 && iy < a.H && ix >= 0 && ix < a.W)
-          val = *reinterpret_cast<const uint4*>(inrow[r] + (code & 0xFFFFFF));
-        ra[r][j] = val;
+        const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+        const v4u* src = reinterpret_cast<const v4u*>(ok ? inrow[r] + off : zp);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) ra[r][j] = src[j];
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int v = (kc >> 3) + ahalf * 4 + j;
+        int code = 0, dy = -(1 << 20), dx = 0;       // k past the end: out of the image
+        if (v < kvec) {
+          code = ktab[v];
+          dy = (code >> 24) & 15;
+          dx = (code >> 28) & 15;
+        }
+#pragma unroll
+        for (int r = 0; r < ROWS_PER_THREAD; ++r) {
+          const int iy = iy0[r] + dy, ix = ix0[r] + dx;
+          const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+          ra[r][j] = *reinterpret_cast<const v4u*>(ok ? inrow[r] + (code & 0xFFFFFF) : zp);
+        }
       }
     }
 #pragma unroll
     for (int j = 0; j < BPT; ++j) {
       const int i = tid + j * THREADS;
-      uint4 val = make_uint4(0, 0, 0, 0);
+      v4u val = v4u{0u, 0u, 0u, 0u};
       if (i < BVEC) {
         const int row = i / (BK / 8), kv = i % (BK / 8);
         const int k = kc + kv * 8;
         if (n0 + row < a.Cout && k < a.K)
-          val = *reinterpret_cast<const uint4*>(Wt + (int64_t)(n0 + row) * a.K + k);
+          val = *reinterpret_cast<const v4u*>(Wt + (int64_t)(n0 + row) * a.K + k);
       }
       rb[j] = val;
     }
@@ -114,13 +140,13 @@ void conv_big_kernel(ConvArgs a) {
     for (int r = 0; r < ROWS_PER_THREAD; ++r)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        *reinterpret_cast<uint4*>(&As[(arow + RSTEP * r) * LD + (ahalf * 4 + j) * 8]) = ra[r][j];
+        *reinterpret_cast<v4u*>(&As[(arow + RSTEP * r) * LD + (ahalf * 4 + j) * 8]) = ra[r][j];
 #pragma unroll
     for (int j = 0; j < BPT; ++j) {
       const int i = tid + j * THREADS;
       if (i < BVEC) {
         const int row = i / (BK / 8), kv = i % (BK / 8);
-        *reinterpret_cast<uint4*>(&Bs[row * LD + kv * 8]) = rb[j];
+        *reinterpret_cast<v4u*>(&Bs[row * LD + kv * 8]) = rb[j];
       }
     }
   };
@@ -156,14 +182,23 @@ void conv_big_kernel(ConvArgs a) {
 
   const float* __restrict__ bias = a.btab[slot];
 #pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int n = n0 + wn * WN + j * 16 + (lane & 15);
-    if (n >= a.Cout) continue;
-    const float bv = bias[n];
+  for (int i = 0; i < TM; ++i) {
+    const int mb = m0 + wm * WM + i * 16 + (lane >> 4) * 4;
+    if (mb >= Mslot) continue;
+    // the 4 rows of a lane are one pool window, or 4 consecutive pixels of one
+    // input (P % 4 == 0)
+    int xo, pb;
+    divmodu(a.dP, (uint32_t)mb, xo, pb);
+    const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xo, a.nx, a.x0);
+    const bf16_t* sp = nullptr;
+    if (a.add_mode)
+      sp = reinterpret_cast<const bf16_t*>(a.skip.p) +
+           row_index(a.skip.mode, (int64_t)slot * a.nx + xo, a.nx, a.x0) * a.skip.row_elems;
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      const int64_t mb = m0 + wm * WM + i * 16 + (lane >> 4) * 4;
-      if (mb >= Mslot) continue;
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + wn * WN + j * 16 + (lane & 15);
+      if (n >= a.Cout) continue;
+      const float bv = bias[n];
       float v[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -172,38 +207,29 @@ void conv_big_kernel(ConvArgs a) {
       }
       if (a.pool) {
         const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-        const int xo = (int)(mb / a.P);
-        const int q = (int)(mb % a.P) >> 2;
-        const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xo, a.nx, a.x0);
-        store_out<bf16_t>(a.out, a.out_f32, ro * a.out_row + (int64_t)q * a.Cout + n, mx);
-      } else {
-        const int xo = (int)(mb / a.P);
-        const int pp = (int)(mb % a.P);
-        // the 4 rows of a lane are consecutive pixels of one input (P % 4 == 0)
-        const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xo, a.nx, a.x0);
-        if (a.add_mode) {
-          // conv_b's output (rounded) + the shortcut, in float32, then ReLU
-          const bf16_t* sp = reinterpret_cast<const bf16_t*>(a.skip.p) +
-                             row_index(a.skip.mode, (int64_t)slot * a.nx + xo, a.nx, a.x0) * a.skip.row_elems;
-          const int cs = a.add_mode == 1 ? n : n - (a.Cout - a.Cs) / 2;
+        store_out<bf16_t>(a.out, a.out_f32, ro * a.out_row + (int64_t)(pb >> 2) * a.Cout + n, mx);
+      } else if (a.add_mode) {
+        // conv_b's output (rounded) + the shortcut, in float32, then ReLU
+        const int cs = a.add_mode == 1 ? n : n - (a.Cout - a.Cs) / 2;
+        int y = 0, x = 0;
+        if (a.add_mode == 2) divmodu(a.dWc, (uint32_t)pb, y, x);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            float sv = 0.f;
-            if (a.add_mode == 1) {
-              sv = bf2f(sp[(int64_t)(pp + e) * a.Cout + n]);
-            } else if (cs >= 0 && cs < a.Cs) {
-              const int y = (pp + e) / a.Wc, x = (pp + e) % a.Wc;
-              sv = bf2f(sp[((int64_t)(2 * y) * a.Ws + 2 * x) * a.Cs + cs]);
-            }
-            float t = bf2f(f2bf(v[e])) + sv;
-            if (a.add_relu) t = fmaxf(t, 0.f);
-            store_out<bf16_t>(a.out, a.add_out_f32, ro * a.out_row + (int64_t)(pp + e) * a.Cout + n, t);
+        for (int e = 0; e < 4; ++e) {
+          float sv = 0.f;
+          if (a.add_mode == 1) {
+            sv = bf2f(sp[(int64_t)(pb + e) * a.Cout + n]);
+          } else if (cs >= 0 && cs < a.Cs) {
+            sv = bf2f(sp[((int64_t)(2 * y) * a.Ws + 2 * x) * a.Cs + cs]);
           }
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            store_out<bf16_t>(a.out, a.out_f32, ro * a.out_row + (int64_t)(pp + e) * a.Cout + n, v[e]);
+          if (a.add_mode == 2 && ++x == a.Wc) { x = 0; ++y; }
+          float t = bf2f(f2bf(v[e])) + sv;
+          if (a.add_relu) t = fmaxf(t, 0.f);
+          store_out<bf16_t>(a.out, a.add_out_f32, ro * a.out_row + (int64_t)(pb + e) * a.Cout + n, t);
         }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          store_out<bf16_t>(a.out, a.out_f32, ro * a.out_row + (int64_t)(pb + e) * a.Cout + n, v[e]);
       }
     }
   }
@@ -211,30 +237,41 @@ void conv_big_kernel(ConvArgs a) {
 
 int conv_big_bn(int cout) { return cout <= 16 ? 16 : cout <= 32 ? 32 : cout <= 64 ? 64 : 128; }
 
-hipError_t launch_conv_big(const ConvArgs& a, int nslots, hipStream_t s) {
-  if (nslots <= 0 || a.nx <= 0) return hipSuccess;
-  if (a.C % 8 || a.K > 8 * 1024 || a.P % 4) return hipErrorInvalidValue;
-  const int bn = conv_big_bn(a.Cout);
-  // tile: 0 automatic, 1 = 128 rows x BN (4 waves), 2 = 256 rows x BN (8 waves of 64 x 32..64)
-  const int bm = a.tile == 1 ? 128 : 256;
-  const int64_t Mslot = (int64_t)a.nx * a.P;
-  dim3 grid((unsigned)((Mslot + bm - 1) / bm), (unsigned)nslots, (unsigned)((a.Cout + bn - 1) / bn));
+template <bool TAP64>
+static hipError_t launch_big(const ConvArgs& a, dim3 grid, int bm, int bn, hipStream_t s) {
   if (bm == 128) {
     switch (bn) {
-      case 16: hipLaunchKernelGGL((conv_big_kernel<128, 16, 4, 1>), grid, dim3(256), 0, s, a); break;
-      case 32: hipLaunchKernelGGL((conv_big_kernel<128, 32, 4, 1>), grid, dim3(256), 0, s, a); break;
-      case 64: hipLaunchKernelGGL((conv_big_kernel<128, 64, 4, 1>), grid, dim3(256), 0, s, a); break;
-      default: hipLaunchKernelGGL((conv_big_kernel<128, 128, 2, 2>), grid, dim3(256), 0, s, a); break;
+      case 16: hipLaunchKernelGGL((conv_big_kernel<128, 16, 4, 1, TAP64>), grid, dim3(256), 0, s, a); break;
+      case 32: hipLaunchKernelGGL((conv_big_kernel<128, 32, 4, 1, TAP64>), grid, dim3(256), 0, s, a); break;
+      case 64: hipLaunchKernelGGL((conv_big_kernel<128, 64, 4, 1, TAP64>), grid, dim3(256), 0, s, a); break;
+      default: hipLaunchKernelGGL((conv_big_kernel<128, 128, 2, 2, TAP64>), grid, dim3(256), 0, s, a); break;
     }
   } else {
     switch (bn) {
-      case 16: hipLaunchKernelGGL((conv_big_kernel<256, 16, 8, 1>), grid, dim3(512), 0, s, a); break;
-      case 32: hipLaunchKernelGGL((conv_big_kernel<256, 32, 8, 1>), grid, dim3(512), 0, s, a); break;
-      case 64: hipLaunchKernelGGL((conv_big_kernel<256, 64, 4, 2>), grid, dim3(512), 0, s, a); break;
-      default: hipLaunchKernelGGL((conv_big_kernel<256, 128, 4, 2>), grid, dim3(512), 0, s, a); break;
+      case 16: hipLaunchKernelGGL((conv_big_kernel<256, 16, 8, 1, TAP64>), grid, dim3(512), 0, s, a); break;
+      case 32: hipLaunchKernelGGL((conv_big_kernel<256, 32, 8, 1, TAP64>), grid, dim3(512), 0, s, a); break;
+      case 64: hipLaunchKernelGGL((conv_big_kernel<256, 64, 4, 2, TAP64>), grid, dim3(512), 0, s, a); break;
+      default: hipLaunchKernelGGL((conv_big_kernel<256, 128, 4, 2, TAP64>), grid, dim3(512), 0, s, a); break;
     }
   }
   return hipGetLastError();
+}
+
+hipError_t launch_conv_big(const ConvArgs& a0, int nslots, hipStream_t s) {
+  if (nslots <= 0 || a0.nx <= 0) return hipSuccess;
+  if (a0.C % 8 || a0.K > 8 * 1024 || a0.P % 4 || (int64_t)a0.nx * a0.P + 256 >= INT32_MAX)
+    return hipErrorInvalidValue;
+  ConvArgs a = a0;
+  a.dP = make_divu32((uint32_t)a.P);
+  a.dWp = make_divu32((uint32_t)std::max(1, a.Wp));
+  a.dWc = make_divu32((uint32_t)std::max(1, a.Wc));
+  const int bn = conv_big_bn(a.Cout);
+  // tile: 0 automatic, 1 = 128 rows x BN (4 waves), 2 = 256 rows x BN (8 waves of 64 x 32..64)
+  const int bm = a.tile == 2 ? 256 : 128;
+  const int64_t Mslot = (int64_t)a.nx * a.P;
+  dim3 grid((unsigned)((Mslot + bm - 1) / bm), (unsigned)nslots, (unsigned)((a.Cout + bn - 1) / bn));
+  if (a.C % 64 == 0) return launch_big<true>(a, grid, bm, bn, s);
+  return launch_big<false>(a, grid, bm, bn, s);
 }
 
 }  // namespace mure

@@ -24,26 +24,29 @@ namespace mure {
 template <int BN>
 __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap, int kpad, int iters) {
   extern __shared__ __attribute__((aligned(16))) float smem[];
+  constexpr int KST = BN == 16 ? 16 : BN + 16;   // conv_lds_kst
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int slot = a.slot0 + (int)blockIdx.y;
   const int n0 = (int)blockIdx.z * BN;
-  const int64_t Mslot = (int64_t)a.nx * a.P;
+  const int Mslot = a.nx * a.P;                  // < 2^31 (checked by the launcher)
   const int Hp2 = a.H + 2 * a.pad, Wp2 = a.W + 2 * a.pad;
   const int img = Hp2 * Wp2 * a.C;
   const bool virt = a.vin.chmap != nullptr;
   float* imgs = smem;
-  float* Ws = imgs + (int64_t)nimg_cap * img;
-  int* koff = reinterpret_cast<int*>(Ws + BN * kpad);
-  int* chrow = koff + kpad;
+  float* Ws = imgs + (int64_t)nimg_cap * img;    // [kpad + 16][KST], k-major, zero padded
+  int* koff = reinterpret_cast<int*>(Ws + KST * (kpad + 16));  // [kpad + 32]
+  int* chrow = koff + kpad + 32;
   const float* __restrict__ X = reinterpret_cast<const float*>(a.in.p);
   const float* __restrict__ Wt = reinterpret_cast<const float*>(a.wtab[slot]);
   const float* __restrict__ bias = a.btab[slot];
 
-  for (int e = tid; e < BN * kpad; e += 256) {
-    const int n = e / kpad, k = e % kpad;
-    Ws[e] = (n0 + n < a.Cout && k < a.K) ? Wt[(int64_t)(n0 + n) * a.K + k] : 0.f;
+  // weights: read along k (coalesced), stored k-major
+  for (int n = 0; n < BN; ++n) {
+    const bool nv = n0 + n < a.Cout;
+    const float* wr = Wt + (int64_t)(n0 + n) * a.K;
+    for (int k = tid; k < kpad + 16; k += 256) Ws[k * KST + n] = (nv && k < a.K) ? wr[k] : 0.f;
   }
-  for (int k = tid; k < kpad; k += 256) {
+  for (int k = tid; k < kpad + 32; k += 256) {
     int o = 0;
     if (k < a.K) {
       const int ci = k % a.C, t = k / a.C;
@@ -72,10 +75,10 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
   }
 
   for (int it = 0; it < iters; ++it) {
-    const int64_t m0 = ((int64_t)blockIdx.x * iters + it) * 256;
+    const int m0 = ((int)blockIdx.x * iters + it) * 256;
     if (m0 >= Mslot) break;
-    const int xi_first = (int)(m0 / a.P);
-    const int xi_last = (int)min((int64_t)a.nx - 1, (m0 + 255) / a.P);
+    const int xi_first = (int)divu(a.dP, (uint32_t)m0);
+    const int xi_last = min(a.nx - 1, (int)divu(a.dP, (uint32_t)(m0 + 255)));
     const int nimg = xi_last - xi_first + 1;
     __syncthreads();                               // previous piece done with imgs
     if (virt && a.pad == 0 && (img & 3) == 0 && a.C <= 64) {
@@ -88,13 +91,15 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
       if (nc > 0) {
         __syncthreads();
         const int HW = a.H * a.W;
-        for (int e = tid; e < nimg * HW * nc; e += 256) {
-          const int j = e % nc, t = e / nc;
-          const int pix = t % HW, ii = t / HW;
-          const int c = chg[j];
+        for (int e = tid; e < nimg * HW; e += 256) {
+          int ii, pix;
+          divmodu(a.dHW, (uint32_t)e, ii, pix);
           const int xi = xi_first + ii;
-          imgs[(ii * HW + pix) * a.C + c] =
-              virtual_elem<float>(a.vin, chrow, (int64_t)slot * a.nx + xi, xi, a.x0, pix, c);
+          const int64_t r = (int64_t)slot * a.nx + xi;
+          for (int j = 0; j < nc; ++j) {
+            const int c = chg[j];
+            imgs[e * a.C + c] = virtual_elem<float>(a.vin, chrow, r, xi, a.x0, pix, c);
+          }
         }
       }
     } else if (!virt && a.pad == 0 && (img & 3) == 0 && a.in.row_elems == img) {
@@ -131,22 +136,22 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
     }
     __syncthreads();
 
-    const int64_t mw = m0 + wave * 64;
+    const int mw = m0 + wave * 64;
     int base[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int64_t m = mw + i * 16 + (lane & 15);
+      const int m = mw + i * 16 + (lane & 15);
       int b = 0;
       if (m < Mslot) {
-        const int xi = (int)(m / a.P), p = (int)(m % a.P);
-        int oy, ox;
+        int xi, p, oy, ox;
+        divmodu(a.dP, (uint32_t)m, xi, p);
         if (a.pool) {
-          const int q = p >> 2, sub = p & 3;
-          oy = 2 * (q / a.Wp) + (sub >> 1);
-          ox = 2 * (q % a.Wp) + (sub & 1);
+          int qy, qx;
+          divmodu(a.dWp, (uint32_t)(p >> 2), qy, qx);
+          oy = 2 * qy + ((p >> 1) & 1);
+          ox = 2 * qx + (p & 1);
         } else {
-          oy = p / a.Wc;
-          ox = p % a.Wc;
+          divmodu(a.dWc, (uint32_t)p, oy, ox);
         }
         b = (xi - xi_first) * img + (oy * a.stride * Wp2 + ox * a.stride) * a.C;
       }
@@ -157,29 +162,60 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
-    for (int ks = 0; ks < kpad; ks += 4) {
-      const int k = ks + (lane >> 4);
-      const int ko = koff[k];
-      float bw[TN], av[4];
-#pragma unroll
-      for (int j = 0; j < TN; ++j) bw[j] = Ws[(j * 16 + (lane & 15)) * kpad + k];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) av[i] = imgs[base[i] + ko];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bw[j], acc[i][j], 0, 0, 0);
+    const float* wl = Ws + (lane >> 4) * KST + (lane & 15);
+    const int* kl = koff + (lane >> 4);
+    // software pipeline over steps of 8 k with two register sets: the reads
+    // of step s + 1 are issued before the MFMAs of step s, and the offsets
+    // of step s + 2 before those (the padded table rows past kpad are zero)
+    float a0[2][4], b0[2][TN], a1[2][4], b1[2][TN];
+    int ko[2];
+#define MURE_LDS_READ(A, B, KB, O0, O1)                                         \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                            \
+      A[0][i] = imgs[base[i] + (O0)];                                          \
+      A[1][i] = imgs[base[i] + (O1)];                                          \
+    }                                                                          \
+    _Pragma("unroll") for (int j = 0; j < TN; ++j) {                           \
+      B[0][j] = wl[(KB) * KST + j * 16];                                       \
+      B[1][j] = wl[((KB) + 4) * KST + j * 16];                                 \
     }
+#define MURE_LDS_MFMA(A, B)                                                    \
+    _Pragma("unroll") for (int h = 0; h < 2; ++h)                              \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i)                              \
+    _Pragma("unroll") for (int j = 0; j < TN; ++j)                             \
+      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[h][i], B[h][j], acc[i][j], 0, 0, 0);
+    MURE_LDS_READ(a0, b0, 0, kl[0], kl[4])
+    ko[0] = kl[8];
+    ko[1] = kl[12];
+    int k8 = 0;
+    for (; k8 + 16 <= kpad; k8 += 16) {
+      MURE_LDS_READ(a1, b1, k8 + 8, ko[0], ko[1])
+      ko[0] = kl[k8 + 16];
+      ko[1] = kl[k8 + 20];
+      __builtin_amdgcn_sched_barrier(0);
+      MURE_LDS_MFMA(a0, b0)
+      __builtin_amdgcn_sched_barrier(0);
+      MURE_LDS_READ(a0, b0, k8 + 16, ko[0], ko[1])
+      ko[0] = kl[k8 + 24];
+      ko[1] = kl[k8 + 28];
+      __builtin_amdgcn_sched_barrier(0);
+      MURE_LDS_MFMA(a1, b1)
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (k8 < kpad) { MURE_LDS_MFMA(a0, b0) }        // kpad % 16 == 8: the last step
+#undef MURE_LDS_READ
+#undef MURE_LDS_MFMA
 
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int n = n0 + j * 16 + (lane & 15);
-      if (n >= a.Cout) continue;
+    for (int i = 0; i < 4; ++i) {
+      const int mb = mw + i * 16 + (lane >> 4) * 4;
+      if (mb >= Mslot) continue;
+      int xo, pb;
+      divmodu(a.dP, (uint32_t)mb, xo, pb);
+      const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xo, a.nx, a.x0);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int64_t mb = mw + i * 16 + (lane >> 4) * 4;
-        if (mb >= Mslot) continue;
+      for (int j = 0; j < TN; ++j) {
+        const int n = n0 + j * 16 + (lane & 15);
+        if (n >= a.Cout) continue;
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -188,19 +224,20 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
         }
         if (a.pool) {
           const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-          const int xo = (int)(mb / a.P);
-          const int q = (int)(mb % a.P) >> 2;
-          const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xo, a.nx, a.x0);
-          store_out<float>(a.out, a.out_f32, ro * a.out_row + (int64_t)q * a.Cout + n, mx);
+          store_out<float>(a.out, a.out_f32, ro * a.out_row + (int64_t)(pb >> 2) * a.Cout + n, mx);
         } else {
+          // the lane's 4 rows may cross into the next input when P % 4 != 0
+          int xe = xo, pe = pb;
+          int64_t re = ro;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const int64_t mm = mb + e;
-            if (mm >= Mslot) break;
-            const int xo = (int)(mm / a.P);
-            const int pp = (int)(mm % a.P);
-            const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xo, a.nx, a.x0);
-            store_out<float>(a.out, a.out_f32, ro * a.out_row + (int64_t)pp * a.Cout + n, v[e]);
+            if (mb + e >= Mslot) break;
+            if (pe == a.P) {
+              ++xe; pe = 0;
+              re = row_index(a.out_mode, (int64_t)slot * a.nx + xe, a.nx, a.x0);
+            }
+            store_out<float>(a.out, a.out_f32, re * a.out_row + (int64_t)pe * a.Cout + n, v[e]);
+            ++pe;
           }
         }
       }
@@ -208,11 +245,17 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
   }
 }
 
-hipError_t launch_conv_lds(const ConvArgs& a, int nslots, hipStream_t s) {
-  if (nslots <= 0 || a.nx <= 0) return hipSuccess;
-  if (a.Cout > 64) return hipErrorInvalidValue;
+hipError_t launch_conv_lds(const ConvArgs& a0, int nslots, hipStream_t s) {
+  if (nslots <= 0 || a0.nx <= 0) return hipSuccess;
+  if (a0.Cout > 64 || (int64_t)a0.nx * a0.P + 256 >= INT32_MAX) return hipErrorInvalidValue;
+  if (a0.pool && a0.P % 4) return hipErrorInvalidValue;
+  ConvArgs a = a0;
+  a.dP = make_divu32((uint32_t)a.P);
+  a.dWp = make_divu32((uint32_t)std::max(1, a.Wp));
+  a.dWc = make_divu32((uint32_t)std::max(1, a.Wc));
+  a.dHW = make_divu32((uint32_t)std::max(1, a.H * a.W));
   const int bn = conv_lds_bn(a.Cout);
-  const int kpad = (a.K + 3) / 4 * 4;
+  const int kpad = (a.K + 7) / 8 * 8;
   const int cap = conv_lds_nimg_cap(a.P);
   const size_t lds = (size_t)conv_lds_bytes(a.H, a.W, a.C, a.pad, a.P, a.Cout, a.K);
   if (lds > 64 * 1024) return hipErrorInvalidValue;

@@ -14,6 +14,28 @@ namespace mure {
 
 enum { MODE_BUF = 0, MODE_CACHE = 1 };
 
+// Unsigned 32-bit division by a divisor fixed at launch, as a multiply-high,
+// add and shifts (Granlund and Montgomery, "Division by invariant integers
+// using multiplication", PLDI 1994, Figure 4.1): exact for every 32-bit
+// dividend.  With l = ceil(log2 d) and mul = floor(2^32 (2^l - d) / d) + 1,
+//   t = mulhi(mul, n),  n / d = (t + ((n - t) >> min(l, 1))) >> max(l - 1, 0).
+struct DivU32 {
+  uint32_t d = 1, mul = 1;
+  int sh1 = 0, sh2 = 0;
+};
+
+inline DivU32 make_divu32(uint32_t d) {
+  DivU32 v;
+  if (d == 0) return v;                      // callers never divide by 0; keep d = 1
+  int l = 0;
+  while (l < 32 && (uint64_t(1) << l) < d) ++l;
+  v.d = d;
+  v.mul = (uint32_t)(((uint64_t(1) << 32) * ((uint64_t(1) << l) - d)) / d + 1);
+  v.sh1 = l < 1 ? l : 1;
+  v.sh2 = l > 1 ? l - 1 : 0;
+  return v;
+}
+
 struct TensorArg {
   const void* p = nullptr;
   int mode = MODE_BUF;
@@ -58,6 +80,8 @@ struct ConvArgs {
   TensorArg skip;
   int Hs = 0, Ws = 0, Cs = 0;            // skip geometry
   int tile = 0;                          // tiled kernel's block shape (0 automatic)
+  // filled by the launchers: dividers by P, Wp, Wc and H*W
+  DivU32 dP, dWp, dWc, dHW;
 };
 
 // DENSE on MFMA: out[r][n] = sum_k in[r][k] * W[n][k] + b[n] (k in increasing

@@ -81,6 +81,20 @@ def test_identity_mutants_have_no_plan():
     assert m.stats()["n_identity_mutants"] == 2
 
 
+def test_records_without_a_permutation_list_are_accepted():
+    # Mutants built field by field carry an empty perm list (no WS records)
+    wl = W.make_workload("cfg1", n_inputs=1, n_mutants=4)
+    mu = wl.mutants
+    bare = W.Mutants(mu.n_mutants, mu.mutant_id, mu.op, mu.layer, mu.neuron, mu.partner,
+                     list(mu.noise))
+    assert bare.perm == []
+    m = _plan_ctx(wl.model)
+    m.apply(bare)
+    assert [m.mutant_plan(i)[0] for i in range(4)] == [
+        int(mu.layer[mu.records_of(i)].min()) for i in range(4)]
+    m.close()
+
+
 def test_invalid_calls_are_rejected_atomically():
     wl = W.make_workload("cfg2", n_inputs=1, n_mutants=4)
     m = B.Mure(device=-1)
