@@ -45,6 +45,7 @@ void conv_big_kernel(ConvArgs a) {
   const int m0 = (int)blockIdx.x * BM;
   const int n0 = (int)blockIdx.z * BN;
   const bf16_t* __restrict__ Wt = reinterpret_cast<const bf16_t*>(a.wtab[slot]);
+  const int ncol = a.cols ? a.ncols : a.Cout;
   const bf16_t* const zp = reinterpret_cast<const bf16_t*>(g_zero_page);
   const int kvec = (a.K + 7) / 8;
   if constexpr (!TAP64) {
@@ -87,6 +88,24 @@ void conv_big_kernel(ConvArgs a) {
                  ((int64_t)iy0[r] * a.W + ix0[r]) * a.C;
     }
   }
+  // the weight rows this thread loads (a gathered delta takes each column's
+  // row from its own mutant's weights); nullptr past the last column
+  const bf16_t* brow[BPT];
+#pragma unroll
+  for (int j = 0; j < BPT; ++j) {
+    const int i = tid + j * THREADS;
+    const int n = n0 + i / (BK / 8);
+    brow[j] = nullptr;
+    if (i < BVEC && n < ncol) {
+      if (a.cols) {
+        const DeltaCol cd = a.cols[n];
+        brow[j] = reinterpret_cast<const bf16_t*>(a.wtab[a.slot0 + cd.slot - a.col_slot0]) + (int64_t)cd.c * a.K;
+      } else {
+        brow[j] = Wt + (int64_t)n * a.K;
+      }
+      brow[j] += (i % (BK / 8)) * 8;
+    }
+  }
   __syncthreads();
 
   v4u ra[ROWS_PER_THREAD][4], rb[BPT];
@@ -126,12 +145,7 @@ void conv_big_kernel(ConvArgs a) {
     for (int j = 0; j < BPT; ++j) {
       const int i = tid + j * THREADS;
       v4u val = v4u{0u, 0u, 0u, 0u};
-      if (i < BVEC) {
-        const int row = i / (BK / 8), kv = i % (BK / 8);
-        const int k = kc + kv * 8;
-        if (n0 + row < a.Cout && k < a.K)
-          val = *reinterpret_cast<const v4u*>(Wt + (int64_t)(n0 + row) * a.K + k);
-      }
+      if (brow[j] && kc + (i % (BK / 8)) * 8 < a.K) val = *reinterpret_cast<const v4u*>(brow[j] + kc);
       rb[j] = val;
     }
   };
@@ -189,16 +203,27 @@ void conv_big_kernel(ConvArgs a) {
     // input (P % 4 == 0)
     int xo, pb;
     divmodu(a.dP, (uint32_t)mb, xo, pb);
-    const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xo, a.nx, a.x0);
     const bf16_t* sp = nullptr;
     if (a.add_mode)
       sp = reinterpret_cast<const bf16_t*>(a.skip.p) +
            row_index(a.skip.mode, (int64_t)slot * a.nx + xo, a.nx, a.x0) * a.skip.row_elems;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-      const int n = n0 + wn * WN + j * 16 + (lane & 15);
-      if (n >= a.Cout) continue;
-      const float bv = bias[n];
+      const int nc = n0 + wn * WN + j * 16 + (lane & 15);
+      if (nc >= ncol) continue;
+      // output slot, channel and channel stride of this column
+      int os = slot, n = nc, ostride = a.Cout;
+      float bv;
+      if (a.cols) {
+        const DeltaCol cd = a.cols[nc];
+        os = a.slot0 + cd.slot - a.col_slot0;
+        bv = a.btab[os][cd.c];
+        n = a.delta_T > 0 ? cd.t : cd.c;
+        if (a.delta_T > 0) ostride = a.delta_T;
+      } else {
+        bv = bias[nc];
+      }
+      const int64_t ro = row_index(a.out_mode, (int64_t)os * a.nx + xo, a.nx, a.x0);
       float v[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -207,7 +232,7 @@ void conv_big_kernel(ConvArgs a) {
       }
       if (a.pool) {
         const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-        store_out<bf16_t>(a.out, a.out_f32, ro * a.out_row + (int64_t)(pb >> 2) * a.Cout + n, mx);
+        store_out<bf16_t>(a.out, a.out_f32, ro * a.out_row + (int64_t)(pb >> 2) * ostride + n, mx);
       } else if (a.add_mode) {
         // conv_b's output (rounded) + the shortcut, in float32, then ReLU
         const int cs = a.add_mode == 1 ? n : n - (a.Cout - a.Cs) / 2;
@@ -229,7 +254,7 @@ void conv_big_kernel(ConvArgs a) {
       } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          store_out<bf16_t>(a.out, a.out_f32, ro * a.out_row + (int64_t)(pb + e) * a.Cout + n, v[e]);
+          store_out<bf16_t>(a.out, a.out_f32, ro * a.out_row + (int64_t)(pb + e) * ostride + n, v[e]);
       }
     }
   }
@@ -261,15 +286,18 @@ hipError_t launch_conv_big(const ConvArgs& a0, int nslots, hipStream_t s) {
   if (nslots <= 0 || a0.nx <= 0) return hipSuccess;
   if (a0.C % 8 || a0.K > 8 * 1024 || a0.P % 4 || (int64_t)a0.nx * a0.P + 256 >= INT32_MAX)
     return hipErrorInvalidValue;
+  if (a0.cols && (a0.in.mode != MODE_CACHE || a0.add_mode || a0.ncols <= 0)) return hipErrorInvalidValue;
+  if (a0.cols) nslots = 1;
   ConvArgs a = a0;
   a.dP = make_divu32((uint32_t)a.P);
   a.dWp = make_divu32((uint32_t)std::max(1, a.Wp));
   a.dWc = make_divu32((uint32_t)std::max(1, a.Wc));
-  const int bn = conv_big_bn(a.Cout);
+  const int bn = conv_big_bn(a.cols ? a.ncols : a.Cout);
   // tile: 0 automatic, 1 = 128 rows x BN (4 waves), 2 = 256 rows x BN (8 waves of 64 x 32..64)
   const int bm = a.tile == 2 ? 256 : 128;
   const int64_t Mslot = (int64_t)a.nx * a.P;
-  dim3 grid((unsigned)((Mslot + bm - 1) / bm), (unsigned)nslots, (unsigned)((a.Cout + bn - 1) / bn));
+  const int ncol = a.cols ? a.ncols : a.Cout;
+  dim3 grid((unsigned)((Mslot + bm - 1) / bm), (unsigned)nslots, (unsigned)((ncol + bn - 1) / bn));
   if (a.C % 64 == 0) return launch_big<true>(a, grid, bm, bn, s);
   return launch_big<false>(a, grid, bm, bn, s);
 }

@@ -40,10 +40,19 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
   const float* __restrict__ Wt = reinterpret_cast<const float*>(a.wtab[slot]);
   const float* __restrict__ bias = a.btab[slot];
 
+  const int ncol = a.cols ? a.ncols : a.Cout;
   // weights: read along k (coalesced), stored k-major
   for (int n = 0; n < BN; ++n) {
-    const bool nv = n0 + n < a.Cout;
-    const float* wr = Wt + (int64_t)(n0 + n) * a.K;
+    const bool nv = n0 + n < ncol;
+    const float* wr = nullptr;
+    if (nv) {
+      if (a.cols) {
+        const DeltaCol cd = a.cols[n0 + n];
+        wr = reinterpret_cast<const float*>(a.wtab[a.slot0 + cd.slot - a.col_slot0]) + (int64_t)cd.c * a.K;
+      } else {
+        wr = Wt + (int64_t)(n0 + n) * a.K;
+      }
+    }
     for (int k = tid; k < kpad + 16; k += 256) Ws[k * KST + n] = (nv && k < a.K) ? wr[k] : 0.f;
   }
   for (int k = tid; k < kpad + 32; k += 256) {
@@ -67,11 +76,26 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
     }
   }
   constexpr int TN = BN / 16;
+  // per column of this lane: bias, output slot, channel offset and stride
   float bv[TN];
+  int oslot[TN], ochan[TN];
+  const int ostride = a.cols && a.delta_T > 0 ? a.delta_T : a.Cout;
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const int n = n0 + j * 16 + (lane & 15);
-    bv[j] = n < a.Cout ? bias[n] : 0.f;
+    bv[j] = 0.f;
+    oslot[j] = slot;
+    ochan[j] = n;
+    if (n < ncol) {
+      if (a.cols) {
+        const DeltaCol cd = a.cols[n];
+        bv[j] = a.btab[a.slot0 + cd.slot - a.col_slot0][cd.c];
+        oslot[j] = a.slot0 + cd.slot - a.col_slot0;
+        ochan[j] = a.delta_T > 0 ? cd.t : cd.c;
+      } else {
+        bv[j] = bias[n];
+      }
+    }
   }
 
   for (int it = 0; it < iters; ++it) {
@@ -211,11 +235,11 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
       if (mb >= Mslot) continue;
       int xo, pb;
       divmodu(a.dP, (uint32_t)mb, xo, pb);
-      const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xo, a.nx, a.x0);
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int n = n0 + j * 16 + (lane & 15);
-        if (n >= a.Cout) continue;
+        if (n >= ncol) continue;
+        const int64_t ro = row_index(a.out_mode, (int64_t)oslot[j] * a.nx + xo, a.nx, a.x0);
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -224,7 +248,7 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
         }
         if (a.pool) {
           const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-          store_out<float>(a.out, a.out_f32, ro * a.out_row + (int64_t)(pb >> 2) * a.Cout + n, mx);
+          store_out<float>(a.out, a.out_f32, ro * a.out_row + (int64_t)(pb >> 2) * ostride + ochan[j], mx);
         } else {
           // the lane's 4 rows may cross into the next input when P % 4 != 0
           int xe = xo, pe = pb;
@@ -234,9 +258,9 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
             if (mb + e >= Mslot) break;
             if (pe == a.P) {
               ++xe; pe = 0;
-              re = row_index(a.out_mode, (int64_t)slot * a.nx + xe, a.nx, a.x0);
+              re = row_index(a.out_mode, (int64_t)oslot[j] * a.nx + xe, a.nx, a.x0);
             }
-            store_out<float>(a.out, a.out_f32, re * a.out_row + (int64_t)pe * a.Cout + n, v[e]);
+            store_out<float>(a.out, a.out_f32, re * a.out_row + (int64_t)pe * ostride + ochan[j], v[e]);
             ++pe;
           }
         }
@@ -247,23 +271,35 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
 
 hipError_t launch_conv_lds(const ConvArgs& a0, int nslots, hipStream_t s) {
   if (nslots <= 0 || a0.nx <= 0) return hipSuccess;
-  if (a0.Cout > 64 || (int64_t)a0.nx * a0.P + 256 >= INT32_MAX) return hipErrorInvalidValue;
+  if ((int64_t)a0.nx * a0.P + 256 >= INT32_MAX) return hipErrorInvalidValue;
   if (a0.pool && a0.P % 4) return hipErrorInvalidValue;
+  if (a0.cols && (a0.vin.chmap || a0.in.mode != MODE_CACHE || a0.ncols <= 0)) return hipErrorInvalidValue;
+  if (!a0.cols && a0.Cout > 64) return hipErrorInvalidValue;
   ConvArgs a = a0;
   a.dP = make_divu32((uint32_t)a.P);
   a.dWp = make_divu32((uint32_t)std::max(1, a.Wp));
   a.dWc = make_divu32((uint32_t)std::max(1, a.Wc));
   a.dHW = make_divu32((uint32_t)std::max(1, a.H * a.W));
-  const int bn = conv_lds_bn(a.Cout);
+  // columns per block: the node's channels, or for a gathered delta the
+  // widest tile whose LDS fits
+  int bn = conv_lds_bn(a.Cout);
+  size_t lds = (size_t)conv_lds_bytes(a.H, a.W, a.C, a.pad, a.P, a.Cout, a.K);
+  if (a.cols) {
+    for (bn = conv_lds_bn(std::min(a.ncols, 64)); bn > 16; bn /= 2)
+      if (conv_lds_bytes(a.H, a.W, a.C, a.pad, a.P, bn, a.K) <= 64 * 1024) break;
+    lds = (size_t)conv_lds_bytes(a.H, a.W, a.C, a.pad, a.P, bn, a.K);
+    nslots = 1;
+  }
   const int kpad = (a.K + 7) / 8 * 8;
   const int cap = conv_lds_nimg_cap(a.P);
-  const size_t lds = (size_t)conv_lds_bytes(a.H, a.W, a.C, a.pad, a.P, a.Cout, a.K);
   if (lds > 64 * 1024) return hipErrorInvalidValue;
   const int64_t Mslot = (int64_t)a.nx * a.P;
   const int64_t pieces = (Mslot + 255) / 256;
+  const int ncol = a.cols ? a.ncols : a.Cout;
+  const int64_t ztiles = (ncol + bn - 1) / bn;
   // about 2048 blocks in flight, at most 8 pieces per block
-  int iters = (int)std::max<int64_t>(1, std::min<int64_t>(8, pieces * nslots / 2048));
-  dim3 grid((unsigned)((pieces + iters - 1) / iters), (unsigned)nslots, (unsigned)((a.Cout + bn - 1) / bn));
+  int iters = (int)std::max<int64_t>(1, std::min<int64_t>(8, pieces * nslots * ztiles / 2048));
+  dim3 grid((unsigned)((pieces + iters - 1) / iters), (unsigned)nslots, (unsigned)ztiles);
   switch (bn) {
     case 16: hipLaunchKernelGGL((conv_lds_kernel<16>), grid, dim3(256), lds, s, a, cap, kpad, iters); break;
     case 32: hipLaunchKernelGGL((conv_lds_kernel<32>), grid, dim3(256), lds, s, a, cap, kpad, iters); break;

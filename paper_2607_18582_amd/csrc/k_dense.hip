@@ -43,6 +43,23 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
   const int n0 = (int)blockIdx.z * BN;
   const T* __restrict__ Wt = reinterpret_cast<const T*>(a.wtab[slot]);
   const T* __restrict__ X = reinterpret_cast<const T*>(a.in.p);
+  const int ncol = a.cols ? a.ncols : a.Cout;
+  // the weight row of each column of the block (a gathered delta takes each
+  // column's row from its own mutant's weights); nullptr past the last column
+  __shared__ const T* wrow[BN];
+  for (int n = tid; n < BN; n += 256) {
+    const T* w = nullptr;
+    if (n0 + n < ncol) {
+      if (a.cols) {
+        const DeltaCol cd = a.cols[n0 + n];
+        w = reinterpret_cast<const T*>(a.wtab[a.slot0 + cd.slot - a.col_slot0]) + (int64_t)cd.c * a.K;
+      } else {
+        w = Wt + (int64_t)(n0 + n) * a.K;
+      }
+    }
+    wrow[n] = w;
+  }
+  __syncthreads();
 
   v4f acc[TM][TN];
 #pragma unroll
@@ -71,7 +88,7 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
       if constexpr (VIRT) {
         const int xi = m0 + row;
         const T* crow = reinterpret_cast<const T*>(a.vin.cache) + ((int64_t)a.x0 + xi) * a.K;
-        const T* drow = reinterpret_cast<const T*>(a.vin.delta) + ((int64_t)slot * a.nx + xi) * a.vin.T;
+        const T* drow = reinterpret_cast<const T*>(a.vin.delta) + ((int64_t)slot * a.nx + xi) * a.vin.HW * a.vin.T;
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
           T v = T(0);
@@ -96,7 +113,8 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
       const int row = i / (BK / VEC), kv = i % (BK / VEC);
       const int k = kc + kv * VEC;
       vec_t v{};
-      if (n0 + row < a.Cout && k < a.K) v = *reinterpret_cast<const vec_t*>(Wt + (int64_t)(n0 + row) * a.K + k);
+      const T* w = wrow[row];
+      if (w && k < a.K) v = *reinterpret_cast<const vec_t*>(w + k);
       *reinterpret_cast<vec_t*>(&Bs[row * LD + kv * VEC]) = v;
     }
     __syncthreads();
@@ -135,11 +153,24 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
   }
 
   const float* __restrict__ bias = a.btab[slot];
+  const int orow = a.cols && a.delta_T > 0 ? a.delta_T : a.Cout;   // elements per output row
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const int nl = wn * WN + j * 16 + (lane & 15);
     const int n = n0 + nl;
-    const float bv = n < a.Cout ? bias[n] : 0.f;
+    // output slot and channel of this column
+    int os = slot, oc = n;
+    float bv = 0.f;
+    if (n < ncol) {
+      if (a.cols) {
+        const DeltaCol cd = a.cols[n];
+        os = a.slot0 + cd.slot - a.col_slot0;
+        oc = a.delta_T > 0 ? cd.t : cd.c;
+        bv = a.btab[os][cd.c];
+      } else {
+        bv = bias[n];
+      }
+    }
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -147,9 +178,9 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
         const int rl = wm * WM + i * 16 + (lane >> 4) * 4 + e;
         float v = acc[i][j][e] + bv;
         if (a.relu) v = fmaxf(v, 0.f);
-        if (a.write_out && n < a.Cout && m0 + rl < a.nx) {
-          const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + m0 + rl, a.nx, a.x0);
-          store_out<T>(a.out, a.out_f32, ro * a.Cout + n, v);
+        if (a.write_out && n < ncol && m0 + rl < a.nx) {
+          const int64_t ro = row_index(a.out_mode, (int64_t)os * a.nx + m0 + rl, a.nx, a.x0);
+          store_out<T>(a.out, a.out_f32, ro * orow + oc, v);
         }
         if constexpr (LSN > 1) {
           if (a.do_kill) Ls[rl * (BN + 1) + nl] = v;
@@ -203,8 +234,12 @@ int dense_bn(int cout) {
 
 hipError_t launch_dense(const DenseArgs& a, int nslots, int dtype, hipStream_t s) {
   if (nslots <= 0 || a.nx <= 0) return hipSuccess;
-  const int bn = dense_bn(a.Cout);
-  dim3 grid((unsigned)((a.nx + 63) / 64), (unsigned)nslots, (unsigned)((a.Cout + bn - 1) / bn));
+  if (a.cols && (a.do_kill || a.vin.chmap || a.in.mode != MODE_CACHE || a.ncols <= 0))
+    return hipErrorInvalidValue;
+  if (a.cols) nslots = 1;
+  const int ncol = a.cols ? a.ncols : a.Cout;
+  const int bn = dense_bn(ncol);
+  dim3 grid((unsigned)((a.nx + 63) / 64), (unsigned)nslots, (unsigned)((ncol + bn - 1) / bn));
   if (a.do_kill && (grid.z != 1 || bn > 64)) return hipErrorInvalidValue;
   if (a.vin.chmap) {
     if (a.K > 4096) return hipErrorInvalidValue;

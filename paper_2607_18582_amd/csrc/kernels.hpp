@@ -55,6 +55,16 @@ struct VirtualIn {
   int C = 0, HW = 0, T = 0;
 };
 
+// One gathered output column of the delta at the first mutated node: output
+// channel `c` of mutant slot `slot - col_slot0` (relative to the launch's
+// slot0).  A delta launch shares the cached input among all its columns and
+// computes only the channels the mutants' records changed; column results are
+// stored as compact delta channel `t` (delta_T > 0) or as channel c of the
+// slot's full row.
+struct DeltaCol {
+  int slot, c, t, pad;
+};
+
 // CONV2D / DENSE (a DENSE layer is a 1x1 convolution over a 1x1xC_in input).
 struct ConvArgs {
   TensorArg in;
@@ -80,6 +90,10 @@ struct ConvArgs {
   TensorArg skip;
   int Hs = 0, Ws = 0, Cs = 0;            // skip geometry
   int tile = 0;                          // tiled kernel's block shape (0 automatic)
+  // gathered-column delta (cols != nullptr): ncols columns instead of C_out
+  // channels per slot; the input must be slot independent (prefix cache)
+  const DeltaCol* cols = nullptr;
+  int ncols = 0, delta_T = 0, col_slot0 = 0;
   // filled by the launchers: dividers by P, Wp, Wc and H*W
   DivU32 dP, dWp, dWc, dHW;
 };
@@ -104,6 +118,9 @@ struct DenseArgs {
   int64_t nwords = 0;
   unsigned long long* nonfinite = nullptr;
   float* logits_out = nullptr;
+  // gathered-column delta, as in ConvArgs (no kill, no virtual input)
+  const DeltaCol* cols = nullptr;
+  int ncols = 0, delta_T = 0, col_slot0 = 0;
 };
 
 // CONV2D with tiny C_out on the vector ALU, one output position per thread.

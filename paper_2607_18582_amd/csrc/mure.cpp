@@ -134,10 +134,12 @@ struct mure_ctx {
     int64_t choff = 0;                                // offset (int32) into d_slots: touched-list
                                                       // offsets of the recompute slots (+1)
     int64_t vchmap = 0;                               // offset (int32) into d_chmap: virtual maps
+    int64_t cols = 0;                                 // offset (DeltaCol) into d_cols
+    std::vector<int64_t> colbeg;                      // first column of each recompute slot (+1)
   };
   std::vector<GroupTabs> gtabs;
   std::map<int, int64_t> orig_w, orig_b;              // node -> offset of 1-entry original tables
-  DevBuf d_slots, d_chmap;
+  DevBuf d_slots, d_chmap, d_cols;
   DevBuf d_cargs, d_drecs, d_noise, d_given;          // upload staging
   // prefix cache and original results
   int64_t N = 0;
@@ -203,6 +205,9 @@ struct Extra {
   const int32_t* ch_off = nullptr;    // per-slot channel lists (VALU delta at mmi)
   const int32_t* ch_list = nullptr;
   int delta_T = 0;                    // write compact delta rows of delta_T channels
+  const DeltaCol* cols = nullptr;     // gathered-column delta at mmi (MFMA families)
+  int ncols = 0, col_slot0 = 0;
+  int64_t exec_macs = -1;             // MACs the launch executes, when not slots * rows * node
   const VirtualIn* vin = nullptr;     // read the first mutated node's output virtually
   int fuse_add = -1;                  // ADD node fused into this convolution's epilogue
   Where skip{nullptr, MODE_BUF};      // that ADD's shortcut input
@@ -239,7 +244,7 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
       mure_status st = timing_begin(ctx);
       if (st != MURE_OK) return st;
     }
-    int64_t exec_macs = (int64_t)nslots * nx * n.macs;
+    int64_t exec_macs = ex.exec_macs >= 0 ? ex.exec_macs : (int64_t)nslots * nx * n.macs;
     if (fam == FAM_DENSE) {
       DenseArgs a;
       a.in.p = ins[0].p; a.in.mode = ins[0].mode; a.in.row_elems = n.c_in;
@@ -247,7 +252,10 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
       a.wtab = wtab; a.btab = btab;
       a.slot0 = slot0; a.nx = nx; a.x0 = x0; a.K = n.c_in; a.Cout = n.c_out; a.relu = n.relu;
       if (ex.vin) a.vin = *ex.vin;
-      if (ex.kill && n.c_out <= 64 && out_mode == MODE_BUF) {
+      if (ex.cols) {
+        a.cols = ex.cols; a.ncols = ex.ncols; a.col_slot0 = ex.col_slot0; a.delta_T = ex.delta_T;
+      }
+      if (ex.kill && !ex.cols && n.c_out <= 64 && out_mode == MODE_BUF) {
         const KillArgs& k = *ex.kill;
         a.do_kill = 1;
         a.write_out = 0;
@@ -269,7 +277,7 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
       a.ch_off = ex.ch_off; a.ch_list = ex.ch_list;
       if (ex.delta_T > 0) { a.delta_T = ex.delta_T; a.out_row = (int64_t)n.H * n.W * ex.delta_T; }
       if (ex.vin) return ctx->fail(MURE_E_INVALID, "internal: virtual input to a VALU convolution");
-      if (ex.ch_off) exec_macs = alg_macs;
+
       e = launch_valu(a, g.dtype, ctx->stream);
     } else {
       ConvArgs a;
@@ -299,6 +307,11 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
       a.K = a.kh * a.kw * a.C;
       a.P = a.pool ? 4 * a.Hp * a.Wp : a.Hc * a.Wc;
       a.tile = (int)ctx->conv_tile;
+      if (ex.cols) {
+        if (fam != FAM_LDS && fam != FAM_BIG) return ctx->fail(MURE_E_INVALID, "internal: gathered delta on the im2col kernel");
+        a.cols = ex.cols; a.ncols = ex.ncols; a.col_slot0 = ex.col_slot0; a.delta_T = ex.delta_T;
+        if (ex.delta_T > 0) a.out_row = (int64_t)n.H * n.W * ex.delta_T;
+      }
       if (ex.vin) {
         if (fam != FAM_LDS) return ctx->fail(MURE_E_INVALID, "internal: virtual input to an im2col convolution");
         a.vin = *ex.vin;
@@ -643,6 +656,20 @@ mure_status mure_apply_mutants(mure_ctx* ctx, int32_t n_mutants, const mure_reco
       slots.insert(slots.end(), offs.begin(), offs.end());
       slots.insert(slots.end(), list.begin(), list.end());
     }
+    // gathered delta columns of the recompute slots: (group slot, channel, t)
+    std::vector<DeltaCol> cols;
+    for (size_t gi = 0; gi < plan.groups.size(); ++gi) {
+      const Group& gr = plan.groups[gi];
+      mure_ctx::GroupTabs& gt = gtabs[gi];
+      gt.cols = (int64_t)cols.size();
+      gt.colbeg.assign(1, 0);
+      for (int s = 0; s < gr.n_recompute; ++s) {
+        const std::vector<int>& tl = plan.mutants[gr.mutants[s]].touched_list;
+        for (size_t t = 0; t < tl.size(); ++t) cols.push_back(DeltaCol{s, tl[t], (int)t, 0});
+        gt.colbeg.push_back((int64_t)cols.size() - gt.cols);
+      }
+    }
+    HIPTRY(ctx->d_cols.ensure(std::max<size_t>(1, cols.size()) * sizeof(DeltaCol)));
     HIPTRY(ctx->d_tables.ensure(tabs.size() * sizeof(void*)));
     HIPTRY(ctx->d_slots.ensure(slots.size() * 4));
     HIPTRY(ctx->d_chmap.ensure(chmaps.size() * 4));
@@ -650,6 +677,7 @@ mure_status mure_apply_mutants(mure_ctx* ctx, int32_t n_mutants, const mure_reco
     if (!tabs.empty()) HIPTRY(hipMemcpyAsync(ctx->d_tables.p, tabs.data(), tabs.size() * sizeof(void*), hipMemcpyHostToDevice, st));
     if (!slots.empty()) HIPTRY(hipMemcpyAsync(ctx->d_slots.p, slots.data(), slots.size() * 4, hipMemcpyHostToDevice, st));
     if (!chmaps.empty()) HIPTRY(hipMemcpyAsync(ctx->d_chmap.p, chmaps.data(), chmaps.size() * 4, hipMemcpyHostToDevice, st));
+    if (!cols.empty()) HIPTRY(hipMemcpyAsync(ctx->d_cols.p, cols.data(), cols.size() * sizeof(DeltaCol), hipMemcpyHostToDevice, st));
     if (!cargs.empty()) {
       HIPTRY(ctx->d_cargs.ensure(cargs.size() * sizeof(CowArgs)));
       HIPTRY(ctx->d_drecs.ensure(drecs.size() * sizeof(DevRecord)));
@@ -890,20 +918,30 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
           }
           const int64_t per_ch = nm.macs / nm.c_out;
           Extra ex;
+          int launch_slots = rec_end - cs0;
           if (gr.delta) {
-            ex.ch_off = ctx->d_slots.as<int32_t>() + gt.choff + cs0;
-            ex.ch_list = ctx->d_slots.as<int32_t>();
             if (gr.virt) ex.delta_T = gr.T;
+            ex.exec_macs = tl * per_ch * cnt;
+            if (node_family(g, mmi) == FAM_VALU) {
+              ex.ch_off = ctx->d_slots.as<int32_t>() + gt.choff + cs0;
+              ex.ch_list = ctx->d_slots.as<int32_t>();
+            } else {
+              ex.cols = ctx->d_cols.as<DeltaCol>() + gt.cols + gt.colbeg[cs0];
+              ex.ncols = (int)(gt.colbeg[rec_end] - gt.colbeg[cs0]);
+              ex.col_slot0 = cs0;
+              launch_slots = ex.ncols > 0 ? 1 : 0;
+            }
           }
           // the kill fuses into the output layer only when every slot of the
           // chunk is recomputed here (patched slots need the kill kernel, which
           // reads the logits buffer)
           if (mmi == L && pa >= cs1) { ex.kill = &ka; ex.kill_fused = &fused; }
-          mure_status st = exec_node(ctx, mmi, ins, out, MODE_BUF, tabs + gt.w.at(mmi) + cs0,
-                                     reinterpret_cast<const float* const*>(tabs + gt.b.at(mmi) + cs0),
-                                     0, rec_end - cs0, cnt, (int)x0, rows, touched * per_ch * cnt, true, ex);
-          if (st != MURE_OK) return st;
-          (void)tl;
+          if (launch_slots > 0) {
+            mure_status st = exec_node(ctx, mmi, ins, out, MODE_BUF, tabs + gt.w.at(mmi) + cs0,
+                                       reinterpret_cast<const float* const*>(tabs + gt.b.at(mmi) + cs0),
+                                       0, launch_slots, cnt, (int)x0, rows, touched * per_ch * cnt, true, ex);
+            if (st != MURE_OK) return st;
+          }
         }
       }
       VirtualIn vin;

@@ -243,7 +243,15 @@ std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>&
     for (int m : kv.second) if (p.mutants[m].recompute) gr.mutants.push_back(m);
     gr.n_recompute = (int)gr.mutants.size();
     for (int m : kv.second) if (!p.mutants[m].recompute) gr.mutants.push_back(m);
-    gr.delta = !vanilla && gr.n_recompute > 0 && node_family(g, gr.mmi) == FAM_VALU;
+    // delta at mmi: only the channels the fuzz / inverse / shuffle records
+    // changed are recomputed (VALU kernel per slot, or one gathered-column GEMM
+    // over the shared cached input for the MFMA families); the im2col fallback
+    // recomputes whole nodes
+    {
+      const int fam = node_family(g, gr.mmi);
+      gr.delta = !vanilla && gr.n_recompute > 0 &&
+                 (fam == FAM_VALU || fam == FAM_LDS || fam == FAM_DENSE || fam == FAM_BIG);
+    }
     // virtual mmi output: every consumer is an LDS convolution or a dense layer
     gr.virt = gr.mmi != g.out();
     for (int v = gr.mmi + 1; v < n && gr.virt; ++v)
