@@ -16,13 +16,13 @@ template <typename T> struct DenseCfg;
 template <> struct DenseCfg<float> { static constexpr int BK = 32, VEC = 4, PAD = 4; };
 template <> struct DenseCfg<bf16_t> { static constexpr int BK = 64, VEC = 8, PAD = 8; };
 
-template <int VEC, typename T> struct VecOf;
-template <> struct VecOf<4, float> { typedef float4 type; };
-template <> struct VecOf<8, bf16_t> { typedef uint4 type; };
-
 // VIRT: the input is the first mutated node's output seen through the
 // mutant's channel map: a per-block table maps each k of the flattened row to
 // the cached original, zero, or a compact delta entry.
+//
+// The next k chunk's global loads are issued into registers before the MFMAs
+// of the current chunk (register prefetch); tiles are staged as raw 16-byte
+// vectors.
 template <typename T, int BN, int WAVES_M, bool VIRT>
 __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
   constexpr int BM = 64;
@@ -31,7 +31,9 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int TM = WM / 16, TN = WN / 16;
   constexpr int LSN = BN <= 64 ? BM * (BN + 1) : 1;
-  typedef typename VecOf<VEC, T>::type vec_t;
+  constexpr int KV = BK / VEC;                               // 16-byte vectors per tile row
+  constexpr int APT = BM * KV / 256;                         // A vectors per thread
+  constexpr int BPT = (BN * KV + 255) / 256;                 // B vectors per thread
   __shared__ __attribute__((aligned(16))) T As[BM * LD];
   __shared__ __attribute__((aligned(16))) T Bs[BN * LD];
   __shared__ float Ls[LSN];
@@ -59,13 +61,6 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
     }
     wrow[n] = w;
   }
-  __syncthreads();
-
-  v4f acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
   constexpr int KMAP = VIRT ? 4096 : 1;
   __shared__ int kmap[KMAP];
@@ -77,47 +72,95 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
       kmap[k] = src >= 0 ? pix * a.vin.C + src
               : src == -1 ? INT_MIN : -1 - (pix * a.vin.T + (-2 - src));
     }
-    __syncthreads();
   }
-  for (int kc = 0; kc < a.K; kc += BK) {
-    constexpr int AV = BM * BK / VEC;
+  __syncthreads();
+
+  // this thread's A rows (input rows of the block) and B rows (weight rows)
+  const T* arow[APT];
+  const T* crow[APT];                                        // VIRT: cached original row
+  const T* drow[APT];                                        // VIRT: compact delta row
 #pragma unroll
-    for (int i = tid; i < AV; i += 256) {
-      const int row = i / (BK / VEC), kv = i % (BK / VEC);
-      const int k = kc + kv * VEC;
+  for (int j = 0; j < APT; ++j) {
+    const int i = tid + j * 256, row = i / KV, kv = i % KV;
+    const int xi = m0 + row;
+    arow[j] = crow[j] = drow[j] = nullptr;
+    if (xi < a.nx) {
       if constexpr (VIRT) {
-        const int xi = m0 + row;
-        const T* crow = reinterpret_cast<const T*>(a.vin.cache) + ((int64_t)a.x0 + xi) * a.K;
-        const T* drow = reinterpret_cast<const T*>(a.vin.delta) + ((int64_t)slot * a.nx + xi) * a.vin.HW * a.vin.T;
+        crow[j] = reinterpret_cast<const T*>(a.vin.cache) + ((int64_t)a.x0 + xi) * a.K;
+        drow[j] = reinterpret_cast<const T*>(a.vin.delta) + ((int64_t)slot * a.nx + xi) * a.vin.HW * a.vin.T;
+      } else {
+        const int64_t ri = row_index(a.in.mode, (int64_t)slot * a.nx + xi, a.nx, a.x0);
+        arow[j] = X + ri * a.K + kv * VEC;
+      }
+    }
+  }
+  const T* brow[BPT];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-          T v = T(0);
-          if (xi < a.nx && k + e < a.K) {
-            const int code = kmap[k + e];
-            if (code >= 0) v = crow[code];
-            else if (code != INT_MIN) v = drow[-1 - code];
-          }
-          As[row * LD + kv * VEC + e] = v;
-        }
-        continue;
-      }
-      vec_t v{};
-      if (m0 + row < a.nx && k < a.K) {
-        const int64_t ri = row_index(a.in.mode, (int64_t)slot * a.nx + m0 + row, a.nx, a.x0);
-        v = *reinterpret_cast<const vec_t*>(X + ri * a.K + k);
-      }
-      *reinterpret_cast<vec_t*>(&As[row * LD + kv * VEC]) = v;
-    }
-    constexpr int BV = BN * BK / VEC;
-    for (int i = tid; i < BV; i += 256) {
-      const int row = i / (BK / VEC), kv = i % (BK / VEC);
+  for (int j = 0; j < BPT; ++j) {
+    const int i = tid + j * 256;
+    brow[j] = nullptr;
+    if (i < BN * KV && wrow[i / KV]) brow[j] = wrow[i / KV] + (i % KV) * VEC;
+  }
+
+  v4u ra[APT], rb[BPT];
+  auto load_chunk = [&](int kc) {
+#pragma unroll
+    for (int j = 0; j < APT; ++j) {
+      const int kv = (tid + j * 256) % KV;
       const int k = kc + kv * VEC;
-      vec_t v{};
-      const T* w = wrow[row];
-      if (w && k < a.K) v = *reinterpret_cast<const vec_t*>(w + k);
-      *reinterpret_cast<vec_t*>(&Bs[row * LD + kv * VEC]) = v;
+      v4u v = v4u{0u, 0u, 0u, 0u};
+      if constexpr (VIRT) {
+        if (crow[j]) {
+          T e8[VEC];
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            T x = T(0);
+            if (k + e < a.K) {
+              const int code = kmap[k + e];
+              if (code >= 0) x = crow[j][code];
+              else if (code != INT_MIN) x = drow[j][-1 - code];
+            }
+            e8[e] = x;
+          }
+          __builtin_memcpy(&v, e8, 16);
+        }
+      } else {
+        if (arow[j] && k < a.K) v = *reinterpret_cast<const v4u*>(arow[j] + kc);
+      }
+      ra[j] = v;
     }
+#pragma unroll
+    for (int j = 0; j < BPT; ++j) {
+      const int kv = (tid + j * 256) % KV;
+      v4u v = v4u{0u, 0u, 0u, 0u};
+      if (brow[j] && kc + kv * VEC < a.K) v = *reinterpret_cast<const v4u*>(brow[j] + kc);
+      rb[j] = v;
+    }
+  };
+  auto store_chunk = [&]() {
+#pragma unroll
+    for (int j = 0; j < APT; ++j) {
+      const int i = tid + j * 256;
+      *reinterpret_cast<v4u*>(&As[(i / KV) * LD + (i % KV) * VEC]) = ra[j];
+    }
+#pragma unroll
+    for (int j = 0; j < BPT; ++j) {
+      const int i = tid + j * 256;
+      if (i < BN * KV) *reinterpret_cast<v4u*>(&Bs[(i / KV) * LD + (i % KV) * VEC]) = rb[j];
+    }
+  };
+
+  v4f acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  load_chunk(0);
+  for (int kc = 0; kc < a.K; kc += BK) {
+    store_chunk();
     __syncthreads();
+    if (kc + BK < a.K) load_chunk(kc + BK);                  // next chunk in flight
     if constexpr (sizeof(T) == 4) {
 #pragma unroll
       for (int ks = 0; ks < BK / 4; ++ks) {
