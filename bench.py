@@ -36,7 +36,10 @@ KERNELS = ["dense_kernel (DENSE layers, MFMA GEMM)",
            "conv_lds_kernel (CONV2D, LDS-resident images, MFMA)",
            "conv_mfma_kernel (CONV2D, im2col implicit GEMM with scalar gathers, MFMA)",
            "conv_big_kernel (bf16 CONV2D, tiled implicit GEMM, MFMA)"]
+KERNEL_NAMES = ["dense_kernel", "conv_valu_kernel", "conv_lds_kernel", "conv_mfma_kernel",
+                "conv_big_kernel"]
 PEAK_HBM_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
 ORACLE_SAMPLE = {"cfg1": (100, 500), "cfg2": (24, 6000), "cfg3": (3, 64), "cfg4": (8, 256),
                  "cfg5": (2, 16)}
 
@@ -60,6 +63,132 @@ def cpu_baseline(wl, n_mut: int, n_in: int):
                       f"(vanilla, float64 accumulation), {dt:.1f} s"}
 
 
+def library_source_hash() -> str:
+    """Hash of the library's sources: HBM counters taken on other sources no
+    longer describe the kernels."""
+    import hashlib
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2607_18582_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".hpp", ".cpp")):
+            h.update(f.encode())
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(fh.read())
+    with open(os.path.join(ROOT, "include", "mure.h"), "rb") as fh:
+        h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_path(kernel: str, config: str) -> str:
+    return os.path.join(PROFILES, f"{kernel}_{config}_hbm_traffic.md")
+
+
+def read_traffic(kernel: str, config: str, n_inputs: int, n_mutants: int):
+    """HBM bytes per run_mutants launch of ``kernel`` from its committed
+    counter summary, or None when there is none for this workload or the
+    library changed since the counters were taken."""
+    try:
+        with open(traffic_path(kernel, config)) as f:
+            for ln in f:
+                if ln.startswith('{"traffic_bytes_per_launch"'):
+                    d = json.loads(ln)
+                    if (d["source_hash"] == library_source_hash() and d["n_inputs"] == n_inputs
+                            and d["n_mutants"] == n_mutants):
+                        return d
+    except OSError:
+        pass
+    return None
+
+
+def _run_mutants_windows(rows):
+    """Dispatch ids bracketing each run_mutants call: after run_original's
+    label kernel, up to and including the score kernel."""
+    wins, start = [], None
+    for r in rows:
+        name = r["Kernel_Name"]
+        if "labels_kernel" in name:
+            start = int(r["Dispatch_Id"])
+        elif "score_kernel" in name and start is not None:
+            wins.append((start, int(r["Dispatch_Id"])))
+            start = None
+    return wins
+
+
+def summarize_pmc(fetch_csv: str, write_csv: str, kernel: str, args) -> str:
+    """Markdown summary of two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE)
+    of ``bench.py --steps 1 --warmup 0 --gain 0 --copy-calibration-mib M``:
+    the copy of M MiB calibrates each counter (bytes it should see / bytes
+    it reports); the kernel's run_mutants dispatches give the scaled HBM
+    bytes per launch."""
+    import csv
+    per = {}
+    calib = {}
+    nbytes = args.copy_calibration_mib << 20
+    for ctr, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
+        rows = [r for r in rows if r["Counter_Name"] == ctr]
+        copies = [r for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        big = max(copies, key=lambda r: float(r["Counter_Value"]))
+        calib[ctr] = nbytes / (float(big["Counter_Value"]) * 1024.0)
+        wins = _run_mutants_windows(rows)
+        for r in rows:
+            d = int(r["Dispatch_Id"])
+            if kernel in r["Kernel_Name"] and any(a < d < b for a, b in wins):
+                per.setdefault(d, {})[ctr] = float(r["Counter_Value"]) * 1024.0 * calib[ctr]
+    ids = sorted(per)
+    fetch = sum(per[d].get("FETCH_SIZE", 0.0) for d in ids)
+    write = sum(per[d].get("WRITE_SIZE", 0.0) for d in ids)
+    n = max(len(ids), 1)
+    cmd = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 240 rocprofv3 --pmc {C} --output-format csv "
+           "-d <dir> -o pmc -- python3 bench.py --config %s --steps 1 --warmup 0 --no-cpu-baseline --gain 0 "
+           "--copy-calibration-mib %d" % (args.config, args.copy_calibration_mib))
+    out = [f"# HBM traffic of {kernel}, {args.config} ({args.inputs or 'default'} inputs, "
+           f"{args.mutants or 'default'} mutants)", "",
+           "Commands (one run per counter, C = FETCH_SIZE, then WRITE_SIZE), from the repository root:", "",
+           "```", cmd, "python3 bench.py --summarize-pmc <fetch csv> <write csv> --kernel %s --config %s "
+           "--copy-calibration-mib %d" % (kernel, args.config, args.copy_calibration_mib), "```", "",
+           f"Calibration: a {args.copy_calibration_mib} MiB device-to-device copy (`__amd_rocclr_copyBuffer`) "
+           f"moves {nbytes} bytes each way; bytes per reported byte: FETCH_SIZE x{calib['FETCH_SIZE']:.3f}, "
+           f"WRITE_SIZE x{calib['WRITE_SIZE']:.3f}.", "",
+           "| run_mutants dispatch | FETCH bytes (scaled) | WRITE bytes (scaled) |", "|---|---|---|"]
+    for d in ids:
+        out.append(f"| {d} | {per[d].get('FETCH_SIZE', 0):.4g} | {per[d].get('WRITE_SIZE', 0):.4g} |")
+    rec = {"traffic_bytes_per_launch": (fetch + write) / n, "fetch_bytes_per_launch": fetch / n,
+           "write_bytes_per_launch": write / n, "launches": len(ids), "kernel": kernel,
+           "config": args.config, "n_inputs": args.n_inputs_resolved, "n_mutants": args.n_mutants_resolved,
+           "calibration": calib, "source_hash": library_source_hash()}
+    out += ["", "Per launch (machine-read by bench.py while the library sources hash to `source_hash`):",
+            "", "```json", json.dumps(rec), "```", ""]
+    return "\n".join(out)
+
+
+def summarize_trace(trace_csv: str, stats_csv: str, kernel: str, args) -> str:
+    """Markdown summary of ``rocprofv3 --kernel-trace --stats`` over a default
+    bench run: per-kernel totals, and the average duration of ``kernel``'s
+    launches inside the timed memoized run_mutants calls (the figure bench.py
+    measures with HIP events)."""
+    import csv
+    stats = list(csv.DictReader(open(stats_csv)))
+    trace = sorted(csv.DictReader(open(trace_csv)), key=lambda r: int(r["Dispatch_Id"]))
+    wins = _run_mutants_windows(trace)[args.warmup:args.warmup + args.steps]
+    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6 for r in trace
+            if kernel in r["Kernel_Name"] and any(a < int(r["Dispatch_Id"]) < b for a, b in wins)]
+    cmd = ("cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats --output-format csv "
+           "-d <dir> -o kt -- python3 bench.py --config %s --steps %d --warmup %d"
+           % (args.config, args.steps, args.warmup))
+    out = [f"# Kernel trace, {args.config} bench run", "", "Command, from the repository root:", "",
+           "```", cmd, "python3 bench.py --summarize-trace <kernel_trace.csv> <kernel_stats.csv> --kernel %s "
+           "--config %s --steps %d --warmup %d" % (kernel, args.config, args.steps, args.warmup), "```", "",
+           f"`{kernel}` inside the {len(wins)} timed memoized run_mutants calls: {len(durs)} launches, "
+           f"average {np.mean(durs) if durs else 0:.4f} ms, total {np.sum(durs):.3f} ms.", "",
+           "All dispatches of the run (warm-up, timed, vanilla-mode gain steps, run_original):", "",
+           "| kernel | calls | total ms | average us | % |", "|---|---|---|---|---|"]
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:20]:
+        out.append(f"| `{r['Name'][:80]}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.3f} | "
+                   f"{float(r['AverageNs']) / 1e3:.1f} | {float(r['Percentage']):.1f} |")
+    return "\n".join(out) + "\n"
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -81,7 +210,21 @@ def main():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first copy a buffer of this many MiB device to device (a plain copy "
                          "kernel of known size, to scale the HBM byte counters of a profile)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="print the HBM traffic summary of two rocprofv3 --pmc runs and exit")
+    ap.add_argument("--summarize-trace", nargs=2, metavar=("TRACE_CSV", "STATS_CSV"),
+                    help="print the kernel-trace summary of a rocprofv3 run and exit")
+    ap.add_argument("--kernel", default="conv_lds_kernel", help="kernel the summaries follow")
     args = ap.parse_args()
+    if args.summarize_pmc or args.summarize_trace:
+        cfgd = W.CONFIGS[args.config]
+        args.n_inputs_resolved = args.inputs or cfgd["n_inputs"]
+        args.n_mutants_resolved = args.mutants or cfgd["n_mutants"]
+        if args.summarize_pmc:
+            print(summarize_pmc(*args.summarize_pmc, args.kernel, args), end="")
+        else:
+            print(summarize_trace(*args.summarize_trace, args.kernel, args), end="")
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
               "(the inputs would shard across GPUs with one small all-gather of the "
@@ -142,6 +285,7 @@ def main():
     ms_gemm = float(np.mean([s["ms_gemm"] for s in stats]))
     all_flops = 2.0 * st["gemm_macs_algorithmic"]
     all_achieved = all_flops / (ms_gemm * 1e-3) / 1e12 if ms_gemm > 0 else 0.0
+    tr = read_traffic(KERNEL_NAMES[fam], args.config, N, M)
     line = {
         "metric": "mutant-input suffix evals/sec + MFMA/HBM roofline fraction, 1 MI355X",
         "value": M * N / dt,
@@ -164,7 +308,10 @@ def main():
         "mutation_score": [score["ms_num"], score["ms_den"]],
         "roofline": {"bound": "alu" if fam == 1 else "mfma", "kernel": KERNELS[fam],
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                     "frac": achieved / peak, "traffic": None,
+                     "frac": achieved / peak,
+                     "traffic": tr["traffic_bytes_per_launch"] if tr else None,
+                     "traffic_source": os.path.relpath(traffic_path(KERNEL_NAMES[fam], args.config), ROOT)
+                     if tr else None,
                      "launches": launches, "avg_launch_ms": ms_k / max(launches, 1),
                      "alg_flops_per_launch": alg_flops / max(launches, 1),
                      "share_of_run_mutants": ms_k / ms_mut if ms_mut else None,
