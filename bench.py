@@ -12,7 +12,7 @@ second of the whole job.  The line also carries the suffix-only rate
 MFMA peak of its dtype (per-launch HIP events on the library's stream), and
 the CPU oracle timed on a bounded sample.
 
-    python bench.py [--steps K] [--warmup W] [--config cfg2] [--gpus 1]
+    python bench.py [--steps K] [--warmup W] [--config lenet5] [--gpus 1]
 """
 from __future__ import annotations
 
@@ -40,8 +40,8 @@ KERNEL_NAMES = ["dense_kernel", "conv_valu_kernel", "conv_lds_kernel", "conv_mfm
                 "conv_big_kernel"]
 PEAK_HBM_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
-ORACLE_SAMPLE = {"cfg1": (100, 500), "cfg2": (24, 6000), "cfg3": (3, 64), "cfg4": (8, 256),
-                 "cfg5": (2, 16)}
+ORACLE_SAMPLE = {"mlp": (100, 500), "lenet5": (24, 6000), "vgg": (3, 64), "resnet20": (8, 256),
+                 "resnet18w": (2, 16)}
 
 
 def cpu_baseline(wl, n_mut: int, n_in: int):
@@ -194,7 +194,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--config", default="cfg2")
+    ap.add_argument("--config", default="lenet5")
     ap.add_argument("--ratio-index", type=int, default=1)
     ap.add_argument("--inputs", type=int, default=None)
     ap.add_argument("--mutants", type=int, default=None)
@@ -206,7 +206,7 @@ def main():
     ap.add_argument("--gain", type=int, default=None,
                     help="also time vanilla mutation testing (every mutant from the raw "
                          "input) and report the paper's gain (t_v - t) / t_v (default: on "
-                         "for cfg1/cfg2)")
+                         "for mlp/lenet5)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first copy a buffer of this many MiB device to device (a plain copy "
                          "kernel of known size, to scale the HBM byte counters of a profile)")
@@ -322,7 +322,7 @@ def main():
                  "groups": st["n_groups"], "cache_bytes": st["cache_bytes"],
                  "launches_run_mutants": st["launches"]},
     }
-    if args.gain if args.gain is not None else args.config in ("cfg1", "cfg2"):
+    if args.gain if args.gain is not None else args.config in ("mlp", "lenet5"):
         # the paper's measure (Section 6.2): gain = (t_v - t) / t_v with every
         # overhead in both times; vanilla = the same library with memoization off
         m.set_option("vanilla", 1)

@@ -36,7 +36,7 @@ def _plan_ctx(model):
     return m
 
 
-@pytest.mark.parametrize("cfg", ["cfg1", "cfg2", "cfg3", "cfg4", "cfg5"])
+@pytest.mark.parametrize("cfg", ["mlp", "lenet5", "vgg", "resnet20", "resnet18w"])
 def test_planner_matches_oracle_boundaries_and_ledger(cfg):
     wl = W.make_workload(cfg, n_inputs=1, n_mutants=60)
     m = _plan_ctx(wl.model)
@@ -62,7 +62,7 @@ def test_planner_matches_oracle_boundaries_and_ledger(cfg):
 
 
 def test_vanilla_mode_starts_every_mutant_at_the_first_layer():
-    wl = W.make_workload("cfg4", n_inputs=1, n_mutants=40)
+    wl = W.make_workload("resnet20", n_inputs=1, n_mutants=40)
     m = _plan_ctx(wl.model)
     m.set_option("vanilla", 1)
     m.apply(wl.mutants)
@@ -73,7 +73,7 @@ def test_vanilla_mode_starts_every_mutant_at_the_first_layer():
 
 
 def test_identity_mutants_have_no_plan():
-    wl = W.make_workload("cfg1", n_inputs=1, n_mutants=3)
+    wl = W.make_workload("mlp", n_inputs=1, n_mutants=3)
     m = _plan_ctx(wl.model)
     mu = wl.mutants
     m.apply_mutants(5, mu.mutant_id, mu.op, mu.layer, mu.neuron, mu.partner, mu.noise)
@@ -83,7 +83,7 @@ def test_identity_mutants_have_no_plan():
 
 def test_records_without_a_permutation_list_are_accepted():
     # Mutants built field by field carry an empty perm list (no WS records)
-    wl = W.make_workload("cfg1", n_inputs=1, n_mutants=4)
+    wl = W.make_workload("mlp", n_inputs=1, n_mutants=4)
     mu = wl.mutants
     bare = W.Mutants(mu.n_mutants, mu.mutant_id, mu.op, mu.layer, mu.neuron, mu.partner,
                      list(mu.noise))
@@ -96,7 +96,7 @@ def test_records_without_a_permutation_list_are_accepted():
 
 
 def test_invalid_calls_are_rejected_atomically():
-    wl = W.make_workload("cfg2", n_inputs=1, n_mutants=4)
+    wl = W.make_workload("lenet5", n_inputs=1, n_mutants=4)
     m = B.Mure(device=-1)
     mu = wl.mutants
     with pytest.raises(B.MureError) as e:                       # before load_model
@@ -136,7 +136,7 @@ def test_invalid_calls_are_rejected_atomically():
 
 def test_planning_context_refuses_device_work():
     import ctypes as C
-    wl = W.make_workload("cfg1", n_inputs=1, n_mutants=2)
+    wl = W.make_workload("mlp", n_inputs=1, n_mutants=2)
     m = _plan_ctx(wl.model)
     m.apply(wl.mutants)
     st = m.lib.mure_run_original(m.ctx, C.c_void_p(1), 1, None)

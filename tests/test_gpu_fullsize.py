@@ -65,18 +65,18 @@ def _sampled_parity(cfg, ratio_index, n_mut, n_in):
     assert bad == 0
 
 
-def test_cfg2_full_size():
-    _sampled_parity("cfg2", 1, 24, 400)
+def test_lenet5_full_size():
+    _sampled_parity("lenet5", 1, 24, 400)
 
 
-def test_cfg4_full_size():
-    _sampled_parity("cfg4", 1, 24, 48)
+def test_resnet20_full_size():
+    _sampled_parity("resnet20", 1, 24, 48)
 
 
-@pytest.mark.parametrize("ri", [0, 1, 2])
-def test_cfg3_full_size(ri):
-    _sampled_parity("cfg3", ri, 8, 24)
+@pytest.mark.parametrize("ri", [0, 1, 2, 3])
+def test_vgg_full_size(ri):
+    _sampled_parity("vgg", ri, 8, 24)
 
 
-def test_cfg5_full_size():
-    _sampled_parity("cfg5", 0, 3, 10)
+def test_resnet18w_full_size():
+    _sampled_parity("resnet18w", 0, 3, 10)

@@ -27,42 +27,42 @@ def _parity(wl, n_sample_logits=8, tau=1e-3, labels=None, **opts):
     return m, res, words
 
 
-def test_cfg1_full():
-    _parity(W.make_workload("cfg1"))
+def test_mlp_full():
+    _parity(W.make_workload("mlp"))
 
 
-def test_cfg2_ragged_inputs():
-    _parity(W.make_workload("cfg2", n_inputs=1000, n_mutants=60))
+def test_lenet5_ragged_inputs():
+    _parity(W.make_workload("lenet5", n_inputs=1000, n_mutants=60))
 
 
-def test_cfg3_small_each_ratio():
-    for ri in range(3):
-        _parity(W.make_workload("cfg3", n_inputs=70, n_mutants=10, ratio_index=ri))
+def test_vgg_small_each_ratio():
+    for ri in range(4):
+        _parity(W.make_workload("vgg", n_inputs=70, n_mutants=10, ratio_index=ri))
 
 
-def test_cfg4_small():
-    _parity(W.make_workload("cfg4", n_inputs=66, n_mutants=24))
+def test_resnet20_small():
+    _parity(W.make_workload("resnet20", n_inputs=66, n_mutants=24))
 
 
-def test_cfg5_small():
-    _parity(W.make_workload("cfg5", n_inputs=12, n_mutants=4))
+def test_resnet18w_small():
+    _parity(W.make_workload("resnet18w", n_inputs=12, n_mutants=4))
 
 
 def test_ground_truth_labels_path():
-    wl = W.make_workload("cfg2", n_inputs=300, n_mutants=30)
+    wl = W.make_workload("lenet5", n_inputs=300, n_mutants=30)
     labels = np.random.default_rng(9).integers(0, 10, wl.n_inputs).astype(np.int32)
     _parity(wl, labels=labels)
 
 
 def test_chunking_does_not_change_results():
-    wl = W.make_workload("cfg2", n_inputs=700, n_mutants=40)
+    wl = W.make_workload("lenet5", n_inputs=700, n_mutants=40)
     _, w0, k0, s0 = run_gpu(wl)
     _, w1, k1, s1 = run_gpu(wl, chunk_inputs=128, max_workspace_mb=1)
     assert np.array_equal(w0, w1) and np.array_equal(k0, k1) and s0 == s1
 
 
 def test_repeat_is_deterministic():
-    wl = W.make_workload("cfg4", n_inputs=64, n_mutants=12)
+    wl = W.make_workload("resnet20", n_inputs=64, n_mutants=12)
     m = gpu_context(wl)
     m.run_original(device_inputs(wl))
     a = m.run_mutants()
@@ -73,7 +73,7 @@ def test_repeat_is_deterministic():
     assert np.array_equal(z1, z2)
 
 
-@pytest.mark.parametrize("cfg", ["cfg2", "cfg4"])
+@pytest.mark.parametrize("cfg", ["lenet5", "resnet20"])
 def test_identity_mutants_bit_exact(cfg):
     """Zero-noise fuzz at every layer and a mutant without records reproduce
     the original's logits bit for bit and are never killed."""
@@ -96,7 +96,7 @@ def test_identity_mutants_bit_exact(cfg):
 def test_output_layer_closed_forms_on_gpu():
     """On the output layer a switch swaps two logits, an inverse negates one
     and a block zeroes one -- exactly, relative to the GPU's own original."""
-    base = W.make_workload("cfg3", n_inputs=64, n_mutants=1, ratio_index=0)
+    base = W.make_workload("vgg", n_inputs=64, n_mutants=1, ratio_index=0)
     md = base.model
     out = len(md.nodes) - 1
     muts = W.Mutants(3, np.array([0, 1, 2], np.int32), np.array([W.NS, W.NAI, W.NEB], np.int32),
@@ -117,7 +117,7 @@ def test_output_layer_closed_forms_on_gpu():
 
 def test_state_machine_errors():
     from paper_2607_18582_amd import MureError, MURE_E_STATE
-    wl = W.make_workload("cfg1", n_inputs=64, n_mutants=4)
+    wl = W.make_workload("mlp", n_inputs=64, n_mutants=4)
     m = gpu_context(wl)
     with pytest.raises(MureError) as e:
         m.run_mutants()
@@ -132,12 +132,12 @@ def test_state_machine_errors():
 
 def test_weight_shuffle_operator():
     """The paper's fourth mutator (weight shuffle) against the oracle."""
-    for cfg, ni, nm in (("cfg2", 300, 40), ("cfg4", 66, 20)):
+    for cfg, ni, nm in (("lenet5", 300, 40), ("resnet20", 66, 20)):
         _parity(W.make_workload(cfg, n_inputs=ni, n_mutants=nm,
                                 ops=(W.GF, W.NEB, W.NAI, W.NS, W.WS)))
 
 
-@pytest.mark.parametrize("cfg", ["cfg2", "cfg3", "cfg4"])
+@pytest.mark.parametrize("cfg", ["lenet5", "vgg", "resnet20"])
 def test_vanilla_mode_equals_memoized_bit_for_bit(cfg):
     """Theorem 1 on the GPU: running every mutant from the raw input gives
     exactly the memoized result -- kill bits, score and logits, bit for bit."""

@@ -230,7 +230,7 @@ def _edge_set(m):
     return {(p, v) for v, n in enumerate(m.nodes) for p in n.inputs}
 
 
-@pytest.mark.parametrize("cfg", ["cfg1", "cfg2", "cfg3", "cfg4", "cfg5"])
+@pytest.mark.parametrize("cfg", ["mlp", "lenet5", "vgg", "resnet20", "resnet18w"])
 def test_dep_graph_and_boundary_definitions_agree(cfg):
     c = W.CONFIGS[cfg]
     m = W.make_model(c["graph"], c["dtype"], c["bias_std"])
@@ -280,7 +280,7 @@ def test_identity_mutants_never_killed(dtype):
 
 
 def test_prefix_activations_equal_original():
-    wl = W.make_workload("cfg2", n_inputs=8, n_mutants=40)
+    wl = W.make_workload("lenet5", n_inputs=8, n_mutants=40)
     om = O.OracleModel(wl.model)
     orig = O.forward_all(om, wl.inputs)
     for mid in range(wl.mutants.n_mutants):
@@ -293,7 +293,7 @@ def test_prefix_activations_equal_original():
 
 # ---------------------------------------------------------------- Lemma 4 / Theorem 2
 
-@pytest.mark.parametrize("cfg", ["cfg1", "cfg2", "cfg4"])
+@pytest.mark.parametrize("cfg", ["mlp", "lenet5", "resnet20"])
 def test_acceleration_closed_form(cfg):
     wl = W.make_workload(cfg, n_inputs=1, n_mutants=200)
     om = O.OracleModel(wl.model)
@@ -304,4 +304,4 @@ def test_acceleration_closed_form(cfg):
         assert c["cost_prefix"] >= 0
         total_v += c["vanilla"]; total_m += c["memoized"]
     assert total_m < total_v                                # strict (Theorem 2)
-    assert sum(macs) == {"cfg1": 109184, "cfg2": 281640, "cfg4": 40551040}[cfg]
+    assert sum(macs) == {"mlp": 109184, "lenet5": 281640, "resnet20": 40551040}[cfg]

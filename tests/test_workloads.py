@@ -6,8 +6,8 @@ import workloads as W
 
 
 def test_config_sizes():
-    expect = {"cfg1": (109386, 202, 4), "cfg2": (44426, 236, 6), "cfg3": (2196810, 1162, 9),
-              "cfg4": (269034, 698, 31), "cfg5": (11266632, 5000, 31)}
+    expect = {"mlp": (109386, 202, 4), "lenet5": (44426, 236, 6), "vgg": (2196810, 1162, 9),
+              "resnet20": (269034, 698, 31), "resnet18w": (11266632, 5000, 31)}
     for cfg, (params, neurons, nodes) in expect.items():
         c = W.CONFIGS[cfg]
         m = W.make_model(c["graph"], c["dtype"], c["bias_std"])
@@ -19,15 +19,15 @@ def test_config_sizes():
 
 
 def test_prefix_stable_inputs_and_mutants():
-    a = W.make_workload("cfg2", n_inputs=300, n_mutants=30)
-    b = W.make_workload("cfg2", n_inputs=100, n_mutants=10)
+    a = W.make_workload("lenet5", n_inputs=300, n_mutants=30)
+    b = W.make_workload("lenet5", n_inputs=100, n_mutants=10)
     assert np.array_equal(a.inputs[:100], b.inputs)
     s = a.mutants.subset(10)
     for f in ("mutant_id", "op", "layer", "neuron", "partner"):
         assert np.array_equal(getattr(s, f), getattr(b.mutants, f))
 
 
-@pytest.mark.parametrize("cfg,k", [("cfg1", 1), ("cfg2", 2), ("cfg4", 7)])
+@pytest.mark.parametrize("cfg,k", [("mlp", 1), ("lenet5", 2), ("resnet20", 7)])
 def test_layer_first_sampling(cfg, k):
     wl = W.make_workload(cfg, n_inputs=1, n_mutants=200)
     mu = wl.mutants
@@ -46,19 +46,19 @@ def test_layer_first_sampling(cfg, k):
                 assert mu.partner[i] != mu.neuron[i] and 0 <= mu.partner[i] < node.c_out
             if mu.op[i] == W.GF:
                 assert mu.noise[i].shape == (node.fan_in,) and mu.noise[i].dtype == np.float32
-    if cfg == "cfg4":
+    if cfg == "resnet20":
         names = {wl.model.nodes[l].name for l in mu.layer}
         assert "stem" not in names
 
 
 def test_uniform_sampling_k_per_ratio():
-    for ri, k in enumerate((1, 12, 58)):
-        wl = W.make_workload("cfg3", n_inputs=1, n_mutants=5, ratio_index=ri)
+    for ri, k in enumerate((1, 12, 58, 35)):
+        wl = W.make_workload("vgg", n_inputs=1, n_mutants=5, ratio_index=ri)
         assert wl.mutants.n_records == 5 * k
 
 
 def test_gf_noise_sigma():
-    wl = W.make_workload("cfg2", n_inputs=1, n_mutants=400)
+    wl = W.make_workload("lenet5", n_inputs=1, n_mutants=400)
     mu = wl.mutants
     for l in wl.model.weighted_nodes():
         recs = [i for i in range(mu.n_records) if mu.op[i] == W.GF and mu.layer[i] == l]

@@ -256,23 +256,24 @@ def _k(ratio: float, n_neurons: int) -> int:
 # the five workloads
 
 CONFIGS: Dict[str, dict] = {
-    "cfg1": dict(graph="mlp", dtype="f32", bias_std=0.0, n_inputs=500, dist="uniform",
-                 n_mutants=100, ratio=None, k=1, mode="layer_first", variant=0,
-                 desc="MLP 784-128-64-10 fp32, 500 inputs U[0,1), 100 mutants of 1 neuron"),
-    "cfg2": dict(graph="lenet5", dtype="f32", bias_std=0.01, n_inputs=10000, dist="uniform",
-                 n_mutants=1000, ratio=0.01, mode="layer_first", variant=0,
-                 desc="LeNet-5 28x28x1 fp32, 10,000 inputs U[0,1), 1,000 mutants at 1%"),
-    "cfg3": dict(graph="vgg", dtype="bf16", bias_std=0.01, n_inputs=10000, dist="normal",
-                 n_mutants=2000, ratios=(0.001, 0.01, 0.05), mode="uniform",
-                 desc="VGG-style 32x32x3 bf16, 10,000 inputs N(0,1), 2,000 mutants per ratio"),
-    "cfg4": dict(graph="resnet20", dtype="bf16", bias_std=0.01, n_inputs=10000, dist="normal",
-                 n_mutants=1000, ratio=0.01, mode="layer_first", variant=0,
-                 desc="ResNet-20 32x32x3 bf16, 10,000 inputs N(0,1), 1,000 mutants, "
-                      "first mutated layer uniform over 19 layers"),
-    "cfg5": dict(graph="resnet18w", dtype="bf16", bias_std=0.01, n_inputs=5000, dist="normal",
-                 n_mutants=500, ratio=0.05, mode="uniform", variant=0,
-                 desc="ResNet-18-style 64x64x3 bf16 FC200, 5,000 inputs N(0,1), "
-                      "500 mutants at 5%"),
+    "mlp": dict(graph="mlp", dtype="f32", bias_std=0.0, n_inputs=500, dist="uniform",
+                n_mutants=100, ratio=None, k=1, mode="layer_first", variant=0,
+                desc="MLP 784-128-64-10 fp32, 500 inputs U[0,1), 100 mutants of 1 neuron"),
+    "lenet5": dict(graph="lenet5", dtype="f32", bias_std=0.01, n_inputs=10000, dist="uniform",
+                   n_mutants=1000, ratio=0.01, mode="layer_first", variant=0,
+                   desc="LeNet-5 28x28x1 fp32, 10,000 inputs U[0,1), 1,000 mutants at 1%"),
+    # mutation ratios 0.1%, 1%, 3%, 5% (the sweep of the paper's RQ2)
+    "vgg": dict(graph="vgg", dtype="bf16", bias_std=0.01, n_inputs=10000, dist="normal",
+                n_mutants=2000, ratios=(0.001, 0.01, 0.05, 0.03), mode="uniform",
+                desc="VGG-style 32x32x3 bf16, 10,000 inputs N(0,1), 2,000 mutants per ratio"),
+    "resnet20": dict(graph="resnet20", dtype="bf16", bias_std=0.01, n_inputs=10000, dist="normal",
+                     n_mutants=1000, ratio=0.01, mode="layer_first", variant=0,
+                     desc="ResNet-20 32x32x3 bf16, 10,000 inputs N(0,1), 1,000 mutants, "
+                          "first mutated layer uniform over 19 layers"),
+    "resnet18w": dict(graph="resnet18w", dtype="bf16", bias_std=0.01, n_inputs=5000, dist="normal",
+                      n_mutants=500, ratio=0.05, mode="uniform", variant=0,
+                      desc="ResNet-18-style 64x64x3 bf16 FC200, 5,000 inputs N(0,1), "
+                           "500 mutants at 5%"),
 }
 
 _MODEL_CACHE: Dict[str, Model] = {}
@@ -297,8 +298,8 @@ def _candidates(graph: str, model: Model) -> List[int]:
 
 def make_workload(cfg: str, n_inputs: Optional[int] = None, n_mutants: Optional[int] = None,
                   ratio_index: int = 1, ops: Sequence[int] = (GF, NEB, NAI, NS)) -> Workload:
-    """Build workload ``cfg`` ("cfg1".."cfg5"); ``n_inputs``/``n_mutants``
-    truncate it (prefix-stable); ``ratio_index`` picks cfg3's ratio; ``ops``
+    """Build workload ``cfg`` ("mlp".."resnet18w"); ``n_inputs``/``n_mutants``
+    truncate it (prefix-stable); ``ratio_index`` picks vgg's ratio; ``ops``
     the operators drawn (the paper's fourth, weight shuffle, is WS)."""
     c = CONFIGS[cfg]
     model = make_model(c["graph"], c["dtype"], c["bias_std"])
