@@ -21,10 +21,12 @@ constexpr int BIG_BK = 64, BIG_LD = BIG_BK + 8;   // padded LDS rows (bf16)
 // input, so every gather is an unconditional 16-byte load.
 static __device__ __attribute__((aligned(16))) v4u g_zero_page[16] = {};
 
-// TAP64: C_in % 64 == 0, so every 64-wide k chunk lies inside one filter tap
-// and each thread's 4 vectors are 64 contiguous bytes of one input pixel (one
-// bounds check, one address per chunk).
-template <int BM, int BN, int WAVES_M, int WAVES_N, bool TAP64>
+// G: 16-byte vectors (8 input channels each) per filter tap in a thread's
+// half chunk of 32 k -- 4 when C_in % 32 == 0, 2 when C_in % 16 == 0, else 1.
+// The tap of each group is the same for the whole wavefront, so its index
+// math runs once per wave on the scalar unit and each row needs one bounds
+// check and one address per group.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int G>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N)
 void conv_big_kernel(ConvArgs a) {
   constexpr int THREADS = 64 * WAVES_M * WAVES_N;
@@ -34,9 +36,11 @@ void conv_big_kernel(ConvArgs a) {
   constexpr int TM = WM / 16, TN = WN / 16;
   constexpr int BVEC = BN * BK / 8;                    // 16-byte vectors of a B chunk
   constexpr int BPT = (BVEC + THREADS - 1) / THREADS;  // per thread
-  __shared__ __attribute__((aligned(16))) bf16_t As[BM * LD];
-  __shared__ __attribute__((aligned(16))) bf16_t Bs[BN * LD];
-  __shared__ int ktab[1024];                           // per 8-k vector: tap offset | (dy, dx)
+  __shared__ __attribute__((aligned(16))) bf16_t smem[(BM + BN) * LD];
+  bf16_t* const As = smem;
+  bf16_t* const Bs = smem + BM * LD;
+  // the epilogue stages each wave's rounded tile here: WM x (WN + 8) per wave
+  constexpr bool STAGE_FITS = BM * (BN + 8 * WAVES_N) <= (BM + BN) * LD;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WAVES_M, wn = wave / WAVES_M;
@@ -47,20 +51,13 @@ void conv_big_kernel(ConvArgs a) {
   const bf16_t* __restrict__ Wt = reinterpret_cast<const bf16_t*>(a.wtab[slot]);
   const int ncol = a.cols ? a.ncols : a.Cout;
   const bf16_t* const zp = reinterpret_cast<const bf16_t*>(g_zero_page);
-  const int kvec = (a.K + 7) / 8;
-  if constexpr (!TAP64) {
-    for (int v = tid; v < kvec; v += THREADS) {
-      const int k = v * 8, ci = k % a.C, t = k / a.C;
-      const int dy = t / a.kw, dx = t % a.kw;
-      ktab[v] = ((dy * a.W + dx) * a.C + ci) | (dy << 24) | (dx << 28);
-    }
-  }
 
   // the A rows this thread gathers: rows arow + RSTEP*r, k half ahalf (a wave
   // covers 64 consecutive rows of one half, so its 16-byte LDS stores hit
   // distinct banks)
   constexpr int RSTEP = THREADS / 2;
-  const int arow = tid % RSTEP, ahalf = tid / RSTEP;
+  const int arow = tid % RSTEP;
+  const int ahalf = __builtin_amdgcn_readfirstlane(tid / RSTEP);   // wave-uniform
   bool mvalid[ROWS_PER_THREAD];
   int iy0[ROWS_PER_THREAD], ix0[ROWS_PER_THREAD];
   const bf16_t* inrow[ROWS_PER_THREAD];
@@ -110,35 +107,22 @@ void conv_big_kernel(ConvArgs a) {
 
   v4u ra[ROWS_PER_THREAD][4], rb[BPT];
   auto load_chunk = [&](int kc) {
-    if constexpr (TAP64) {
-      // chunk kc: tap t = kc / C (uniform), channels ci0 .. ci0 + 63
-      const int t = kc / a.C, ci0 = kc - t * a.C;
-      const int dy = t / a.kw, dx = t - dy * a.kw;
-      const int off = (dy * a.W + dx) * a.C + ci0 + ahalf * 32;
+#pragma unroll
+    for (int jg = 0; jg < 4; jg += G) {
+      // k of this group (wave-uniform): tap t, first channel ci
+      const int k = kc + ahalf * 32 + jg * 8;
+      int t, ci, dy, dx;
+      divmodu(a.dC, (uint32_t)k, t, ci);
+      divmodu(a.dKW, (uint32_t)t, dy, dx);
+      const int off = (dy * a.W + dx) * a.C + ci;
+      if (k >= a.K) dy = -(1 << 20);                 // past the end: every row reads zeros
 #pragma unroll
       for (int r = 0; r < ROWS_PER_THREAD; ++r) {
         const int iy = iy0[r] + dy, ix = ix0[r] + dx;
         const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
         const v4u* src = reinterpret_cast<const v4u*>(ok ? inrow[r] + off : zp);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) ra[r][j] = src[j];
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int v = (kc >> 3) + ahalf * 4 + j;
-        int code = 0, dy = -(1 << 20), dx = 0;       // k past the end: out of the image
-        if (v < kvec) {
-          code = ktab[v];
-          dy = (code >> 24) & 15;
-          dx = (code >> 28) & 15;
-        }
-#pragma unroll
-        for (int r = 0; r < ROWS_PER_THREAD; ++r) {
-          const int iy = iy0[r] + dy, ix = ix0[r] + dx;
-          const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
-          ra[r][j] = *reinterpret_cast<const v4u*>(ok ? inrow[r] + (code & 0xFFFFFF) : zp);
-        }
+        for (int g = 0; g < G; ++g) ra[r][jg + g] = src[g];
       }
     }
 #pragma unroll
@@ -171,30 +155,102 @@ void conv_big_kernel(ConvArgs a) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
+  auto mma_step = [&](int ks) {
+    v8bf av[TM], bv[TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+      av[i] = *reinterpret_cast<const v8bf*>(&As[(wm * WM + i * 16 + (lane & 15)) * LD + ks * 32 + (lane >> 4) * 8]);
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      bv[j] = *reinterpret_cast<const v8bf*>(&Bs[(wn * WN + j * 16 + (lane & 15)) * LD + ks * 32 + (lane >> 4) * 8]);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+  };
+
   load_chunk(0);
   for (int kc = 0; kc < a.K; kc += BK) {
     store_chunk();
     __syncthreads();
     if (kc + BK < a.K) load_chunk(kc + BK);             // next chunk in flight
-#pragma unroll
-    for (int ks = 0; ks < BK / 32; ++ks) {
-      v8bf av[TM], bv[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-        av[i] = *reinterpret_cast<const v8bf*>(&As[(wm * WM + i * 16 + (lane & 15)) * LD + ks * 32 + (lane >> 4) * 8]);
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bv[j] = *reinterpret_cast<const v8bf*>(&Bs[(wn * WN + j * 16 + (lane & 15)) * LD + ks * 32 + (lane >> 4) * 8]);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+    if (kc + BK <= a.K) {
+      mma_step(0);
+      mma_step(1);
+    } else {                                          // the tail: skip the all-zero half
+      mma_step(0);
+      if (kc + 32 < a.K) mma_step(1);
     }
     __syncthreads();
   }
 
   const float* __restrict__ bias = a.btab[slot];
+  if constexpr (STAGE_FITS) {
+    if (!a.cols && a.Cout % 8 == 0 && !a.out_f32 && (a.add_mode == 0 || (a.add_mode == 1 && !a.add_out_f32))) {
+      // Round the wave's tile into LDS (bias, ReLU, pool applied), then store
+      // whole 16-byte channel vectors: rows of the output are [pixel][C_out].
+      constexpr int OLD = WN + 8;
+      bf16_t* Os = smem + wave * WM * OLD;
+      const int RW = a.pool ? WM / 4 : WM;               // staged rows
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int nl = j * 16 + (lane & 15);
+        const int n = n0 + wn * WN + nl;
+        const float bv = n < a.Cout ? bias[n] : 0.f;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[e] = acc[i][j][e] + bv;
+            if (a.relu) v[e] = fmaxf(v[e], 0.f);
+          }
+          if (a.pool) {
+            Os[(i * 4 + (lane >> 4)) * OLD + nl] = f2bf(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) Os[(i * 16 + (lane >> 4) * 4 + e) * OLD + nl] = f2bf(v[e]);
+          }
+        }
+      }
+      __syncthreads();                                   // the staged tiles are complete
+      const int Pout = a.pool ? a.P / 4 : a.P;
+      const int Mout = a.pool ? Mslot / 4 : Mslot;
+      const int g0 = (m0 + wm * WM) / (a.pool ? 4 : 1);
+      const DivU32 dpo = a.pool ? a.dPq : a.dP;
+      for (int idx = lane; idx < RW * (WN / 8); idx += 64) {
+        const int row = idx / (WN / 8), vc = idx % (WN / 8);
+        const int g = g0 + row;
+        const int n = n0 + wn * WN + vc * 8;
+        if (g >= Mout || n >= a.Cout) continue;
+        int xo, q;
+        divmodu(dpo, (uint32_t)g, xo, q);
+        const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xo, a.nx, a.x0);
+        v4u val = *reinterpret_cast<const v4u*>(&Os[row * OLD + vc * 8]);
+        if (a.add_mode == 1) {
+          // conv_b's rounded output + the identity shortcut, in float32, then ReLU
+          const v4u sk = *reinterpret_cast<const v4u*>(
+              reinterpret_cast<const bf16_t*>(a.skip.p) +
+              row_index(a.skip.mode, (int64_t)slot * a.nx + xo, a.nx, a.x0) * a.skip.row_elems +
+              (int64_t)q * a.Cout + n);
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            uint32_t o = 0;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              float t = bf2f((bf16_t)(val[w] >> (16 * h))) + bf2f((bf16_t)(sk[w] >> (16 * h)));
+              if (a.add_relu) t = fmaxf(t, 0.f);
+              o |= (uint32_t)f2bf(t) << (16 * h);
+            }
+            val[w] = o;
+          }
+        }
+        *reinterpret_cast<v4u*>(reinterpret_cast<bf16_t*>(a.out) + ro * a.out_row + (int64_t)q * a.Cout + n) = val;
+      }
+      return;
+    }
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int mb = m0 + wm * WM + i * 16 + (lane >> 4) * 4;
@@ -262,21 +318,21 @@ void conv_big_kernel(ConvArgs a) {
 
 int conv_big_bn(int cout) { return cout <= 16 ? 16 : cout <= 32 ? 32 : cout <= 64 ? 64 : 128; }
 
-template <bool TAP64>
+template <int G>
 static hipError_t launch_big(const ConvArgs& a, dim3 grid, int bm, int bn, hipStream_t s) {
   if (bm == 128) {
     switch (bn) {
-      case 16: hipLaunchKernelGGL((conv_big_kernel<128, 16, 4, 1, TAP64>), grid, dim3(256), 0, s, a); break;
-      case 32: hipLaunchKernelGGL((conv_big_kernel<128, 32, 4, 1, TAP64>), grid, dim3(256), 0, s, a); break;
-      case 64: hipLaunchKernelGGL((conv_big_kernel<128, 64, 4, 1, TAP64>), grid, dim3(256), 0, s, a); break;
-      default: hipLaunchKernelGGL((conv_big_kernel<128, 128, 2, 2, TAP64>), grid, dim3(256), 0, s, a); break;
+      case 16: hipLaunchKernelGGL((conv_big_kernel<128, 16, 4, 1, G>), grid, dim3(256), 0, s, a); break;
+      case 32: hipLaunchKernelGGL((conv_big_kernel<128, 32, 4, 1, G>), grid, dim3(256), 0, s, a); break;
+      case 64: hipLaunchKernelGGL((conv_big_kernel<128, 64, 4, 1, G>), grid, dim3(256), 0, s, a); break;
+      default: hipLaunchKernelGGL((conv_big_kernel<128, 128, 2, 2, G>), grid, dim3(256), 0, s, a); break;
     }
   } else {
     switch (bn) {
-      case 16: hipLaunchKernelGGL((conv_big_kernel<256, 16, 8, 1, TAP64>), grid, dim3(512), 0, s, a); break;
-      case 32: hipLaunchKernelGGL((conv_big_kernel<256, 32, 8, 1, TAP64>), grid, dim3(512), 0, s, a); break;
-      case 64: hipLaunchKernelGGL((conv_big_kernel<256, 64, 4, 2, TAP64>), grid, dim3(512), 0, s, a); break;
-      default: hipLaunchKernelGGL((conv_big_kernel<256, 128, 4, 2, TAP64>), grid, dim3(512), 0, s, a); break;
+      case 16: hipLaunchKernelGGL((conv_big_kernel<256, 16, 8, 1, G>), grid, dim3(512), 0, s, a); break;
+      case 32: hipLaunchKernelGGL((conv_big_kernel<256, 32, 8, 1, G>), grid, dim3(512), 0, s, a); break;
+      case 64: hipLaunchKernelGGL((conv_big_kernel<256, 64, 4, 2, G>), grid, dim3(512), 0, s, a); break;
+      default: hipLaunchKernelGGL((conv_big_kernel<256, 128, 4, 2, G>), grid, dim3(512), 0, s, a); break;
     }
   }
   return hipGetLastError();
@@ -298,8 +354,12 @@ hipError_t launch_conv_big(const ConvArgs& a0, int nslots, hipStream_t s) {
   const int64_t Mslot = (int64_t)a.nx * a.P;
   const int ncol = a.cols ? a.ncols : a.Cout;
   dim3 grid((unsigned)((Mslot + bm - 1) / bm), (unsigned)nslots, (unsigned)((ncol + bn - 1) / bn));
-  if (a.C % 64 == 0) return launch_big<true>(a, grid, bm, bn, s);
-  return launch_big<false>(a, grid, bm, bn, s);
+  a.dPq = make_divu32((uint32_t)std::max(1, a.P / 4));
+  a.dC = make_divu32((uint32_t)a.C);
+  a.dKW = make_divu32((uint32_t)a.kw);
+  if (a.C % 32 == 0) return launch_big<4>(a, grid, bm, bn, s);
+  if (a.C % 16 == 0) return launch_big<2>(a, grid, bm, bn, s);
+  return launch_big<1>(a, grid, bm, bn, s);
 }
 
 }  // namespace mure

@@ -52,21 +52,64 @@ __global__ void gap_kernel(GapArgs a) {
 // ---------------------------------------------------------------- channel patch
 // Node mmi of an effect-block / switch mutant: the original's output with
 // channel c taken from original channel chmap[c] (-1: zero).  Bitwise copy.
+// A block copies `rows` consecutive inputs of one slot: a contiguous span of
+// the cache and of the chunk buffer.  16-byte vectors whose channels the map
+// keeps in place are copied whole, the others element by element.
+constexpr int PATCH_MAXC = 4096;
+
 template <typename E>
-__global__ void patch_kernel(PatchArgs a) {
-  const int64_t per = (int64_t)a.P * a.C;
-  const int64_t total = (int64_t)a.nslots * a.nx * per;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t rr = i / per;               // row within this launch
-    const int64_t e = i % per;
-    const int c = (int)(e % a.C);
-    const int sl = (int)(rr / a.nx);
-    const int xi = (int)(rr % a.nx);
-    const int src = a.chmap[(int64_t)(a.chmap_slot0 + sl) * a.C + c];
-    const E* cp = reinterpret_cast<const E*>(a.cache) + ((int64_t)a.x0 + xi) * per;
-    E v = src < 0 ? E(0) : cp[e - c + src];
-    reinterpret_cast<E*>(a.out)[((int64_t)(a.slot0 + sl) * a.nx + xi) * per + e] = v;
+__global__ __launch_bounds__(256) void patch_kernel(PatchArgs a, int rows, DivU32 dcv, DivU32 dc) {
+  constexpr int VEC = 16 / sizeof(E);
+  __shared__ int map[PATCH_MAXC];
+  __shared__ unsigned char keep[PATCH_MAXC / VEC];
+  const int tid = threadIdx.x;
+  const int sl = (int)blockIdx.y;
+  const int32_t* cm = a.chmap + (int64_t)(a.chmap_slot0 + sl) * a.C;
+  for (int c = tid; c < a.C; c += 256) map[c] = cm[c];
+  __syncthreads();
+  const bool vec = a.C % VEC == 0;
+  const int CV = a.C / VEC;
+  if (vec) {
+    for (int v = tid; v < CV; v += 256) {
+      bool k = true;
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) k = k && map[v * VEC + j] == v * VEC + j;
+      keep[v] = k ? 1 : 0;
+    }
+    __syncthreads();
+  }
+  const int xi0 = (int)blockIdx.x * rows;
+  const int nr = min(rows, a.nx - xi0);
+  if (nr <= 0) return;
+  const int per = a.P * a.C;
+  const E* src = reinterpret_cast<const E*>(a.cache) + ((int64_t)a.x0 + xi0) * per;
+  E* dst = reinterpret_cast<E*>(a.out) + ((int64_t)(a.slot0 + sl) * a.nx + xi0) * per;
+  if (vec) {
+    const int nv = nr * (per / VEC);
+    for (int v = tid; v < nv; v += 256) {
+      const int cv = (int)(v - divu(dcv, (uint32_t)v) * CV);
+      if (keep[cv]) {
+        reinterpret_cast<v4u*>(dst)[v] = reinterpret_cast<const v4u*>(src)[v];
+      } else {
+        const int e0 = v * VEC, pix0 = e0 - cv * VEC;
+        E t[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+          const int m = map[cv * VEC + j];
+          t[j] = m < 0 ? E(0) : src[pix0 + m];
+        }
+        v4u o;
+        __builtin_memcpy(&o, t, 16);
+        reinterpret_cast<v4u*>(dst)[v] = o;
+      }
+    }
+  } else {
+    const int ne = nr * per;
+    for (int e = tid; e < ne; e += 256) {
+      const int c = (int)(e - divu(dc, (uint32_t)e) * a.C);
+      const int m = map[c];
+      dst[e] = m < 0 ? E(0) : src[e - c + m];
+    }
   }
 }
 
@@ -231,10 +274,17 @@ hipError_t launch_gap(const GapArgs& a, int dtype, hipStream_t s) {
 }
 
 hipError_t launch_patch(const PatchArgs& a, hipStream_t s) {
-  const int64_t total = (int64_t)a.nslots * a.nx * a.P * a.C;
-  if (total == 0) return hipSuccess;
-  if (a.esize == 4) hipLaunchKernelGGL(patch_kernel<uint32_t>, dim3(grid_for(total)), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(patch_kernel<uint16_t>, dim3(grid_for(total)), dim3(256), 0, s, a);
+  if (a.nslots <= 0 || a.nx <= 0 || a.P <= 0 || a.C <= 0) return hipSuccess;
+  if (a.C > PATCH_MAXC || a.nslots > 65535 || (a.esize != 2 && a.esize != 4)) return hipErrorInvalidValue;
+  const int64_t per = (int64_t)a.P * a.C;
+  // about 16K elements per block
+  const int rows = (int)std::max<int64_t>(1, std::min<int64_t>(a.nx, 16384 / per));
+  if (per * rows >= INT32_MAX) return hipErrorInvalidValue;
+  const int vec = 16 / a.esize;
+  const DivU32 dcv = make_divu32((uint32_t)std::max(1, a.C / vec)), dc = make_divu32((uint32_t)a.C);
+  dim3 grid((unsigned)((a.nx + rows - 1) / rows), (unsigned)a.nslots);
+  if (a.esize == 4) hipLaunchKernelGGL(patch_kernel<uint32_t>, grid, dim3(256), 0, s, a, rows, dcv, dc);
+  else hipLaunchKernelGGL(patch_kernel<uint16_t>, grid, dim3(256), 0, s, a, rows, dcv, dc);
   return hipGetLastError();
 }
 

@@ -94,8 +94,8 @@ struct ConvArgs {
   // channels per slot; the input must be slot independent (prefix cache)
   const DeltaCol* cols = nullptr;
   int ncols = 0, delta_T = 0, col_slot0 = 0;
-  // filled by the launchers: dividers by P, Wp, Wc and H*W
-  DivU32 dP, dWp, dWc, dHW;
+  // filled by the launchers: dividers by P, P/4, Wp, Wc, H*W, C and kw
+  DivU32 dP, dPq, dWp, dWc, dHW, dC, dKW;
 };
 
 // DENSE on MFMA: out[r][n] = sum_k in[r][k] * W[n][k] + b[n] (k in increasing

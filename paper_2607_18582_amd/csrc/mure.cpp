@@ -67,9 +67,6 @@ Placement place_buffers(const Graph& g, const std::vector<int>& nodes, const std
   for (int v : nodes) {
     for (int k = 0; k < g.nodes[v].n_in; ++k) last_use[g.nodes[v].in[k]] = v;
   }
-  for (const auto& kv : fused) {                 // the ADD's inputs are read at conv_b's step or later
-    (void)kv;
-  }
   struct Blk { int64_t off, size; int owner; };
   std::vector<Blk> blocks;
   Placement pl;
