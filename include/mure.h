@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define MURE_VERSION 1
+#define MURE_VERSION 2
 
 typedef struct mure_ctx mure_ctx;
 
@@ -73,14 +73,18 @@ typedef enum {
 
 typedef enum {
   MURE_INPUT = 0,    /* the model input (must be node 0, and only node 0) */
-  MURE_DENSE = 1,    /* y = x W^T + b, optional ReLU */
-  MURE_CONV2D = 2,   /* cross-correlation, stride, zero padding, + b, optional ReLU,
+  MURE_DENSE = 1,    /* y = x W^T + b, optional activation */
+  MURE_CONV2D = 2,   /* cross-correlation, stride, zero padding, + b, optional activation,
                         optional 2x2 stride-2 max-pool (floor) */
-  MURE_ADD = 3,      /* y = in[0] + s(in[1]) in float32, optional ReLU; shortcut 1
+  MURE_ADD = 3,      /* y = in[0] + s(in[1]) in float32, optional activation; shortcut 1
                         ("option A") subsamples in[1] by 2 in H and W and zero-pads
                         its channels, (C_out - C_in)/2 before and the rest after */
   MURE_GAP = 4,      /* global average pool to 1x1xC */
-  MURE_FLATTEN = 5   /* view as 1x1x(H*W*C) */
+  MURE_FLATTEN = 5,  /* view as 1x1x(H*W*C) */
+  MURE_DWCONV = 6    /* depthwise convolution (MobileNetV2): output channel c filters
+                        input channel c with its own kh x kw taps, stride, zero
+                        padding, + b, optional activation; c_in = c_out = C;
+                        weights [C][kh][kw] (fan_in = kh*kw) */
 } mure_kind;
 
 /* One node of the model graph.  The array order is a topological order
@@ -92,11 +96,12 @@ typedef struct {
   int32_t kind;       /* mure_kind */
   int32_t n_in;       /* 0 for INPUT, 2 for ADD, 1 otherwise */
   int32_t in[2];
-  int32_t c_in;       /* CONV2D: input channels; DENSE: H*W*C of its input;
+  int32_t c_in;       /* CONV2D/DWCONV: input channels; DENSE: H*W*C of its input;
                          ADD: channels of in[1]; GAP/FLATTEN: input channels */
   int32_t c_out;      /* output channels (DENSE: units) */
-  int32_t kh, kw, stride, pad;   /* CONV2D only (DENSE: 1,1,1,0) */
-  int32_t relu;       /* 0/1 */
+  int32_t kh, kw, stride, pad;   /* CONV2D/DWCONV only (DENSE: 1,1,1,0) */
+  int32_t relu;       /* activation after the bias (or the sum): 0 none, 1 ReLU,
+                         2 ReLU6 = min(max(x, 0), 6), in float32 */
   int32_t maxpool;    /* CONV2D: 0 or 2 */
   int32_t shortcut;   /* ADD: 0 identity, 1 option A */
 } mure_layer;
@@ -106,12 +111,13 @@ typedef struct {
 typedef struct {
   int32_t mutant;       /* 0 <= mutant < n_mutants */
   int32_t op;           /* mure_op */
-  int32_t layer;        /* a DENSE or CONV2D node */
+  int32_t layer;        /* a DENSE, CONV2D or DWCONV node */
   int32_t neuron;       /* 0 <= neuron < c_out of that node */
   int32_t partner;      /* NEURON_SWITCH: the other neuron (!= neuron); else -1 */
   int32_t reserved;     /* 0 */
   const float* noise;   /* GAUSS_FUZZ: host, fan_in values in W[neuron] order; else NULL */
-  int64_t noise_len;    /* GAUSS_FUZZ: = fan_in (c_in*kh*kw for CONV2D, c_in for DENSE);
+  int64_t noise_len;    /* GAUSS_FUZZ: = fan_in (c_in*kh*kw for CONV2D, kh*kw for DWCONV,
+                           c_in for DENSE);
                            WEIGHT_SHUFFLE: = fan_in (length of perm) */
   const int32_t* perm;  /* WEIGHT_SHUFFLE: host, a permutation of 0..fan_in-1; else NULL */
 } mure_record;
@@ -151,10 +157,11 @@ typedef struct {
   int64_t gemm_macs_algorithmic, gemm_macs_executed;
   /* The same, split by kernel: [0] dense GEMM, [1] vector-ALU convolution
    * (few output channels), [2] LDS-resident convolution, [3] im2col implicit
-   * GEMM with scalar gathers, [4] tiled bf16 implicit GEMM. */
-  int64_t kernel_launches[5];
-  double kernel_ms[5];
-  int64_t kernel_macs_algorithmic[5];
+   * GEMM with scalar gathers, [4] tiled bf16 implicit GEMM, [5] depthwise
+   * convolution. */
+  int64_t kernel_launches[6];
+  double kernel_ms[6];
+  int64_t kernel_macs_algorithmic[6];
 } mure_stats;
 
 /* Version of this interface (MURE_VERSION). */

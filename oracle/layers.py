@@ -4,13 +4,18 @@ Semantics (the same on both sides of the parity check; see the design notes):
   * tensors are NHWC; a DENSE layer reads its input flattened in HWC order;
   * CONV2D: cross-correlation with stride s and zero padding p,
       acc[n,i,j,o] = sum_{dy,dx,c} x[n, i*s+dy-p, j*s+dx-p, c] * W[o,dy,dx,c],
-    then t = fl32(acc + b[o]), optional ReLU, optional 2x2 stride-2 max-pool
-    (floor), then the node-output rounding;
-  * DENSE: t = fl32(sum_c x[n,c] * W[o,c] + b[o]), optional ReLU, rounding;
+    then t = fl32(acc + b[o]), optional activation, optional 2x2 stride-2
+    max-pool (floor), then the node-output rounding;
+  * DWCONV (depthwise): the same with each output channel reading only its
+    own input channel,
+      acc[n,i,j,c] = sum_{dy,dx} x[n, i*s+dy-p, j*s+dx-p, c] * W[c,dy,dx];
+  * DENSE: t = fl32(sum_c x[n,c] * W[o,c] + b[o]), optional activation,
+    rounding;
+  * activation: ReLU max(t, 0) or ReLU6 min(max(t, 0), 6), in float32;
   * ADD: t = fl32(a + s) computed in float32, where s is the second input,
     for option A first subsampled s[:, ::2, ::2, :] and zero-padded in the
     channel dimension ((C_a - C_s)//2 zero channels before, the rest after);
-    optional ReLU; rounding;
+    optional activation; rounding;
   * GAP: t = fl32(mean over H and W); rounding;
   * FLATTEN: a view.
   * Node-output rounding: bf16 models round every node output except the
@@ -27,7 +32,7 @@ from typing import Dict, List, Optional, Sequence
 import numpy as np
 from numpy.lib.stride_tricks import sliding_window_view
 
-from workloads.graph import INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, Model
+from workloads.graph import INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV, Model
 from .numerics import rne_bf16, bf16_bits_to_f32, to_f32
 
 
@@ -53,6 +58,15 @@ def _round_node(model: OracleModel, v: int, t32: np.ndarray) -> np.ndarray:
     if model.dtype == "bf16" and v != model.out:
         return rne_bf16(t32)
     return t32
+
+
+def _act(t: np.ndarray, relu: int) -> np.ndarray:
+    """The node's activation on float32 values: 1 ReLU, 2 ReLU6."""
+    if relu:
+        t = np.maximum(t, np.float32(0))
+    if relu == 2:
+        t = np.minimum(t, np.float32(6))
+    return t
 
 
 def _matmul64(a64: np.ndarray, w2: np.ndarray, accumulate: str) -> np.ndarray:
@@ -86,22 +100,33 @@ def phi(model: OracleModel, v: int, ins: Sequence[np.ndarray], W=None, b=None,
         x = ins[0]
         n = x.shape[0]
         acc = _matmul64(x.reshape(n, -1).astype(np.float64), W, accumulate)
-        t = to_f32(acc + b.astype(np.float64)[None, :])
-        if node.relu:
-            t = np.maximum(t, np.float32(0))
+        t = _act(to_f32(acc + b.astype(np.float64)[None, :]), node.relu)
         return _round_node(model, v, t.reshape(n, 1, 1, node.c_out))
     if node.kind == CONV2D:
         x = ins[0]
         n = x.shape[0]
         cols, ho, wo = _im2col(x.astype(np.float64), node.kh, node.kw, node.stride, node.pad)
         acc = _matmul64(cols, W.reshape(node.c_out, -1), accumulate)
-        t = to_f32(acc + b.astype(np.float64)[None, :]).reshape(n, ho, wo, node.c_out)
-        if node.relu:
-            t = np.maximum(t, np.float32(0))
+        t = _act(to_f32(acc + b.astype(np.float64)[None, :]).reshape(n, ho, wo, node.c_out), node.relu)
         if node.maxpool:
             q = node.maxpool
             h2, w2 = ho // q, wo // q
             t = t[:, :h2 * q, :w2 * q].reshape(n, h2, q, w2, q, node.c_out).max(axis=(2, 4))
+        return _round_node(model, v, np.ascontiguousarray(t))
+    if node.kind == DWCONV:
+        x = ins[0].astype(np.float64)
+        n, h, w, c = x.shape
+        p, st = node.pad, node.stride
+        xp = np.pad(x, ((0, 0), (p, p), (p, p), (0, 0))) if p else x
+        ho = (h + 2 * p - node.kh) // st + 1
+        wo = (w + 2 * p - node.kw) // st + 1
+        W64 = W.reshape(c, node.kh, node.kw).astype(np.float64)
+        acc = np.zeros((n, ho, wo, c), np.float64)
+        for dy in range(node.kh):                  # taps in (dy, dx) order
+            for dx in range(node.kw):
+                tap = xp[:, dy:dy + st * (ho - 1) + 1:st, dx:dx + st * (wo - 1) + 1:st, :]
+                acc += tap * W64[None, None, None, :, dy, dx]
+        t = _act(to_f32(acc + b.astype(np.float64)[None, None, None, :]), node.relu)
         return _round_node(model, v, np.ascontiguousarray(t))
     if node.kind == ADD:
         a, s = ins
@@ -110,9 +135,7 @@ def phi(model: OracleModel, v: int, ins: Sequence[np.ndarray], W=None, b=None,
             extra = a.shape[3] - s.shape[3]
             before = extra // 2
             s = np.pad(s, ((0, 0), (0, 0), (0, 0), (before, extra - before)))
-        t = a.astype(np.float32) + s.astype(np.float32)        # float32 addition
-        if node.relu:
-            t = np.maximum(t, np.float32(0))
+        t = _act(a.astype(np.float32) + s.astype(np.float32), node.relu)   # float32 addition
         return _round_node(model, v, t)
     if node.kind == GAP:
         x = ins[0]

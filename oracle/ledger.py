@@ -1,7 +1,8 @@
 """The additive cost model of Section 5.2, counted in multiply-accumulates.
 
 cost(v) per input = MACs of node v (CONV2D: pre-pool output pixels * C_out *
-kh*kw*C_in; DENSE: C_in*C_out; other kinds 0).  It is non-negative (C1),
+kh*kw*C_in; DWCONV: output pixels * C * kh*kw; DENSE: C_in*C_out; other
+kinds 0).  It is non-negative (C1),
 additive over a prefix/suffix split (C2) and depends only on the layer shapes
 (C3).  For a cluster C of mutants sharing mmi, the prefix P is every node
 before mmi and the chopped mutant every node from mmi on, so
@@ -11,7 +12,7 @@ from __future__ import annotations
 
 from typing import Dict, List
 
-from workloads.graph import CONV2D, DENSE, Mutants
+from workloads.graph import CONV2D, DENSE, DWCONV, Mutants
 from .layers import OracleModel
 from .memoized import boundary, get_dep_graph, mutated_layers
 
@@ -19,11 +20,12 @@ from .memoized import boundary, get_dep_graph, mutated_layers
 def node_macs(model: OracleModel) -> List[int]:
     out = []
     for v, n in enumerate(model.nodes):
-        if n.kind == CONV2D:
+        if n.kind in (CONV2D, DWCONV):
             h, w, _ = model.nodes[n.inputs[0]].out_hwc
             ho = (h + 2 * n.pad - n.kh) // n.stride + 1
             wo = (w + 2 * n.pad - n.kw) // n.stride + 1
-            out.append(ho * wo * n.c_out * n.kh * n.kw * n.c_in)
+            per_channel = n.kh * n.kw * (1 if n.kind == DWCONV else n.c_in)
+            out.append(ho * wo * n.c_out * per_channel)
         elif n.kind == DENSE:
             out.append(n.c_in * n.c_out)
         else:

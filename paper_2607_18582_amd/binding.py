@@ -22,7 +22,7 @@ STATUS_NAMES = {0: "MURE_OK", -1: "MURE_E_INVALID", -2: "MURE_E_STATE", -3: "MUR
                 -4: "MURE_E_DEVICE", -5: "MURE_E_UNSUPPORTED"}
 MURE_F32, MURE_BF16 = 0, 1
 OP_GAUSS_FUZZ, OP_EFFECT_BLOCK, OP_ACT_INVERSE, OP_NEURON_SWITCH, OP_WEIGHT_SHUFFLE = 0, 1, 2, 3, 4
-INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN = 0, 1, 2, 3, 4, 5
+INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV = 0, 1, 2, 3, 4, 5, 6
 
 EXPORTED = ["mure_version", "mure_create", "mure_load_model", "mure_apply_mutants",
             "mure_run_original", "mure_run_mutants", "mure_get_logits", "mure_mutant_plan",
@@ -58,8 +58,8 @@ class mure_stats(C.Structure):
                 ("ms_apply", C.c_double), ("ms_run_original", C.c_double),
                 ("ms_run_mutants", C.c_double), ("gemm_launches", C.c_int64),
                 ("ms_gemm", C.c_double), ("gemm_macs_algorithmic", C.c_int64),
-                ("gemm_macs_executed", C.c_int64), ("kernel_launches", C.c_int64 * 5),
-                ("kernel_ms", C.c_double * 5), ("kernel_macs_algorithmic", C.c_int64 * 5)]
+                ("gemm_macs_executed", C.c_int64), ("kernel_launches", C.c_int64 * 6),
+                ("kernel_ms", C.c_double * 6), ("kernel_macs_algorithmic", C.c_int64 * 6)]
 
 
 class MureError(RuntimeError):
@@ -123,13 +123,13 @@ def layer_descriptors(nodes) -> "C.Array":
         L.n_in = len(ins)
         L.in_[0] = ins[0] if len(ins) > 0 else 0
         L.in_[1] = ins[1] if len(ins) > 1 else 0
-        if n.kind in (CONV2D, DENSE):
+        if n.kind in (CONV2D, DENSE, DWCONV):
             L.c_in, L.c_out = int(n.c_in), int(n.c_out)
             L.kh, L.kw, L.stride, L.pad = int(n.kh), int(n.kw), int(n.stride), int(n.pad)
             L.maxpool = int(n.maxpool)
         elif n.kind in (ADD, GAP):
             L.c_in, L.c_out = int(n.c_in), int(n.c_out)
-        L.relu = int(bool(n.relu))
+        L.relu = int(n.relu)
         L.shortcut = int(n.shortcut) if n.kind == ADD else 0
     return arr
 

@@ -31,6 +31,13 @@ template <typename T> __device__ __forceinline__ T from_f(float v);
 template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
 template <> __device__ __forceinline__ bf16_t from_f<bf16_t>(float v) { return f2bf(v); }
 
+// node activation: relu 1 = ReLU, 2 = ReLU6 (min(max(v, 0), 6)), in float32
+__device__ __forceinline__ float act(float v, int relu) {
+  if (relu) v = fmaxf(v, 0.f);
+  if (relu == 2) v = fminf(v, 6.f);
+  return v;
+}
+
 // index of a tensor row for chunk row r (slot-major, nx inputs per slot)
 __device__ __forceinline__ int64_t row_index(int mode, int64_t r, int nx, int x0) {
   return mode == MODE_BUF ? r : (int64_t)x0 + (r % nx);

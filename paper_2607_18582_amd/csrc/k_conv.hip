@@ -140,7 +140,7 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(ConvArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         v[e] = acc[i][j][e] + bv;
-        if (a.relu) v[e] = fmaxf(v[e], 0.f);
+        v[e] = act(v[e], a.relu);
       }
       if (a.pool) {
         const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));

@@ -204,7 +204,7 @@ void conv_big_kernel(ConvArgs a) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             v[e] = acc[i][j][e] + bv;
-            if (a.relu) v[e] = fmaxf(v[e], 0.f);
+            v[e] = act(v[e], a.relu);
           }
           if (a.pool) {
             Os[(i * 4 + (lane >> 4)) * OLD + nl] = f2bf(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
@@ -240,7 +240,7 @@ void conv_big_kernel(ConvArgs a) {
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
               float t = bf2f((bf16_t)(val[w] >> (16 * h))) + bf2f((bf16_t)(sk[w] >> (16 * h)));
-              if (a.add_relu) t = fmaxf(t, 0.f);
+              t = act(t, a.add_relu);
               o |= (uint32_t)f2bf(t) << (16 * h);
             }
             val[w] = o;
@@ -284,7 +284,7 @@ void conv_big_kernel(ConvArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         v[e] = acc[i][j][e] + bv;
-        if (a.relu) v[e] = fmaxf(v[e], 0.f);
+        v[e] = act(v[e], a.relu);
       }
       if (a.pool) {
         const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
@@ -304,7 +304,7 @@ void conv_big_kernel(ConvArgs a) {
           }
           if (a.add_mode == 2 && ++x == a.Wc) { x = 0; ++y; }
           float t = bf2f(f2bf(v[e])) + sv;
-          if (a.add_relu) t = fmaxf(t, 0.f);
+          t = act(t, a.add_relu);
           store_out<bf16_t>(a.out, a.add_out_f32, ro * a.out_row + (int64_t)(pb + e) * a.Cout + n, t);
         }
       } else {

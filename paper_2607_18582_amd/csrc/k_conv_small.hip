@@ -244,7 +244,7 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           v[e] = acc[i][j][e] + bv[j];
-          if (a.relu) v[e] = fmaxf(v[e], 0.f);
+          v[e] = act(v[e], a.relu);
         }
         if (a.pool) {
           const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
@@ -385,7 +385,7 @@ __global__ __launch_bounds__(256) void conv_valu_kernel(ValuArgs a, int R) {
         const int c = a.ch_list ? a.ch_list[c_beg + u] : c_beg + u;
         const float bv = bias[c];
         float v0 = a0 + bv, v1 = a1 + bv, v2 = a2 + bv, v3 = a3 + bv;
-        if (a.relu) { v0 = fmaxf(v0, 0.f); v1 = fmaxf(v1, 0.f); v2 = fmaxf(v2, 0.f); v3 = fmaxf(v3, 0.f); }
+        v0 = act(v0, a.relu); v1 = act(v1, a.relu); v2 = act(v2, a.relu); v3 = act(v3, a.relu);
         const float v = fmaxf(fmaxf(v0, v1), fmaxf(v2, v3));
         if (a.delta_T > 0) store_out<T>(a.out, 0, ro * a.out_row + (int64_t)q * a.delta_T + u, v);
         else store_out<T>(a.out, a.out_f32, ro * a.out_row + (int64_t)q * a.Cout + c, v);
@@ -430,10 +430,10 @@ __global__ __launch_bounds__(256) void conv_valu_kernel(ValuArgs a, int R) {
           const int c = a.ch_list ? a.ch_list[c_beg + ub + u] : c_beg + ub + u;
           const float bv = bias[c];
           float v = acc[0][u] + bv;
-          if (a.relu) v = fmaxf(v, 0.f);
+          v = act(v, a.relu);
           for (int j = 1; j < npix; ++j) {
             float w2 = acc[j][u] + bv;
-            if (a.relu) w2 = fmaxf(w2, 0.f);
+            w2 = act(w2, a.relu);
             v = fmaxf(v, w2);
           }
           if (a.delta_T > 0)

@@ -220,7 +220,7 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
       for (int e = 0; e < 4; ++e) {
         const int rl = wm * WM + i * 16 + (lane >> 4) * 4 + e;
         float v = acc[i][j][e] + bv;
-        if (a.relu) v = fmaxf(v, 0.f);
+        v = act(v, a.relu);
         if (a.write_out && n < ncol && m0 + rl < a.nx) {
           const int64_t ro = row_index(a.out_mode, (int64_t)os * a.nx + m0 + rl, a.nx, a.x0);
           store_out<T>(a.out, a.out_f32, ro * orow + oc, v);

@@ -1,0 +1,145 @@
+// Depthwise convolution (MobileNetV2's 3x3 filters) on the vector ALU.
+//
+// Output channel c reads only input channel c, so the node is a per-element
+// chain of kh*kw fused multiply-adds: memory-bound, no contraction for the
+// matrix cores.  Each element's chain runs over the in-image taps in (dy, dx)
+// order, starting from 0, then adds the bias -- the same chain in the full
+// kernel and in the channel-list (delta) kernel, so a delta is bit-identical
+// to the full node.  The full kernel moves 16-byte channel vectors (8 bf16 or
+// 4 fp32 channels of one pixel); the block's slot weights sit in LDS as fp32.
+#include "dev.hpp"
+
+namespace mure {
+
+namespace {
+constexpr int DW_MAXW = 8192;                         // C * kh * kw staged in LDS
+constexpr int DW_MAXC = 2048;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void dw_full_kernel(DwArgs a, int rows, DivU32 dcv, DivU32 dpix,
+                                                      DivU32 dwo) {
+  constexpr int VEC = 16 / sizeof(T);
+  __shared__ float wl[DW_MAXW];
+  __shared__ float bl[DW_MAXC];
+  const int tid = threadIdx.x;
+  const int sl = a.slot0 + (int)blockIdx.y;
+  const int taps = a.kh * a.kw;
+  const T* __restrict__ Wt = reinterpret_cast<const T*>(a.wtab[sl]);
+  for (int e = tid; e < a.C * taps; e += 256) wl[e] = to_f<T>(Wt[e]);
+  for (int c = tid; c < a.C; c += 256) bl[c] = a.btab[sl][c];
+  __syncthreads();
+  const int CV = a.C / VEC;
+  const int xi0 = (int)blockIdx.x * rows;
+  const int nr = min(rows, a.nx - xi0);
+  const int per = a.Ho * a.Wo * CV;                   // vectors per output row
+  const T* __restrict__ X = reinterpret_cast<const T*>(a.in.p);
+  for (int it = tid; it < nr * per; it += 256) {
+    int ii, rem, pix, cv, oy, ox;
+    divmodu(dpix, (uint32_t)it, ii, rem);             // rem = pixel * CV + cv
+    divmodu(dcv, (uint32_t)rem, pix, cv);
+    divmodu(dwo, (uint32_t)pix, oy, ox);
+    const int xi = xi0 + ii;
+    const int64_t r = (int64_t)sl * a.nx + xi;
+    const T* xr = X + row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems + cv * VEC;
+    float acc[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
+    const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
+    for (int dy = 0; dy < a.kh; ++dy) {
+      const int iy = iy0 + dy;
+      if ((unsigned)iy >= (unsigned)a.H) continue;
+      for (int dx = 0; dx < a.kw; ++dx) {
+        const int ix = ix0 + dx;
+        if ((unsigned)ix >= (unsigned)a.W) continue;
+        const v4u raw = *reinterpret_cast<const v4u*>(xr + ((int64_t)iy * a.W + ix) * a.C);
+        T xv[VEC];
+        __builtin_memcpy(xv, &raw, 16);
+        const float* wt = wl + (cv * VEC) * taps + dy * a.kw + dx;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) acc[j] = fmaf(to_f<T>(xv[j]), wt[j * taps], acc[j]);
+      }
+    }
+    T ov[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) ov[j] = from_f<T>(act(acc[j] + bl[cv * VEC + j], a.relu));
+    v4u o;
+    __builtin_memcpy(&o, ov, 16);
+    const int64_t ro = row_index(a.out_mode, r, a.nx, a.x0);
+    *reinterpret_cast<v4u*>(reinterpret_cast<T*>(a.out) + ro * a.out_row + (int64_t)pix * a.C + cv * VEC) = o;
+  }
+}
+
+// One element per thread: (input, pixel, listed channel).  Used for the delta
+// channel lists, for C % 16-byte-vector != 0, and for float32 network outputs.
+template <typename T>
+__global__ __launch_bounds__(256) void dw_list_kernel(DwArgs a, int rows, DivU32 dwo) {
+  const int tid = threadIdx.x;
+  const int sl = a.slot0 + (int)blockIdx.y;
+  int c_beg = 0, c_end = a.C;
+  if (a.ch_off) { c_beg = a.ch_off[sl]; c_end = a.ch_off[sl + 1]; }
+  const int nch = c_end - c_beg;
+  if (nch <= 0) return;
+  const int taps = a.kh * a.kw;
+  const T* __restrict__ Wt = reinterpret_cast<const T*>(a.wtab[sl]);
+  const float* __restrict__ bias = a.btab[sl];
+  const int xi0 = (int)blockIdx.x * rows;
+  const int nr = min(rows, a.nx - xi0);
+  const int per = a.Ho * a.Wo * nch;
+  const T* __restrict__ X = reinterpret_cast<const T*>(a.in.p);
+  for (int it = tid; it < nr * per; it += 256) {
+    int oy, ox;
+    const int ii = it / per, rem = it - ii * per;      // rem = pixel * nch + u
+    const int pix = rem / nch, u = rem - pix * nch;
+    divmodu(dwo, (uint32_t)pix, oy, ox);
+    const int c = a.ch_list ? a.ch_list[c_beg + u] : c_beg + u;
+    const int xi = xi0 + ii;
+    const int64_t r = (int64_t)sl * a.nx + xi;
+    const T* xr = X + row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems + c;
+    const T* wr = Wt + (int64_t)c * taps;
+    float acc = 0.f;
+    const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
+    for (int dy = 0; dy < a.kh; ++dy) {
+      const int iy = iy0 + dy;
+      if ((unsigned)iy >= (unsigned)a.H) continue;
+      for (int dx = 0; dx < a.kw; ++dx) {
+        const int ix = ix0 + dx;
+        if ((unsigned)ix >= (unsigned)a.W) continue;
+        acc = fmaf(to_f<T>(xr[((int64_t)iy * a.W + ix) * a.C]), to_f<T>(wr[dy * a.kw + dx]), acc);
+      }
+    }
+    const float v = act(acc + bias[c], a.relu);
+    const int64_t ro = row_index(a.out_mode, r, a.nx, a.x0);
+    if (a.delta_T > 0) store_out<T>(a.out, 0, ro * a.out_row + (int64_t)pix * a.delta_T + u, v);
+    else store_out<T>(a.out, a.out_f32, ro * a.out_row + (int64_t)pix * a.C + c, v);
+  }
+}
+
+hipError_t launch_dw(const DwArgs& a, int dtype, hipStream_t s) {
+  if (a.nslots <= 0 || a.nx <= 0) return hipSuccess;
+  if (a.nslots > 65535) return hipErrorInvalidValue;
+  const int esize = dtype == 0 ? 4 : 2;
+  const int vec = 16 / esize;
+  const bool full = !a.ch_off && !a.out_f32 && a.C % vec == 0 && a.C * a.kh * a.kw <= DW_MAXW &&
+                    a.C <= DW_MAXC && a.in.row_elems % vec == 0;
+  const int64_t pix = (int64_t)a.Ho * a.Wo;
+  // about 4K items per block
+  const int64_t items_per_row = full ? pix * (a.C / vec) : pix * a.C;
+  const int rows = (int)std::max<int64_t>(1, std::min<int64_t>(a.nx, 4096 / std::max<int64_t>(1, items_per_row)));
+  if (items_per_row * rows >= INT32_MAX) return hipErrorInvalidValue;
+  dim3 grid((unsigned)((a.nx + rows - 1) / rows), (unsigned)a.nslots);
+  const DivU32 dwo = make_divu32((uint32_t)a.Wo);
+  if (full) {
+    const DivU32 dcv = make_divu32((uint32_t)(a.C / vec));
+    const DivU32 dpix = make_divu32((uint32_t)(pix * (a.C / vec)));
+    if (dtype == 0) hipLaunchKernelGGL(dw_full_kernel<float>, grid, dim3(256), 0, s, a, rows, dcv, dpix, dwo);
+    else hipLaunchKernelGGL(dw_full_kernel<bf16_t>, grid, dim3(256), 0, s, a, rows, dcv, dpix, dwo);
+  } else {
+    // the row split assumes every channel (the largest list)
+    if (dtype == 0) hipLaunchKernelGGL(dw_list_kernel<float>, grid, dim3(256), 0, s, a, rows, dwo);
+    else hipLaunchKernelGGL(dw_list_kernel<bf16_t>, grid, dim3(256), 0, s, a, rows, dwo);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mure

@@ -28,7 +28,7 @@ __global__ void add_kernel(AddArgs a) {
       sv = (cs >= 0 && cs < a.Cs) ? to_f<T>(sp[((int64_t)(2 * y) * a.Ws + 2 * x) * a.Cs + cs]) : 0.f;
     }
     float v = to_f<T>(ap[e]) + sv;
-    if (a.relu) v = fmaxf(v, 0.f);
+    v = act(v, a.relu);
     store_out<T>(a.out, a.out_f32, row_index(a.out_mode, r, a.nx, a.x0) * per + e, v);
   }
 }

@@ -142,6 +142,25 @@ struct ValuArgs {
                                          // delta row out[r][q][t] (out_row = Hp*Wp*delta_T)
 };
 
+// Depthwise CONV2D: output channel c filters input channel c with its own
+// kh x kw taps.  ch_off/ch_list (optional) restrict slot sl to the channels
+// ch_list[ch_off[sl] .. ch_off[sl+1]) (the delta at the first mutated layer),
+// written as compact delta entries (delta_T > 0) or into full rows.
+struct DwArgs {
+  TensorArg in;
+  void* out = nullptr;
+  int out_mode = MODE_BUF, out_f32 = 0;
+  int64_t out_row = 0;
+  const void* const* wtab = nullptr;     // [slots] weights [C][kh][kw]
+  const float* const* btab = nullptr;
+  int slot0 = 0, nslots = 0, nx = 0, x0 = 0;
+  int H = 0, W = 0, C = 0, Ho = 0, Wo = 0;
+  int kh = 3, kw = 3, stride = 1, pad = 0, relu = 0;
+  const int32_t* ch_off = nullptr;
+  const int32_t* ch_list = nullptr;
+  int delta_T = 0;
+};
+
 struct AddArgs {
   TensorArg a, s;
   void* out = nullptr;
@@ -220,6 +239,7 @@ hipError_t launch_conv_lds(const ConvArgs& a, int nslots, hipStream_t s);
 hipError_t launch_conv_big(const ConvArgs& a, int nslots, hipStream_t s);
 hipError_t launch_dense(const DenseArgs& a, int nslots, int dtype, hipStream_t s);
 hipError_t launch_valu(const ValuArgs& a, int dtype, hipStream_t s);
+hipError_t launch_dw(const DwArgs& a, int dtype, hipStream_t s);
 hipError_t launch_add(const AddArgs& a, int dtype, hipStream_t s);
 hipError_t launch_gap(const GapArgs& a, int dtype, hipStream_t s);
 hipError_t launch_patch(const PatchArgs& a, hipStream_t s);

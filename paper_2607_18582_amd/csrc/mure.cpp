@@ -234,7 +234,7 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
   const Node& n = g.nodes[v];
   const int out_f32 = v == g.out() ? 1 : 0;
   hipError_t e = hipSuccess;
-  if (n.kind == K_CONV || n.kind == K_DENSE) {
+  if (n.kind == K_CONV || n.kind == K_DENSE || n.kind == K_DWCONV) {
     const int fam = node_family(g, v);
     timed = timed && ctx->kernel_timing;
     if (timed) {
@@ -262,6 +262,18 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
         if (ex.kill_fused) *ex.kill_fused = true;
       }
       e = launch_dense(a, nslots, g.dtype, ctx->stream);
+    } else if (fam == FAM_DW) {
+      DwArgs a;
+      a.in.p = ins[0].p; a.in.mode = ins[0].mode; a.in.row_elems = (int64_t)n.inH * n.inW * n.inC;
+      a.out = out; a.out_mode = out_mode; a.out_f32 = out_f32; a.out_row = n.out_elems();
+      a.wtab = wtab; a.btab = btab;
+      a.slot0 = slot0; a.nslots = nslots; a.nx = nx; a.x0 = x0;
+      a.H = n.inH; a.W = n.inW; a.C = n.C; a.Ho = n.H; a.Wo = n.W;
+      a.kh = n.kh; a.kw = n.kw; a.stride = n.stride; a.pad = n.pad; a.relu = n.relu;
+      a.ch_off = ex.ch_off; a.ch_list = ex.ch_list;
+      if (ex.delta_T > 0) { a.delta_T = ex.delta_T; a.out_row = (int64_t)n.H * n.W * ex.delta_T; }
+      if (ex.vin || ex.cols) return ctx->fail(MURE_E_INVALID, "internal: virtual input or columns to a depthwise convolution");
+      e = launch_dw(a, g.dtype, ctx->stream);
     } else if (fam == FAM_VALU) {
       ValuArgs a;
       a.in.p = ins[0].p; a.in.mode = ins[0].mode; a.in.row_elems = (int64_t)n.inH * n.inW * n.inC;
@@ -919,7 +931,7 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
           if (gr.delta) {
             if (gr.virt) ex.delta_T = gr.T;
             ex.exec_macs = tl * per_ch * cnt;
-            if (node_family(g, mmi) == FAM_VALU) {
+            if (node_family(g, mmi) == FAM_VALU || node_family(g, mmi) == FAM_DW) {
               ex.ch_off = ctx->d_slots.as<int32_t>() + gt.choff + cs0;
               ex.ch_list = ctx->d_slots.as<int32_t>();
             } else {

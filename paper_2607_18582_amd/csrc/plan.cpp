@@ -37,7 +37,7 @@ std::string build_graph(Graph& g, int in_h, int in_w, int in_c, int dtype) {
   for (int i = 0; i < n; ++i) {
     Node& v = g.nodes[i];
     if ((i == 0) != (v.kind == K_INPUT)) return fmt_node(i, "the input must be node 0 and only node 0");
-    if (v.kind < K_INPUT || v.kind > K_FLATTEN) return fmt_node(i, "unknown kind");
+    if (v.kind < K_INPUT || v.kind > K_DWCONV) return fmt_node(i, "unknown kind");
     if (i == 0) {
       if (v.n_in != 0) return fmt_node(0, "the input node reads nothing");
       v.H = in_h; v.W = in_w; v.C = in_c;
@@ -52,7 +52,7 @@ std::string build_graph(Graph& g, int in_h, int in_w, int in_c, int dtype) {
     v.inH = a.H; v.inW = a.W; v.inC = a.C;
     if (v.kind != K_CONV && v.maxpool) return fmt_node(i, "only CONV2D may pool");
     if (v.kind != K_ADD && v.shortcut) return fmt_node(i, "only ADD has a shortcut mode");
-    if (v.relu != 0 && v.relu != 1) return fmt_node(i, "relu must be 0 or 1");
+    if (v.relu < 0 || v.relu > 2) return fmt_node(i, "relu must be 0 (none), 1 (ReLU) or 2 (ReLU6)");
     switch (v.kind) {
       case K_CONV: {
         if (v.c_in != a.C) return fmt_node(i, "c_in must equal the input channels");
@@ -68,6 +68,18 @@ std::string build_graph(Graph& g, int in_h, int in_w, int in_c, int dtype) {
         if (v.H < 1 || v.W < 1) return fmt_node(i, "pooling leaves nothing");
         v.C = v.c_out;
         v.fan_in = (int64_t)v.c_in * v.kh * v.kw;
+        v.macs = (int64_t)v.Hc * v.Wc * v.c_out * v.fan_in;
+        break;
+      }
+      case K_DWCONV: {
+        if (v.c_in != a.C || v.c_out != a.C) return fmt_node(i, "DWCONV keeps the channels (c_in = c_out = C)");
+        if (v.kh < 1 || v.kw < 1 || v.stride < 1 || v.pad < 0) return fmt_node(i, "bad convolution geometry");
+        v.Hc = (a.H + 2 * v.pad - v.kh) / v.stride + 1;
+        v.Wc = (a.W + 2 * v.pad - v.kw) / v.stride + 1;
+        if (a.H + 2 * v.pad < v.kh || a.W + 2 * v.pad < v.kw || v.Hc < 1 || v.Wc < 1)
+          return fmt_node(i, "kernel larger than the padded input");
+        v.H = v.Hc; v.W = v.Wc; v.C = v.c_out;
+        v.fan_in = (int64_t)v.kh * v.kw;
         v.macs = (int64_t)v.Hc * v.Wc * v.c_out * v.fan_in;
         break;
       }
@@ -123,6 +135,7 @@ std::string build_graph(Graph& g, int in_h, int in_w, int in_c, int dtype) {
 
 int node_family(const Graph& g, int v) {
   const Node& n = g.nodes[v];
+  if (n.kind == K_DWCONV) return FAM_DW;
   if (n.kind == K_DENSE) {
     const int vec = g.dtype == DT_F32 ? 4 : 8;       // 16-byte rows
     return (n.c_in % vec == 0 && n.c_out <= 256) ? FAM_DENSE : FAM_GEMM;
@@ -191,10 +204,16 @@ std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>&
     }
     mp.K = boundary(g, mp.mmi);
     std::set<int> fuzzed;
+    // a switch on a depthwise layer pairs each filter with the other
+    // channel's input, so it is recomputed like a fuzz (its output is not a
+    // channel exchange of the original's)
+    const bool dw = g.nodes[mp.mmi].kind == K_DWCONV;
     for (int r : rs)
-      if (recs[r].layer == mp.mmi && (recs[r].op == OP_GF || recs[r].op == OP_NAI || recs[r].op == OP_WS)) {
+      if (recs[r].layer == mp.mmi && (recs[r].op == OP_GF || recs[r].op == OP_NAI || recs[r].op == OP_WS ||
+                                      (dw && recs[r].op == OP_NS))) {
         mp.recompute = true;
         fuzzed.insert(recs[r].neuron);
+        if (recs[r].op == OP_NS) fuzzed.insert(recs[r].partner);
       }
     if (vanilla) mp.recompute = true;    // the whole first layer, with its own weights
     mp.touched = (int64_t)fuzzed.size();
@@ -250,7 +269,7 @@ std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>&
     {
       const int fam = node_family(g, gr.mmi);
       gr.delta = !vanilla && gr.n_recompute > 0 &&
-                 (fam == FAM_VALU || fam == FAM_LDS || fam == FAM_DENSE || fam == FAM_BIG);
+                 (fam == FAM_VALU || fam == FAM_LDS || fam == FAM_DENSE || fam == FAM_BIG || fam == FAM_DW);
     }
     // virtual mmi output: every consumer is an LDS convolution or a dense layer
     gr.virt = gr.mmi != g.out();

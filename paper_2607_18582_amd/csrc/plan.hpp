@@ -14,7 +14,7 @@
 
 namespace mure {
 
-enum Kind { K_INPUT = 0, K_DENSE = 1, K_CONV = 2, K_ADD = 3, K_GAP = 4, K_FLATTEN = 5 };
+enum Kind { K_INPUT = 0, K_DENSE = 1, K_CONV = 2, K_ADD = 3, K_GAP = 4, K_FLATTEN = 5, K_DWCONV = 6 };
 enum Op { OP_GF = 0, OP_NEB = 1, OP_NAI = 2, OP_NS = 3, OP_WS = 4 };
 enum DType { DT_F32 = 0, DT_BF16 = 1 };
 
@@ -28,7 +28,7 @@ struct Node {
   int inH = 0, inW = 0, inC = 0;  // shape of in[0]
   int64_t fan_in = 0;             // weights per neuron
   int64_t macs = 0;               // multiply-accumulates per input
-  bool weighted() const { return kind == K_DENSE || kind == K_CONV; }
+  bool weighted() const { return kind == K_DENSE || kind == K_CONV || kind == K_DWCONV; }
   int64_t out_elems() const { return (int64_t)H * W * C; }
   int64_t n_weights() const { return weighted() ? (int64_t)c_out * fan_in : 0; }
 };
@@ -62,9 +62,10 @@ enum Family {
   FAM_VALU = 1,    // tiny C_out: per-output fused multiply-add chains (vector ALU)
   FAM_LDS = 2,     // fp32 conv whose padded input image and weights fit in LDS
   FAM_GEMM = 3,    // implicit GEMM with a scalar im2col gather (any shape)
-  FAM_BIG = 4      // bf16 tiled implicit GEMM with 16-byte gathers (C_in % 8 == 0)
+  FAM_BIG = 4,     // bf16 tiled implicit GEMM with 16-byte gathers (C_in % 8 == 0)
+  FAM_DW = 5       // depthwise convolution (per-channel taps on the vector ALU)
 };
-constexpr int N_FAMILIES = 5;
+constexpr int N_FAMILIES = 6;
 int node_family(const Graph& g, int v);
 
 // Launch geometry shared by the planner (family choice) and the kernels.

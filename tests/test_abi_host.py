@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) == set(B.EXPORTED)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.mure_version() == 1
+    assert lib.mure_version() == 2
 
 
 def _plan_ctx(model):
@@ -36,7 +36,7 @@ def _plan_ctx(model):
     return m
 
 
-@pytest.mark.parametrize("cfg", ["mlp", "lenet5", "vgg", "resnet20", "resnet18w"])
+@pytest.mark.parametrize("cfg", ["mlp", "lenet5", "vgg", "resnet20", "resnet18w", "mobilenetv2"])
 def test_planner_matches_oracle_boundaries_and_ledger(cfg):
     wl = W.make_workload(cfg, n_inputs=1, n_mutants=60)
     m = _plan_ctx(wl.model)
@@ -163,3 +163,24 @@ def test_model_validation():
     with pytest.raises(B.MureError):
         m.load_model(nodes, model.in_hwc, "f32", w, model.biases)
     m.load_model(nodes, model.in_hwc, "f32", model.weights, model.biases)
+
+
+def test_depthwise_switch_recomputes_at_mmi():
+    """A switch on a depthwise layer is not a channel exchange of the
+    original's output (each filter meets the other channel's input), so the
+    planner recomputes both channels there; on an ordinary convolution it
+    remaps the cached output."""
+    m = W.make_model("mobilenetv2", "bf16", 0.01)
+    dw = next(i for i, n in enumerate(m.nodes) if n.kind == W.DWCONV)
+    pw = next(i for i, n in enumerate(m.nodes) if n.kind == W.CONV2D and i > dw)
+    ctx = _plan_ctx(m)
+    z = np.zeros(0, np.int32)
+    ctx.apply_mutants(2, np.array([0, 1], np.int32), np.array([W.NS, W.NS], np.int32),
+                      np.array([dw, pw], np.int32), np.array([0, 0], np.int32),
+                      np.array([1, 1], np.int32), [None, None])
+    st = ctx.stats()
+    per_dw = m.nodes[dw].out_hwc[0] * m.nodes[dw].out_hwc[1] * 9
+    # algorithmic MACs at mmi: two depthwise channels for mutant 0, none for mutant 1
+    after = lambda l: sum(O.node_macs(O.OracleModel(m))[l + 1:])
+    assert st["macs_algorithmic"] == 2 * per_dw + after(dw) + after(pw)
+    ctx.close()

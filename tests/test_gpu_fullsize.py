@@ -80,3 +80,7 @@ def test_vgg_full_size(ri):
 
 def test_resnet18w_full_size():
     _sampled_parity("resnet18w", 0, 3, 10)
+
+
+def test_mobilenetv2_full_size():
+    _sampled_parity("mobilenetv2", 1, 16, 48)

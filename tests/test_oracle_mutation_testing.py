@@ -203,13 +203,16 @@ def _all_single_mutants(m: W.Model, seed=0):
     return _mutants(recs, mid + 1)          # the last mutant has no records (identity)
 
 
-@pytest.mark.parametrize("builder", ["mlp", "lenet", "resnetA", "resnetP", "resnetA_bf16"])
+@pytest.mark.parametrize("builder", ["mlp", "lenet", "resnetA", "resnetP", "resnetA_bf16",
+                                     "mobilenet", "mobilenet_bf16"])
 def test_soundness_memoized_equals_vanilla(builder):
     m = {"mlp": lambda: W.tiny_mlp(),
          "lenet": lambda: W.tiny_lenet(),
          "resnetA": lambda: W.tiny_resnet("f32", shortcut="optionA"),
          "resnetP": lambda: W.tiny_resnet("f32", shortcut="proj"),
-         "resnetA_bf16": lambda: W.tiny_resnet("bf16", shortcut="optionA")}[builder]()
+         "resnetA_bf16": lambda: W.tiny_resnet("bf16", shortcut="optionA"),
+         "mobilenet": lambda: W.tiny_mobilenet(),
+         "mobilenet_bf16": lambda: W.tiny_mobilenet("bf16")}[builder]()
     om = O.OracleModel(m)
     x = W.make_inputs(m, 12, "normal")
     muts = _all_single_mutants(m)
@@ -230,7 +233,7 @@ def _edge_set(m):
     return {(p, v) for v, n in enumerate(m.nodes) for p in n.inputs}
 
 
-@pytest.mark.parametrize("cfg", ["mlp", "lenet5", "vgg", "resnet20", "resnet18w"])
+@pytest.mark.parametrize("cfg", ["mlp", "lenet5", "vgg", "resnet20", "resnet18w", "mobilenetv2"])
 def test_dep_graph_and_boundary_definitions_agree(cfg):
     c = W.CONFIGS[cfg]
     m = W.make_model(c["graph"], c["dtype"], c["bias_std"])

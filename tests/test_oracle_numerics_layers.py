@@ -192,3 +192,68 @@ def test_table1_parameter_counts():
         acts = O.forward_all(om, x)
         for v, n in enumerate(m.nodes):
             assert acts[v].shape[1:] == tuple(n.out_hwc), (r["row"], v)
+
+
+# ---------------------------------------------------------------- depthwise conv, ReLU6
+
+def _dw_as_conv(m, v):
+    """The depthwise node v as an ordinary CONV2D whose weights are zero off
+    the channel diagonal: W_full[o, dy, dx, c] = W_dw[o, dy, dx] if c == o."""
+    node = m.nodes[v]
+    conv = W.Node(W.CONV2D, node.inputs, node.c_in, node.c_out, node.kh, node.kw, node.stride,
+                  node.pad, node.relu, 0, 0, node.out_hwc, node.name)
+    wd = O.OracleModel(m).weights[v].reshape(node.c_out, node.kh, node.kw)
+    full = np.zeros((node.c_out, node.kh, node.kw, node.c_in), np.float32)
+    for c in range(node.c_out):
+        full[c, :, :, c] = wd[c]
+    return conv, full
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_depthwise_equals_block_diagonal_conv(dtype):
+    """A depthwise convolution is a convolution with a block-diagonal weight
+    tensor; the oracle's two layer functions (tap loop vs im2col GEMM) agree."""
+    m = W.tiny_mobilenet(dtype)
+    om = O.OracleModel(m)
+    x = W.make_inputs(m, 6, "normal")
+    acts = O.forward_all(om, x)
+    for v, node in enumerate(m.nodes):
+        if node.kind != W.DWCONV:
+            continue
+        conv, full = _dw_as_conv(m, v)
+        nodes = list(m.nodes)
+        nodes[v] = conv
+        cm = W.Model("dw_as_conv", dtype, nodes, list(m.weights), list(m.biases))
+        com = O.OracleModel(cm)
+        got = phi(com, v, [acts[node.inputs[0]]], W=full)
+        np.testing.assert_allclose(got, acts[v], rtol=1e-6, atol=1e-7)
+        assert node.stride in (1, 2)
+
+
+def test_relu6_clamps_both_ends():
+    b = W.configs._Builder((1, 1, 3))
+    b.dense(0, 3, relu=2, name="d")
+    nodes = b.nodes
+    w = np.eye(3, dtype=np.float32) * np.float32(2.0)
+    bias = np.array([0.0, -1.0, 1.0], np.float32)
+    m = W.Model("relu6", "f32", nodes, [None, w], [None, bias])
+    x = np.array([[[[-1.0, 1.0, 4.0]]], [[[0.25, 3.5, 2.5]]]], np.float32)
+    z = phi(O.OracleModel(m), 1, [x]).reshape(2, 3)
+    # 2x + b: (-2, 1, 9) -> (0, 1, 6); (0.5, 6, 6) -> (0.5, 6, 6)
+    np.testing.assert_array_equal(z, np.array([[0, 1, 6], [0.5, 6, 6]], np.float32))
+
+
+def test_mobilenetv2_shape_and_parameters():
+    """Inverted residuals: identity ADD only at stride 1 with equal channels;
+    the depthwise layers hold 9 weights per channel."""
+    m = W.make_model("mobilenetv2", "bf16", 0.01)
+    kinds = [n.kind for n in m.nodes]
+    assert kinds.count(W.DWCONV) == sum(n for (_, _, n, _) in W.configs.MOBILENETV2_BLOCKS)
+    for v, n in enumerate(m.nodes):
+        if n.kind == W.DWCONV:
+            assert m.weights[v].shape == (n.c_out, 3, 3) and n.fan_in == 9 and n.relu == 2
+        if n.kind == W.ADD:
+            a, s = (m.nodes[i] for i in n.inputs)
+            assert a.out_hwc == s.out_hwc and n.relu == 0
+    assert m.nodes[-1].out_hwc == (1, 1, 10)
+    assert m.n_params() == 215210

@@ -67,3 +67,17 @@ def test_gf_noise_sigma():
         eps = np.concatenate([mu.noise[i] for i in recs]).astype(np.float64)
         sigma = 0.1 * wl.model.weights[l].astype(np.float64).std()
         assert abs(eps.std() / sigma - 1) < 0.25
+
+
+def test_layer_first_draws_cap_at_the_neurons_left():
+    """MobileNetV2 at 1% draws k = 46 neurons; a mutant whose first layer is
+    near the output keeps every neuron at or after it instead."""
+    wl = W.make_workload("mobilenetv2", n_inputs=1, n_mutants=300)
+    m, mu = wl.model, wl.mutants
+    k = max(1, int(0.01 * sum(m.nodes[i].c_out for i in m.weighted_nodes()) + 0.5))
+    for mid in range(mu.n_mutants):
+        r = mu.records_of(mid)
+        first = int(mu.layer[r[0]])
+        left = sum(m.nodes[l].c_out for l in m.weighted_nodes() if l >= first)
+        assert len(r) == min(k, left)
+        assert (mu.layer[r] >= first).all()

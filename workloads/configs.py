@@ -28,7 +28,7 @@ from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
-from .graph import (INPUT, DENSE, CONV2D, ADD, GAP, GF, NEB, NAI, NS, WS, Node,
+from .graph import (INPUT, DENSE, CONV2D, ADD, GAP, DWCONV, GF, NEB, NAI, NS, WS, Node,
                     Model, Mutants, Workload)
 
 
@@ -46,20 +46,28 @@ class _Builder:
         wo = (w + 2 * pad - k) // stride + 1
         if pool:
             ho, wo = ho // pool, wo // pool
-        self.nodes.append(Node(CONV2D, (src,), c, c_out, k, k, stride, pad, relu,
+        self.nodes.append(Node(CONV2D, (src,), c, c_out, k, k, stride, pad, int(relu),
                                pool, 0, (ho, wo, c_out), name))
+        return len(self.nodes) - 1
+
+    def dwconv(self, src, k, stride=1, pad=0, relu=2, name=""):
+        h, w, c = self.nodes[src].out_hwc
+        ho = (h + 2 * pad - k) // stride + 1
+        wo = (w + 2 * pad - k) // stride + 1
+        self.nodes.append(Node(DWCONV, (src,), c, c, k, k, stride, pad, int(relu),
+                               0, 0, (ho, wo, c), name))
         return len(self.nodes) - 1
 
     def dense(self, src, c_out, relu=True, name=""):
         h, w, c = self.nodes[src].out_hwc
-        self.nodes.append(Node(DENSE, (src,), h * w * c, c_out, 1, 1, 1, 0, relu,
+        self.nodes.append(Node(DENSE, (src,), h * w * c, c_out, 1, 1, 1, 0, int(relu),
                                0, 0, (1, 1, c_out), name))
         return len(self.nodes) - 1
 
     def add(self, a, skip, relu=True, shortcut=0, name=""):
         ha = self.nodes[a].out_hwc
         self.nodes.append(Node(ADD, (a, skip), self.nodes[skip].out_hwc[2], ha[2],
-                               relu=relu, shortcut=shortcut, out_hwc=ha, name=name))
+                               relu=int(relu), shortcut=shortcut, out_hwc=ha, name=name))
         return len(self.nodes) - 1
 
     def gap(self, src, name="gap"):
@@ -80,6 +88,25 @@ def _basic_block(b, src, c_out, stride, shortcut_kind, name):
     c = b.conv(a, c_out, 3, stride=1, pad=1, relu=False, name=name + ".b")
     return b.add(c, skip, relu=True, shortcut=1 if shortcut_kind == "optionA" else 0,
                  name=name + ".add")
+
+
+def _inverted_residual(b, src, expand, c_out, stride, name):
+    """MobileNetV2 block: 1x1 expansion (ReLU6, skipped when expand == 1), 3x3
+    depthwise (stride s, ReLU6), 1x1 linear projection, and an identity ADD
+    (no activation) when the stride is 1 and the channels agree."""
+    c_in = b.nodes[src].out_hwc[2]
+    x = src
+    if expand != 1:
+        x = b.conv(x, c_in * expand, 1, relu=2, name=name + ".expand")
+    x = b.dwconv(x, 3, stride=stride, pad=1, relu=2, name=name + ".dw")
+    x = b.conv(x, c_out, 1, relu=0, name=name + ".project")
+    if stride == 1 and c_in == c_out:
+        x = b.add(x, src, relu=0, name=name + ".add")
+    return x
+
+
+# MobileNetV2 for 32x32 inputs: (expansion t, channels c, repeats n, stride s)
+MOBILENETV2_BLOCKS = ((1, 8, 1, 1), (6, 16, 2, 2), (6, 24, 3, 2), (6, 48, 3, 2), (6, 64, 2, 1))
 
 
 def _graph(name: str, hwc=None, classes: int = 10) -> List[Node]:
@@ -131,6 +158,15 @@ def _graph(name: str, hwc=None, classes: int = 10) -> List[Node]:
                                  "proj" if first else "identity", f"s{s}b{k}")
         x = b.gap(x)
         b.dense(x, 200 if classes == 10 else classes, False, "fc")
+    elif name == "mobilenetv2":
+        b = _Builder((32, 32, 3))
+        x = b.conv(0, 16, 3, pad=1, relu=2, name="stem")
+        for bi, (t, c, n, s) in enumerate(MOBILENETV2_BLOCKS):
+            for r in range(n):
+                x = _inverted_residual(b, x, t, c, s if r == 0 else 1, f"b{bi}.{r}")
+        x = b.conv(x, 320, 1, relu=2, name="head")
+        x = b.gap(x)
+        b.dense(x, classes, False, "fc")
     else:
         raise KeyError(name)
     return b.nodes
@@ -161,7 +197,12 @@ def _draw_weights(nodes: List[Node], dtype: str, bias_std: float, seed: int = 0)
             weights.append(None)
             biases.append(None)
             continue
-        shape = (n.c_out, n.kh, n.kw, n.c_in) if n.kind == CONV2D else (n.c_out, n.c_in)
+        if n.kind == CONV2D:
+            shape = (n.c_out, n.kh, n.kw, n.c_in)
+        elif n.kind == DWCONV:
+            shape = (n.c_out, n.kh, n.kw)
+        else:
+            shape = (n.c_out, n.c_in)
         w64 = rng.standard_normal(shape) * math.sqrt(2.0 / n.fan_in)
         weights.append(w64.astype(np.float32) if dtype == "f32" else _to_bf16_bits(w64))
         if bias_std > 0:
@@ -223,7 +264,8 @@ def make_mutants(model: Model, n_mutants: int, k: int, mode: str,
             l0 = cands[int(rng.integers(len(cands)))]
             n0 = int(rng.integers(model.nodes[l0].c_out))
             rest = np.nonzero((pool_layer >= l0) & ~((pool_layer == l0) & (pool_neuron == n0)))[0]
-            pick = rng.choice(rest.size, size=k - 1, replace=False) if k > 1 else []
+            # (a first layer near the output may leave fewer than k-1 neurons)
+            pick = rng.choice(rest.size, size=min(k - 1, rest.size), replace=False) if k > 1 else []
             sel = [(l0, n0)] + [(int(pool_layer[rest[i]]), int(pool_neuron[rest[i]])) for i in pick]
         elif mode == "uniform":
             pick = rng.choice(pool_layer.size, size=k, replace=False)
@@ -270,6 +312,11 @@ CONFIGS: Dict[str, dict] = {
                      n_mutants=1000, ratio=0.01, mode="layer_first", variant=0,
                      desc="ResNet-20 32x32x3 bf16, 10,000 inputs N(0,1), 1,000 mutants, "
                           "first mutated layer uniform over 19 layers"),
+    "mobilenetv2": dict(graph="mobilenetv2", dtype="bf16", bias_std=0.01, n_inputs=10000,
+                        dist="normal", n_mutants=1000, ratio=0.01, mode="layer_first", variant=0,
+                        desc="MobileNetV2 32x32x3 bf16 (inverted residuals, depthwise 3x3, ReLU6), "
+                             "10,000 inputs N(0,1), 1,000 mutants at 1%, first mutated layer "
+                             "uniform over the weighted layers"),
     "resnet18w": dict(graph="resnet18w", dtype="bf16", bias_std=0.01, n_inputs=5000, dist="normal",
                       n_mutants=500, ratio=0.05, mode="uniform", variant=0,
                       desc="ResNet-18-style 64x64x3 bf16 FC200, 5,000 inputs N(0,1), "
@@ -356,3 +403,17 @@ def tiny_lenet(dtype: str = "f32", seed: int = 7) -> Model:
     b.dense(x, 3, False, "f2")
     w, bb = _draw_weights(b.nodes, dtype, 0.1, seed=seed)
     return Model("tiny_lenet", dtype, b.nodes, w, bb)
+
+
+def tiny_mobilenet(dtype: str = "f32", seed: int = 8) -> Model:
+    """6x6x3 input; stem 3x3 -> 4 (ReLU6); an inverted residual with identity
+    ADD (expand 2, depthwise stride 1); one with stride 2 and no ADD; GAP;
+    dense 3."""
+    b = _Builder((6, 6, 3))
+    x = b.conv(0, 4, 3, pad=1, relu=2, name="stem")
+    x = _inverted_residual(b, x, 2, 4, 1, "r0")
+    x = _inverted_residual(b, x, 2, 6, 2, "r1")
+    x = b.gap(x)
+    b.dense(x, 3, False, "out")
+    w, bb = _draw_weights(b.nodes, dtype, 0.1, seed=seed)
+    return Model("tiny_mobilenet", dtype, b.nodes, w, bb)

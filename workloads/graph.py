@@ -5,18 +5,22 @@ A model is a DAG given in topological order (Section 4: the order tau); node
 Algorithm 2 stated explicitly), every index smaller than ``i``.  Node 0 is the
 single input, the last node is the single output (logits).
 
-Kinds: INPUT, DENSE, CONV2D (bias, optional ReLU and 2x2/2 max-pool fused into
-the node), ADD (two inputs, optional ReLU, optional "option A" shortcut:
-subsample the second input by 2 in H and W and zero-pad its channels evenly),
-GAP (global average pool to 1x1xC), FLATTEN (a view, HWC order).
+Kinds: INPUT, DENSE, CONV2D (bias, optional activation and 2x2/2 max-pool
+fused into the node), ADD (two inputs, optional activation, optional "option
+A" shortcut: subsample the second input by 2 in H and W and zero-pad its
+channels evenly), GAP (global average pool to 1x1xC), FLATTEN (a view, HWC
+order), DWCONV (depthwise convolution: output channel c filters input channel
+c only; C_in = C_out).
 
-Weights: CONV2D ``[C_out][kh][kw][C_in]``; DENSE ``[C_out][C_in]`` where the
-C_in index runs over the flattened HWC input.  fp32 models hold float32
+Activation (``relu``): 0 none, 1 ReLU, 2 ReLU6 (min(max(x, 0), 6)).
+
+Weights: CONV2D ``[C_out][kh][kw][C_in]``; DWCONV ``[C][kh][kw]``; DENSE
+``[C_out][C_in]`` where the C_in index runs over the flattened HWC input.  fp32 models hold float32
 arrays; bf16 models hold uint16 arrays of bfloat16 bit patterns.  Biases are
 float32 ``[C_out]``.
 
 Mutation records (one per mutated neuron, Section 3.1 and Section 4):
-``op`` in {GF, NEB, NAI, NS, WS}; ``layer`` is a DENSE/CONV2D node index;
+``op`` in {GF, NEB, NAI, NS, WS}; ``layer`` is a DENSE/CONV2D/DWCONV node index;
 ``neuron`` an output channel (a neuron of a conv layer is one filter, Section
 2.1); ``partner`` the other neuron of a switch; GF records carry their noise,
 ``fan_in`` float32 values in the row order of ``W[neuron]``; WS records a
@@ -29,9 +33,9 @@ from typing import List, Optional, Tuple
 
 import numpy as np
 
-INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN = 0, 1, 2, 3, 4, 5
+INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV = 0, 1, 2, 3, 4, 5, 6
 KIND_NAMES = {INPUT: "input", DENSE: "dense", CONV2D: "conv2d", ADD: "add",
-              GAP: "gap", FLATTEN: "flatten"}
+              GAP: "gap", FLATTEN: "flatten", DWCONV: "dwconv"}
 
 # mutation operators (Section 3.1): Gaussian fuzzing, neuron effect block,
 # neuron activation inverse, neuron switch, weight shuffle
@@ -49,7 +53,7 @@ class Node:
     kw: int = 1
     stride: int = 1
     pad: int = 0
-    relu: bool = False
+    relu: int = 0             # 0 none, 1 ReLU, 2 ReLU6
     maxpool: int = 0          # 0 or 2
     shortcut: int = 0         # ADD only: 0 identity, 1 option A
     out_hwc: Tuple[int, int, int] = (0, 0, 0)
@@ -57,10 +61,12 @@ class Node:
 
     @property
     def weighted(self) -> bool:
-        return self.kind in (DENSE, CONV2D)
+        return self.kind in (DENSE, CONV2D, DWCONV)
 
     @property
     def fan_in(self) -> int:
+        if self.kind == DWCONV:
+            return self.kh * self.kw
         return self.c_in * self.kh * self.kw
 
 
