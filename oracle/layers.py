@@ -12,6 +12,14 @@ Semantics (the same on both sides of the parity check; see the design notes):
   * DENSE: t = fl32(sum_c x[n,c] * W[o,c] + b[o]), optional activation,
     rounding;
   * activation: ReLU max(t, 0) or ReLU6 min(max(t, 0), 6), in float32;
+  * EMBED: out[n,0,t,d] = W[d, token], the token id being the input value;
+  * LSTM (float32 models): for t = 0..T-1, with h = c = 0 at the start and
+    each unit's row holding, per gate (input, forget, cell, output), its input
+    weights, recurrent weights and bias,
+      z_q = fl32(x_t . Wx_q + h . Wh_q + b_q)                (float64 sums),
+      i, f, o = fl32(sigmoid(z)), g = fl32(tanh(z_g))        (float64, rounded),
+      c = fl32(f*c + i*g),  h = fl32(o * fl32(tanh(c)));
+    the output is every step's h, or the last one;
   * ADD: t = fl32(a + s) computed in float32, where s is the second input,
     for option A first subsampled s[:, ::2, ::2, :] and zero-padded in the
     channel dimension ((C_a - C_s)//2 zero channels before, the rest after);
@@ -32,7 +40,7 @@ from typing import Dict, List, Optional, Sequence
 import numpy as np
 from numpy.lib.stride_tricks import sliding_window_view
 
-from workloads.graph import INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV, Model
+from workloads.graph import INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV, EMBED, LSTM, Model
 from .numerics import rne_bf16, bf16_bits_to_f32, to_f32
 
 
@@ -128,6 +136,36 @@ def phi(model: OracleModel, v: int, ins: Sequence[np.ndarray], W=None, b=None,
                 acc += tap * W64[None, None, None, :, dy, dx]
         t = _act(to_f32(acc + b.astype(np.float64)[None, None, None, :]), node.relu)
         return _round_node(model, v, np.ascontiguousarray(t))
+    if node.kind == EMBED:
+        x = ins[0]
+        n, t = x.shape[0], x.shape[2]
+        tok = x.reshape(n, t)
+        ids = tok.astype(np.int64)
+        if not np.array_equal(ids, tok) or ids.min() < 0 or ids.max() >= node.c_in:
+            raise ValueError(f"node {v}: token ids must be integers in [0, {node.c_in})")
+        out = np.asarray(W).reshape(node.c_out, node.c_in)[:, ids]         # [D, n, T]
+        return _round_node(model, v, np.ascontiguousarray(out.transpose(1, 2, 0)).reshape(n, 1, t, node.c_out))
+    if node.kind == LSTM:
+        if model.dtype != "f32":
+            raise ValueError("LSTM layers are defined for float32 models")
+        x = ins[0]
+        n, t, d = x.shape[0], x.shape[2], x.shape[3]
+        hu = node.c_out
+        Wr = np.asarray(W, np.float64).reshape(hu, 4, d + hu + 1)
+        h = np.zeros((n, hu), np.float32)
+        c = np.zeros((n, hu), np.float32)
+        outs = []
+        sig = lambda z: to_f32(1.0 / (1.0 + np.exp(-z.astype(np.float64))))
+        th = lambda z: to_f32(np.tanh(z.astype(np.float64)))
+        for step in range(t):
+            a64 = np.concatenate([x[:, 0, step, :], h, np.ones((n, 1), np.float32)], axis=1).astype(np.float64)
+            z = [to_f32(_matmul64(a64, Wr[:, q, :], accumulate)) for q in range(4)]
+            i, f, g, o = sig(z[0]), sig(z[1]), th(z[2]), sig(z[3])
+            c = to_f32(f.astype(np.float64) * c + i.astype(np.float64) * g)
+            h = to_f32(o.astype(np.float64) * th(c))
+            outs.append(h)
+        y = np.stack(outs, axis=1) if node.seq else outs[-1][:, None, :]
+        return y.reshape(n, 1, y.shape[1], hu)
     if node.kind == ADD:
         a, s = ins
         if node.shortcut == 1:

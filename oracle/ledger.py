@@ -1,8 +1,8 @@
 """The additive cost model of Section 5.2, counted in multiply-accumulates.
 
 cost(v) per input = MACs of node v (CONV2D: pre-pool output pixels * C_out *
-kh*kw*C_in; DWCONV: output pixels * C * kh*kw; DENSE: C_in*C_out; other
-kinds 0).  It is non-negative (C1),
+kh*kw*C_in; DWCONV: output pixels * C * kh*kw; DENSE: C_in*C_out; LSTM:
+T * 4H * (D + H + 1); other kinds, the embedding lookup included, 0).  It is non-negative (C1),
 additive over a prefix/suffix split (C2) and depends only on the layer shapes
 (C3).  For a cluster C of mutants sharing mmi, the prefix P is every node
 before mmi and the chopped mutant every node from mmi on, so
@@ -12,7 +12,7 @@ from __future__ import annotations
 
 from typing import Dict, List
 
-from workloads.graph import CONV2D, DENSE, DWCONV, Mutants
+from workloads.graph import CONV2D, DENSE, DWCONV, LSTM, Mutants
 from .layers import OracleModel
 from .memoized import boundary, get_dep_graph, mutated_layers
 
@@ -28,6 +28,9 @@ def node_macs(model: OracleModel) -> List[int]:
             out.append(ho * wo * n.c_out * per_channel)
         elif n.kind == DENSE:
             out.append(n.c_in * n.c_out)
+        elif n.kind == LSTM:
+            steps = model.nodes[n.inputs[0]].out_hwc[1]
+            out.append(steps * 4 * n.c_out * (n.c_in + n.c_out + 1))
         else:
             out.append(0)
     return out

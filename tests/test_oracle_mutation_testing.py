@@ -204,7 +204,7 @@ def _all_single_mutants(m: W.Model, seed=0):
 
 
 @pytest.mark.parametrize("builder", ["mlp", "lenet", "resnetA", "resnetP", "resnetA_bf16",
-                                     "mobilenet", "mobilenet_bf16"])
+                                     "mobilenet", "mobilenet_bf16", "rnn"])
 def test_soundness_memoized_equals_vanilla(builder):
     m = {"mlp": lambda: W.tiny_mlp(),
          "lenet": lambda: W.tiny_lenet(),
@@ -212,9 +212,10 @@ def test_soundness_memoized_equals_vanilla(builder):
          "resnetP": lambda: W.tiny_resnet("f32", shortcut="proj"),
          "resnetA_bf16": lambda: W.tiny_resnet("bf16", shortcut="optionA"),
          "mobilenet": lambda: W.tiny_mobilenet(),
-         "mobilenet_bf16": lambda: W.tiny_mobilenet("bf16")}[builder]()
+         "mobilenet_bf16": lambda: W.tiny_mobilenet("bf16"),
+         "rnn": lambda: W.tiny_rnn()}[builder]()
     om = O.OracleModel(m)
-    x = W.make_inputs(m, 12, "normal")
+    x = W.make_inputs(m, 12, "tokens" if builder == "rnn" else "normal")
     muts = _all_single_mutants(m)
     memo = O.mure(om, x, muts)
     van = O.run_vanilla(om, x, muts, keep_logits=range(muts.n_mutants), accumulate="ordered")
@@ -233,7 +234,7 @@ def _edge_set(m):
     return {(p, v) for v, n in enumerate(m.nodes) for p in n.inputs}
 
 
-@pytest.mark.parametrize("cfg", ["mlp", "lenet5", "vgg", "resnet20", "resnet18w", "mobilenetv2"])
+@pytest.mark.parametrize("cfg", ["mlp", "lenet5", "vgg", "resnet20", "resnet18w", "mobilenetv2", "lstm"])
 def test_dep_graph_and_boundary_definitions_agree(cfg):
     c = W.CONFIGS[cfg]
     m = W.make_model(c["graph"], c["dtype"], c["bias_std"])

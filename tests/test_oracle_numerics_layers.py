@@ -257,3 +257,50 @@ def test_mobilenetv2_shape_and_parameters():
             assert a.out_hwc == s.out_hwc and n.relu == 0
     assert m.nodes[-1].out_hwc == (1, 1, 10)
     assert m.n_params() == 215210
+
+
+# ---------------------------------------------------------------- embedding, LSTM
+
+def test_embedding_and_lstm_match_torch():
+    """The oracle's embedding lookup and LSTM recursion against torch's
+    float64 reference modules with the same parameters (gate order input,
+    forget, cell, output; one bias per gate)."""
+    m = W.tiny_rnn()
+    om = O.OracleModel(m)
+    x = W.make_inputs(m, 6, "tokens")
+    acts = O.forward_all(om, x)
+    emb, l1, l2 = 1, 2, 3
+    E = om.weights[emb].reshape(m.nodes[emb].c_out, m.nodes[emb].c_in)      # [D][V]
+    tok = torch.from_numpy(x.reshape(6, -1).astype(np.int64))
+    ref = F.embedding(tok, torch.from_numpy(E.T.astype(np.float64)))
+    np.testing.assert_array_equal(acts[emb].reshape(6, -1, E.shape[0]), ref.numpy().astype(np.float32))
+    for v in (l1, l2):
+        node = m.nodes[v]
+        d, hu = node.c_in, node.c_out
+        Wr = om.weights[v].reshape(hu, 4, d + hu + 1).astype(np.float64)
+        mod = torch.nn.LSTM(d, hu, batch_first=True).double()
+        with torch.no_grad():
+            mod.weight_ih_l0.copy_(torch.from_numpy(Wr[:, :, :d].transpose(1, 0, 2).reshape(4 * hu, d)))
+            mod.weight_hh_l0.copy_(torch.from_numpy(Wr[:, :, d:d + hu].transpose(1, 0, 2).reshape(4 * hu, hu)))
+            mod.bias_ih_l0.copy_(torch.from_numpy(Wr[:, :, -1].T.reshape(4 * hu)))
+            mod.bias_hh_l0.zero_()
+        inp = torch.from_numpy(acts[node.inputs[0]].reshape(6, -1, d).astype(np.float64))
+        with torch.no_grad():
+            y, _ = mod(inp)
+        want = y.numpy() if node.seq else y.numpy()[:, -1:, :]
+        np.testing.assert_allclose(acts[v].reshape(want.shape), want, rtol=2e-6, atol=2e-6)
+
+
+def test_lstm_effect_block_silences_the_unit():
+    """Zeroing a unit's incoming weights and gate biases gives i = f = o = 1/2
+    and g = 0 at every step, so c and h stay exactly 0."""
+    m = W.tiny_rnn()
+    om = O.OracleModel(m)
+    x = W.make_inputs(m, 5, "tokens")
+    l1 = 2
+    muts = W.Mutants(1, np.array([0], np.int32), np.array([W.NEB], np.int32), np.array([l1], np.int32),
+                     np.array([1], np.int32), np.array([-1], np.int32), [None])
+    Wm, Bm, _ = O.apply_records(om, muts, 0)
+    acts = O.forward_all(om, x, Wm, Bm)
+    assert np.all(acts[l1][..., 1] == 0)
+    assert np.any(acts[l1][..., 0] != 0)

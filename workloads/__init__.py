@@ -6,16 +6,18 @@ holds none of the method's arithmetic (no layer functions, no operator
 application, no kill or score logic), so both the CPU oracle and the GPU path
 can consume it without sharing code.
 """
-from .graph import (INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV, KIND_NAMES,
+from .graph import (INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV, EMBED, LSTM, KIND_NAMES,
                     GF, NEB, NAI, NS, WS, OP_NAMES, Node, Model, Mutants, Workload)
 from .configs import (CONFIGS, make_workload, make_model, make_inputs,
                       make_mutants, neuron_layers, tiny_mlp, tiny_resnet,
-                      tiny_lenet, tiny_mobilenet, bf16_bits_to_f32)
+                      tiny_lenet, tiny_mobilenet, tiny_rnn, lstm_bias_positions,
+                      bf16_bits_to_f32)
 
 __all__ = [
-    "INPUT", "DENSE", "CONV2D", "ADD", "GAP", "FLATTEN", "DWCONV", "KIND_NAMES",
+    "INPUT", "DENSE", "CONV2D", "ADD", "GAP", "FLATTEN", "DWCONV", "EMBED", "LSTM", "KIND_NAMES",
     "GF", "NEB", "NAI", "NS", "WS", "OP_NAMES", "Node", "Model", "Mutants", "Workload",
     "CONFIGS", "make_workload", "make_model", "make_inputs", "make_mutants",
-    "neuron_layers", "tiny_mlp", "tiny_resnet", "tiny_lenet", "tiny_mobilenet",
+    "neuron_layers", "tiny_mlp", "tiny_resnet", "tiny_lenet", "tiny_mobilenet", "tiny_rnn",
+    "lstm_bias_positions",
     "bf16_bits_to_f32",
 ]

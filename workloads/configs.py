@@ -28,8 +28,8 @@ from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
-from .graph import (INPUT, DENSE, CONV2D, ADD, GAP, DWCONV, GF, NEB, NAI, NS, WS, Node,
-                    Model, Mutants, Workload)
+from .graph import (INPUT, DENSE, CONV2D, ADD, GAP, DWCONV, EMBED, LSTM, GF, NEB, NAI, NS,
+                    WS, Node, Model, Mutants, Workload)
 
 
 # --------------------------------------------------------------------------
@@ -56,6 +56,19 @@ class _Builder:
         wo = (w + 2 * pad - k) // stride + 1
         self.nodes.append(Node(DWCONV, (src,), c, c, k, k, stride, pad, int(relu),
                                0, 0, (ho, wo, c), name))
+        return len(self.nodes) - 1
+
+    def embed(self, src, vocab, dim, name=""):
+        h, t, c = self.nodes[src].out_hwc
+        assert h == 1 and c == 1, "an embedding reads a [1][T][1] token sequence"
+        self.nodes.append(Node(EMBED, (src,), vocab, dim, out_hwc=(1, t, dim), name=name))
+        return len(self.nodes) - 1
+
+    def lstm(self, src, units, seq, name=""):
+        h, t, c = self.nodes[src].out_hwc
+        assert h == 1
+        self.nodes.append(Node(LSTM, (src,), c, units, out_hwc=(1, t if seq else 1, units),
+                               name=name, seq=int(seq)))
         return len(self.nodes) - 1
 
     def dense(self, src, c_out, relu=True, name=""):
@@ -103,6 +116,15 @@ def _inverted_residual(b, src, expand, c_out, stride, name):
     if stride == 1 and c_in == c_out:
         x = b.add(x, src, relu=0, name=name + ".add")
     return x
+
+
+LSTM_VOCAB, LSTM_STEPS = 2000, 40
+
+
+def lstm_bias_positions(node: Node) -> np.ndarray:
+    """Positions of the four gate biases in an LSTM unit's weight row."""
+    k = node.c_in + node.c_out + 1
+    return np.arange(4) * k + (k - 1)
 
 
 # MobileNetV2 for 32x32 inputs: (expansion t, channels c, repeats n, stride s)
@@ -167,6 +189,14 @@ def _graph(name: str, hwc=None, classes: int = 10) -> List[Node]:
         x = b.conv(x, 320, 1, relu=2, name="head")
         x = b.gap(x)
         b.dense(x, classes, False, "fc")
+    elif name == "lstm":
+        # embedding, two LSTM layers (the first returns its sequence), output
+        # layer (the paper's RNN shape; softmax does not change the argmax)
+        b = _Builder(hwc or (1, LSTM_STEPS, 1))
+        x = b.embed(0, LSTM_VOCAB, 32, name="embed")
+        x = b.lstm(x, 32, seq=1, name="lstm1")
+        x = b.lstm(x, 32, seq=0, name="lstm2")
+        b.dense(x, 2 if classes == 10 else classes, False, "out")
     else:
         raise KeyError(name)
     return b.nodes
@@ -201,11 +231,21 @@ def _draw_weights(nodes: List[Node], dtype: str, bias_std: float, seed: int = 0)
             shape = (n.c_out, n.kh, n.kw, n.c_in)
         elif n.kind == DWCONV:
             shape = (n.c_out, n.kh, n.kw)
+        elif n.kind in (EMBED, LSTM):
+            shape = (n.c_out, n.fan_in)
         else:
             shape = (n.c_out, n.c_in)
-        w64 = rng.standard_normal(shape) * math.sqrt(2.0 / n.fan_in)
+        if n.kind == EMBED:                       # unit-scale token vectors
+            w64 = rng.standard_normal(shape)
+        elif n.kind == LSTM:                      # N(0, 1/(D+H)); gate biases 0, forget gate 1
+            w64 = rng.standard_normal(shape) * math.sqrt(1.0 / (n.c_in + n.c_out))
+            pos = lstm_bias_positions(n)
+            w64[:, pos] = 0.0
+            w64[:, pos[1]] = 1.0
+        else:
+            w64 = rng.standard_normal(shape) * math.sqrt(2.0 / n.fan_in)
         weights.append(w64.astype(np.float32) if dtype == "f32" else _to_bf16_bits(w64))
-        if bias_std > 0:
+        if bias_std > 0 and n.kind not in (EMBED, LSTM):
             biases.append((rng.standard_normal(n.c_out) * bias_std).astype(np.float32))
         else:
             biases.append(np.zeros(n.c_out, np.float32))
@@ -221,6 +261,9 @@ def make_inputs(model: Model, n: int, dist: str, seed: int = 1,
         e = min(n, s + chunk)
         if dist == "uniform":
             x = rng.random((e - s, h, w, c))
+        elif dist == "tokens":                    # token ids, uniform over the vocabulary
+            vocab = next(n.c_in for n in model.nodes if n.kind == EMBED)
+            x = rng.integers(0, vocab, size=(e - s, h, w, c)).astype(np.float64)
         else:
             x = rng.standard_normal((e - s, h, w, c))
         out[s:e] = x.astype(np.float32) if model.dtype == "f32" else _to_bf16_bits(x)
@@ -278,12 +321,20 @@ def make_mutants(model: Model, n_mutants: int, k: int, mode: str,
             if op == NS:
                 j = int(rng.integers(c_out - 1))
                 j += int(j >= i)
+            node = model.nodes[l]
             eps = None
             if op == GF:
-                eps = (rng.standard_normal(model.nodes[l].fan_in) * sigma[l]).astype(np.float32)
+                eps = (rng.standard_normal(node.fan_in) * sigma[l]).astype(np.float32)
+                if node.kind == LSTM:             # the gate biases are kept
+                    eps[lstm_bias_positions(node)] = 0.0
             perm = None
             if op == WS:
-                perm = rng.permutation(model.nodes[l].fan_in).astype(np.int32)
+                perm = rng.permutation(node.fan_in).astype(np.int32)
+                if node.kind == LSTM:             # shuffle the weights, keep the biases in place
+                    pos = lstm_bias_positions(node)
+                    keep = np.setdiff1d(np.arange(node.fan_in), pos)
+                    perm = np.arange(node.fan_in, dtype=np.int32)
+                    perm[keep] = keep[rng.permutation(keep.size)]
             mid.append(m); opl.append(op); lay.append(l); neu.append(i); par.append(j)
             noise.append(eps); perms.append(perm)
     a = lambda v: np.asarray(v, np.int32)
@@ -317,6 +368,11 @@ CONFIGS: Dict[str, dict] = {
                         desc="MobileNetV2 32x32x3 bf16 (inverted residuals, depthwise 3x3, ReLU6), "
                              "10,000 inputs N(0,1), 1,000 mutants at 1%, first mutated layer "
                              "uniform over the weighted layers"),
+    "lstm": dict(graph="lstm", dtype="f32", bias_std=0.0, n_inputs=10000, dist="tokens",
+                 n_mutants=1000, ratio=0.01, mode="layer_first", variant=0,
+                 desc="RNN: embedding 2000x32, LSTM 32 (sequence), LSTM 32, dense 2, fp32, "
+                      "40-token sequences uniform over the vocabulary, 10,000 inputs, "
+                      "1,000 mutants at 1%"),
     "resnet18w": dict(graph="resnet18w", dtype="bf16", bias_std=0.01, n_inputs=5000, dist="normal",
                       n_mutants=500, ratio=0.05, mode="uniform", variant=0,
                       desc="ResNet-18-style 64x64x3 bf16 FC200, 5,000 inputs N(0,1), "
@@ -417,3 +473,15 @@ def tiny_mobilenet(dtype: str = "f32", seed: int = 8) -> Model:
     b.dense(x, 3, False, "out")
     w, bb = _draw_weights(b.nodes, dtype, 0.1, seed=seed)
     return Model("tiny_mobilenet", dtype, b.nodes, w, bb)
+
+
+def tiny_rnn(dtype: str = "f32", seed: int = 9) -> Model:
+    """Tokens [1][5][1] over a 7-word vocabulary; embedding 3; LSTM 4
+    (sequence); LSTM 3 (last state); dense 3."""
+    b = _Builder((1, 5, 1))
+    x = b.embed(0, 7, 3, name="embed")
+    x = b.lstm(x, 4, seq=1, name="lstm1")
+    x = b.lstm(x, 3, seq=0, name="lstm2")
+    b.dense(x, 3, False, "out")
+    w, bb = _draw_weights(b.nodes, dtype, 0.1, seed=seed)
+    return Model("tiny_rnn", dtype, b.nodes, w, bb)

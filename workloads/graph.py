@@ -10,17 +10,24 @@ fused into the node), ADD (two inputs, optional activation, optional "option
 A" shortcut: subsample the second input by 2 in H and W and zero-pad its
 channels evenly), GAP (global average pool to 1x1xC), FLATTEN (a view, HWC
 order), DWCONV (depthwise convolution: output channel c filters input channel
-c only; C_in = C_out).
+c only; C_in = C_out), EMBED (token embedding: input values are token ids,
+output [1][T][D]), LSTM (a long short-term memory layer over the T steps of
+its [1][T][D] input; output the whole sequence [1][T][H] or, with ``seq`` = 0,
+the last hidden state [1][1][H]).
 
 Activation (``relu``): 0 none, 1 ReLU, 2 ReLU6 (min(max(x, 0), 6)).
 
 Weights: CONV2D ``[C_out][kh][kw][C_in]``; DWCONV ``[C][kh][kw]``; DENSE
-``[C_out][C_in]`` where the C_in index runs over the flattened HWC input.  fp32 models hold float32
+``[C_out][C_in]`` where the C_in index runs over the flattened HWC input;
+EMBED ``[D][V]`` (neuron d's incoming weights are its value for every token);
+LSTM ``[H][4][D + H + 1]``: unit j's incoming weights are, for each gate in
+the order input, forget, cell, output, its D input weights, its H recurrent
+weights and the gate's bias (the node's own bias array is unused and zero).  fp32 models hold float32
 arrays; bf16 models hold uint16 arrays of bfloat16 bit patterns.  Biases are
 float32 ``[C_out]``.
 
 Mutation records (one per mutated neuron, Section 3.1 and Section 4):
-``op`` in {GF, NEB, NAI, NS, WS}; ``layer`` is a DENSE/CONV2D/DWCONV node index;
+``op`` in {GF, NEB, NAI, NS, WS}; ``layer`` is a weighted node's index;
 ``neuron`` an output channel (a neuron of a conv layer is one filter, Section
 2.1); ``partner`` the other neuron of a switch; GF records carry their noise,
 ``fan_in`` float32 values in the row order of ``W[neuron]``; WS records a
@@ -33,9 +40,9 @@ from typing import List, Optional, Tuple
 
 import numpy as np
 
-INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV = 0, 1, 2, 3, 4, 5, 6
+INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV, EMBED, LSTM = 0, 1, 2, 3, 4, 5, 6, 7, 8
 KIND_NAMES = {INPUT: "input", DENSE: "dense", CONV2D: "conv2d", ADD: "add",
-              GAP: "gap", FLATTEN: "flatten", DWCONV: "dwconv"}
+              GAP: "gap", FLATTEN: "flatten", DWCONV: "dwconv", EMBED: "embed", LSTM: "lstm"}
 
 # mutation operators (Section 3.1): Gaussian fuzzing, neuron effect block,
 # neuron activation inverse, neuron switch, weight shuffle
@@ -58,15 +65,18 @@ class Node:
     shortcut: int = 0         # ADD only: 0 identity, 1 option A
     out_hwc: Tuple[int, int, int] = (0, 0, 0)
     name: str = ""
+    seq: int = 0              # LSTM only: 1 = output every step, 0 = the last one
 
     @property
     def weighted(self) -> bool:
-        return self.kind in (DENSE, CONV2D, DWCONV)
+        return self.kind in (DENSE, CONV2D, DWCONV, EMBED, LSTM)
 
     @property
     def fan_in(self) -> int:
         if self.kind == DWCONV:
             return self.kh * self.kw
+        if self.kind == LSTM:
+            return 4 * (self.c_in + self.c_out + 1)
         return self.c_in * self.kh * self.kw
 
 
