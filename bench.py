@@ -36,15 +36,17 @@ KERNELS = ["dense_kernel (DENSE layers, MFMA GEMM)",
            "conv_lds_kernel (CONV2D, LDS-resident images, MFMA)",
            "conv_mfma_kernel (CONV2D, im2col implicit GEMM with scalar gathers, MFMA)",
            "conv_big_kernel (bf16 CONV2D, tiled implicit GEMM, MFMA)",
-           "dw_full_kernel (depthwise CONV2D, vector ALU)"]
+           "dw_full_kernel (depthwise CONV2D, vector ALU)",
+           "embed_kernel (token embedding gather)",
+           "lstm_kernel (LSTM recursion, MFMA per step)"]
 KERNEL_NAMES = ["dense_kernel", "conv_valu_kernel", "conv_lds_kernel", "conv_mfma_kernel",
-                "conv_big_kernel", "dw_full_kernel"]
+                "conv_big_kernel", "dw_full_kernel", "embed_kernel", "lstm_kernel"]
 VALU_FAMILIES = (1, 5)                           # fused multiply-add chains on the vector ALU
 PEAK_VALU_TFLOPS = 78.6                          # fp32 FMA without packed-fp32 instructions
 PEAK_HBM_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
 ORACLE_SAMPLE = {"mlp": (100, 500), "lenet5": (24, 6000), "vgg": (3, 64), "resnet20": (8, 256),
-                 "resnet18w": (2, 16), "mobilenetv2": (8, 256)}
+                 "resnet18w": (2, 16), "mobilenetv2": (8, 256), "lstm": (8, 500)}
 
 
 def cpu_baseline(wl, n_mut: int, n_in: int):

@@ -81,10 +81,24 @@ typedef enum {
                         its channels, (C_out - C_in)/2 before and the rest after */
   MURE_GAP = 4,      /* global average pool to 1x1xC */
   MURE_FLATTEN = 5,  /* view as 1x1x(H*W*C) */
-  MURE_DWCONV = 6    /* depthwise convolution (MobileNetV2): output channel c filters
+  MURE_DWCONV = 6,   /* depthwise convolution (MobileNetV2): output channel c filters
                         input channel c with its own kh x kw taps, stride, zero
                         padding, + b, optional activation; c_in = c_out = C;
                         weights [C][kh][kw] (fan_in = kh*kw) */
+  MURE_EMBED = 7,    /* token embedding: reads a 1 x T x 1 node whose values are
+                        token ids (integers in [0, c_in), as float32), writes
+                        1 x T x c_out with out[t][d] = W[d][token_t]; weights
+                        [c_out][c_in] (fan_in = c_in, the vocabulary); no bias */
+  MURE_LSTM = 8      /* LSTM over the T steps of a 1 x T x c_in node (float32
+                        models), h = c = 0 at the start; per step and unit j,
+                        z_q = x_t . Wx_q[j] + h . Wh_q[j] + b_q[j] for the gates
+                        q = input, forget, cell, output; i, f, o = sigmoid(z),
+                        g = tanh(z_g), c = f*c + i*g, h = o*tanh(c).  Output
+                        1 x T x c_out (seq = 1) or the last h, 1 x 1 x c_out.
+                        Weights [c_out][4][c_in + c_out + 1]: unit j's row holds
+                        per gate its input weights, recurrent weights and bias
+                        (fan_in = 4*(c_in + c_out + 1)); the bias array is
+                        ignored (pass zeros). */
 } mure_kind;
 
 /* One node of the model graph.  The array order is a topological order
@@ -104,6 +118,7 @@ typedef struct {
                          2 ReLU6 = min(max(x, 0), 6), in float32 */
   int32_t maxpool;    /* CONV2D: 0 or 2 */
   int32_t shortcut;   /* ADD: 0 identity, 1 option A */
+  int32_t seq;        /* LSTM: 1 = output every step, 0 = only the last */
 } mure_layer;
 
 /* One mutation record: operator `op` applied to neuron `neuron` of node
@@ -111,13 +126,13 @@ typedef struct {
 typedef struct {
   int32_t mutant;       /* 0 <= mutant < n_mutants */
   int32_t op;           /* mure_op */
-  int32_t layer;        /* a DENSE, CONV2D or DWCONV node */
+  int32_t layer;        /* a DENSE, CONV2D, DWCONV, EMBED or LSTM node */
   int32_t neuron;       /* 0 <= neuron < c_out of that node */
   int32_t partner;      /* NEURON_SWITCH: the other neuron (!= neuron); else -1 */
   int32_t reserved;     /* 0 */
   const float* noise;   /* GAUSS_FUZZ: host, fan_in values in W[neuron] order; else NULL */
   int64_t noise_len;    /* GAUSS_FUZZ: = fan_in (c_in*kh*kw for CONV2D, kh*kw for DWCONV,
-                           c_in for DENSE);
+                           c_in for DENSE and EMBED, 4*(c_in + c_out + 1) for LSTM);
                            WEIGHT_SHUFFLE: = fan_in (length of perm) */
   const int32_t* perm;  /* WEIGHT_SHUFFLE: host, a permutation of 0..fan_in-1; else NULL */
 } mure_record;
@@ -158,10 +173,10 @@ typedef struct {
   /* The same, split by kernel: [0] dense GEMM, [1] vector-ALU convolution
    * (few output channels), [2] LDS-resident convolution, [3] im2col implicit
    * GEMM with scalar gathers, [4] tiled bf16 implicit GEMM, [5] depthwise
-   * convolution. */
-  int64_t kernel_launches[6];
-  double kernel_ms[6];
-  int64_t kernel_macs_algorithmic[6];
+   * convolution, [6] embedding lookup, [7] LSTM recursion. */
+  int64_t kernel_launches[8];
+  double kernel_ms[8];
+  int64_t kernel_macs_algorithmic[8];
 } mure_stats;
 
 /* Version of this interface (MURE_VERSION). */

@@ -22,7 +22,7 @@ STATUS_NAMES = {0: "MURE_OK", -1: "MURE_E_INVALID", -2: "MURE_E_STATE", -3: "MUR
                 -4: "MURE_E_DEVICE", -5: "MURE_E_UNSUPPORTED"}
 MURE_F32, MURE_BF16 = 0, 1
 OP_GAUSS_FUZZ, OP_EFFECT_BLOCK, OP_ACT_INVERSE, OP_NEURON_SWITCH, OP_WEIGHT_SHUFFLE = 0, 1, 2, 3, 4
-INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV = 0, 1, 2, 3, 4, 5, 6
+INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV, EMBED, LSTM = 0, 1, 2, 3, 4, 5, 6, 7, 8
 
 EXPORTED = ["mure_version", "mure_create", "mure_load_model", "mure_apply_mutants",
             "mure_run_original", "mure_run_mutants", "mure_get_logits", "mure_mutant_plan",
@@ -33,7 +33,7 @@ class mure_layer(C.Structure):
     _fields_ = [("kind", C.c_int32), ("n_in", C.c_int32), ("in_", C.c_int32 * 2),
                 ("c_in", C.c_int32), ("c_out", C.c_int32), ("kh", C.c_int32), ("kw", C.c_int32),
                 ("stride", C.c_int32), ("pad", C.c_int32), ("relu", C.c_int32),
-                ("maxpool", C.c_int32), ("shortcut", C.c_int32)]
+                ("maxpool", C.c_int32), ("shortcut", C.c_int32), ("seq", C.c_int32)]
 
 
 class mure_record(C.Structure):
@@ -58,8 +58,8 @@ class mure_stats(C.Structure):
                 ("ms_apply", C.c_double), ("ms_run_original", C.c_double),
                 ("ms_run_mutants", C.c_double), ("gemm_launches", C.c_int64),
                 ("ms_gemm", C.c_double), ("gemm_macs_algorithmic", C.c_int64),
-                ("gemm_macs_executed", C.c_int64), ("kernel_launches", C.c_int64 * 6),
-                ("kernel_ms", C.c_double * 6), ("kernel_macs_algorithmic", C.c_int64 * 6)]
+                ("gemm_macs_executed", C.c_int64), ("kernel_launches", C.c_int64 * 8),
+                ("kernel_ms", C.c_double * 8), ("kernel_macs_algorithmic", C.c_int64 * 8)]
 
 
 class MureError(RuntimeError):
@@ -127,6 +127,9 @@ def layer_descriptors(nodes) -> "C.Array":
             L.c_in, L.c_out = int(n.c_in), int(n.c_out)
             L.kh, L.kw, L.stride, L.pad = int(n.kh), int(n.kw), int(n.stride), int(n.pad)
             L.maxpool = int(n.maxpool)
+        elif n.kind in (EMBED, LSTM):
+            L.c_in, L.c_out = int(n.c_in), int(n.c_out)
+            L.seq = int(getattr(n, "seq", 0)) if n.kind == LSTM else 0
         elif n.kind in (ADD, GAP):
             L.c_in, L.c_out = int(n.c_in), int(n.c_out)
         L.relu = int(n.relu)

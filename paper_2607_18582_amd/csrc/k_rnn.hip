@@ -1,0 +1,148 @@
+// Sequence layers of the RNN family (float32 models).
+//
+// embed_kernel: one thread per (row, step, feature) gathers W[d][token];
+// blocks of one launch row split over the slots.
+//
+// lstm_kernel: a block owns 64 rows (inputs) of one mutant slot and runs all T
+// steps.  The slot's weights sit in LDS k-major ([D + H + 1][4H]); each wave
+// keeps its 16 rows' step input [x_t, h_{t-1}, 1] in LDS and per step computes
+// the 4H gate pre-activations as one 16 x 4H GEMM on MFMA
+// (v_mfma_f32_16x16x4_f32).  Gate q of unit j is column q*H + j, so with H a
+// multiple of 16 one lane holds all four gates of its units in the same
+// accumulator position: the cell state stays in registers and the gates never
+// leave the lane.
+#include "dev.hpp"
+#include "plan.hpp"
+
+namespace mure {
+
+__global__ __launch_bounds__(256) void embed_kernel(SeqArgs a, DivU32 dd, DivU32 dt) {
+  const int sl = a.slot0 + (int)blockIdx.y;
+  const int total = a.nx * a.T * a.D;                  // < 2^31 (checked by the launcher)
+  const float* __restrict__ X = reinterpret_cast<const float*>(a.in.p);
+  const float* __restrict__ Wt = reinterpret_cast<const float*>(a.wtab[sl]);
+  for (int i = (int)blockIdx.x * 256 + threadIdx.x; i < total; i += (int)gridDim.x * 256) {
+    int rt, d, xi, t;
+    divmodu(dd, (uint32_t)i, rt, d);                   // rt = xi * T + t
+    divmodu(dt, (uint32_t)rt, xi, t);
+    const int64_t r = (int64_t)sl * a.nx + xi;
+    const float tokf = X[row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems + t];
+    const int tok = (int)tokf;
+    // an id outside the vocabulary (or not an integer) embeds to zeros
+    float v = 0.f;
+    if ((float)tok == tokf && tok >= 0 && tok < a.V) v = Wt[(int64_t)d * a.V + tok];
+    reinterpret_cast<float*>(a.out)[row_index(a.out_mode, r, a.nx, a.x0) * a.out_row + (int64_t)t * a.D + d] = v;
+  }
+}
+
+__device__ __forceinline__ float sigmoidf_(float z) { return 1.f / (1.f + expf(-z)); }
+
+template <int HT>                                      // H = 16 * HT units
+__global__ __launch_bounds__(256) void lstm_kernel(SeqArgs a) {
+  extern __shared__ __attribute__((aligned(16))) float lsm[];
+  constexpr int H = 16 * HT, NT = 4 * HT, NS = 4 * H + 16;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int sl = a.slot0 + (int)blockIdx.y;
+  const int D = a.D, K = D + H + 1;
+  const int KP = lstm_kpad(D, H), KA = lstm_ka(D, H);
+  float* Ws = lsm;                                     // [KP][NS]
+  float* As = lsm + KP * NS;                           // [64][KA]
+  const float* __restrict__ Wt = reinterpret_cast<const float*>(a.wtab[sl]);
+  // weights: unit j, gate q, k -> Ws[k][q*H + j]
+  for (int e = tid; e < KP * 4 * H; e += 256) {
+    const int k = e / (4 * H), n = e - k * (4 * H);
+    const int q = n / H, j = n - q * H;
+    Ws[k * NS + n] = k < K ? Wt[((int64_t)j * 4 + q) * K + k] : 0.f;
+  }
+  // step tile: x_t (filled per step), h = 0, the bias input 1, zero padding
+  for (int e = tid; e < 64 * KA; e += 256) {
+    const int k = e % KA;
+    As[e] = k == D + H ? 1.f : 0.f;
+  }
+  __syncthreads();
+
+  const int xi0 = (int)blockIdx.x * 64 + wave * 16;    // this wave's 16 rows
+  const float* __restrict__ X = reinterpret_cast<const float*>(a.in.p);
+  float* A = As + wave * 16 * KA;
+  float cst[HT][4];
+#pragma unroll
+  for (int jj = 0; jj < HT; ++jj)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) cst[jj][e] = 0.f;
+
+  for (int t = 0; t < a.T; ++t) {
+    // x_t of the wave's rows
+    for (int e = lane; e < 16 * D; e += 64) {
+      const int rr = e / D, d = e - rr * D;
+      const int xi = xi0 + rr;
+      float v = 0.f;
+      if (xi < a.nx) {
+        const int64_t r = (int64_t)sl * a.nx + xi;
+        v = X[row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems + (int64_t)t * D + d];
+      }
+      A[rr * KA + d] = v;
+    }
+    __syncthreads();
+    v4f acc[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[j] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int ks = 0; ks < KP; ks += 4) {
+      const int k = ks + (lane >> 4);
+      const float av = A[(lane & 15) * KA + k];
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, Ws[k * NS + j * 16 + (lane & 15)], acc[j], 0, 0, 0);
+    }
+    __syncthreads();                                   // every lane done reading h_{t-1}
+    // gates: unit u = 16*jj + (lane & 15), rows 4*(lane >> 4) + e of the wave
+#pragma unroll
+    for (int jj = 0; jj < HT; ++jj) {
+      const int u = jj * 16 + (lane & 15);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float ig = sigmoidf_(acc[0 * HT + jj][e]);
+        const float fg = sigmoidf_(acc[1 * HT + jj][e]);
+        const float gg = tanhf(acc[2 * HT + jj][e]);
+        const float og = sigmoidf_(acc[3 * HT + jj][e]);
+        const float c = fmaf(fg, cst[jj][e], ig * gg);
+        cst[jj][e] = c;
+        const float h = og * tanhf(c);
+        const int rr = (lane >> 4) * 4 + e;
+        A[rr * KA + D + u] = h;
+        const int xi = xi0 + rr;
+        if (xi < a.nx && (a.seq || t == a.T - 1)) {
+          const int64_t r = (int64_t)sl * a.nx + xi;
+          const int64_t o = row_index(a.out_mode, r, a.nx, a.x0) * a.out_row + (int64_t)(a.seq ? t : 0) * H + u;
+          reinterpret_cast<float*>(a.out)[o] = h;
+        }
+      }
+    }
+  }
+}
+
+hipError_t launch_embed(const SeqArgs& a, hipStream_t s) {
+  if (a.nslots <= 0 || a.nx <= 0) return hipSuccess;
+  const int64_t per_slot = (int64_t)a.nx * a.T * a.D;
+  if (per_slot >= INT32_MAX || a.nslots > 65535) return hipErrorInvalidValue;
+  const int64_t blocks = std::min<int64_t>((per_slot + 255) / 256, 4096);
+  hipLaunchKernelGGL(embed_kernel, dim3((unsigned)blocks, (unsigned)a.nslots), dim3(256), 0, s, a,
+                     make_divu32((uint32_t)a.D), make_divu32((uint32_t)a.T));
+  return hipGetLastError();
+}
+
+hipError_t launch_lstm(const SeqArgs& a, hipStream_t s) {
+  if (a.nslots <= 0 || a.nx <= 0) return hipSuccess;
+  if (a.H % 16 || a.H < 16 || a.H > 64 || a.nslots > 65535) return hipErrorInvalidValue;
+  const size_t lds = (size_t)lstm_lds_bytes(a.D, a.H);
+  if (lds > 64 * 1024) return hipErrorInvalidValue;
+  dim3 grid((unsigned)((a.nx + 63) / 64), (unsigned)a.nslots);
+  switch (a.H / 16) {
+    case 1: hipLaunchKernelGGL(lstm_kernel<1>, grid, dim3(256), lds, s, a); break;
+    case 2: hipLaunchKernelGGL(lstm_kernel<2>, grid, dim3(256), lds, s, a); break;
+    case 3: hipLaunchKernelGGL(lstm_kernel<3>, grid, dim3(256), lds, s, a); break;
+    default: hipLaunchKernelGGL(lstm_kernel<4>, grid, dim3(256), lds, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mure

@@ -161,6 +161,20 @@ struct DwArgs {
   int delta_T = 0;
 };
 
+// Sequence layers (float32): EMBED out[row][t][d] = W[d][token] for T tokens
+// of a row (V = vocabulary, D = width); LSTM over T steps of [row][T][D] with
+// H units, weights [H][4][D + H + 1] per slot, output every step (seq) or the
+// last one.
+struct SeqArgs {
+  TensorArg in;
+  void* out = nullptr;
+  int out_mode = MODE_BUF, out_f32 = 0;
+  int64_t out_row = 0;
+  const void* const* wtab = nullptr;
+  int slot0 = 0, nslots = 0, nx = 0, x0 = 0;
+  int T = 0, D = 0, H = 0, V = 0, seq = 0;
+};
+
 struct AddArgs {
   TensorArg a, s;
   void* out = nullptr;
@@ -240,6 +254,8 @@ hipError_t launch_conv_big(const ConvArgs& a, int nslots, hipStream_t s);
 hipError_t launch_dense(const DenseArgs& a, int nslots, int dtype, hipStream_t s);
 hipError_t launch_valu(const ValuArgs& a, int dtype, hipStream_t s);
 hipError_t launch_dw(const DwArgs& a, int dtype, hipStream_t s);
+hipError_t launch_embed(const SeqArgs& a, hipStream_t s);
+hipError_t launch_lstm(const SeqArgs& a, hipStream_t s);
 hipError_t launch_add(const AddArgs& a, int dtype, hipStream_t s);
 hipError_t launch_gap(const GapArgs& a, int dtype, hipStream_t s);
 hipError_t launch_patch(const PatchArgs& a, hipStream_t s);

@@ -234,7 +234,7 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
   const Node& n = g.nodes[v];
   const int out_f32 = v == g.out() ? 1 : 0;
   hipError_t e = hipSuccess;
-  if (n.kind == K_CONV || n.kind == K_DENSE || n.kind == K_DWCONV) {
+  if (n.weighted()) {
     const int fam = node_family(g, v);
     timed = timed && ctx->kernel_timing;
     if (timed) {
@@ -262,6 +262,15 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
         if (ex.kill_fused) *ex.kill_fused = true;
       }
       e = launch_dense(a, nslots, g.dtype, ctx->stream);
+    } else if (fam == FAM_EMBED || fam == FAM_LSTM) {
+      if (ex.vin || ex.cols || ex.ch_off) return ctx->fail(MURE_E_INVALID, "internal: delta or virtual input to a sequence layer");
+      SeqArgs a;
+      a.in.p = ins[0].p; a.in.mode = ins[0].mode; a.in.row_elems = (int64_t)n.inH * n.inW * n.inC;
+      a.out = out; a.out_mode = out_mode; a.out_f32 = out_f32; a.out_row = n.out_elems();
+      a.wtab = wtab;
+      a.slot0 = slot0; a.nslots = nslots; a.nx = nx; a.x0 = x0;
+      a.T = n.inW; a.D = fam == FAM_EMBED ? n.c_out : n.c_in; a.H = n.c_out; a.V = n.c_in; a.seq = n.seq;
+      e = fam == FAM_EMBED ? launch_embed(a, ctx->stream) : launch_lstm(a, ctx->stream);
     } else if (fam == FAM_DW) {
       DwArgs a;
       a.in.p = ins[0].p; a.in.mode = ins[0].mode; a.in.row_elems = (int64_t)n.inH * n.inW * n.inC;
@@ -472,7 +481,7 @@ mure_status mure_load_model(mure_ctx* ctx, const mure_layer* layers, int32_t n_l
     Node& v = g.nodes[i];
     v.kind = L.kind; v.n_in = L.n_in; v.in[0] = L.in[0]; v.in[1] = L.in[1];
     v.c_in = L.c_in; v.c_out = L.c_out; v.kh = L.kh; v.kw = L.kw; v.stride = L.stride; v.pad = L.pad;
-    v.relu = L.relu; v.maxpool = L.maxpool; v.shortcut = L.shortcut;
+    v.relu = L.relu; v.maxpool = L.maxpool; v.shortcut = L.shortcut; v.seq = L.seq;
     if (v.kind == K_ADD || v.kind == K_GAP || v.kind == K_FLATTEN || v.kind == K_INPUT) {
       if (v.kh > 1 || v.kw > 1) return ctx->fail(MURE_E_INVALID, "geometry given for a node without weights");
     }

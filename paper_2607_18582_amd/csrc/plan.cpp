@@ -37,7 +37,7 @@ std::string build_graph(Graph& g, int in_h, int in_w, int in_c, int dtype) {
   for (int i = 0; i < n; ++i) {
     Node& v = g.nodes[i];
     if ((i == 0) != (v.kind == K_INPUT)) return fmt_node(i, "the input must be node 0 and only node 0");
-    if (v.kind < K_INPUT || v.kind > K_DWCONV) return fmt_node(i, "unknown kind");
+    if (v.kind < K_INPUT || v.kind > K_LSTM) return fmt_node(i, "unknown kind");
     if (i == 0) {
       if (v.n_in != 0) return fmt_node(0, "the input node reads nothing");
       v.H = in_h; v.W = in_w; v.C = in_c;
@@ -52,6 +52,7 @@ std::string build_graph(Graph& g, int in_h, int in_w, int in_c, int dtype) {
     v.inH = a.H; v.inW = a.W; v.inC = a.C;
     if (v.kind != K_CONV && v.maxpool) return fmt_node(i, "only CONV2D may pool");
     if (v.kind != K_ADD && v.shortcut) return fmt_node(i, "only ADD has a shortcut mode");
+    if (v.kind != K_LSTM && v.seq) return fmt_node(i, "only LSTM has the seq flag");
     if (v.relu < 0 || v.relu > 2) return fmt_node(i, "relu must be 0 (none), 1 (ReLU) or 2 (ReLU6)");
     switch (v.kind) {
       case K_CONV: {
@@ -81,6 +82,31 @@ std::string build_graph(Graph& g, int in_h, int in_w, int in_c, int dtype) {
         v.H = v.Hc; v.W = v.Wc; v.C = v.c_out;
         v.fan_in = (int64_t)v.kh * v.kw;
         v.macs = (int64_t)v.Hc * v.Wc * v.c_out * v.fan_in;
+        break;
+      }
+      case K_EMBED: {
+        if (a.H != 1 || a.C != 1) return fmt_node(i, "EMBED reads a 1 x T x 1 token sequence");
+        if (v.c_in < 1 || v.c_out < 1) return fmt_node(i, "EMBED needs a vocabulary (c_in) and a width (c_out)");
+        if (v.relu) return fmt_node(i, "EMBED has no activation");
+        v.kh = v.kw = v.stride = 1; v.pad = 0;
+        v.H = 1; v.W = a.W; v.C = v.c_out;
+        v.Hc = v.H; v.Wc = v.W;
+        v.fan_in = v.c_in;
+        v.macs = 0;
+        break;
+      }
+      case K_LSTM: {
+        if (dtype != DT_F32) return fmt_node(i, "LSTM layers need a float32 model");
+        if (a.H != 1 || v.c_in != a.C) return fmt_node(i, "LSTM reads a 1 x T x c_in sequence");
+        if (v.c_out < 16 || v.c_out > 64 || v.c_out % 16) return fmt_node(i, "LSTM units must be 16, 32, 48 or 64");
+        if (v.seq != 0 && v.seq != 1) return fmt_node(i, "seq must be 0 or 1");
+        if (v.relu) return fmt_node(i, "LSTM has its own gate activations (relu must be 0)");
+        if (lstm_lds_bytes(v.c_in, v.c_out) > 64 * 1024) return fmt_node(i, "LSTM too wide for the kernel's LDS");
+        v.kh = v.kw = v.stride = 1; v.pad = 0;
+        v.H = 1; v.W = v.seq ? a.W : 1; v.C = v.c_out;
+        v.Hc = v.H; v.Wc = v.W;
+        v.fan_in = 4LL * (v.c_in + v.c_out + 1);
+        v.macs = (int64_t)a.W * 4 * v.c_out * (v.c_in + v.c_out + 1);
         break;
       }
       case K_DENSE: {
@@ -136,6 +162,8 @@ std::string build_graph(Graph& g, int in_h, int in_w, int in_c, int dtype) {
 int node_family(const Graph& g, int v) {
   const Node& n = g.nodes[v];
   if (n.kind == K_DWCONV) return FAM_DW;
+  if (n.kind == K_EMBED) return FAM_EMBED;
+  if (n.kind == K_LSTM) return FAM_LSTM;
   if (n.kind == K_DENSE) {
     const int vec = g.dtype == DT_F32 ? 4 : 8;       // 16-byte rows
     return (n.c_in % vec == 0 && n.c_out <= 256) ? FAM_DENSE : FAM_GEMM;
@@ -215,6 +243,12 @@ std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>&
         fuzzed.insert(recs[r].neuron);
         if (recs[r].op == OP_NS) fuzzed.insert(recs[r].partner);
       }
+    // an LSTM unit feeds every unit's next step: any record there changes
+    // the whole layer, which is recomputed
+    if (g.nodes[mp.mmi].kind == K_LSTM) {
+      mp.recompute = true;
+      for (int c = 0; c < g.nodes[mp.mmi].c_out; ++c) fuzzed.insert(c);
+    }
     if (vanilla) mp.recompute = true;    // the whole first layer, with its own weights
     mp.touched = (int64_t)fuzzed.size();
     const int C = g.nodes[mp.mmi].c_out;

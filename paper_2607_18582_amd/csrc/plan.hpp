@@ -14,21 +14,26 @@
 
 namespace mure {
 
-enum Kind { K_INPUT = 0, K_DENSE = 1, K_CONV = 2, K_ADD = 3, K_GAP = 4, K_FLATTEN = 5, K_DWCONV = 6 };
+enum Kind {
+  K_INPUT = 0, K_DENSE = 1, K_CONV = 2, K_ADD = 3, K_GAP = 4, K_FLATTEN = 5, K_DWCONV = 6,
+  K_EMBED = 7, K_LSTM = 8
+};
 enum Op { OP_GF = 0, OP_NEB = 1, OP_NAI = 2, OP_NS = 3, OP_WS = 4 };
 enum DType { DT_F32 = 0, DT_BF16 = 1 };
 
 struct Node {
   int kind = 0, n_in = 0, in[2] = {-1, -1};
   int c_in = 0, c_out = 0, kh = 1, kw = 1, stride = 1, pad = 0;
-  int relu = 0, maxpool = 0, shortcut = 0;
+  int relu = 0, maxpool = 0, shortcut = 0, seq = 0;
   // derived
   int H = 0, W = 0, C = 0;        // output shape (after pool)
   int Hc = 0, Wc = 0;             // convolution output before pooling
   int inH = 0, inW = 0, inC = 0;  // shape of in[0]
   int64_t fan_in = 0;             // weights per neuron
   int64_t macs = 0;               // multiply-accumulates per input
-  bool weighted() const { return kind == K_DENSE || kind == K_CONV || kind == K_DWCONV; }
+  bool weighted() const {
+    return kind == K_DENSE || kind == K_CONV || kind == K_DWCONV || kind == K_EMBED || kind == K_LSTM;
+  }
   int64_t out_elems() const { return (int64_t)H * W * C; }
   int64_t n_weights() const { return weighted() ? (int64_t)c_out * fan_in : 0; }
 };
@@ -63,9 +68,18 @@ enum Family {
   FAM_LDS = 2,     // fp32 conv whose padded input image and weights fit in LDS
   FAM_GEMM = 3,    // implicit GEMM with a scalar im2col gather (any shape)
   FAM_BIG = 4,     // bf16 tiled implicit GEMM with 16-byte gathers (C_in % 8 == 0)
-  FAM_DW = 5       // depthwise convolution (per-channel taps on the vector ALU)
+  FAM_DW = 5,      // depthwise convolution (per-channel taps on the vector ALU)
+  FAM_EMBED = 6,   // embedding lookup (a gather)
+  FAM_LSTM = 7     // LSTM recursion: per step one MFMA GEMM over [x_t, h, 1], gates on the VALU
 };
-constexpr int N_FAMILIES = 6;
+constexpr int N_FAMILIES = 8;
+// LSTM kernel: units a multiple of 16, at most 64; LDS for the weights
+// (k-major, row stride 4H + 16) and a 64-row step tile
+constexpr int lstm_kpad(int d, int h) { return (d + h + 1 + 3) / 4 * 4; }
+constexpr int lstm_ka(int d, int h) { const int k = lstm_kpad(d, h); return (k / 4) % 2 ? k : k + 4; }
+constexpr int64_t lstm_lds_bytes(int d, int h) {
+  return ((int64_t)lstm_kpad(d, h) * (4 * h + 16) + 64LL * lstm_ka(d, h)) * 4;
+}
 int node_family(const Graph& g, int v);
 
 // Launch geometry shared by the planner (family choice) and the kernels.

@@ -36,7 +36,7 @@ def _plan_ctx(model):
     return m
 
 
-@pytest.mark.parametrize("cfg", ["mlp", "lenet5", "vgg", "resnet20", "resnet18w", "mobilenetv2"])
+@pytest.mark.parametrize("cfg", ["mlp", "lenet5", "vgg", "resnet20", "resnet18w", "mobilenetv2", "lstm"])
 def test_planner_matches_oracle_boundaries_and_ledger(cfg):
     wl = W.make_workload(cfg, n_inputs=1, n_mutants=60)
     m = _plan_ctx(wl.model)
@@ -183,4 +183,31 @@ def test_depthwise_switch_recomputes_at_mmi():
     # algorithmic MACs at mmi: two depthwise channels for mutant 0, none for mutant 1
     after = lambda l: sum(O.node_macs(O.OracleModel(m))[l + 1:])
     assert st["macs_algorithmic"] == 2 * per_dw + after(dw) + after(pw)
+    ctx.close()
+
+
+def test_lstm_records_recompute_the_whole_layer():
+    """Every record on an LSTM layer changes all of its units' trajectories
+    (the recurrence), so even an effect block recomputes the layer, while an
+    effect block on the embedding only remaps one feature."""
+    m = W.make_model("lstm", "f32", 0.0)
+    emb, l1 = 1, 2
+    ctx = _plan_ctx(m)
+    ctx.apply_mutants(2, np.array([0, 1], np.int32), np.array([W.NEB, W.NEB], np.int32),
+                      np.array([l1, emb], np.int32), np.array([3, 3], np.int32),
+                      np.array([-1, -1], np.int32), [None, None])
+    macs = O.node_macs(O.OracleModel(m))
+    st = ctx.stats()
+    assert st["macs_algorithmic"] == sum(macs[l1:]) + sum(macs[emb + 1:])
+    assert st["n_groups"] == 2
+    ctx.close()
+
+
+def test_sequence_layer_validation():
+    m = W.make_model("lstm", "f32", 0.0)
+    bad = list(m.nodes)
+    bad[2] = W.Node(W.LSTM, (1,), 32, 24, out_hwc=(1, 40, 24), name="odd", seq=1)
+    ctx = B.Mure(device=-1)
+    with pytest.raises(B.MureError, match="units"):
+        ctx.load_model(bad, m.in_hwc, "f32", m.weights, m.biases)
     ctx.close()

@@ -84,3 +84,7 @@ def test_resnet18w_full_size():
 
 def test_mobilenetv2_full_size():
     _sampled_parity("mobilenetv2", 1, 16, 48)
+
+
+def test_lstm_full_size():
+    _sampled_parity("lstm", 1, 24, 256)

@@ -48,6 +48,12 @@ def test_resnet18w_small():
     _parity(W.make_workload("resnet18w", n_inputs=12, n_mutants=4))
 
 
+def test_lstm_small():
+    # embedding gathers, the LSTM recursion on MFMA, every operator
+    _parity(W.make_workload("lstm", n_inputs=130, n_mutants=40,
+                            ops=(W.GF, W.NEB, W.NAI, W.NS, W.WS)))
+
+
 def test_mobilenetv2_small():
     # depthwise layers (full and channel-list kernels), ReLU6, inverted
     # residuals; weight shuffles included, switches on depthwise layers recompute
@@ -80,7 +86,7 @@ def test_repeat_is_deterministic():
     assert np.array_equal(z1, z2)
 
 
-@pytest.mark.parametrize("cfg", ["lenet5", "resnet20", "mobilenetv2"])
+@pytest.mark.parametrize("cfg", ["lenet5", "resnet20", "mobilenetv2", "lstm"])
 def test_identity_mutants_bit_exact(cfg):
     """Zero-noise fuzz at every layer and a mutant without records reproduce
     the original's logits bit for bit and are never killed."""
@@ -144,7 +150,7 @@ def test_weight_shuffle_operator():
                                 ops=(W.GF, W.NEB, W.NAI, W.NS, W.WS)))
 
 
-@pytest.mark.parametrize("cfg", ["lenet5", "vgg", "resnet20", "mobilenetv2"])
+@pytest.mark.parametrize("cfg", ["lenet5", "vgg", "resnet20", "mobilenetv2", "lstm"])
 def test_vanilla_mode_equals_memoized_bit_for_bit(cfg):
     """Theorem 1 on the GPU: running every mutant from the raw input gives
     exactly the memoized result -- kill bits, score and logits, bit for bit."""
