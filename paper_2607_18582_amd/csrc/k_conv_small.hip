@@ -64,17 +64,22 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
     koff[k] = o;
   }
   __shared__ int nchg;                   // channels the mutant's map changes
-  __shared__ int chg[64];
+  __shared__ int chg[64], chsrc[64];     // ... and their map entries
   if (virt) {
     for (int c = tid; c < a.C; c += 256) chrow[c] = a.vin.chmap[(int64_t)slot * a.C + c];
     __syncthreads();
     if (tid == 0) {
       int n = 0;
       for (int c = 0; c < a.C && n < 64; ++c)
-        if (chrow[c] != c) chg[n++] = c;
+        if (chrow[c] != c) { chg[n] = c; chsrc[n] = chrow[c]; ++n; }
       nchg = n;
     }
   }
+  // per piece: the image offset of each GEMM row's receptive field, and the
+  // output offset of each group of 4 rows (a pool window, or 4 pixels)
+  __shared__ int rowbase[256];
+  __shared__ int64_t grpout[64];
+  const bool grp_ok = !a.cols && (a.pool || a.P % 4 == 0);
   constexpr int TN = BN / 16;
   // per column of this lane: bias, output slot, channel offset and stride
   float bv[TN];
@@ -115,14 +120,17 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
       if (nc > 0) {
         __syncthreads();
         const int HW = a.H * a.W;
+        const float* __restrict__ cache = reinterpret_cast<const float*>(a.vin.cache);
+        const float* __restrict__ delta = reinterpret_cast<const float*>(a.vin.delta);
         for (int e = tid; e < nimg * HW; e += 256) {
           int ii, pix;
           divmodu(a.dHW, (uint32_t)e, ii, pix);
-          const int xi = xi_first + ii;
-          const int64_t r = (int64_t)slot * a.nx + xi;
+          // this pixel's original channels and compact delta entries
+          const float* cp = cache + ((int64_t)a.x0 + xi_first) * img + (int64_t)e * a.C;
+          const float* dp = delta + (((int64_t)slot * a.nx + xi_first + ii) * HW + pix) * a.vin.T;
           for (int j = 0; j < nc; ++j) {
-            const int c = chg[j];
-            imgs[e * a.C + c] = virtual_elem<float>(a.vin, chrow, r, xi, a.x0, pix, c);
+            const int src = chsrc[j];
+            imgs[e * a.C + chg[j]] = src >= 0 ? cp[src] : src == -1 ? 0.f : dp[-2 - src];
           }
         }
       }
@@ -160,11 +168,8 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
     }
     __syncthreads();
 
-    const int mw = m0 + wave * 64;
-    int base[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = mw + i * 16 + (lane & 15);
+    {
+      const int m = m0 + tid;
       int b = 0;
       if (m < Mslot) {
         int xi, p, oy, ox;
@@ -178,9 +183,18 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
           divmodu(a.dWc, (uint32_t)p, oy, ox);
         }
         b = (xi - xi_first) * img + (oy * a.stride * Wp2 + ox * a.stride) * a.C;
+        if (grp_ok && (tid & 3) == 0) {
+          const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xi, a.nx, a.x0);
+          grpout[tid >> 2] = ro * a.out_row + (int64_t)(a.pool ? (p >> 2) : p) * a.Cout;
+        }
       }
-      base[i] = b;
+      rowbase[tid] = b;
     }
+    __syncthreads();
+    const int mw = m0 + wave * 64;
+    int base[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) base[i] = rowbase[wave * 64 + i * 16 + (lane & 15)];
     v4f acc[4][TN];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -229,6 +243,29 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
 #undef MURE_LDS_READ
 #undef MURE_LDS_MFMA
 
+    if (grp_ok) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int mb = mw + i * 16 + (lane >> 4) * 4;
+        if (mb >= Mslot) continue;
+        const int64_t go = grpout[(wave * 64 + i * 16 + (lane >> 4) * 4) >> 2];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int n = n0 + j * 16 + (lane & 15);
+          if (n >= ncol) continue;
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = act(acc[i][j][e] + bv[j], a.relu);
+          if (a.pool) {
+            store_out<float>(a.out, a.out_f32, go + n, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) store_out<float>(a.out, a.out_f32, go + (int64_t)e * a.Cout + n, v[e]);
+          }
+        }
+      }
+      continue;
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int mb = mw + i * 16 + (lane >> 4) * 4;
