@@ -292,6 +292,19 @@ def main():
     all_flops = 2.0 * st["gemm_macs_algorithmic"]
     all_achieved = all_flops / (ms_gemm * 1e-3) / 1e12 if ms_gemm > 0 else 0.0
     tr = read_traffic(KERNEL_NAMES[fam], args.config, N, M)
+    # the kernel's bound: HBM when its algorithmic FLOP per byte sits below
+    # the ridge point of its compute peak
+    alg_bytes = float(st["kernel_bytes_algorithmic"][fam])
+    intensity = alg_flops / alg_bytes if alg_bytes > 0 else float("inf")
+    ridge = kernel_peak(fam) * 1e12 / (PEAK_HBM_GBS * 1e9)
+    hbm_bound = intensity < ridge
+    if hbm_bound:
+        roof = {"bound": "hbm", "achieved": alg_bytes / (ms_k * 1e-3) / 1e9 if ms_k > 0 else 0.0,
+                "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    else:
+        roof = {"bound": "alu" if fam in VALU_FAMILIES else "mfma", "achieved": achieved,
+                "peak": kernel_peak(fam), "unit": "TFLOP/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
     line = {
         "metric": "mutant-input suffix evals/sec + MFMA/HBM roofline fraction, 1 MI355X",
         "value": M * N / dt,
@@ -312,14 +325,15 @@ def main():
         "ms_run_original": float(np.median([s["ms_run_original"] for s in stats])),
         "ms_apply": float(np.median([s["ms_apply"] for s in stats])),
         "mutation_score": [score["ms_num"], score["ms_den"]],
-        "roofline": {"bound": "alu" if fam in VALU_FAMILIES else "mfma", "kernel": KERNELS[fam],
-                     "achieved": achieved, "peak": kernel_peak(fam), "unit": "TFLOP/s",
-                     "frac": achieved / kernel_peak(fam),
+        "roofline": {**roof, "kernel": KERNELS[fam],
                      "traffic": tr["traffic_bytes_per_launch"] if tr else None,
                      "traffic_source": os.path.relpath(traffic_path(KERNEL_NAMES[fam], args.config), ROOT)
                      if tr else None,
                      "launches": launches, "avg_launch_ms": ms_k / max(launches, 1),
                      "alg_flops_per_launch": alg_flops / max(launches, 1),
+                     "alg_bytes_per_launch": alg_bytes / max(launches, 1),
+                     "flop_per_byte": intensity, "ridge_flop_per_byte": ridge,
+                     "compute_frac": achieved / kernel_peak(fam),
                      "share_of_run_mutants": ms_k / ms_mut if ms_mut else None,
                      "all_weighted_layers": {"achieved": all_achieved, "frac": all_achieved / peak,
                                              "ms": ms_gemm, "launches": st["gemm_launches"]}},

@@ -177,6 +177,10 @@ typedef struct {
   int64_t kernel_launches[8];
   double kernel_ms[8];
   int64_t kernel_macs_algorithmic[8];
+  /* Algorithmic HBM bytes of those launches: every input row read once (a
+   * prefix-cache tensor once for all mutants), every output element written
+   * once, every mutant's weights read once. */
+  double kernel_bytes_algorithmic[8];
 } mure_stats;
 
 /* Version of this interface (MURE_VERSION). */

@@ -59,7 +59,8 @@ class mure_stats(C.Structure):
                 ("ms_run_mutants", C.c_double), ("gemm_launches", C.c_int64),
                 ("ms_gemm", C.c_double), ("gemm_macs_algorithmic", C.c_int64),
                 ("gemm_macs_executed", C.c_int64), ("kernel_launches", C.c_int64 * 8),
-                ("kernel_ms", C.c_double * 8), ("kernel_macs_algorithmic", C.c_int64 * 8)]
+                ("kernel_ms", C.c_double * 8), ("kernel_macs_algorithmic", C.c_int64 * 8),
+                ("kernel_bytes_algorithmic", C.c_double * 8)]
 
 
 class MureError(RuntimeError):

@@ -2,11 +2,13 @@
 //
 // Output channel c reads only input channel c, so the node is a per-element
 // chain of kh*kw fused multiply-adds: memory-bound, no contraction for the
-// matrix cores.  Each element's chain runs over the in-image taps in (dy, dx)
-// order, starting from 0, then adds the bias -- the same chain in the full
-// kernel and in the channel-list (delta) kernel, so a delta is bit-identical
-// to the full node.  The full kernel moves 16-byte channel vectors (8 bf16 or
-// 4 fp32 channels of one pixel); the block's slot weights sit in LDS as fp32.
+// matrix cores.  Each element's chain runs over the kh*kw taps in (dy, dx)
+// order, starting from 0 (a tap outside the image multiplies a zero input),
+// then adds the bias -- the same chain in the full kernel and in the
+// channel-list (delta) kernel, so a delta is bit-identical to the full node.
+// The full kernel moves 16-byte channel vectors (8 bf16 or 4 fp32 channels of
+// one pixel), issuing all taps' loads before the arithmetic; the block's slot
+// weights sit in LDS as fp32, tap-major, so a lane's channels are contiguous.
 #include "dev.hpp"
 
 namespace mure {
@@ -16,48 +18,72 @@ constexpr int DW_MAXW = 8192;                         // C * kh * kw staged in L
 constexpr int DW_MAXC = 2048;
 }
 
-template <typename T>
+// zeros that taps outside the image read instead of the input
+static __device__ __attribute__((aligned(16))) v4u g_dw_zero[1] = {};
+
+// KH, KW: the filter size when known at compile time (3 x 3), else 0.
+template <typename T, int KH, int KW>
 __global__ __launch_bounds__(256) void dw_full_kernel(DwArgs a, int rows, DivU32 dcv, DivU32 dpix,
                                                       DivU32 dwo) {
   constexpr int VEC = 16 / sizeof(T);
-  __shared__ float wl[DW_MAXW];
-  __shared__ float bl[DW_MAXC];
+  __shared__ __attribute__((aligned(16))) float wl[DW_MAXW];   // [tap][C]
+  __shared__ __attribute__((aligned(16))) float bl[DW_MAXC];
   const int tid = threadIdx.x;
   const int sl = a.slot0 + (int)blockIdx.y;
-  const int taps = a.kh * a.kw;
+  const int kh = KH ? KH : a.kh, kw = KW ? KW : a.kw;
+  const int taps = kh * kw;
   const T* __restrict__ Wt = reinterpret_cast<const T*>(a.wtab[sl]);
-  for (int e = tid; e < a.C * taps; e += 256) wl[e] = to_f<T>(Wt[e]);
+  for (int e = tid; e < a.C * taps; e += 256) {
+    const int c = e / taps, tp = e - c * taps;
+    wl[tp * a.C + c] = to_f<T>(Wt[e]);
+  }
   for (int c = tid; c < a.C; c += 256) bl[c] = a.btab[sl][c];
   __syncthreads();
-  const int CV = a.C / VEC;
+  const v4u* const zp = reinterpret_cast<const v4u*>(g_dw_zero);
   const int xi0 = (int)blockIdx.x * rows;
   const int nr = min(rows, a.nx - xi0);
-  const int per = a.Ho * a.Wo * CV;                   // vectors per output row
+  const int per = a.Ho * a.Wo * (a.C / VEC);          // vectors per output row
   const T* __restrict__ X = reinterpret_cast<const T*>(a.in.p);
   for (int it = tid; it < nr * per; it += 256) {
     int ii, rem, pix, cv, oy, ox;
-    divmodu(dpix, (uint32_t)it, ii, rem);             // rem = pixel * CV + cv
+    divmodu(dpix, (uint32_t)it, ii, rem);             // rem = pixel * (C / VEC) + cv
     divmodu(dcv, (uint32_t)rem, pix, cv);
     divmodu(dwo, (uint32_t)pix, oy, ox);
-    const int xi = xi0 + ii;
-    const int64_t r = (int64_t)sl * a.nx + xi;
+    const int64_t r = (int64_t)sl * a.nx + xi0 + ii;
     const T* xr = X + row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems + cv * VEC;
+    const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
     float acc[VEC];
 #pragma unroll
     for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
-    const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
-    for (int dy = 0; dy < a.kh; ++dy) {
-      const int iy = iy0 + dy;
-      if ((unsigned)iy >= (unsigned)a.H) continue;
-      for (int dx = 0; dx < a.kw; ++dx) {
-        const int ix = ix0 + dx;
-        if ((unsigned)ix >= (unsigned)a.W) continue;
-        const v4u raw = *reinterpret_cast<const v4u*>(xr + ((int64_t)iy * a.W + ix) * a.C);
-        T xv[VEC];
-        __builtin_memcpy(xv, &raw, 16);
-        const float* wt = wl + (cv * VEC) * taps + dy * a.kw + dx;
+    // every tap's 16-byte input vector first (zeros outside the image), then
+    // the chains in (dy, dx) order
+    constexpr int NT = KH * KW > 0 ? KH * KW : 1;
+    if constexpr (KH > 0) {
+      v4u xv[NT];
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) acc[j] = fmaf(to_f<T>(xv[j]), wt[j * taps], acc[j]);
+      for (int tp = 0; tp < NT; ++tp) {
+        const int iy = iy0 + tp / KW, ix = ix0 + tp % KW;
+        const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+        xv[tp] = *(ok ? reinterpret_cast<const v4u*>(xr + ((int64_t)iy * a.W + ix) * a.C) : zp);
+      }
+#pragma unroll
+      for (int tp = 0; tp < NT; ++tp) {
+        T x8[VEC];
+        __builtin_memcpy(x8, &xv[tp], 16);
+        const float* wt = wl + tp * a.C + cv * VEC;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) acc[j] = fmaf(to_f<T>(x8[j]), wt[j], acc[j]);
+      }
+    } else {
+      for (int tp = 0; tp < taps; ++tp) {
+        const int iy = iy0 + tp / kw, ix = ix0 + tp % kw;
+        const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+        const v4u raw = *(ok ? reinterpret_cast<const v4u*>(xr + ((int64_t)iy * a.W + ix) * a.C) : zp);
+        T x8[VEC];
+        __builtin_memcpy(x8, &raw, 16);
+        const float* wt = wl + tp * a.C + cv * VEC;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) acc[j] = fmaf(to_f<T>(x8[j]), wt[j], acc[j]);
       }
     }
     T ov[VEC];
@@ -101,11 +127,12 @@ __global__ __launch_bounds__(256) void dw_list_kernel(DwArgs a, int rows, DivU32
     const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
     for (int dy = 0; dy < a.kh; ++dy) {
       const int iy = iy0 + dy;
-      if ((unsigned)iy >= (unsigned)a.H) continue;
       for (int dx = 0; dx < a.kw; ++dx) {
         const int ix = ix0 + dx;
-        if ((unsigned)ix >= (unsigned)a.W) continue;
-        acc = fmaf(to_f<T>(xr[((int64_t)iy * a.W + ix) * a.C]), to_f<T>(wr[dy * a.kw + dx]), acc);
+        // taps outside the image contribute a zero input, as in the full kernel
+        const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+        const float x = ok ? to_f<T>(xr[((int64_t)iy * a.W + ix) * a.C]) : 0.f;
+        acc = fmaf(x, to_f<T>(wr[dy * a.kw + dx]), acc);
       }
     }
     const float v = act(acc + bias[c], a.relu);
@@ -132,8 +159,14 @@ hipError_t launch_dw(const DwArgs& a, int dtype, hipStream_t s) {
   if (full) {
     const DivU32 dcv = make_divu32((uint32_t)(a.C / vec));
     const DivU32 dpix = make_divu32((uint32_t)(pix * (a.C / vec)));
-    if (dtype == 0) hipLaunchKernelGGL(dw_full_kernel<float>, grid, dim3(256), 0, s, a, rows, dcv, dpix, dwo);
-    else hipLaunchKernelGGL(dw_full_kernel<bf16_t>, grid, dim3(256), 0, s, a, rows, dcv, dpix, dwo);
+    const bool k3 = a.kh == 3 && a.kw == 3;
+    if (dtype == 0) {
+      if (k3) hipLaunchKernelGGL((dw_full_kernel<float, 3, 3>), grid, dim3(256), 0, s, a, rows, dcv, dpix, dwo);
+      else hipLaunchKernelGGL((dw_full_kernel<float, 0, 0>), grid, dim3(256), 0, s, a, rows, dcv, dpix, dwo);
+    } else {
+      if (k3) hipLaunchKernelGGL((dw_full_kernel<bf16_t, 3, 3>), grid, dim3(256), 0, s, a, rows, dcv, dpix, dwo);
+      else hipLaunchKernelGGL((dw_full_kernel<bf16_t, 0, 0>), grid, dim3(256), 0, s, a, rows, dcv, dpix, dwo);
+    }
   } else {
     // the row split assumes every channel (the largest list)
     if (dtype == 0) hipLaunchKernelGGL(dw_list_kernel<float>, grid, dim3(256), 0, s, a, rows, dwo);

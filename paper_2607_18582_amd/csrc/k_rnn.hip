@@ -35,7 +35,11 @@ __global__ __launch_bounds__(256) void embed_kernel(SeqArgs a, DivU32 dd, DivU32
   }
 }
 
-__device__ __forceinline__ float sigmoidf_(float z) { return 1.f / (1.f + expf(-z)); }
+// Gate activations from the hardware exponential: sigmoid(z) = 1/(1 + e^-z)
+// and tanh(z) = 2 sigmoid(2z) - 1 (a few ulp from the correctly rounded
+// values; every launch of a layer uses the same formulas).
+__device__ __forceinline__ float sigmoidf_(float z) { return __fdividef(1.f, 1.f + __expf(-z)); }
+__device__ __forceinline__ float tanhf_(float z) { return 2.f * sigmoidf_(2.f * z) - 1.f; }
 
 template <int HT>                                      // H = 16 * HT units
 __global__ __launch_bounds__(256) void lstm_kernel(SeqArgs a) {
@@ -102,11 +106,11 @@ __global__ __launch_bounds__(256) void lstm_kernel(SeqArgs a) {
       for (int e = 0; e < 4; ++e) {
         const float ig = sigmoidf_(acc[0 * HT + jj][e]);
         const float fg = sigmoidf_(acc[1 * HT + jj][e]);
-        const float gg = tanhf(acc[2 * HT + jj][e]);
+        const float gg = tanhf_(acc[2 * HT + jj][e]);
         const float og = sigmoidf_(acc[3 * HT + jj][e]);
         const float c = fmaf(fg, cst[jj][e], ig * gg);
         cst[jj][e] = c;
-        const float h = og * tanhf(c);
+        const float h = og * tanhf_(c);
         const int rr = (lane >> 4) * 4 + e;
         A[rr * KA + D + u] = h;
         const int xi = xi0 + rr;

@@ -205,6 +205,7 @@ struct Extra {
   const DeltaCol* cols = nullptr;     // gathered-column delta at mmi (MFMA families)
   int ncols = 0, col_slot0 = 0;
   int64_t exec_macs = -1;             // MACs the launch executes, when not slots * rows * node
+  int64_t delta_channels = -1;        // channels a per-slot channel-list delta computes
   const VirtualIn* vin = nullptr;     // read the first mutated node's output virtually
   int fuse_add = -1;                  // ADD node fused into this convolution's epilogue
   Where skip{nullptr, MODE_BUF};      // that ADD's shortcut input
@@ -357,6 +358,29 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
       ctx->stats.gemm_macs_executed += exec_macs;
       ctx->stats.kernel_launches[fam]++;
       ctx->stats.kernel_macs_algorithmic[fam] += alg_macs;
+      // algorithmic HBM bytes: each input row read once (a prefix-cache
+      // tensor once for all slots), each output element written once, each
+      // slot's (or column's) weights read once
+      const int64_t es = g.dtype == DT_F32 ? 4 : 2;
+      const int64_t in_row = (int64_t)n.inH * n.inW * n.inC * es;
+      const int64_t out_ch = (int64_t)n.H * n.W * (out_f32 ? 4 : es);       // one channel of a row
+      const int64_t w_row = n.fan_in * es;                                  // one neuron's weights
+      int64_t bytes;
+      const bool shared_in = ins[0].mode == MODE_CACHE && !ex.vin;
+      if (ex.cols) {
+        bytes = nx * in_row + (int64_t)ex.ncols * (nx * out_ch + w_row);
+      } else if (ex.ch_off) {
+        const int64_t ch = ex.delta_channels >= 0 ? ex.delta_channels : (int64_t)nslots * n.c_out;
+        bytes = nx * in_row + ch * (nx * out_ch + w_row);
+      } else {
+        bytes = (shared_in ? nx : (int64_t)nslots * nx) * in_row +
+                (int64_t)nslots * nx * n.c_out * out_ch + (int64_t)nslots * n.c_out * w_row;
+        if (ex.fuse_add >= 0) {
+          const int64_t skip_row = g.nodes[g.nodes[ex.fuse_add].in[1]].out_elems() * es;
+          bytes += (ex.skip.mode == MODE_CACHE ? nx : (int64_t)nslots * nx) * skip_row;
+        }
+      }
+      ctx->stats.kernel_bytes_algorithmic[fam] += (double)bytes;
     }
   } else if (n.kind == K_ADD) {
     const Node& s = g.nodes[n.in[1]];
@@ -940,6 +964,7 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
           if (gr.delta) {
             if (gr.virt) ex.delta_T = gr.T;
             ex.exec_macs = tl * per_ch * cnt;
+            ex.delta_channels = tl;
             if (node_family(g, mmi) == FAM_VALU || node_family(g, mmi) == FAM_DW) {
               ex.ch_off = ctx->d_slots.as<int32_t>() + gt.choff + cs0;
               ex.ch_list = ctx->d_slots.as<int32_t>();
@@ -1054,6 +1079,7 @@ mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* ki
     ctx->stats.kernel_launches[f] = 0;
     ctx->stats.kernel_ms[f] = 0;
     ctx->stats.kernel_macs_algorithmic[f] = 0;
+    ctx->stats.kernel_bytes_algorithmic[f] = 0;
   }
   ctx->tevents_used = 0;
   ctx->tevent_family.clear();
