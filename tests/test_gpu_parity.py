@@ -161,3 +161,41 @@ def test_vanilla_mode_equals_memoized_bit_for_bit(cfg):
     for mid in sample_mutants(m1, wl):
         assert np.array_equal(m1.get_logits(mid).cpu().numpy(), m2.get_logits(mid).cpu().numpy()), mid
     assert m2.stats()["n_groups"] == 1
+
+
+def test_edge_cases_zero_mutants_identity_only_single_input():
+    from paper_2607_18582_amd import MureError, MURE_E_INVALID
+    wl = W.make_workload("lenet5", n_inputs=1, n_mutants=6)
+    _parity(wl)                                             # one input: one ragged kill word
+    # no mutants at all: an empty kill matrix and the score 0/0
+    empty = W.Mutants(0, np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.int32),
+                      np.zeros(0, np.int32), np.zeros(0, np.int32), [])
+    m, words, kills, score = run_gpu(W.Workload("none", wl.model, wl.inputs, empty))
+    assert words.size == 0 and len(kills) == 0 and (score["ms_num"], score["ms_den"]) == (0, 0)
+    # mutants without records (identity): never killed, the denominator still counts them
+    ident = W.Mutants(3, np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.int32),
+                      np.zeros(0, np.int32), np.zeros(0, np.int32), [])
+    wl3 = W.make_workload("lenet5", n_inputs=70, n_mutants=1)
+    m, words, kills, score = run_gpu(W.Workload("identity", wl3.model, wl3.inputs, ident))
+    assert not words.any() and score["ms_num"] == 0 and score["ms_den"] == 3 * score["n_labels"]
+    assert m.stats()["n_groups"] == 0
+    # an empty input set is rejected
+    with pytest.raises(MureError) as e:
+        m.run_original(device_inputs(wl3)[:0])
+    assert e.value.status == MURE_E_INVALID
+
+
+def test_largest_class_count():
+    """512 classes (the library's maximum): the kill runs on its own kernel
+    with an 8-word class mask; ground-truth labels spread over the classes."""
+    b = W.configs._Builder((1, 1, 24))
+    x = b.dense(0, 32, True, "h")
+    b.dense(x, 512, False, "out")
+    w, bb = W.configs._draw_weights(b.nodes, "f32", 0.1, seed=3)
+    model = W.Model("mlp512", "f32", b.nodes, w, bb)
+    x = W.make_inputs(model, 200, "uniform")
+    mu = W.make_mutants(model, 24, 2, "layer_first", variant=5, ops=(W.GF, W.NEB, W.NAI, W.NS, W.WS))
+    wl = W.Workload("mlp512", model, x, mu)
+    _parity(wl)
+    labels = np.random.default_rng(4).integers(0, 512, size=200).astype(np.int32)
+    _parity(wl, labels=labels)
