@@ -23,9 +23,10 @@ template <> struct DenseCfg<bf16_t> { static constexpr int BK = 64, VEC = 8, PAD
 // The next k chunk's global loads are issued into registers before the MFMAs
 // of the current chunk (register prefetch); tiles are staged as raw 16-byte
 // vectors.
-template <typename T, int BN, int WAVES_M, bool VIRT>
+// BM: rows (inputs) per block; 64 whenever the kill is fused (one wave's
+// ballot is one kill word).
+template <typename T, int BN, int WAVES_M, bool VIRT, int BM>
 __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
-  constexpr int BM = 64;
   constexpr int BK = DenseCfg<T>::BK, VEC = DenseCfg<T>::VEC, LD = BK + DenseCfg<T>::PAD;
   constexpr int WAVES_N = 4 / WAVES_M;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
@@ -64,6 +65,7 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
 
   constexpr int KMAP = VIRT ? 4096 : 1;
   __shared__ int kmap[KMAP];
+  __shared__ unsigned char kdirect[VIRT ? KMAP / VEC : 1];   // the vector's k map is the identity
   if constexpr (VIRT) {
     const int32_t* chrow = a.vin.chmap + (int64_t)slot * a.vin.C;
     for (int k = tid; k < a.K; k += 256) {
@@ -71,6 +73,13 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
       const int src = chrow[c];
       kmap[k] = src >= 0 ? pix * a.vin.C + src
               : src == -1 ? INT_MIN : -1 - (pix * a.vin.T + (-2 - src));
+    }
+    __syncthreads();
+    for (int kv = tid; kv < a.K / VEC; kv += 256) {
+      bool id = true;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) id = id && kmap[kv * VEC + e] == kv * VEC + e;
+      kdirect[kv] = id ? 1 : 0;
     }
   }
   __syncthreads();
@@ -110,7 +119,9 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
       const int k = kc + kv * VEC;
       v4u v = v4u{0u, 0u, 0u, 0u};
       if constexpr (VIRT) {
-        if (crow[j]) {
+        if (crow[j] && k < a.K && kdirect[k / VEC]) {
+          v = *reinterpret_cast<const v4u*>(crow[j] + k);   // unchanged channels: one vector
+        } else if (crow[j]) {
           T e8[VEC];
 #pragma unroll
           for (int e = 0; e < VEC; ++e) {
@@ -262,11 +273,11 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
 template <typename T, bool VIRT>
 static hipError_t dense_dispatch(const DenseArgs& a, dim3 grid, int bn, hipStream_t s) {
   switch (bn) {
-    case 16: hipLaunchKernelGGL((dense_kernel<T, 16, 4, VIRT>), grid, dim3(256), 0, s, a); break;
-    case 32: hipLaunchKernelGGL((dense_kernel<T, 32, 4, VIRT>), grid, dim3(256), 0, s, a); break;
-    case 64: hipLaunchKernelGGL((dense_kernel<T, 64, 2, VIRT>), grid, dim3(256), 0, s, a); break;
-    case 128: hipLaunchKernelGGL((dense_kernel<T, 128, 2, VIRT>), grid, dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL((dense_kernel<T, 256, 1, VIRT>), grid, dim3(256), 0, s, a); break;
+    case 16: hipLaunchKernelGGL((dense_kernel<T, 16, 4, VIRT, 64>), grid, dim3(256), 0, s, a); break;
+    case 32: hipLaunchKernelGGL((dense_kernel<T, 32, 4, VIRT, 64>), grid, dim3(256), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((dense_kernel<T, 64, 2, VIRT, 64>), grid, dim3(256), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((dense_kernel<T, 128, 2, VIRT, 64>), grid, dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((dense_kernel<T, 256, 1, VIRT, 64>), grid, dim3(256), 0, s, a); break;
   }
   return hipGetLastError();
 }
@@ -282,7 +293,8 @@ hipError_t launch_dense(const DenseArgs& a, int nslots, int dtype, hipStream_t s
   if (a.cols) nslots = 1;
   const int ncol = a.cols ? a.ncols : a.Cout;
   const int bn = dense_bn(ncol);
-  dim3 grid((unsigned)((a.nx + 63) / 64), (unsigned)nslots, (unsigned)((ncol + bn - 1) / bn));
+  const int bm = 64;
+  dim3 grid((unsigned)((a.nx + bm - 1) / bm), (unsigned)nslots, (unsigned)((ncol + bn - 1) / bn));
   if (a.do_kill && (grid.z != 1 || bn > 64)) return hipErrorInvalidValue;
   if (a.vin.chmap) {
     if (a.K > 4096) return hipErrorInvalidValue;
