@@ -208,6 +208,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--fused", type=int, default=1)
     ap.add_argument("--conv-tile", type=int, default=0)
+    ap.add_argument("--workspace-mb", type=int, default=0,
+                    help="cap the per-chunk activation workspace (0: the library default)")
     ap.add_argument("--gain", type=int, default=None,
                     help="also time vanilla mutation testing (every mutant from the raw "
                          "input) and report the paper's gain (t_v - t) / t_v (default: on "
@@ -260,6 +262,8 @@ def main():
     m.set_option("kernel_timing", 1)
     m.set_option("fused_paths", args.fused)
     m.set_option("conv_tile", args.conv_tile)
+    if args.workspace_mb:
+        m.set_option("max_workspace_mb", args.workspace_mb)
 
     def step():
         m.load_model(md.nodes, md.in_hwc, md.dtype, md.weights, md.biases)
