@@ -1,4 +1,5 @@
-// Layer-by-layer engine: CONV2D / DENSE as an implicit GEMM on MFMA (gfx950).
+// The general CONV2D kernel (any shape; here the bf16 stems with C_in = 3):
+// an implicit GEMM on MFMA with a scalar im2col gather.
 //
 // GEMM view of one node over a chunk: rows m = (slot, input, output pixel),
 // columns n = output channel, reduction k = (dy, dx, c_in) in the weight
@@ -37,6 +38,7 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(ConvArgs a) {
   const int64_t m_tile0 = (int64_t)blockIdx.x * BM;
   const int n_tile0 = (int)blockIdx.z * BN;
   const T* __restrict__ Wt = reinterpret_cast<const T*>(a.wtab[slot]);
+  const int ncol = a.cols ? a.ncols : a.Cout;
 
   // the A row this thread gathers (fixed for the block)
   const int m_local = tid & (BM - 1);
@@ -60,8 +62,16 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(ConvArgs a) {
       reinterpret_cast<const T*>(a.in.p) + row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems;
   // the B row (output channel) this thread loads
   const int n_ld = n_tile0 + (tid & 63);
-  const bool nvalid = n_ld < a.Cout;
-  const T* __restrict__ wrow = Wt + (int64_t)(nvalid ? n_ld : 0) * a.K;
+  const bool nvalid = n_ld < ncol;
+  const T* __restrict__ wrow = Wt;
+  if (nvalid) {
+    if (a.cols) {   // a gathered delta column: its own mutant's weight row
+      const DeltaCol cd = a.cols[n_ld];
+      wrow = reinterpret_cast<const T*>(a.wtab[a.slot0 + cd.slot - a.col_slot0]) + (int64_t)cd.c * a.K;
+    } else {
+      wrow = Wt + (int64_t)n_ld * a.K;
+    }
+  }
 
   v4f acc[2][2];
 #pragma unroll
@@ -132,10 +142,21 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(ConvArgs a) {
   for (int i = 0; i < 2; ++i) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const int n = n_tile0 + wn * 32 + j * 16 + (lane & 15);
+      const int nc = n_tile0 + wn * 32 + j * 16 + (lane & 15);
       const int64_t mb = m_tile0 + wm * 32 + i * 16 + (lane >> 4) * 4;
-      if (n >= a.Cout || mb >= Mslot) continue;
-      const float bv = bias[n];
+      if (nc >= ncol || mb >= Mslot) continue;
+      // output slot, channel and channel stride of this column
+      int os = slot, n = nc, ostride = a.Cout;
+      float bv;
+      if (a.cols) {
+        const DeltaCol cd = a.cols[nc];
+        os = a.slot0 + cd.slot - a.col_slot0;
+        bv = a.btab[os][cd.c];
+        n = a.delta_T > 0 ? cd.t : cd.c;
+        if (a.delta_T > 0) ostride = a.delta_T;
+      } else {
+        bv = bias[nc];
+      }
       float v[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -146,8 +167,8 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(ConvArgs a) {
         const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
         const int xo = (int)(mb / a.P);
         const int q = (int)(mb % a.P) >> 2;
-        const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xo, a.nx, a.x0);
-        store_out<T>(a.out, a.out_f32, ro * a.out_row + (int64_t)q * a.Cout + n, mx);
+        const int64_t ro = row_index(a.out_mode, (int64_t)os * a.nx + xo, a.nx, a.x0);
+        store_out<T>(a.out, a.out_f32, ro * a.out_row + (int64_t)q * ostride + n, mx);
       } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -155,8 +176,8 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(ConvArgs a) {
           if (mm >= Mslot) break;
           const int xo = (int)(mm / a.P);
           const int pp = (int)(mm % a.P);
-          const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xo, a.nx, a.x0);
-          store_out<T>(a.out, a.out_f32, ro * a.out_row + (int64_t)pp * a.Cout + n, v[e]);
+          const int64_t ro = row_index(a.out_mode, (int64_t)os * a.nx + xo, a.nx, a.x0);
+          store_out<T>(a.out, a.out_f32, ro * a.out_row + (int64_t)pp * ostride + n, v[e]);
         }
       }
     }
@@ -165,8 +186,11 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(ConvArgs a) {
 
 hipError_t launch_conv(const ConvArgs& a, int nslots, int dtype, hipStream_t s) {
   if (nslots <= 0 || a.nx <= 0) return hipSuccess;
+  if (a.cols && (a.in.mode != MODE_CACHE || a.add_mode || a.ncols <= 0)) return hipErrorInvalidValue;
+  if (a.cols) nslots = 1;
   const int64_t Mslot = (int64_t)a.nx * a.P;
-  dim3 grid((unsigned)((Mslot + 63) / 64), (unsigned)nslots, (unsigned)((a.Cout + 63) / 64));
+  const int ncol = a.cols ? a.ncols : a.Cout;
+  dim3 grid((unsigned)((Mslot + 63) / 64), (unsigned)nslots, (unsigned)((ncol + 63) / 64));
   if (dtype == 0)
     hipLaunchKernelGGL((conv_mfma_kernel<float, 64, 64>), grid, dim3(256), 0, s, a);
   else

@@ -327,7 +327,8 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
       a.P = a.pool ? 4 * a.Hp * a.Wp : a.Hc * a.Wc;
       a.tile = (int)ctx->conv_tile;
       if (ex.cols) {
-        if (fam != FAM_LDS && fam != FAM_BIG) return ctx->fail(MURE_E_INVALID, "internal: gathered delta on the im2col kernel");
+        if (fam != FAM_LDS && fam != FAM_BIG && fam != FAM_GEMM)
+          return ctx->fail(MURE_E_INVALID, "internal: gathered delta on a kernel without columns");
         a.cols = ex.cols; a.ncols = ex.ncols; a.col_slot0 = ex.col_slot0; a.delta_T = ex.delta_T;
         if (ex.delta_T > 0) a.out_row = (int64_t)n.H * n.W * ex.delta_T;
       }

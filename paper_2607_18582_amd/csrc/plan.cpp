@@ -297,13 +297,14 @@ std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>&
     gr.n_recompute = (int)gr.mutants.size();
     for (int m : kv.second) if (!p.mutants[m].recompute) gr.mutants.push_back(m);
     // delta at mmi: only the channels the fuzz / inverse / shuffle records
-    // changed are recomputed (VALU kernel per slot, or one gathered-column GEMM
-    // over the shared cached input for the MFMA families); the im2col fallback
-    // recomputes whole nodes
+    // changed are recomputed (per slot on the VALU and depthwise kernels, or
+    // one gathered-column GEMM over the shared cached input for the MFMA
+    // families); the sequence layers recompute whole nodes
     {
       const int fam = node_family(g, gr.mmi);
       gr.delta = !vanilla && gr.n_recompute > 0 &&
-                 (fam == FAM_VALU || fam == FAM_LDS || fam == FAM_DENSE || fam == FAM_BIG || fam == FAM_DW);
+                 (fam == FAM_VALU || fam == FAM_LDS || fam == FAM_DENSE || fam == FAM_BIG || fam == FAM_DW ||
+                  fam == FAM_GEMM);
     }
     // virtual mmi output: every consumer is an LDS convolution or a dense layer
     gr.virt = gr.mmi != g.out();
