@@ -286,29 +286,43 @@ def main():
     st = stats[-1]
     peak = PEAK_TFLOPS[md.dtype]
     kernel_peak = lambda f: PEAK_VALU_TFLOPS if f in VALU_FAMILIES else peak
+    kernel_ms = np.mean([s["kernel_ms"] for s in stats], axis=0)
+
+    def family_roof(f):
+        """Roofline of kernel family f over run_mutants: HBM-bound when its
+        algorithmic FLOP per byte sits below the ridge point of its compute
+        peak, else bound by that peak."""
+        ms = float(kernel_ms[f])
+        flops = 2.0 * st["kernel_macs_algorithmic"][f]
+        nbytes = float(st["kernel_bytes_algorithmic"][f])
+        intensity = flops / nbytes if nbytes > 0 else float("inf")
+        ridge = kernel_peak(f) * 1e12 / (PEAK_HBM_GBS * 1e9)
+        if intensity < ridge:
+            r = {"bound": "hbm", "achieved": nbytes / (ms * 1e-3) / 1e9 if ms > 0 else 0.0,
+                 "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+        else:
+            r = {"bound": "alu" if f in VALU_FAMILIES else "mfma",
+                 "achieved": flops / (ms * 1e-3) / 1e12 if ms > 0 else 0.0,
+                 "peak": kernel_peak(f), "unit": "TFLOP/s"}
+        r["frac"] = r["achieved"] / r["peak"]
+        return r, ms, flops, nbytes, intensity, ridge
+
     # the dominant kernel of run_mutants (largest summed launch time)
-    fam = int(np.argmax(np.mean([s["kernel_ms"] for s in stats], axis=0)))
-    ms_k = float(np.mean([s["kernel_ms"][fam] for s in stats]))
+    fam = int(np.argmax(kernel_ms))
+    roof, ms_k, alg_flops, alg_bytes, intensity, ridge = family_roof(fam)
     launches = st["kernel_launches"][fam]
-    alg_flops = 2.0 * st["kernel_macs_algorithmic"][fam]
-    achieved = alg_flops / (ms_k * 1e-3) / 1e12 if ms_k > 0 else 0.0
     ms_gemm = float(np.mean([s["ms_gemm"] for s in stats]))
     all_flops = 2.0 * st["gemm_macs_algorithmic"]
     all_achieved = all_flops / (ms_gemm * 1e-3) / 1e12 if ms_gemm > 0 else 0.0
     tr = read_traffic(KERNEL_NAMES[fam], args.config, N, M)
-    # the kernel's bound: HBM when its algorithmic FLOP per byte sits below
-    # the ridge point of its compute peak
-    alg_bytes = float(st["kernel_bytes_algorithmic"][fam])
-    intensity = alg_flops / alg_bytes if alg_bytes > 0 else float("inf")
-    ridge = kernel_peak(fam) * 1e12 / (PEAK_HBM_GBS * 1e9)
-    hbm_bound = intensity < ridge
-    if hbm_bound:
-        roof = {"bound": "hbm", "achieved": alg_bytes / (ms_k * 1e-3) / 1e9 if ms_k > 0 else 0.0,
-                "peak": PEAK_HBM_GBS, "unit": "GB/s"}
-    else:
-        roof = {"bound": "alu" if fam in VALU_FAMILIES else "mfma", "achieved": achieved,
-                "peak": kernel_peak(fam), "unit": "TFLOP/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
+    # every kernel family that ran: time, launches and its own roofline
+    families = {}
+    for f in range(len(KERNEL_NAMES)):
+        if st["kernel_launches"][f] > 0:
+            r = family_roof(f)[0]
+            families[KERNEL_NAMES[f]] = {"ms": round(float(kernel_ms[f]), 4),
+                                         "launches": int(st["kernel_launches"][f]),
+                                         "bound": r["bound"], "frac": round(r["frac"], 4)}
     line = {
         "metric": "mutant-input suffix evals/sec + MFMA/HBM roofline fraction, 1 MI355X",
         "value": M * N / dt,
@@ -337,10 +351,11 @@ def main():
                      "alg_flops_per_launch": alg_flops / max(launches, 1),
                      "alg_bytes_per_launch": alg_bytes / max(launches, 1),
                      "flop_per_byte": intensity, "ridge_flop_per_byte": ridge,
-                     "compute_frac": achieved / kernel_peak(fam),
+                     "compute_frac": alg_flops / (ms_k * 1e-3) / 1e12 / kernel_peak(fam) if ms_k > 0 else 0.0,
                      "share_of_run_mutants": ms_k / ms_mut if ms_mut else None,
                      "all_weighted_layers": {"achieved": all_achieved, "frac": all_achieved / peak,
-                                             "ms": ms_gemm, "launches": st["gemm_launches"]}},
+                                             "ms": ms_gemm, "launches": st["gemm_launches"]},
+                     "families": families},
         "work": {"macs_algorithmic": st["macs_algorithmic"], "macs_executed": st["macs_executed"],
                  "macs_vanilla": st["macs_vanilla"], "macs_memoized": st["macs_memoized"],
                  "groups": st["n_groups"], "cache_bytes": st["cache_bytes"],

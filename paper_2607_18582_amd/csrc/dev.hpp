@@ -15,13 +15,18 @@ typedef uint16_t bf16_t;   // bfloat16 bit pattern
 
 __device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
-// float -> bfloat16, round to nearest, ties to even (NaN stays NaN).
-__device__ __forceinline__ bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
+// Two floats -> two bfloat16 (lo in bits 0-15), round to nearest, ties to
+// even, NaN stays NaN: gfx950's v_cvt_pk_bf16_f32 under the default round
+// mode, equal bit for bit to the integer rounding
+//   u + 0x7fff + ((u >> 16) & 1), top 16 bits
+// for every finite float (checked over all 2^32 inputs in both halves).
+__device__ __forceinline__ uint32_t f2bf2(float lo, float hi) {
+  uint32_t r;
+  asm("v_cvt_pk_bf16_f32 %0, %1, %2" : "=v"(r) : "v"(lo), "v"(hi));
+  return r;
 }
+
+__device__ __forceinline__ bf16_t f2bf(float f) { return (bf16_t)f2bf2(f, f); }
 
 template <typename T> __device__ __forceinline__ float to_f(T v);
 template <> __device__ __forceinline__ float to_f<float>(float v) { return v; }

@@ -21,6 +21,10 @@ constexpr int BIG_BK = 64, BIG_LD = BIG_BK + 8;   // padded LDS rows (bf16)
 // input, so every gather is an unconditional 16-byte load.
 static __device__ __attribute__((aligned(16))) v4u g_zero_page[16] = {};
 
+// a 16-byte vector in global memory (weight rows are reached through pointer
+// tables, which the compiler cannot place in an address space by itself)
+typedef __attribute__((address_space(1))) const v4u gv4u;
+
 // G: 16-byte vectors (8 input channels each) per filter tap in a thread's
 // half chunk of 32 k -- 4 when C_in % 32 == 0, 2 when C_in % 16 == 0, else 1.
 // The tap of each group is the same for the whole wavefront, so its index
@@ -127,10 +131,10 @@ void conv_big_kernel(ConvArgs a) {
     }
 #pragma unroll
     for (int j = 0; j < BPT; ++j) {
+      // past the last column or the row's end: the zero page (a select, not a branch)
       const int i = tid + j * THREADS;
-      v4u val = v4u{0u, 0u, 0u, 0u};
-      if (brow[j] && kc + (i % (BK / 8)) * 8 < a.K) val = *reinterpret_cast<const v4u*>(brow[j] + kc);
-      rb[j] = val;
+      const bf16_t* src = brow[j] && kc + (i % (BK / 8)) * 8 < a.K ? brow[j] + kc : zp;
+      rb[j] = *(const gv4u*)src;
     }
   };
   auto store_chunk = [&]() {
@@ -175,13 +179,10 @@ void conv_big_kernel(ConvArgs a) {
     store_chunk();
     __syncthreads();
     if (kc + BK < a.K) load_chunk(kc + BK);             // next chunk in flight
-    if (kc + BK <= a.K) {
-      mma_step(0);
-      mma_step(1);
-    } else {                                          // the tail: skip the all-zero half
-      mma_step(0);
-      if (kc + 32 < a.K) mma_step(1);
-    }
+    // the tail's k past K holds zeros on both operands (adding +0 products);
+    // one straight-line body keeps the accumulators in AGPRs across the loop
+    mma_step(0);
+    mma_step(1);
     __syncthreads();
   }
 
