@@ -38,7 +38,8 @@
 extern "C" {
 #endif
 
-#define MURE_VERSION 2
+#define MURE_VERSION 3
+#define MURE_N_KERNELS 9   /* kernel families in mure_stats */
 
 typedef struct mure_ctx mure_ctx;
 
@@ -170,17 +171,18 @@ typedef struct {
   int64_t gemm_launches;
   double ms_gemm;
   int64_t gemm_macs_algorithmic, gemm_macs_executed;
-  /* The same, split by kernel: [0] dense GEMM, [1] vector-ALU convolution
-   * (few output channels), [2] LDS-resident convolution, [3] im2col implicit
-   * GEMM with scalar gathers, [4] tiled bf16 implicit GEMM, [5] depthwise
-   * convolution, [6] embedding lookup, [7] LSTM recursion. */
-  int64_t kernel_launches[8];
-  double kernel_ms[8];
-  int64_t kernel_macs_algorithmic[8];
+  /* The same, split by kernel (MURE_N_KERNELS entries): [0] dense GEMM,
+   * [1] vector-ALU convolution (few output channels), [2] LDS-resident
+   * convolution, [3] im2col implicit GEMM with scalar gathers, [4] tiled bf16
+   * implicit GEMM, [5] depthwise convolution, [6] embedding lookup, [7] LSTM
+   * recursion, [8] bf16 3x3 convolution over LDS halo tiles. */
+  int64_t kernel_launches[MURE_N_KERNELS];
+  double kernel_ms[MURE_N_KERNELS];
+  int64_t kernel_macs_algorithmic[MURE_N_KERNELS];
   /* Algorithmic HBM bytes of those launches: every input row read once (a
    * prefix-cache tensor once for all mutants), every output element written
    * once, every mutant's weights read once. */
-  double kernel_bytes_algorithmic[8];
+  double kernel_bytes_algorithmic[MURE_N_KERNELS];
 } mure_stats;
 
 /* Version of this interface (MURE_VERSION). */

@@ -251,6 +251,7 @@ struct DevRecord { int op, neuron, partner, pad; int64_t noise_off, scratch_off;
 hipError_t launch_conv(const ConvArgs& a, int nslots, int dtype, hipStream_t s);
 hipError_t launch_conv_lds(const ConvArgs& a, int nslots, hipStream_t s);
 hipError_t launch_conv_big(const ConvArgs& a, int nslots, hipStream_t s);
+hipError_t launch_conv_halo(const ConvArgs& a, int nslots, hipStream_t s);
 hipError_t launch_dense(const DenseArgs& a, int nslots, int dtype, hipStream_t s);
 hipError_t launch_valu(const ValuArgs& a, int dtype, hipStream_t s);
 hipError_t launch_dw(const DwArgs& a, int dtype, hipStream_t s);

@@ -182,12 +182,14 @@ int64_t esize_of(const Graph& g, int v) { return (v == g.out() || g.dtype == DT_
 // epilogue adds the shortcut.  -1 if v is not such a convolution.
 int fused_add_of(const Graph& g, int v) {
   const Node& n = g.nodes[v];
-  if (n.kind != K_CONV || n.maxpool || node_family(g, v) != FAM_BIG) return -1;
+  const int fam = node_family(g, v);
+  if (n.kind != K_CONV || n.maxpool || (fam != FAM_BIG && fam != FAM_HALO)) return -1;
   int reader = -1, count = 0;
   for (int j = v + 1; j < (int)g.nodes.size(); ++j)
     for (int k = 0; k < g.nodes[j].n_in; ++k)
       if (g.nodes[j].in[k] == v) { reader = j; ++count; }
   if (count != 1 || g.nodes[reader].kind != K_ADD || g.nodes[reader].in[0] != v) return -1;
+  if (fam == FAM_HALO && reader == g.out()) return -1;   // the halo kernel stores bf16 only
   return reader;
 }
 
@@ -327,7 +329,7 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
       a.P = a.pool ? 4 * a.Hp * a.Wp : a.Hc * a.Wc;
       a.tile = (int)ctx->conv_tile;
       if (ex.cols) {
-        if (fam != FAM_LDS && fam != FAM_BIG && fam != FAM_GEMM)
+        if (fam != FAM_LDS && fam != FAM_BIG && fam != FAM_GEMM && fam != FAM_HALO)
           return ctx->fail(MURE_E_INVALID, "internal: gathered delta on a kernel without columns");
         a.cols = ex.cols; a.ncols = ex.ncols; a.col_slot0 = ex.col_slot0; a.delta_T = ex.delta_T;
         if (ex.delta_T > 0) a.out_row = (int64_t)n.H * n.W * ex.delta_T;
@@ -347,6 +349,7 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
       }
       e = fam == FAM_LDS ? launch_conv_lds(a, nslots, ctx->stream)
         : fam == FAM_BIG ? launch_conv_big(a, nslots, ctx->stream)
+        : fam == FAM_HALO ? launch_conv_halo(a, nslots, ctx->stream)
         : launch_conv(a, nslots, g.dtype, ctx->stream);
     }
     if (timed && e == hipSuccess) {

@@ -175,6 +175,9 @@ int node_family(const Graph& g, int v) {
   if (g.dtype == DT_F32 && n.c_out <= 64 &&
       conv_lds_bytes(n.inH, n.inW, n.inC, n.pad, P, n.c_out, n.fan_in) <= 48 * 1024)
     return FAM_LDS;
+  if (g.dtype == DT_BF16 && v != g.out() && n.c_out % 8 == 0 &&
+      conv_halo_fits(n.inH, n.inW, n.inC, n.kh, n.kw, n.stride, n.pad))
+    return FAM_HALO;
   if (g.dtype == DT_BF16 && n.inC % 8 == 0 && n.kh <= 15 && n.kw <= 15 && n.fan_in <= 8192 &&
       P % 4 == 0 && ((int64_t)n.kh * n.inW + n.kw) * n.inC < (1 << 24))
     return FAM_BIG;
@@ -304,7 +307,7 @@ std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>&
       const int fam = node_family(g, gr.mmi);
       gr.delta = !vanilla && gr.n_recompute > 0 &&
                  (fam == FAM_VALU || fam == FAM_LDS || fam == FAM_DENSE || fam == FAM_BIG || fam == FAM_DW ||
-                  fam == FAM_GEMM);
+                  fam == FAM_GEMM || fam == FAM_HALO);
     }
     // virtual mmi output: every consumer is an LDS convolution or a dense layer
     gr.virt = gr.mmi != g.out();

@@ -70,9 +70,21 @@ enum Family {
   FAM_BIG = 4,     // bf16 tiled implicit GEMM with 16-byte gathers (C_in % 8 == 0)
   FAM_DW = 5,      // depthwise convolution (per-channel taps on the vector ALU)
   FAM_EMBED = 6,   // embedding lookup (a gather)
-  FAM_LSTM = 7     // LSTM recursion: per step one MFMA GEMM over [x_t, h, 1], gates on the VALU
+  FAM_LSTM = 7,    // LSTM recursion: per step one MFMA GEMM over [x_t, h, 1], gates on the VALU
+  FAM_HALO = 8     // bf16 3x3 stride-1 conv, operands from LDS halo and weight tiles per 16-channel chunk
 };
-constexpr int N_FAMILIES = 8;
+constexpr int N_FAMILIES = 9;
+// Halo convolution: 256-pixel bands of TR = 256 / W image rows, halo pixels
+// per band at most HALO_MAXPX (the bands never straddle two images).
+constexpr int HALO_MAXPX = 400;
+inline bool conv_halo_fits(int H, int W, int C, int kh, int kw, int stride, int pad) {
+  if (kh != 3 || kw != 3 || stride != 1 || pad != 1 || C % 16 || C <= 0 || H % 2) return false;
+  if (W != 8 && W != 16 && W != 32 && W != 64) return false;
+  const int TR = 256 / W;
+  if (H % TR && TR % H) return false;
+  const int RI = H < TR ? H : TR, IMGS = TR / RI;
+  return IMGS * (RI + 2) * (W + 2) <= HALO_MAXPX && (int64_t)9 * C <= (1 << 20);
+}
 // LSTM kernel: units a multiple of 16, at most 64; LDS for the weights
 // (k-major, row stride 4H + 16) and a 64-row step tile
 constexpr int lstm_kpad(int d, int h) { return (d + h + 1 + 3) / 4 * 4; }
