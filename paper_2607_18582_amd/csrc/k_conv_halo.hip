@@ -2,9 +2,10 @@
 // width 8, 16, 32 or 64) as an implicit GEMM on MFMA whose operands both come
 // from LDS (v_mfma_f32_16x16x32_bf16).
 //
-// Block tile: 256 output pixels x BN output channels, four waves of 64 rows.
-// The pixels are TR = 256 / W consecutive image rows -- a band of one image,
-// or 256 / (H W) whole images -- so a tile never mixes two images' borders.
+// Block tile: 512 output pixels x BN output channels, eight waves of 64 rows
+// (one block per CU: the LDS stages below take most of it).  The pixels are
+// TR = 512 / W consecutive image rows -- a band of one image, or 512 / (H W)
+// whole images -- so a tile never mixes two images' borders.
 // The input channels go in chunks of 16.  Per chunk the block stages in LDS
 // (a) the band's input rows plus a one-pixel border (the halo, zero outside
 // the image): every input element crosses the memory pipeline once per block
@@ -33,16 +34,16 @@ typedef __attribute__((address_space(1))) const v4u gv4u;
 static __device__ __attribute__((aligned(16))) v4u g_halo_zero[4] = {};
 
 template <int W, int BN>
-__global__ __launch_bounds__(256, 2)                   // two blocks per CU: at most 256 registers
+__global__ __launch_bounds__(512)
 void conv_halo_kernel(ConvArgs a) {
-  constexpr int BM = 256, TR = BM / W, W2 = W + 2;
+  constexpr int NT = 512, BM = 512, TR = BM / W, W2 = W + 2;
   constexpr int TM = 4, TN = BN / 16;                  // a wave: 64 rows x BN columns
   constexpr int B_ELEMS = 5 * BN * 32;                 // weight part of a stage: [pair][column][32]
   constexpr int STAGE = HALO_ELEMS + B_ELEMS;
   constexpr int OLD = BN + 8;                          // staged output row (bf16)
   constexpr int LDS_ELEMS = 2 * STAGE > BM * OLD ? 2 * STAGE : BM * OLD;
-  constexpr int HV = (HALO_MAXPX * 2 + 255) / 256;     // halo vectors per thread and chunk
-  constexpr int BV = (5 * BN * 4 + 255) / 256;         // weight vectors per thread and chunk
+  constexpr int HV = (HALO_MAXPX * 2 + NT - 1) / NT;   // halo vectors per thread and chunk
+  constexpr int BV = (5 * BN * 4 + NT - 1) / NT;       // weight vectors per thread and chunk
   __shared__ __attribute__((aligned(16))) bf16_t smem[LDS_ELEMS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -58,7 +59,7 @@ void conv_halo_kernel(ConvArgs a) {
   const int npx = IMGS * (RI + 2) * W2;                // halo pixels (<= HALO_MAXPX, checked by the launcher)
   const bf16_t* const zp = reinterpret_cast<const bf16_t*>(g_halo_zero);
 
-  // halo vectors of this thread: vector v = tid + 256 j is pixel v / 2,
+  // halo vectors of this thread: vector v = tid + NT j is pixel v / 2,
   // channels (v % 2) * 8 .. + 8 of the chunk, at element offset hoff[j] from
   // the band's first input row (consecutive inputs are consecutive rows in
   // both tensor modes); -1 reads zeros, -2 is past the halo (not stored)
@@ -68,7 +69,7 @@ void conv_halo_kernel(ConvArgs a) {
   int hoff[HV];
 #pragma unroll
   for (int j = 0; j < HV; ++j) {
-    const int v = tid + 256 * j;
+    const int v = tid + NT * j;
     const int px = v >> 1, h = v & 1;
     hoff[j] = -2;
     if (px < npx) {
@@ -80,7 +81,7 @@ void conv_halo_kernel(ConvArgs a) {
         hoff[j] = (int)(im * a.in.row_elems) + (y * W + x) * a.C + h * 8;
     }
   }
-  // weight vectors of this thread: vector v = tid + 256 j is tap pair p,
+  // weight vectors of this thread: vector v = tid + NT j is tap pair p,
   // column n, quarter q (8 of the pair's 32 k: tap 2p + q / 2, channels
   // (q % 2) * 8 ..); bsrc is its source at chunk 0 (nullptr: zeros), bdst its
   // LDS slot, the quarter rotated by (n / 4) % 4 so that the 16 lanes reading
@@ -89,7 +90,7 @@ void conv_halo_kernel(ConvArgs a) {
   int bdst[BV];
 #pragma unroll
   for (int j = 0; j < BV; ++j) {
-    const int v = tid + 256 * j;
+    const int v = tid + NT * j;
     const int p = v / (BN * 4), rem = v % (BN * 4);
     const int n = rem >> 2, q = rem & 3;
     const int tap = 2 * p + (q >> 1);
@@ -122,7 +123,7 @@ void conv_halo_kernel(ConvArgs a) {
     bf16_t* st = smem + buf * STAGE;
 #pragma unroll
     for (int j = 0; j < HV; ++j) {
-      const int v = tid + 256 * j;
+      const int v = tid + NT * j;
       if (hoff[j] != -2) *reinterpret_cast<v4u*>(&st[(v >> 1) * HALO_PS + (v & 1) * 8]) = r.h[j];
     }
 #pragma unroll
@@ -238,7 +239,7 @@ void conv_halo_kernel(ConvArgs a) {
   if (a.cols) {
     // gathered columns: each column has its own slot and channel
     const int PX = a.pool ? BM / 4 : BM;
-    for (int idx = tid; idx < PX * BN; idx += 256) {
+    for (int idx = tid; idx < PX * BN; idx += NT) {
       const int nl = idx / PX, p = idx % PX;
       const int nc = n0 + nl;
       if (nc >= ncol) continue;
@@ -269,7 +270,7 @@ void conv_halo_kernel(ConvArgs a) {
   }
   constexpr int VPR = BN / 8;                          // 16-byte vectors per staged row
   if (a.pool) {
-    for (int idx = tid; idx < (BM / 4) * VPR; idx += 256) {
+    for (int idx = tid; idx < (BM / 4) * VPR; idx += NT) {
       const int p = idx / VPR, vc = idx % VPR;
       const int n = n0 + vc * 8;
       if (n >= a.Cout) continue;
@@ -302,7 +303,7 @@ void conv_halo_kernel(ConvArgs a) {
     }
     return;
   }
-  for (int idx = tid; idx < BM * VPR; idx += 256) {
+  for (int idx = tid; idx < BM * VPR; idx += NT) {
     const int m = idx / VPR, vc = idx % VPR;
     const int n = n0 + vc * 8;
     if (n >= a.Cout) continue;
@@ -345,9 +346,9 @@ int conv_halo_bn(int cout) { return cout <= 16 ? 16 : cout <= 32 ? 32 : 64; }
 template <int W>
 static hipError_t launch_halo_w(const ConvArgs& a, dim3 grid, int bn, hipStream_t s) {
   switch (bn) {
-    case 16: hipLaunchKernelGGL((conv_halo_kernel<W, 16>), grid, dim3(256), 0, s, a); break;
-    case 32: hipLaunchKernelGGL((conv_halo_kernel<W, 32>), grid, dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL((conv_halo_kernel<W, 64>), grid, dim3(256), 0, s, a); break;
+    case 16: hipLaunchKernelGGL((conv_halo_kernel<W, 16>), grid, dim3(512), 0, s, a); break;
+    case 32: hipLaunchKernelGGL((conv_halo_kernel<W, 32>), grid, dim3(512), 0, s, a); break;
+    default: hipLaunchKernelGGL((conv_halo_kernel<W, 64>), grid, dim3(512), 0, s, a); break;
   }
   return hipGetLastError();
 }
@@ -360,7 +361,7 @@ hipError_t launch_conv_halo(const ConvArgs& a0, int nslots, hipStream_t s) {
   if (a0.cols && (a0.in.mode != MODE_CACHE || a0.add_mode || a0.ncols <= 0)) return hipErrorInvalidValue;
   ConvArgs a = a0;
   if (a.cols) nslots = 1;
-  const int TR = 256 / a.W;
+  const int TR = 512 / a.W;
   const int ncol = a.cols ? a.ncols : a.Cout;
   const int bn = conv_halo_bn(ncol);
   const int64_t bands = ((int64_t)a.nx * a.H + TR - 1) / TR;

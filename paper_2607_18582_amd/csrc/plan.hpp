@@ -74,13 +74,13 @@ enum Family {
   FAM_HALO = 8     // bf16 3x3 stride-1 conv, operands from LDS halo and weight tiles per 16-channel chunk
 };
 constexpr int N_FAMILIES = 9;
-// Halo convolution: 256-pixel bands of TR = 256 / W image rows, halo pixels
+// Halo convolution: 512-pixel bands of TR = 512 / W image rows, halo pixels
 // per band at most HALO_MAXPX (the bands never straddle two images).
-constexpr int HALO_MAXPX = 400;
+constexpr int HALO_MAXPX = 800;
 inline bool conv_halo_fits(int H, int W, int C, int kh, int kw, int stride, int pad) {
   if (kh != 3 || kw != 3 || stride != 1 || pad != 1 || C % 16 || C <= 0 || H % 2) return false;
   if (W != 8 && W != 16 && W != 32 && W != 64) return false;
-  const int TR = 256 / W;
+  const int TR = 512 / W;
   if (H % TR && TR % H) return false;
   const int RI = H < TR ? H : TR, IMGS = TR / RI;
   return IMGS * (RI + 2) * (W + 2) <= HALO_MAXPX && (int64_t)9 * C <= (1 << 20);
