@@ -21,17 +21,22 @@ constexpr int DW_MAXC = 2048;
 // zeros that taps outside the image read instead of the input
 static __device__ __attribute__((aligned(16))) v4u g_dw_zero[1] = {};
 
-// KH, KW: the filter size when known at compile time (3 x 3), else 0.
+// KH, KW: the filter size when known at compile time (3 x 3), else 0.  The
+// block's LDS (dynamic, sized to the node) holds the slot's weights [tap][C]
+// and bias; each thread takes work items it and it + 256 of every 512 and
+// requests both items' tap vectors before their arithmetic.
 template <typename T, int KH, int KW>
 __global__ __launch_bounds__(256) void dw_full_kernel(DwArgs a, int rows, DivU32 dcv, DivU32 dpix,
                                                       DivU32 dwo) {
   constexpr int VEC = 16 / sizeof(T);
-  __shared__ __attribute__((aligned(16))) float wl[DW_MAXW];   // [tap][C]
-  __shared__ __attribute__((aligned(16))) float bl[DW_MAXC];
+  constexpr int NT = KH * KW > 0 ? KH * KW : 1, KWC = KW > 0 ? KW : 1;
+  extern __shared__ __attribute__((aligned(16))) float dw_lds[];
   const int tid = threadIdx.x;
   const int sl = a.slot0 + (int)blockIdx.y;
   const int kh = KH ? KH : a.kh, kw = KW ? KW : a.kw;
   const int taps = kh * kw;
+  float* const wl = dw_lds;                           // [tap][C]
+  float* const bl = dw_lds + a.C * taps;              // [C]
   const T* __restrict__ Wt = reinterpret_cast<const T*>(a.wtab[sl]);
   for (int e = tid; e < a.C * taps; e += 256) {
     const int c = e / taps, tp = e - c * taps;
@@ -43,38 +48,73 @@ __global__ __launch_bounds__(256) void dw_full_kernel(DwArgs a, int rows, DivU32
   const int xi0 = (int)blockIdx.x * rows;
   const int nr = min(rows, a.nx - xi0);
   const int per = a.Ho * a.Wo * (a.C / VEC);          // vectors per output row
+  const int total = nr * per;
   const T* __restrict__ X = reinterpret_cast<const T*>(a.in.p);
-  for (int it = tid; it < nr * per; it += 256) {
-    int ii, rem, pix, cv, oy, ox;
+
+  // one work item: output vector (input ii, pixel, channel vector cv)
+  struct Item {
+    int cv, pix;
+    int64_t r;
+    v4u xv[NT];
+  };
+  auto request = [&](Item& w, int it) {
+    int ii, rem, oy, ox;
     divmodu(dpix, (uint32_t)it, ii, rem);             // rem = pixel * (C / VEC) + cv
-    divmodu(dcv, (uint32_t)rem, pix, cv);
-    divmodu(dwo, (uint32_t)pix, oy, ox);
-    const int64_t r = (int64_t)sl * a.nx + xi0 + ii;
-    const T* xr = X + row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems + cv * VEC;
+    divmodu(dcv, (uint32_t)rem, w.pix, w.cv);
+    divmodu(dwo, (uint32_t)w.pix, oy, ox);
+    w.r = (int64_t)sl * a.nx + xi0 + ii;
+    const T* xr = X + row_index(a.in.mode, w.r, a.nx, a.x0) * a.in.row_elems + w.cv * VEC;
     const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
+#pragma unroll
+    for (int tp = 0; tp < NT; ++tp) {
+      const int iy = iy0 + tp / KWC, ix = ix0 + tp % KWC;
+      const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+      w.xv[tp] = *(ok ? reinterpret_cast<const v4u*>(xr + ((int64_t)iy * a.W + ix) * a.C) : zp);
+    }
+  };
+  auto finish = [&](const Item& w) {
+    // the chains in (dy, dx) order from 0, then the bias
     float acc[VEC];
 #pragma unroll
     for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
-    // every tap's 16-byte input vector first (zeros outside the image), then
-    // the chains in (dy, dx) order
-    constexpr int NT = KH * KW > 0 ? KH * KW : 1;
-    if constexpr (KH > 0) {
-      v4u xv[NT];
 #pragma unroll
-      for (int tp = 0; tp < NT; ++tp) {
-        const int iy = iy0 + tp / KW, ix = ix0 + tp % KW;
-        const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
-        xv[tp] = *(ok ? reinterpret_cast<const v4u*>(xr + ((int64_t)iy * a.W + ix) * a.C) : zp);
-      }
+    for (int tp = 0; tp < NT; ++tp) {
+      T x8[VEC];
+      __builtin_memcpy(x8, &w.xv[tp], 16);
+      const float* wt = wl + tp * a.C + w.cv * VEC;
 #pragma unroll
-      for (int tp = 0; tp < NT; ++tp) {
-        T x8[VEC];
-        __builtin_memcpy(x8, &xv[tp], 16);
-        const float* wt = wl + tp * a.C + cv * VEC;
+      for (int j = 0; j < VEC; ++j) acc[j] = fmaf(to_f<T>(x8[j]), wt[j], acc[j]);
+    }
+    T ov[VEC];
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) acc[j] = fmaf(to_f<T>(x8[j]), wt[j], acc[j]);
-      }
-    } else {
+    for (int j = 0; j < VEC; ++j) ov[j] = from_f<T>(act(acc[j] + bl[w.cv * VEC + j], a.relu));
+    v4u o;
+    __builtin_memcpy(&o, ov, 16);
+    const int64_t ro = row_index(a.out_mode, w.r, a.nx, a.x0);
+    *reinterpret_cast<v4u*>(reinterpret_cast<T*>(a.out) + ro * a.out_row + (int64_t)w.pix * a.C + w.cv * VEC) = o;
+  };
+
+  if constexpr (KH > 0) {
+    for (int base = 0; base < total; base += 512) {
+      const int i0 = base + tid, i1 = base + 256 + tid;
+      Item w0, w1;
+      if (i0 < total) request(w0, i0);
+      if (i1 < total) request(w1, i1);
+      if (i0 < total) finish(w0);
+      if (i1 < total) finish(w1);
+    }
+  } else {
+    for (int it = tid; it < total; it += 256) {
+      int ii, rem, pix, cv, oy, ox;
+      divmodu(dpix, (uint32_t)it, ii, rem);
+      divmodu(dcv, (uint32_t)rem, pix, cv);
+      divmodu(dwo, (uint32_t)pix, oy, ox);
+      const int64_t r = (int64_t)sl * a.nx + xi0 + ii;
+      const T* xr = X + row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems + cv * VEC;
+      const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
+      float acc[VEC];
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
       for (int tp = 0; tp < taps; ++tp) {
         const int iy = iy0 + tp / kw, ix = ix0 + tp % kw;
         const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
@@ -85,14 +125,14 @@ __global__ __launch_bounds__(256) void dw_full_kernel(DwArgs a, int rows, DivU32
 #pragma unroll
         for (int j = 0; j < VEC; ++j) acc[j] = fmaf(to_f<T>(x8[j]), wt[j], acc[j]);
       }
-    }
-    T ov[VEC];
+      T ov[VEC];
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) ov[j] = from_f<T>(act(acc[j] + bl[cv * VEC + j], a.relu));
-    v4u o;
-    __builtin_memcpy(&o, ov, 16);
-    const int64_t ro = row_index(a.out_mode, r, a.nx, a.x0);
-    *reinterpret_cast<v4u*>(reinterpret_cast<T*>(a.out) + ro * a.out_row + (int64_t)pix * a.C + cv * VEC) = o;
+      for (int j = 0; j < VEC; ++j) ov[j] = from_f<T>(act(acc[j] + bl[cv * VEC + j], a.relu));
+      v4u o;
+      __builtin_memcpy(&o, ov, 16);
+      const int64_t ro = row_index(a.out_mode, r, a.nx, a.x0);
+      *reinterpret_cast<v4u*>(reinterpret_cast<T*>(a.out) + ro * a.out_row + (int64_t)pix * a.C + cv * VEC) = o;
+    }
   }
 }
 
@@ -160,12 +200,13 @@ hipError_t launch_dw(const DwArgs& a, int dtype, hipStream_t s) {
     const DivU32 dcv = make_divu32((uint32_t)(a.C / vec));
     const DivU32 dpix = make_divu32((uint32_t)(pix * (a.C / vec)));
     const bool k3 = a.kh == 3 && a.kw == 3;
+    const size_t lds = (size_t)a.C * (a.kh * a.kw + 1) * sizeof(float);
     if (dtype == 0) {
-      if (k3) hipLaunchKernelGGL((dw_full_kernel<float, 3, 3>), grid, dim3(256), 0, s, a, rows, dcv, dpix, dwo);
-      else hipLaunchKernelGGL((dw_full_kernel<float, 0, 0>), grid, dim3(256), 0, s, a, rows, dcv, dpix, dwo);
+      if (k3) hipLaunchKernelGGL((dw_full_kernel<float, 3, 3>), grid, dim3(256), lds, s, a, rows, dcv, dpix, dwo);
+      else hipLaunchKernelGGL((dw_full_kernel<float, 0, 0>), grid, dim3(256), lds, s, a, rows, dcv, dpix, dwo);
     } else {
-      if (k3) hipLaunchKernelGGL((dw_full_kernel<bf16_t, 3, 3>), grid, dim3(256), 0, s, a, rows, dcv, dpix, dwo);
-      else hipLaunchKernelGGL((dw_full_kernel<bf16_t, 0, 0>), grid, dim3(256), 0, s, a, rows, dcv, dpix, dwo);
+      if (k3) hipLaunchKernelGGL((dw_full_kernel<bf16_t, 3, 3>), grid, dim3(256), lds, s, a, rows, dcv, dpix, dwo);
+      else hipLaunchKernelGGL((dw_full_kernel<bf16_t, 0, 0>), grid, dim3(256), lds, s, a, rows, dcv, dpix, dwo);
     }
   } else {
     // the row split assumes every channel (the largest list)
