@@ -266,8 +266,10 @@ mure_status mure_get_stats(const mure_ctx* ctx, mure_stats* out);
 /* Tuning and testing knobs (name, integer value).  Known names:
  *   "max_workspace_mb"  cap on per-chunk activation buffers (default 16384)
  *   "chunk_inputs"      inputs per chunk, multiple of 64 (0 = automatic)
- *   "fused_paths"       1 (default) use fused kernels where a graph allows, 0
- *                       force the layer-by-layer engine
+ *   "fused_paths"       1 (default) fuse a residual block's ADD into its second
+ *                       convolution and the kill into the output layer where
+ *                       the graph allows; 0 run them as kernels of their own
+ *                       (the same results, bit for bit)
  *   "vanilla"           1: no memoization -- every mutant runs from the first
  *                       layer after the input (exhaustive mutation testing, the
  *                       baseline the paper compares against); takes effect at

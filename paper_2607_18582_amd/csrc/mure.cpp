@@ -800,7 +800,7 @@ mure_status mure_run_original(mure_ctx* ctx, const void* inputs_dev, int64_t n_i
   external.insert(L);
   std::map<int, int> fused;                            // conv_b -> ADD run as one launch
   for (int v = 1; v <= L; ++v) {
-    const int fa = fused_add_of(g, v);
+    const int fa = ctx->fused ? fused_add_of(g, v) : -1;
     if (fa >= 0 && !cached.count(v)) fused[v] = fa;
   }
   Placement pl = place_buffers(g, nodes, external, fused);
@@ -890,7 +890,7 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
   for (int v = mmi; v <= L; ++v) nodes.push_back(v);
   std::map<int, int> fused_adds;                       // conv_b -> ADD run as one launch
   for (int v = mmi + 1; v <= L; ++v) {
-    const int fa = fused_add_of(g, v);
+    const int fa = ctx->fused ? fused_add_of(g, v) : -1;
     if (fa >= 0) fused_adds[v] = fa;
   }
   Placement pl = place_buffers(g, nodes, {}, fused_adds);
@@ -982,7 +982,7 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
           // the kill fuses into the output layer only when every slot of the
           // chunk is recomputed here (patched slots need the kill kernel, which
           // reads the logits buffer)
-          if (mmi == L && pa >= cs1) { ex.kill = &ka; ex.kill_fused = &fused; }
+          if (mmi == L && pa >= cs1 && ctx->fused) { ex.kill = &ka; ex.kill_fused = &fused; }
           if (launch_slots > 0) {
             mure_status st = exec_node(ctx, mmi, ins, out, MODE_BUF, tabs + gt.w.at(mmi) + cs0,
                                        reinterpret_cast<const float* const*>(tabs + gt.b.at(mmi) + cs0),
@@ -1024,7 +1024,7 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
         const void* const* wt = nd.weighted() ? tabs + gt.w.at(v) + cs0 : nullptr;
         const float* const* bt = nd.weighted() ? reinterpret_cast<const float* const*>(tabs + gt.b.at(v) + cs0) : nullptr;
         Extra ex;
-        if (v == L) { ex.kill = &ka; ex.kill_fused = &fused; }
+        if (v == L && ctx->fused) { ex.kill = &ka; ex.kill_fused = &fused; }
         if (gr.virt && nd.n_in == 1 && nd.in[0] == mmi) {
           // the consumer of mmi: delta groups read every slot virtually; in
           // whole-node groups the recomputed slots read their own output rows

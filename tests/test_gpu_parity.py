@@ -199,3 +199,15 @@ def test_largest_class_count():
     _parity(wl)
     labels = np.random.default_rng(4).integers(0, 512, size=200).astype(np.int32)
     _parity(wl, labels=labels)
+
+
+@pytest.mark.parametrize("cfg", ["lenet5", "resnet20"])
+def test_fused_paths_equal_separate_kernels(cfg):
+    """The ADD fused into a residual block's second convolution and the kill
+    fused into the output layer give exactly the separate kernels' results."""
+    wl = W.make_workload(cfg, n_inputs=130, n_mutants=30, ops=(W.GF, W.NEB, W.NAI, W.NS, W.WS))
+    m1, w1, k1, s1 = run_gpu(wl)
+    m2, w2, k2, s2 = run_gpu(wl, fused_paths=0)
+    assert np.array_equal(w1, w2) and np.array_equal(k1, k2) and s1 == s2
+    for mid in sample_mutants(m1, wl):
+        assert np.array_equal(m1.get_logits(mid).cpu().numpy(), m2.get_logits(mid).cpu().numpy()), mid
