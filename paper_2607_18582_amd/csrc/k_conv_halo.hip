@@ -48,13 +48,19 @@ void conv_halo_kernel(ConvArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int slot = a.slot0 + (int)blockIdx.y;
-  const int n0 = (int)blockIdx.z * BN;
+  // XCD-aware order: consecutive blocks go round-robin to the 8 XCDs, so block
+  // b runs on XCD b % 8; the column blocks of one band take consecutive turns
+  // on the same XCD and share its L2 copy of the band's input
+  const int bx = (int)blockIdx.x, xcd = bx & 7, turn = bx >> 3;
+  const int band = (turn / a.zblocks) * 8 + xcd;
+  if (band >= a.bands) return;                           // padding of the order (whole block)
+  const int n0 = (turn % a.zblocks) * BN;
   const int ncol = a.cols ? a.ncols : a.Cout;
   // the band: image rows [r0, r0 + TR) of the flattened (input, row) axis;
   // RI rows of each of IMGS images (RI = H when whole images are packed)
   const int RI = a.H < TR ? a.H : TR;
   const int IMGS = TR / RI;
-  const int64_t r0 = (int64_t)blockIdx.x * TR;
+  const int64_t r0 = (int64_t)band * TR;
   const int xi0 = (int)(r0 / a.H), y0 = (int)(r0 % a.H);
   const int npx = IMGS * (RI + 2) * W2;                // halo pixels (<= HALO_MAXPX, checked by the launcher)
   const bf16_t* const zp = reinterpret_cast<const bf16_t*>(g_halo_zero);
@@ -365,8 +371,11 @@ hipError_t launch_conv_halo(const ConvArgs& a0, int nslots, hipStream_t s) {
   const int ncol = a.cols ? a.ncols : a.Cout;
   const int bn = conv_halo_bn(ncol);
   const int64_t bands = ((int64_t)a.nx * a.H + TR - 1) / TR;
-  if (bands >= (1 << 30)) return hipErrorInvalidValue;
-  dim3 grid((unsigned)bands, (unsigned)nslots, (unsigned)((ncol + bn - 1) / bn));
+  const int zb = (ncol + bn - 1) / bn;
+  if ((bands + 7) / 8 * 8 * zb >= (1 << 30)) return hipErrorInvalidValue;
+  a.bands = (int)bands;
+  a.zblocks = zb;
+  dim3 grid((unsigned)((bands + 7) / 8 * 8 * zb), (unsigned)nslots, 1);
   switch (a.W) {
     case 8: return launch_halo_w<8>(a, grid, bn, s);
     case 16: return launch_halo_w<16>(a, grid, bn, s);

@@ -94,8 +94,10 @@ struct ConvArgs {
   // channels per slot; the input must be slot independent (prefix cache)
   const DeltaCol* cols = nullptr;
   int ncols = 0, delta_T = 0, col_slot0 = 0;
-  // filled by the launchers: dividers by P, P/4, Wp, Wc, H*W, C and kw
+  // filled by the launchers: dividers by P, P/4, Wp, Wc, H*W, C and kw; the
+  // halo kernel's band count and column blocks per band (XCD-aware order)
   DivU32 dP, dPq, dWp, dWc, dHW, dC, dKW;
+  int bands = 0, zblocks = 1;
 };
 
 // DENSE on MFMA: out[r][n] = sum_k in[r][k] * W[n][k] + b[n] (k in increasing
