@@ -276,6 +276,7 @@ static hipError_t dense_dispatch(const DenseArgs& a, dim3 grid, int bn, hipStrea
     case 16: hipLaunchKernelGGL((dense_kernel<T, 16, 4, VIRT, 64>), grid, dim3(256), 0, s, a); break;
     case 32: hipLaunchKernelGGL((dense_kernel<T, 32, 4, VIRT, 64>), grid, dim3(256), 0, s, a); break;
     case 64: hipLaunchKernelGGL((dense_kernel<T, 64, 2, VIRT, 64>), grid, dim3(256), 0, s, a); break;
+    case 96: hipLaunchKernelGGL((dense_kernel<T, 96, 2, VIRT, 64>), grid, dim3(256), 0, s, a); break;
     case 128: hipLaunchKernelGGL((dense_kernel<T, 128, 2, VIRT, 64>), grid, dim3(256), 0, s, a); break;
     default: hipLaunchKernelGGL((dense_kernel<T, 256, 1, VIRT, 64>), grid, dim3(256), 0, s, a); break;
   }
@@ -283,7 +284,7 @@ static hipError_t dense_dispatch(const DenseArgs& a, dim3 grid, int bn, hipStrea
 }
 
 int dense_bn(int cout) {
-  return cout <= 16 ? 16 : cout <= 32 ? 32 : cout <= 64 ? 64 : cout <= 128 ? 128 : 256;
+  return cout <= 16 ? 16 : cout <= 32 ? 32 : cout <= 64 ? 64 : cout <= 96 ? 96 : cout <= 128 ? 128 : 256;
 }
 
 hipError_t launch_dense(const DenseArgs& a, int nslots, int dtype, hipStream_t s) {
