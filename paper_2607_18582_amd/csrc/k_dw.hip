@@ -136,6 +136,105 @@ __global__ __launch_bounds__(256) void dw_full_kernel(DwArgs a, int rows, DivU32
   }
 }
 
+// 3 x 3 filters: each thread walks one (input, output column, channel vector)
+// down the image with the three input rows of the current output row in
+// registers, so a new output row loads only the rows it does not share with
+// the previous one (one for stride 1, two for stride 2), requested before the
+// current row's arithmetic.  The chains are the full kernel's: taps in (dy, dx)
+// order from 0, then the bias.  No LDS: a thread's filters come from global
+// memory once.
+template <typename T>
+__global__ __launch_bounds__(256) void dw_col_kernel(DwArgs a, int tasks, DivU32 dcv, DivU32 dwo) {
+  constexpr int VEC = 16 / sizeof(T);
+  const int sl = a.slot0 + (int)blockIdx.y;
+  const int t = (int)blockIdx.x * 256 + (int)threadIdx.x;
+  if (t >= tasks) return;
+  int rest, cv, xi, ox;
+  divmodu(dcv, (uint32_t)t, rest, cv);                 // t = (xi * Wo + ox) * (C / VEC) + cv
+  divmodu(dwo, (uint32_t)rest, xi, ox);
+  const int64_t r = (int64_t)sl * a.nx + xi;
+  const T* __restrict__ xr = reinterpret_cast<const T*>(a.in.p) +
+                             row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems + cv * VEC;
+  T* const orow = reinterpret_cast<T*>(a.out) + row_index(a.out_mode, r, a.nx, a.x0) * a.out_row + cv * VEC;
+  // the thread's channels' filters ([C][3][3]: VEC * 9 consecutive elements)
+  // and biases, straight from global memory (L2-resident, shared by every
+  // column of the slot)
+  float w[9][VEC], b[VEC];
+  {
+    const T* __restrict__ wsrc = reinterpret_cast<const T*>(a.wtab[sl]) + (int64_t)cv * VEC * 9;
+    T wv[VEC * 9];
+#pragma unroll
+    for (int q = 0; q < 9; ++q) {
+      const v4u raw = reinterpret_cast<const v4u*>(wsrc)[q];
+      __builtin_memcpy(&wv[q * VEC], &raw, 16);
+    }
+#pragma unroll
+    for (int j = 0; j < VEC; ++j)
+#pragma unroll
+      for (int tp = 0; tp < 9; ++tp) w[tp][j] = to_f<T>(wv[j * 9 + tp]);
+    const float* __restrict__ bsrc = a.btab[sl] + cv * VEC;
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) b[j] = bsrc[j];
+  }
+  const int ix0 = ox * a.stride - a.pad;
+  bool colok[3];
+#pragma unroll
+  for (int dx = 0; dx < 3; ++dx) colok[dx] = (unsigned)(ix0 + dx) < (unsigned)a.W;
+  // the three vectors of input row iy under this column (zeros outside the image)
+  auto load_row = [&](int iy, v4u* v) {
+#pragma unroll
+    for (int dx = 0; dx < 3; ++dx)
+      v[dx] = (unsigned)iy < (unsigned)a.H && colok[dx]
+                  ? *reinterpret_cast<const v4u*>(xr + ((int64_t)iy * a.W + ix0 + dx) * a.C)
+                  : v4u{0u, 0u, 0u, 0u};
+  };
+  v4u row[3][3], nx0[3], nx1[3];
+  const int iy0 = -a.pad;
+  load_row(iy0, row[0]);
+  load_row(iy0 + 1, row[1]);
+  load_row(iy0 + 2, row[2]);
+  for (int oy = 0; oy < a.Ho; ++oy) {
+    // the next output row's new input rows, in flight during this row's chains
+    const int iyn = (oy + 1) * a.stride - a.pad;
+    if (a.stride == 1) {
+      load_row(iyn + 2, nx0);
+    } else {
+      load_row(iyn + 1, nx0);
+      load_row(iyn + 2, nx1);
+    }
+    float acc[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
+#pragma unroll
+    for (int dy = 0; dy < 3; ++dy)
+#pragma unroll
+      for (int dx = 0; dx < 3; ++dx) {
+        T x8[VEC];
+        __builtin_memcpy(x8, &row[dy][dx], 16);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) acc[j] = fmaf(to_f<T>(x8[j]), w[dy * 3 + dx][j], acc[j]);
+      }
+    T ov[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) ov[j] = from_f<T>(act(acc[j] + b[j], a.relu));
+    v4u o;
+    __builtin_memcpy(&o, ov, 16);
+    *reinterpret_cast<v4u*>(orow + ((int64_t)oy * a.Wo + ox) * a.C) = o;
+#pragma unroll
+    for (int dx = 0; dx < 3; ++dx) {
+      if (a.stride == 1) {
+        row[0][dx] = row[1][dx];
+        row[1][dx] = row[2][dx];
+        row[2][dx] = nx0[dx];
+      } else {
+        row[0][dx] = row[2][dx];
+        row[1][dx] = nx0[dx];
+        row[2][dx] = nx1[dx];
+      }
+    }
+  }
+}
+
 // One element per thread: (input, pixel, listed channel).  Used for the delta
 // channel lists, for C % 16-byte-vector != 0, and for float32 network outputs.
 template <typename T>
@@ -199,14 +298,18 @@ hipError_t launch_dw(const DwArgs& a, int dtype, hipStream_t s) {
   if (full) {
     const DivU32 dcv = make_divu32((uint32_t)(a.C / vec));
     const DivU32 dpix = make_divu32((uint32_t)(pix * (a.C / vec)));
-    const bool k3 = a.kh == 3 && a.kw == 3;
     const size_t lds = (size_t)a.C * (a.kh * a.kw + 1) * sizeof(float);
-    if (dtype == 0) {
-      if (k3) hipLaunchKernelGGL((dw_full_kernel<float, 3, 3>), grid, dim3(256), lds, s, a, rows, dcv, dpix, dwo);
-      else hipLaunchKernelGGL((dw_full_kernel<float, 0, 0>), grid, dim3(256), lds, s, a, rows, dcv, dpix, dwo);
+    if (a.kh == 3 && a.kw == 3 && (a.stride == 1 || a.stride == 2)) {
+      // one task per (input, output column, channel vector)
+      const int64_t tasks = (int64_t)a.nx * a.Wo * (a.C / vec);
+      if (tasks >= INT32_MAX) return hipErrorInvalidValue;
+      dim3 g2((unsigned)((tasks + 255) / 256), (unsigned)a.nslots);
+      if (dtype == 0) hipLaunchKernelGGL(dw_col_kernel<float>, g2, dim3(256), 0, s, a, (int)tasks, dcv, dwo);
+      else hipLaunchKernelGGL(dw_col_kernel<bf16_t>, g2, dim3(256), 0, s, a, (int)tasks, dcv, dwo);
+    } else if (dtype == 0) {
+      hipLaunchKernelGGL((dw_full_kernel<float, 0, 0>), grid, dim3(256), lds, s, a, rows, dcv, dpix, dwo);
     } else {
-      if (k3) hipLaunchKernelGGL((dw_full_kernel<bf16_t, 3, 3>), grid, dim3(256), lds, s, a, rows, dcv, dpix, dwo);
-      else hipLaunchKernelGGL((dw_full_kernel<bf16_t, 0, 0>), grid, dim3(256), lds, s, a, rows, dcv, dpix, dwo);
+      hipLaunchKernelGGL((dw_full_kernel<bf16_t, 0, 0>), grid, dim3(256), lds, s, a, rows, dcv, dpix, dwo);
     }
   } else {
     // the row split assumes every channel (the largest list)
