@@ -143,9 +143,10 @@ __global__ __launch_bounds__(256) void dw_full_kernel(DwArgs a, int rows, DivU32
 // current row's arithmetic.  The chains are the full kernel's: taps in (dy, dx)
 // order from 0, then the bias.  No LDS: a thread's filters come from global
 // memory once.
-template <typename T>
+template <typename T, int S>
 __global__ __launch_bounds__(256) void dw_col_kernel(DwArgs a, int tasks, DivU32 dcv, DivU32 dwo) {
   constexpr int VEC = 16 / sizeof(T);
+  constexpr int NNEW = S == 1 ? 1 : 2;                 // new input rows per output row
   const int sl = a.slot0 + (int)blockIdx.y;
   const int t = (int)blockIdx.x * 256 + (int)threadIdx.x;
   if (t >= tasks) return;
@@ -156,27 +157,23 @@ __global__ __launch_bounds__(256) void dw_col_kernel(DwArgs a, int tasks, DivU32
   const T* __restrict__ xr = reinterpret_cast<const T*>(a.in.p) +
                              row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems + cv * VEC;
   T* const orow = reinterpret_cast<T*>(a.out) + row_index(a.out_mode, r, a.nx, a.x0) * a.out_row + cv * VEC;
-  // the thread's channels' filters ([C][3][3]: VEC * 9 consecutive elements)
-  // and biases, straight from global memory (L2-resident, shared by every
-  // column of the slot)
-  float w[9][VEC], b[VEC];
+  // the thread's channels' filters ([C][3][3]: VEC * 9 consecutive elements),
+  // kept in the node type and widened at each use, and biases, straight from
+  // global memory (L2-resident, shared by every column of the slot)
+  T wv[VEC * 9];
+  float b[VEC];
   {
     const T* __restrict__ wsrc = reinterpret_cast<const T*>(a.wtab[sl]) + (int64_t)cv * VEC * 9;
-    T wv[VEC * 9];
 #pragma unroll
     for (int q = 0; q < 9; ++q) {
       const v4u raw = reinterpret_cast<const v4u*>(wsrc)[q];
       __builtin_memcpy(&wv[q * VEC], &raw, 16);
     }
-#pragma unroll
-    for (int j = 0; j < VEC; ++j)
-#pragma unroll
-      for (int tp = 0; tp < 9; ++tp) w[tp][j] = to_f<T>(wv[j * 9 + tp]);
     const float* __restrict__ bsrc = a.btab[sl] + cv * VEC;
 #pragma unroll
     for (int j = 0; j < VEC; ++j) b[j] = bsrc[j];
   }
-  const int ix0 = ox * a.stride - a.pad;
+  const int ix0 = ox * S - a.pad;
   bool colok[3];
 #pragma unroll
   for (int dx = 0; dx < 3; ++dx) colok[dx] = (unsigned)(ix0 + dx) < (unsigned)a.W;
@@ -188,20 +185,19 @@ __global__ __launch_bounds__(256) void dw_col_kernel(DwArgs a, int tasks, DivU32
                   ? *reinterpret_cast<const v4u*>(xr + ((int64_t)iy * a.W + ix0 + dx) * a.C)
                   : v4u{0u, 0u, 0u, 0u};
   };
-  v4u row[3][3], nx0[3], nx1[3];
-  const int iy0 = -a.pad;
-  load_row(iy0, row[0]);
-  load_row(iy0 + 1, row[1]);
-  load_row(iy0 + 2, row[2]);
+  // window rows[3] of the current output row; the new rows of the next two
+  // output rows (nr1, nr2: one row each for stride 1, two for stride 2) are in
+  // flight meanwhile
+  v4u row[3][3], nr1[NNEW][3], nr2[NNEW][3];
+  load_row(-a.pad, row[0]);
+  load_row(-a.pad + 1, row[1]);
+  load_row(-a.pad + 2, row[2]);
+#pragma unroll
+  for (int k = 0; k < NNEW; ++k) load_row(S - a.pad + 3 - NNEW + k, nr1[k]);
   for (int oy = 0; oy < a.Ho; ++oy) {
-    // the next output row's new input rows, in flight during this row's chains
-    const int iyn = (oy + 1) * a.stride - a.pad;
-    if (a.stride == 1) {
-      load_row(iyn + 2, nx0);
-    } else {
-      load_row(iyn + 1, nx0);
-      load_row(iyn + 2, nx1);
-    }
+    const int iy2 = (oy + 2) * S - a.pad + 3 - NNEW;  // first new row of output row oy + 2
+#pragma unroll
+    for (int k = 0; k < NNEW; ++k) load_row(iy2 + k, nr2[k]);
     float acc[VEC];
 #pragma unroll
     for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
@@ -212,7 +208,7 @@ __global__ __launch_bounds__(256) void dw_col_kernel(DwArgs a, int tasks, DivU32
         T x8[VEC];
         __builtin_memcpy(x8, &row[dy][dx], 16);
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) acc[j] = fmaf(to_f<T>(x8[j]), w[dy * 3 + dx][j], acc[j]);
+        for (int j = 0; j < VEC; ++j) acc[j] = fmaf(to_f<T>(x8[j]), to_f<T>(wv[j * 9 + dy * 3 + dx]), acc[j]);
       }
     T ov[VEC];
 #pragma unroll
@@ -222,15 +218,17 @@ __global__ __launch_bounds__(256) void dw_col_kernel(DwArgs a, int tasks, DivU32
     *reinterpret_cast<v4u*>(orow + ((int64_t)oy * a.Wo + ox) * a.C) = o;
 #pragma unroll
     for (int dx = 0; dx < 3; ++dx) {
-      if (a.stride == 1) {
+      if constexpr (S == 1) {
         row[0][dx] = row[1][dx];
         row[1][dx] = row[2][dx];
-        row[2][dx] = nx0[dx];
+        row[2][dx] = nr1[0][dx];
       } else {
         row[0][dx] = row[2][dx];
-        row[1][dx] = nx0[dx];
-        row[2][dx] = nx1[dx];
+        row[1][dx] = nr1[0][dx];
+        row[2][dx] = nr1[1][dx];
       }
+#pragma unroll
+      for (int k = 0; k < NNEW; ++k) nr1[k][dx] = nr2[k][dx];
     }
   }
 }
@@ -304,8 +302,10 @@ hipError_t launch_dw(const DwArgs& a, int dtype, hipStream_t s) {
       const int64_t tasks = (int64_t)a.nx * a.Wo * (a.C / vec);
       if (tasks >= INT32_MAX) return hipErrorInvalidValue;
       dim3 g2((unsigned)((tasks + 255) / 256), (unsigned)a.nslots);
-      if (dtype == 0) hipLaunchKernelGGL(dw_col_kernel<float>, g2, dim3(256), 0, s, a, (int)tasks, dcv, dwo);
-      else hipLaunchKernelGGL(dw_col_kernel<bf16_t>, g2, dim3(256), 0, s, a, (int)tasks, dcv, dwo);
+      if (dtype == 0 && a.stride == 1) hipLaunchKernelGGL((dw_col_kernel<float, 1>), g2, dim3(256), 0, s, a, (int)tasks, dcv, dwo);
+      else if (dtype == 0) hipLaunchKernelGGL((dw_col_kernel<float, 2>), g2, dim3(256), 0, s, a, (int)tasks, dcv, dwo);
+      else if (a.stride == 1) hipLaunchKernelGGL((dw_col_kernel<bf16_t, 1>), g2, dim3(256), 0, s, a, (int)tasks, dcv, dwo);
+      else hipLaunchKernelGGL((dw_col_kernel<bf16_t, 2>), g2, dim3(256), 0, s, a, (int)tasks, dcv, dwo);
     } else if (dtype == 0) {
       hipLaunchKernelGGL((dw_full_kernel<float, 0, 0>), grid, dim3(256), lds, s, a, rows, dcv, dpix, dwo);
     } else {
