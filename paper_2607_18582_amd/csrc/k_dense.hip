@@ -63,9 +63,11 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
     wrow[n] = w;
   }
 
-  constexpr int KMAP = VIRT ? 4096 : 1;
-  __shared__ int kmap[KMAP];
-  __shared__ unsigned char kdirect[VIRT ? KMAP / VEC : 1];   // the vector's k map is the identity
+  // VIRT: the k map (K ints) and per-vector identity flags (K / VEC bytes) in
+  // dynamic LDS sized to the layer
+  extern __shared__ __attribute__((aligned(16))) int dense_dyn[];
+  int* const kmap = dense_dyn;
+  unsigned char* const kdirect = reinterpret_cast<unsigned char*>(dense_dyn + (VIRT ? a.K : 0));
   if constexpr (VIRT) {
     const int32_t* chrow = a.vin.chmap + (int64_t)slot * a.vin.C;
     for (int k = tid; k < a.K; k += 256) {
@@ -272,13 +274,14 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
 
 template <typename T, bool VIRT>
 static hipError_t dense_dispatch(const DenseArgs& a, dim3 grid, int bn, hipStream_t s) {
+  const size_t lds = VIRT ? (size_t)a.K * 4 + (size_t)(a.K + 15) / 16 * 16 : 0;
   switch (bn) {
-    case 16: hipLaunchKernelGGL((dense_kernel<T, 16, 4, VIRT, 64>), grid, dim3(256), 0, s, a); break;
-    case 32: hipLaunchKernelGGL((dense_kernel<T, 32, 4, VIRT, 64>), grid, dim3(256), 0, s, a); break;
-    case 64: hipLaunchKernelGGL((dense_kernel<T, 64, 2, VIRT, 64>), grid, dim3(256), 0, s, a); break;
-    case 96: hipLaunchKernelGGL((dense_kernel<T, 96, 2, VIRT, 64>), grid, dim3(256), 0, s, a); break;
-    case 128: hipLaunchKernelGGL((dense_kernel<T, 128, 2, VIRT, 64>), grid, dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL((dense_kernel<T, 256, 1, VIRT, 64>), grid, dim3(256), 0, s, a); break;
+    case 16: hipLaunchKernelGGL((dense_kernel<T, 16, 4, VIRT, 64>), grid, dim3(256), lds, s, a); break;
+    case 32: hipLaunchKernelGGL((dense_kernel<T, 32, 4, VIRT, 64>), grid, dim3(256), lds, s, a); break;
+    case 64: hipLaunchKernelGGL((dense_kernel<T, 64, 2, VIRT, 64>), grid, dim3(256), lds, s, a); break;
+    case 96: hipLaunchKernelGGL((dense_kernel<T, 96, 2, VIRT, 64>), grid, dim3(256), lds, s, a); break;
+    case 128: hipLaunchKernelGGL((dense_kernel<T, 128, 2, VIRT, 64>), grid, dim3(256), lds, s, a); break;
+    default: hipLaunchKernelGGL((dense_kernel<T, 256, 1, VIRT, 64>), grid, dim3(256), lds, s, a); break;
   }
   return hipGetLastError();
 }
