@@ -485,6 +485,78 @@ __global__ __launch_bounds__(256) void conv_valu_kernel(ValuArgs a, int R) {
   }
 }
 
+// The delta of LeNet's first layer (5x5, one input channel, 2x2 pooling) over
+// the shared cached input: a block stages its R images once and computes the
+// listed channels of a group of up to SPB slots from them (the image patch of
+// a pooling window stays in registers across every slot and channel).  Each
+// output's chain is the SPEC = 1 kernel's, so results are bit-identical.
+constexpr int VALU_SPB = 32;
+template <typename T>
+__global__ __launch_bounds__(256) void conv_valu_slots_kernel(ValuArgs a, int R) {
+  extern __shared__ __attribute__((aligned(16))) float vsm[];
+  const int tid = threadIdx.x;
+  const int xi0 = (int)blockIdx.x * R;
+  const int nr = min(R, a.nx - xi0);
+  const int s_beg = a.slot0 + (int)blockIdx.y * VALU_SPB;
+  const int s_end = min(a.slot0 + a.nslots, s_beg + VALU_SPB);
+  const int u_beg = a.ch_off[s_beg], u_end = a.ch_off[s_end];
+  if (nr <= 0 || u_end <= u_beg) return;
+  const int Q = a.Hp * a.Wp;
+  const int Wp2 = a.W, img = a.H * a.W;                // no padding, one input channel
+  float* imgs = vsm;
+  float* Wl = imgs + (int64_t)R * img;                 // [u - u_beg][25]
+  for (int sl = s_beg; sl < s_end; ++sl) {
+    const T* __restrict__ Wt = reinterpret_cast<const T*>(a.wtab[sl]);
+    for (int e = tid; e < (a.ch_off[sl + 1] - a.ch_off[sl]) * 25; e += 256) {
+      const int u = a.ch_off[sl] + e / 25, k = e % 25;
+      Wl[(u - u_beg) * 25 + k] = to_f<T>(Wt[(int64_t)a.ch_list[u] * 25 + k]);
+    }
+  }
+  // the images are the prefix cache's rows x0 + xi0 .. (shared by every slot)
+  const T* src = reinterpret_cast<const T*>(a.in.p) + ((int64_t)a.x0 + xi0) * a.in.row_elems;
+  for (int e = tid; e < nr * img; e += 256) imgs[e] = to_f<T>(src[e]);
+  __syncthreads();
+  const float invWp = 1.0f / (float)a.Wp;
+  for (int p = tid; p < nr * Q; p += 256) {
+    const int rr = p / Q, q = p - rr * Q;
+    int qy, qx;
+    fast_divmod(q, a.Wp, invWp, qy, qx);
+    float pt[6][6];
+    const float* p0 = imgs + (int64_t)rr * img + (2 * qy) * Wp2 + 2 * qx;
+#pragma unroll
+    for (int y = 0; y < 6; ++y)
+#pragma unroll
+      for (int x = 0; x < 6; ++x) pt[y][x] = p0[y * Wp2 + x];
+    for (int sl = s_beg; sl < s_end; ++sl) {
+      const int c_beg = a.ch_off[sl], c_end = a.ch_off[sl + 1];
+      if (c_end <= c_beg) continue;
+      const float* __restrict__ bias = a.btab[sl];
+      const int64_t ro = row_index(a.out_mode, (int64_t)sl * a.nx + xi0 + rr, a.nx, a.x0);
+      for (int u = c_beg; u < c_end; ++u) {
+        const float* wu = Wl + (u - u_beg) * 25;
+        float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+        for (int dy = 0; dy < 5; ++dy)
+#pragma unroll
+          for (int dx = 0; dx < 5; ++dx) {
+            const float w = wu[dy * 5 + dx];
+            a0 = fmaf(pt[dy][dx], w, a0);
+            a1 = fmaf(pt[dy][dx + 1], w, a1);
+            a2 = fmaf(pt[dy + 1][dx], w, a2);
+            a3 = fmaf(pt[dy + 1][dx + 1], w, a3);
+          }
+        const int c = a.ch_list[u];
+        const float bv = bias[c];
+        float v0 = a0 + bv, v1 = a1 + bv, v2 = a2 + bv, v3 = a3 + bv;
+        v0 = act(v0, a.relu); v1 = act(v1, a.relu); v2 = act(v2, a.relu); v3 = act(v3, a.relu);
+        const float v = fmaxf(fmaxf(v0, v1), fmaxf(v2, v3));
+        if (a.delta_T > 0) store_out<T>(a.out, 0, ro * a.out_row + (int64_t)q * a.delta_T + (u - c_beg), v);
+        else store_out<T>(a.out, a.out_f32, ro * a.out_row + (int64_t)q * a.Cout + c, v);
+      }
+    }
+  }
+}
+
 hipError_t launch_valu(const ValuArgs& a, int dtype, hipStream_t s) {
   if (a.nslots <= 0 || a.nx <= 0) return hipSuccess;
   const int Q = a.Hp * a.Wp;
@@ -493,6 +565,17 @@ hipError_t launch_valu(const ValuArgs& a, int dtype, hipStream_t s) {
   if (lds > 64 * 1024) return hipErrorInvalidValue;
   dim3 grid((unsigned)((a.nx + R - 1) / R), (unsigned)a.nslots);
   const bool spec = a.kh == 5 && a.kw == 5 && a.C == 1 && a.stride == 1 && a.pool;
+  if (spec && a.ch_off && a.ch_list && a.in.mode == MODE_CACHE && a.pad == 0 && a.in.row_elems == a.H * a.W &&
+      !a.out_f32) {
+    // channel lists over the shared cached input: slot groups share staged images
+    const size_t lds2 = ((size_t)R * a.H * a.W + (size_t)VALU_SPB * a.Cout * 25) * sizeof(float);
+    if (lds2 <= 64 * 1024) {
+      dim3 g2((unsigned)((a.nx + R - 1) / R), (unsigned)((a.nslots + VALU_SPB - 1) / VALU_SPB));
+      if (dtype == 0) hipLaunchKernelGGL(conv_valu_slots_kernel<float>, g2, dim3(256), lds2, s, a, R);
+      else hipLaunchKernelGGL(conv_valu_slots_kernel<bf16_t>, g2, dim3(256), lds2, s, a, R);
+      return hipGetLastError();
+    }
+  }
   if (dtype == 0) {
     if (spec) hipLaunchKernelGGL((conv_valu_kernel<float, 1>), grid, dim3(256), lds, s, a, R);
     else hipLaunchKernelGGL((conv_valu_kernel<float, 0>), grid, dim3(256), lds, s, a, R);
