@@ -21,8 +21,10 @@
 
 namespace mure {
 
+// Waves per SIMD the register budget must allow: the LDS tile of a 16-column
+// block leaves room for five resident blocks per CU.
 template <int BN>
-__global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap, int kpad, int iters) {
+__global__ __launch_bounds__(256, BN == 16 ? 5 : BN == 32 ? 3 : 2) void conv_lds_kernel(ConvArgs a, int nimg_cap, int kpad, int iters) {
   extern __shared__ __attribute__((aligned(16))) float smem[];
   constexpr int KST = BN == 16 ? 16 : BN + 16;   // conv_lds_kst
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -37,23 +39,25 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
   int* koff = reinterpret_cast<int*>(Ws + KST * (kpad + 16));  // [kpad + 32]
   int* chrow = koff + kpad + 32;
   const float* __restrict__ X = reinterpret_cast<const float*>(a.in.p);
-  const float* __restrict__ Wt = reinterpret_cast<const float*>(a.wtab[slot]);
   const float* __restrict__ bias = a.btab[slot];
+  const float* __restrict__ cache = reinterpret_cast<const float*>(a.vin.cache);
+  const float* __restrict__ delta = reinterpret_cast<const float*>(a.vin.delta);
 
   const int ncol = a.cols ? a.ncols : a.Cout;
-  // weights: read along k (coalesced), stored k-major
-  for (int n = 0; n < BN; ++n) {
-    const bool nv = n0 + n < ncol;
+  __shared__ const float* wrow[BN];      // weight row of each column (nullptr: none)
+  __shared__ uint64_t chmask_s;          // input channels the mutant's map changes
+  if (tid < BN) {
+    const int n = n0 + tid;
     const float* wr = nullptr;
-    if (nv) {
+    if (n < ncol) {
       if (a.cols) {
-        const DeltaCol cd = a.cols[n0 + n];
+        const DeltaCol cd = a.cols[n];
         wr = reinterpret_cast<const float*>(a.wtab[a.slot0 + cd.slot - a.col_slot0]) + (int64_t)cd.c * a.K;
       } else {
-        wr = Wt + (int64_t)(n0 + n) * a.K;
+        wr = reinterpret_cast<const float*>(a.wtab[slot]) + (int64_t)n * a.K;
       }
     }
-    for (int k = tid; k < kpad + 16; k += 256) Ws[k * KST + n] = (nv && k < a.K) ? wr[k] : 0.f;
+    wrow[tid] = wr;
   }
   for (int k = tid; k < kpad + 32; k += 256) {
     int o = 0;
@@ -63,22 +67,40 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
     }
     koff[k] = o;
   }
-  __shared__ int nchg;                   // channels the mutant's map changes
-  __shared__ int chg[64], chsrc[64];     // ... and their map entries
   if (virt) {
     for (int c = tid; c < a.C; c += 256) chrow[c] = a.vin.chmap[(int64_t)slot * a.C + c];
     __syncthreads();
-    if (tid == 0) {
-      int n = 0;
-      for (int c = 0; c < a.C && n < 64; ++c)
-        if (chrow[c] != c) { chg[n] = c; chsrc[n] = chrow[c]; ++n; }
-      nchg = n;
+    if (wave == 0) {
+      const uint64_t m = __ballot(lane < a.C && chrow[lane] != lane);
+      if (lane == 0) chmask_s = m;
     }
   }
+  __syncthreads();
+  // weights, k-major: eight loads per thread in flight, then their writes
+  {
+    typedef __attribute__((address_space(1))) const float gfloat;
+    const int nw = (kpad + 16) * BN;
+    for (int e0 = tid; e0 < nw; e0 += 256 * 8) {
+      float wv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int e = e0 + 256 * u, k = e / BN, n = e % BN;
+        const float* wr = e < nw ? wrow[n] : nullptr;
+        wv[u] = (wr != nullptr && k < a.K) ? ((const gfloat*)wr)[k] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int e = e0 + 256 * u;
+        if (e < nw) Ws[(e / BN) * KST + e % BN] = wv[u];
+      }
+    }
+  }
+  const uint64_t chmask = virt ? chmask_s : 0;
+
   // per piece: the image offset of each GEMM row's receptive field, and the
   // output offset of each group of 4 rows (a pool window, or 4 pixels)
   __shared__ int rowbase[256];
-  __shared__ int64_t grpout[64];
+  __shared__ int64_t grpout[2][64];     // by piece parity (the next piece may overwrite one)
   const bool grp_ok = !a.cols && (a.pool || a.P % 4 == 0);
   constexpr int TN = BN / 16;
   // per column of this lane: bias, output slot, channel offset and stride
@@ -101,73 +123,217 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
         bv[j] = bias[n];
       }
     }
+    // complete these loads here: left pending into the piece loop, every
+    // use in the epilogue would wait for all outstanding memory operations
+    asm volatile("" ::"v"(bv[j]), "v"(oslot[j]), "v"(ochan[j]));
   }
 
-  for (int it = 0; it < iters; ++it) {
+  // A piece is 256 GEMM rows; its images are staged in LDS.  When they fit in
+  // NPF 16-byte registers per thread and need no padding, every load of a
+  // piece (and a virtual input's values for up to NFC changed channels of
+  // NPX pixels per thread) is issued before the first LDS write, so staging
+  // costs one memory round trip; the registers are free again before the k
+  // loop, which keeps the block's register budget at the k loop's.
+  constexpr int NPF = 5, NPX = 4, NFC = 2;
+  const int nfc = __popcll(chmask);
+  const bool pre = a.pad == 0 && (img & 3) == 0 && nimg_cap * img <= 1024 * NPF &&
+                   (virt ? a.C <= 64 && nfc <= NFC && nimg_cap * a.H * a.W <= 256 * NPX
+                         : a.in.row_elems == img);
+  int fc[NFC], fs[NFC];                // changed channels and their map entries
+  {
+    uint64_t m = chmask;
+#pragma unroll
+    for (int q = 0; q < NFC; ++q) {
+      fc[q] = m ? __builtin_ctzll(m) : 0;
+      fs[q] = m ? chrow[fc[q]] : 0;
+      m &= m - 1;
+    }
+  }
+  auto piece = [&](int it, int& xf, int& ni) -> bool {
+    if (it >= iters) return false;
     const int m0 = ((int)blockIdx.x * iters + it) * 256;
-    if (m0 >= Mslot) break;
-    const int xi_first = (int)divu(a.dP, (uint32_t)m0);
-    const int xi_last = min(a.nx - 1, (int)divu(a.dP, (uint32_t)(m0 + 255)));
-    const int nimg = xi_last - xi_first + 1;
-    __syncthreads();                               // previous piece done with imgs
-    if (virt && a.pad == 0 && (img & 3) == 0 && a.C <= 64) {
-      // the cached original images, then the channels the mutant changes
-      const float4* src = reinterpret_cast<const float4*>(
-          reinterpret_cast<const float*>(a.vin.cache) + ((int64_t)a.x0 + xi_first) * img);
-      float4* dst = reinterpret_cast<float4*>(imgs);
-      for (int e = tid; e < nimg * img / 4; e += 256) dst[e] = src[e];
-      const int nc = nchg;
-      if (nc > 0) {
+    if (m0 >= Mslot) return false;
+    xf = (int)divu(a.dP, (uint32_t)m0);
+    ni = min(a.nx - 1, (int)divu(a.dP, (uint32_t)(m0 + 255))) - xf + 1;
+    return true;
+  };
+  // rows of one piece are consecutive in both tensor modes
+  auto src_of = [&](int xf) {
+    return virt ? cache + ((int64_t)a.x0 + xf) * img
+                : X + row_index(a.in.mode, (int64_t)slot * a.nx + xf, a.nx, a.x0) * a.in.row_elems;
+  };
+  // the piece's images: all loads first, then their 16-byte LDS writes, then
+  // (after a barrier) the changed channels of a virtual input, again loads first
+  // tz: the thread index through a move the compiler cannot see through, so
+  // the index arithmetic stays inside each call instead of being hoisted out
+  // of the piece loop and held in registers across the k loop
+  auto put = [&](int xf, int ni) {
+    int tz;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(tz) : "v"(tid));
+    const float* src = src_of(xf);
+    const int nv = ni * img / 4;
+    {
+      v4f pf[NPF] = {};
+#pragma unroll
+      for (int u = 0; u < NPF; ++u) {
+        const int e4 = tz + 256 * u;
+        if (e4 < nv) pf[u] = *reinterpret_cast<const v4f*>(src + 4 * e4);
+      }
+      v4f* dst = reinterpret_cast<v4f*>(imgs);
+#pragma unroll
+      for (int u = 0; u < NPF; ++u) {
+        const int e4 = tz + 256 * u;
+        if (e4 < nv) dst[e4] = pf[u];
+      }
+    }
+    if (nfc) {
+      const int HW = a.H * a.W;
+      float fx[NPX][NFC] = {};
+#pragma unroll
+      for (int w = 0; w < NPX; ++w) {
+        const int e = tz + 256 * w;
+        int ii, pix;
+        divmodu(a.dHW, (uint32_t)e, ii, pix);
+        if (e >= ni * HW) continue;
+#pragma unroll
+        for (int q = 0; q < NFC; ++q) {
+          const int sq = fs[q];
+          if (q < nfc && sq != -1)
+            fx[w][q] = sq >= 0 ? src[(int64_t)e * a.C + sq]
+                     : delta[(((int64_t)slot * a.nx + xf + ii) * HW + pix) * a.vin.T + (-2 - sq)];
+        }
+      }
+      __syncthreads();                 // the 16-byte writes land first
+#pragma unroll
+      for (int w = 0; w < NPX; ++w) {
+        const int e = tz + 256 * w;
+        if (e >= ni * HW) continue;
+#pragma unroll
+        for (int q = 0; q < NFC; ++q)
+          if (q < nfc) imgs[e * a.C + fc[q]] = fx[w][q];
+      }
+    }
+  };
+  // images of one piece without registers in between (padding, or too big)
+  auto stage = [&](int xi_first, int nimg) {
+    if (a.pad == 0 && (img & 3) == 0 && (virt ? a.C <= 64 : a.in.row_elems == img)) {
+      // 16-byte copies of the rows (a virtual input's cached original
+      // images), then the channels the mutant's map changes
+      const float* src = virt ? cache + ((int64_t)a.x0 + xi_first) * img
+                              : X + row_index(a.in.mode, (int64_t)slot * a.nx + xi_first, a.nx, a.x0) * a.in.row_elems;
+      const v4f* src4 = reinterpret_cast<const v4f*>(src);
+      v4f* dst = reinterpret_cast<v4f*>(imgs);
+      for (int e = tid; e < nimg * img / 4; e += 256) dst[e] = src4[e];
+      if (chmask) {
         __syncthreads();
         const int HW = a.H * a.W;
-        const float* __restrict__ cache = reinterpret_cast<const float*>(a.vin.cache);
-        const float* __restrict__ delta = reinterpret_cast<const float*>(a.vin.delta);
         for (int e = tid; e < nimg * HW; e += 256) {
           int ii, pix;
           divmodu(a.dHW, (uint32_t)e, ii, pix);
-          // this pixel's original channels and compact delta entries
-          const float* cp = cache + ((int64_t)a.x0 + xi_first) * img + (int64_t)e * a.C;
+          const float* cp = src + (int64_t)e * a.C;
           const float* dp = delta + (((int64_t)slot * a.nx + xi_first + ii) * HW + pix) * a.vin.T;
-          for (int j = 0; j < nc; ++j) {
-            const int src = chsrc[j];
-            imgs[e * a.C + chg[j]] = src >= 0 ? cp[src] : src == -1 ? 0.f : dp[-2 - src];
+          for (uint64_t m = chmask; m; m &= m - 1) {
+            const int c = __builtin_ctzll(m), s = chrow[c];
+            imgs[e * a.C + c] = s >= 0 ? cp[s] : s == -1 ? 0.f : dp[-2 - s];
           }
         }
       }
-    } else if (!virt && a.pad == 0 && (img & 3) == 0 && a.in.row_elems == img) {
-      // contiguous rows: straight 16-byte copies
-      const int64_t ri = row_index(a.in.mode, (int64_t)slot * a.nx + xi_first, a.nx, a.x0);
-      const float4* src = reinterpret_cast<const float4*>(X + ri * a.in.row_elems);
-      float4* dst = reinterpret_cast<float4*>(imgs);
-      const int nv = nimg * img / 4;
-      if (a.in.mode == MODE_BUF || ri + nimg <= (int64_t)a.x0 + a.nx) {
-        for (int e = tid; e < nv; e += 256) dst[e] = src[e];
-      } else {
-        for (int e = tid; e < nimg * img; e += 256) {
-          const int ii = e / img;
-          imgs[e] = X[row_index(a.in.mode, (int64_t)slot * a.nx + xi_first + ii, a.nx, a.x0) * a.in.row_elems + e % img];
+      return;
+    }
+    for (int e = tid; e < nimg * img; e += 256) {
+      const int ii = e / img, rem = e % img;
+      const int c = rem % a.C, pix = rem / a.C;
+      const int iy = pix / Wp2 - a.pad, ix = pix % Wp2 - a.pad;
+      float v = 0.f;
+      if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W) {
+        const int xi = xi_first + ii;
+        const int64_t r = (int64_t)slot * a.nx + xi;
+        if (virt) {
+          v = virtual_elem<float>(a.vin, chrow, r, xi, a.x0, iy * a.W + ix, c);
+        } else {
+          v = X[row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems + ((int64_t)iy * a.W + ix) * a.C + c];
         }
       }
-    } else {
-      for (int e = tid; e < nimg * img; e += 256) {
-        const int ii = e / img, rem = e % img;
-        const int c = rem % a.C, pix = rem / a.C;
-        const int iy = pix / Wp2 - a.pad, ix = pix % Wp2 - a.pad;
-        float v = 0.f;
-        if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W) {
-          const int xi = xi_first + ii;
-          const int64_t r = (int64_t)slot * a.nx + xi;
-          if (virt) {
-            v = virtual_elem<float>(a.vin, chrow, r, xi, a.x0, iy * a.W + ix, c);
+      imgs[e] = v;
+    }
+  };
+
+  v4f acc[4][TN];
+  auto epilogue = [&](int m0, int par) {
+    const int mw = m0 + wave * 64;
+    if (grp_ok) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int mb = mw + i * 16 + (lane >> 4) * 4;
+        if (mb >= Mslot) continue;
+        const int64_t go = grpout[par][(wave * 64 + i * 16 + (lane >> 4) * 4) >> 2];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int n = n0 + j * 16 + (lane & 15);
+          if (n >= ncol) continue;
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = act(acc[i][j][e] + bv[j], a.relu);
+          if (a.pool) {
+            store_out<float>(a.out, a.out_f32, go + n, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
           } else {
-            v = X[row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems + ((int64_t)iy * a.W + ix) * a.C + c];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) store_out<float>(a.out, a.out_f32, go + (int64_t)e * a.Cout + n, v[e]);
           }
         }
-        imgs[e] = v;
+      }
+      return;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int mb = mw + i * 16 + (lane >> 4) * 4;
+      if (mb >= Mslot) continue;
+      int xo, pb;
+      divmodu(a.dP, (uint32_t)mb, xo, pb);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int n = n0 + j * 16 + (lane & 15);
+        if (n >= ncol) continue;
+        const int64_t ro = row_index(a.out_mode, (int64_t)oslot[j] * a.nx + xo, a.nx, a.x0);
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[e] = acc[i][j][e] + bv[j];
+          v[e] = act(v[e], a.relu);
+        }
+        if (a.pool) {
+          const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+          store_out<float>(a.out, a.out_f32, ro * a.out_row + (int64_t)(pb >> 2) * ostride + ochan[j], mx);
+        } else {
+          // the lane's 4 rows may cross into the next input when P % 4 != 0
+          int xe = xo, pe = pb;
+          int64_t re = ro;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (mb + e >= Mslot) break;
+            if (pe == a.P) {
+              ++xe; pe = 0;
+              re = row_index(a.out_mode, (int64_t)oslot[j] * a.nx + xe, a.nx, a.x0);
+            }
+            store_out<float>(a.out, a.out_f32, re * a.out_row + (int64_t)pe * ostride + ochan[j], v[e]);
+            ++pe;
+          }
+        }
       }
     }
-    __syncthreads();
+  };
 
+  int xf = 0, ni = 0;
+  bool have = piece(0, xf, ni);
+  for (int it = 0; have; ++it) {
+    const int m0 = ((int)blockIdx.x * iters + it) * 256;
+    const int xi_first = xf, nimg = ni;
+    __syncthreads();                   // previous piece done with imgs and rowbase
+    if (pre) {
+      put(xi_first, nimg);
+    } else {
+      stage(xi_first, nimg);
+    }
     {
       const int m = m0 + tid;
       int b = 0;
@@ -184,18 +350,19 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
         }
         b = (xi - xi_first) * img + (oy * a.stride * Wp2 + ox * a.stride) * a.C;
         if (grp_ok && (tid & 3) == 0) {
-          const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xi, a.nx, a.x0);
-          grpout[tid >> 2] = ro * a.out_row + (int64_t)(a.pool ? (p >> 2) : p) * a.Cout;
+          const int64_t ro = a.out_mode == MODE_BUF ? (int64_t)slot * a.nx + xi : (int64_t)a.x0 + xi;
+          grpout[it & 1][tid >> 2] = ro * a.out_row + (int64_t)(a.pool ? (p >> 2) : p) * a.Cout;
         }
       }
       rowbase[tid] = b;
     }
     __syncthreads();
-    const int mw = m0 + wave * 64;
     int base[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) base[i] = rowbase[wave * 64 + i * 16 + (lane & 15)];
-    v4f acc[4][TN];
+    for (int i = 0; i < 4; ++i) {
+      base[i] = rowbase[wave * 64 + i * 16 + (lane & 15)];
+    }
+    have = piece(it + 1, xf, ni);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -242,67 +409,7 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(ConvArgs a, int nimg_cap,
     if (k8 < kpad) { MURE_LDS_MFMA(a0, b0) }        // kpad % 16 == 8: the last step
 #undef MURE_LDS_READ
 #undef MURE_LDS_MFMA
-
-    if (grp_ok) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int mb = mw + i * 16 + (lane >> 4) * 4;
-        if (mb >= Mslot) continue;
-        const int64_t go = grpout[(wave * 64 + i * 16 + (lane >> 4) * 4) >> 2];
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int n = n0 + j * 16 + (lane & 15);
-          if (n >= ncol) continue;
-          float v[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = act(acc[i][j][e] + bv[j], a.relu);
-          if (a.pool) {
-            store_out<float>(a.out, a.out_f32, go + n, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
-          } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) store_out<float>(a.out, a.out_f32, go + (int64_t)e * a.Cout + n, v[e]);
-          }
-        }
-      }
-      continue;
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int mb = mw + i * 16 + (lane >> 4) * 4;
-      if (mb >= Mslot) continue;
-      int xo, pb;
-      divmodu(a.dP, (uint32_t)mb, xo, pb);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int n = n0 + j * 16 + (lane & 15);
-        if (n >= ncol) continue;
-        const int64_t ro = row_index(a.out_mode, (int64_t)oslot[j] * a.nx + xo, a.nx, a.x0);
-        float v[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          v[e] = acc[i][j][e] + bv[j];
-          v[e] = act(v[e], a.relu);
-        }
-        if (a.pool) {
-          const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-          store_out<float>(a.out, a.out_f32, ro * a.out_row + (int64_t)(pb >> 2) * ostride + ochan[j], mx);
-        } else {
-          // the lane's 4 rows may cross into the next input when P % 4 != 0
-          int xe = xo, pe = pb;
-          int64_t re = ro;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            if (mb + e >= Mslot) break;
-            if (pe == a.P) {
-              ++xe; pe = 0;
-              re = row_index(a.out_mode, (int64_t)oslot[j] * a.nx + xe, a.nx, a.x0);
-            }
-            store_out<float>(a.out, a.out_f32, re * a.out_row + (int64_t)pe * ostride + ochan[j], v[e]);
-            ++pe;
-          }
-        }
-      }
-    }
+    epilogue(m0, it & 1);
   }
 }
 
@@ -317,6 +424,8 @@ hipError_t launch_conv_lds(const ConvArgs& a0, int nslots, hipStream_t s) {
   a.dWp = make_divu32((uint32_t)std::max(1, a.Wp));
   a.dWc = make_divu32((uint32_t)std::max(1, a.Wc));
   a.dHW = make_divu32((uint32_t)std::max(1, a.H * a.W));
+  a.dC = make_divu32((uint32_t)std::max(1, a.C));
+  a.dImg = make_divu32((uint32_t)std::max(1, (a.H + 2 * a.pad) * (a.W + 2 * a.pad) * a.C));
   // columns per block: the node's channels, or for a gathered delta the
   // widest tile whose LDS fits
   int bn = conv_lds_bn(a.Cout);

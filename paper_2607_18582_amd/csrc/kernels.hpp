@@ -94,9 +94,10 @@ struct ConvArgs {
   // channels per slot; the input must be slot independent (prefix cache)
   const DeltaCol* cols = nullptr;
   int ncols = 0, delta_T = 0, col_slot0 = 0;
-  // filled by the launchers: dividers by P, P/4, Wp, Wc, H*W, C and kw; the
-  // halo kernel's band count and column blocks per band (XCD-aware order)
-  DivU32 dP, dPq, dWp, dWc, dHW, dC, dKW;
+  // filled by the launchers: dividers by P, P/4, Wp, Wc, H*W, C, kw and the
+  // padded image size; the halo kernel's band count and column blocks per
+  // band (XCD-aware order)
+  DivU32 dP, dPq, dWp, dWc, dHW, dC, dKW, dImg;
   int bands = 0, zblocks = 1;
 };
 
