@@ -9,6 +9,7 @@
 namespace mure {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v2f __attribute__((ext_vector_type(2)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));   // 16 raw bytes in registers
 typedef uint16_t bf16_t;   // bfloat16 bit pattern

@@ -3,9 +3,13 @@
 // conv_lds_kernel (fp32): the zero-padded input images a block needs and the
 // weight matrix of its output channels live in LDS, so the k loop runs without
 // barriers; A operands are read straight from the image through a per-k
-// offset table (k = (dy, dx, c_in), c_in fastest, steps of 4 -- the same
-// reduction order as the im2col kernel).  A block keeps its weights and walks
-// several 256-row pieces of its slot.  Its input may be "virtual": the first
+// offset table (k = (dy, dx, c_in), c_in fastest).  With C_in odd an MFMA
+// takes 4 consecutive k; with C_in even (PAIR) a step of 8 k gives each lane
+// group the pair (2g, 2g + 1), adjacent in the image and in the pair-
+// interleaved weight tile, so one 8-byte read feeds the two MFMAs of the
+// step (even k, then odd k) and the address arithmetic halves.  The order is
+// a function of the node's shape, as for every family.  A block keeps its
+// weights and walks several 256-row pieces of its slot.  Its input may be "virtual": the first
 // mutated node's output seen through the mutant's channel map and compact
 // delta rows, so that output is never materialised per mutant.
 //
@@ -23,7 +27,7 @@ namespace mure {
 
 // Waves per SIMD the register budget must allow: the LDS tile of a 16-column
 // block leaves room for five resident blocks per CU.
-template <int BN>
+template <int BN, bool PAIR>
 __global__ __launch_bounds__(256, BN == 16 ? 5 : BN == 32 ? 3 : 2) void conv_lds_kernel(ConvArgs a, int nimg_cap, int kpad, int iters) {
   extern __shared__ __attribute__((aligned(16))) float smem[];
   constexpr int KST = BN == 16 ? 16 : BN + 16;   // conv_lds_kst
@@ -65,7 +69,7 @@ __global__ __launch_bounds__(256, BN == 16 ? 5 : BN == 32 ? 3 : 2) void conv_lds
       const int ci = k % a.C, t = k / a.C;
       o = ((t / a.kw) * Wp2 + (t % a.kw)) * a.C + ci;
     }
-    koff[k] = o;
+    koff[k] = 4 * o;                     // bytes
   }
   if (virt) {
     for (int c = tid; c < a.C; c += 256) chrow[c] = a.vin.chmap[(int64_t)slot * a.C + c];
@@ -91,7 +95,10 @@ __global__ __launch_bounds__(256, BN == 16 ? 5 : BN == 32 ? 3 : 2) void conv_lds
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int e = e0 + 256 * u;
-        if (e < nw) Ws[(e / BN) * KST + e % BN] = wv[u];
+        if (e < nw) {
+          const int k = e / BN, n = e % BN;
+          Ws[PAIR ? ((k >> 1) * KST + n) * 2 + (k & 1) : k * KST + n] = wv[u];
+        }
       }
     }
   }
@@ -357,58 +364,92 @@ __global__ __launch_bounds__(256, BN == 16 ? 5 : BN == 32 ? 3 : 2) void conv_lds
       rowbase[tid] = b;
     }
     __syncthreads();
+    // row offsets in bytes, with the LDS address of the images folded in
+    const char* imgb = reinterpret_cast<const char*>(imgs);
     int base[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      base[i] = rowbase[wave * 64 + i * 16 + (lane & 15)];
-    }
+    for (int i = 0; i < 4; ++i) base[i] = 4 * rowbase[wave * 64 + i * 16 + (lane & 15)];
     have = piece(it + 1, xf, ni);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
-    const float* wl = Ws + (lane >> 4) * KST + (lane & 15);
-    const int* kl = koff + (lane >> 4);
     // software pipeline over steps of 8 k with two register sets: the reads
     // of step s + 1 are issued before the MFMAs of step s, and the offsets
     // of step s + 2 before those (the padded table rows past kpad are zero)
-    float a0[2][4], b0[2][TN], a1[2][4], b1[2][TN];
-    int ko[2];
-#define MURE_LDS_READ(A, B, KB, O0, O1)                                         \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                            \
-      A[0][i] = imgs[base[i] + (O0)];                                          \
-      A[1][i] = imgs[base[i] + (O1)];                                          \
-    }                                                                          \
-    _Pragma("unroll") for (int j = 0; j < TN; ++j) {                           \
-      B[0][j] = wl[(KB) * KST + j * 16];                                       \
-      B[1][j] = wl[((KB) + 4) * KST + j * 16];                                 \
-    }
-#define MURE_LDS_MFMA(A, B)                                                    \
-    _Pragma("unroll") for (int h = 0; h < 2; ++h)                              \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i)                              \
-    _Pragma("unroll") for (int j = 0; j < TN; ++j)                             \
-      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[h][i], B[h][j], acc[i][j], 0, 0, 0);
-    MURE_LDS_READ(a0, b0, 0, kl[0], kl[4])
-    ko[0] = kl[8];
-    ko[1] = kl[12];
     int k8 = 0;
-    for (; k8 + 16 <= kpad; k8 += 16) {
-      MURE_LDS_READ(a1, b1, k8 + 8, ko[0], ko[1])
-      ko[0] = kl[k8 + 16];
-      ko[1] = kl[k8 + 20];
-      __builtin_amdgcn_sched_barrier(0);
-      MURE_LDS_MFMA(a0, b0)
-      __builtin_amdgcn_sched_barrier(0);
-      MURE_LDS_READ(a0, b0, k8 + 16, ko[0], ko[1])
-      ko[0] = kl[k8 + 24];
-      ko[1] = kl[k8 + 28];
-      __builtin_amdgcn_sched_barrier(0);
-      MURE_LDS_MFMA(a1, b1)
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if (k8 < kpad) { MURE_LDS_MFMA(a0, b0) }        // kpad % 16 == 8: the last step
+    if constexpr (PAIR) {
+      const float* wl = Ws + ((lane >> 4) * KST + (lane & 15)) * 2;
+      const int* kl = koff + 2 * (lane >> 4);
+      v2f a0[4], b0[TN], a1[4], b1[TN];
+      int ko;
+#define MURE_LDS_READ(A, B, KB, O)                                              \
+      _Pragma("unroll") for (int i = 0; i < 4; ++i)                            \
+        A[i] = *reinterpret_cast<const v2f*>(imgb + base[i] + (O));            \
+      _Pragma("unroll") for (int j = 0; j < TN; ++j)                           \
+        B[j] = *reinterpret_cast<const v2f*>(wl + ((KB) / 2 * KST + j * 16) * 2);
+#define MURE_LDS_MFMA(A, B)                                                    \
+      _Pragma("unroll") for (int h = 0; h < 2; ++h)                            \
+      _Pragma("unroll") for (int i = 0; i < 4; ++i)                            \
+      _Pragma("unroll") for (int j = 0; j < TN; ++j)                           \
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[i][h], B[j][h], acc[i][j], 0, 0, 0);
+      MURE_LDS_READ(a0, b0, 0, kl[0])
+      ko = kl[8];
+      for (; k8 + 16 <= kpad; k8 += 16) {
+        MURE_LDS_READ(a1, b1, k8 + 8, ko)
+        ko = kl[k8 + 16];
+        __builtin_amdgcn_sched_barrier(0);
+        MURE_LDS_MFMA(a0, b0)
+        __builtin_amdgcn_sched_barrier(0);
+        MURE_LDS_READ(a0, b0, k8 + 16, ko)
+        ko = kl[k8 + 24];
+        __builtin_amdgcn_sched_barrier(0);
+        MURE_LDS_MFMA(a1, b1)
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (k8 < kpad) { MURE_LDS_MFMA(a0, b0) }      // kpad % 16 == 8: the last step
 #undef MURE_LDS_READ
 #undef MURE_LDS_MFMA
+    } else {
+      const float* wl = Ws + (lane >> 4) * KST + (lane & 15);
+      const int* kl = koff + (lane >> 4);
+      float a0[2][4], b0[2][TN], a1[2][4], b1[2][TN];
+      int ko[2];
+#define MURE_LDS_READ(A, B, KB, O0, O1)                                         \
+      _Pragma("unroll") for (int i = 0; i < 4; ++i) {                          \
+        A[0][i] = *reinterpret_cast<const float*>(imgb + base[i] + (O0));      \
+        A[1][i] = *reinterpret_cast<const float*>(imgb + base[i] + (O1));      \
+      }                                                                        \
+      _Pragma("unroll") for (int j = 0; j < TN; ++j) {                         \
+        B[0][j] = wl[(KB) * KST + j * 16];                                     \
+        B[1][j] = wl[((KB) + 4) * KST + j * 16];                               \
+      }
+#define MURE_LDS_MFMA(A, B)                                                    \
+      _Pragma("unroll") for (int h = 0; h < 2; ++h)                            \
+      _Pragma("unroll") for (int i = 0; i < 4; ++i)                            \
+      _Pragma("unroll") for (int j = 0; j < TN; ++j)                           \
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[h][i], B[h][j], acc[i][j], 0, 0, 0);
+      MURE_LDS_READ(a0, b0, 0, kl[0], kl[4])
+      ko[0] = kl[8];
+      ko[1] = kl[12];
+      for (; k8 + 16 <= kpad; k8 += 16) {
+        MURE_LDS_READ(a1, b1, k8 + 8, ko[0], ko[1])
+        ko[0] = kl[k8 + 16];
+        ko[1] = kl[k8 + 20];
+        __builtin_amdgcn_sched_barrier(0);
+        MURE_LDS_MFMA(a0, b0)
+        __builtin_amdgcn_sched_barrier(0);
+        MURE_LDS_READ(a0, b0, k8 + 16, ko[0], ko[1])
+        ko[0] = kl[k8 + 24];
+        ko[1] = kl[k8 + 28];
+        __builtin_amdgcn_sched_barrier(0);
+        MURE_LDS_MFMA(a1, b1)
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (k8 < kpad) { MURE_LDS_MFMA(a0, b0) }      // kpad % 16 == 8: the last step
+#undef MURE_LDS_READ
+#undef MURE_LDS_MFMA
+    }
     epilogue(m0, it & 1);
   }
 }
@@ -446,10 +487,14 @@ hipError_t launch_conv_lds(const ConvArgs& a0, int nslots, hipStream_t s) {
   // about 2048 blocks in flight, at most 8 pieces per block
   int iters = (int)std::max<int64_t>(1, std::min<int64_t>(8, pieces * nslots * ztiles / 2048));
   dim3 grid((unsigned)((pieces + iters - 1) / iters), (unsigned)nslots, (unsigned)ztiles);
-  switch (bn) {
-    case 16: hipLaunchKernelGGL((conv_lds_kernel<16>), grid, dim3(256), lds, s, a, cap, kpad, iters); break;
-    case 32: hipLaunchKernelGGL((conv_lds_kernel<32>), grid, dim3(256), lds, s, a, cap, kpad, iters); break;
-    default: hipLaunchKernelGGL((conv_lds_kernel<64>), grid, dim3(256), lds, s, a, cap, kpad, iters); break;
+  const bool pair = a.C % 2 == 0;
+  switch (bn * 2 + (pair ? 1 : 0)) {
+    case 32: hipLaunchKernelGGL((conv_lds_kernel<16, false>), grid, dim3(256), lds, s, a, cap, kpad, iters); break;
+    case 33: hipLaunchKernelGGL((conv_lds_kernel<16, true>), grid, dim3(256), lds, s, a, cap, kpad, iters); break;
+    case 64: hipLaunchKernelGGL((conv_lds_kernel<32, false>), grid, dim3(256), lds, s, a, cap, kpad, iters); break;
+    case 65: hipLaunchKernelGGL((conv_lds_kernel<32, true>), grid, dim3(256), lds, s, a, cap, kpad, iters); break;
+    case 128: hipLaunchKernelGGL((conv_lds_kernel<64, false>), grid, dim3(256), lds, s, a, cap, kpad, iters); break;
+    default: hipLaunchKernelGGL((conv_lds_kernel<64, true>), grid, dim3(256), lds, s, a, cap, kpad, iters); break;
   }
   return hipGetLastError();
 }
