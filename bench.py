@@ -36,12 +36,12 @@ KERNELS = ["dense_kernel (DENSE layers, MFMA GEMM)",
            "conv_lds_kernel (CONV2D, LDS-resident images, MFMA)",
            "conv_mfma_kernel (CONV2D, im2col implicit GEMM with scalar gathers, MFMA)",
            "conv_big_kernel (bf16 CONV2D, tiled implicit GEMM, MFMA)",
-           "dw_full_kernel (depthwise CONV2D, vector ALU)",
+           "dw_col_kernel (depthwise CONV2D, vector ALU; dw_full_kernel for filters other than 3x3)",
            "embed_kernel (token embedding gather)",
            "lstm_kernel (LSTM recursion, MFMA per step)",
            "conv_halo_kernel (bf16 3x3 CONV2D, A operand from LDS halo tiles, MFMA)"]
 KERNEL_NAMES = ["dense_kernel", "conv_valu_kernel", "conv_lds_kernel", "conv_mfma_kernel",
-                "conv_big_kernel", "dw_full_kernel", "embed_kernel", "lstm_kernel", "conv_halo_kernel"]
+                "conv_big_kernel", "dw_col_kernel", "embed_kernel", "lstm_kernel", "conv_halo_kernel"]
 VALU_FAMILIES = (1, 5)                           # fused multiply-add chains on the vector ALU
 PEAK_VALU_TFLOPS = 78.6                          # fp32 FMA without packed-fp32 instructions
 PEAK_HBM_GBS = 8000.0
