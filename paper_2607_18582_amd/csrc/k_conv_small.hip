@@ -26,9 +26,9 @@
 namespace mure {
 
 // Waves per SIMD the register budget must allow: the LDS tile of a 16-column
-// block leaves room for five resident blocks per CU.
+// block leaves room for five or six resident blocks per CU.
 template <int BN, bool PAIR>
-__global__ __launch_bounds__(256, BN == 16 ? 5 : BN == 32 ? 3 : 2) void conv_lds_kernel(ConvArgs a, int nimg_cap, int kpad, int iters) {
+__global__ __launch_bounds__(256, BN == 16 ? (PAIR ? 6 : 5) : BN == 32 ? 3 : 2) void conv_lds_kernel(ConvArgs a, int nimg_cap, int kpad, int iters) {
   extern __shared__ __attribute__((aligned(16))) float smem[];
   constexpr int KST = BN == 16 ? 16 : BN + 16;   // conv_lds_kst
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -39,9 +39,9 @@ __global__ __launch_bounds__(256, BN == 16 ? 5 : BN == 32 ? 3 : 2) void conv_lds
   const int img = Hp2 * Wp2 * a.C;
   const bool virt = a.vin.chmap != nullptr;
   float* imgs = smem;
-  float* Ws = imgs + (int64_t)nimg_cap * img;    // [kpad + 16][KST], k-major, zero padded
-  int* koff = reinterpret_cast<int*>(Ws + KST * (kpad + 16));  // [kpad + 32]
-  int* chrow = koff + kpad + 32;
+  float* Ws = imgs + (int64_t)nimg_cap * img;    // [kpad + 8][KST], k-major, zero padded
+  int* koff = reinterpret_cast<int*>(Ws + KST * (kpad + 8));   // [kpad + 16]
+  int* chrow = koff + kpad + 16;
   const float* __restrict__ X = reinterpret_cast<const float*>(a.in.p);
   const float* __restrict__ bias = a.btab[slot];
   const float* __restrict__ cache = reinterpret_cast<const float*>(a.vin.cache);
@@ -63,7 +63,7 @@ __global__ __launch_bounds__(256, BN == 16 ? 5 : BN == 32 ? 3 : 2) void conv_lds
     }
     wrow[tid] = wr;
   }
-  for (int k = tid; k < kpad + 32; k += 256) {
+  for (int k = tid; k < kpad + 16; k += 256) {
     int o = 0;
     if (k < a.K) {
       const int ci = k % a.C, t = k / a.C;
@@ -83,7 +83,7 @@ __global__ __launch_bounds__(256, BN == 16 ? 5 : BN == 32 ? 3 : 2) void conv_lds
   // weights, k-major: eight loads per thread in flight, then their writes
   {
     typedef __attribute__((address_space(1))) const float gfloat;
-    const int nw = (kpad + 16) * BN;
+    const int nw = (kpad + 8) * BN;
     for (int e0 = tid; e0 < nw; e0 += 256 * 8) {
       float wv[8];
 #pragma unroll
@@ -107,7 +107,7 @@ __global__ __launch_bounds__(256, BN == 16 ? 5 : BN == 32 ? 3 : 2) void conv_lds
   // per piece: the image offset of each GEMM row's receptive field, and the
   // output offset of each group of 4 rows (a pool window, or 4 pixels)
   __shared__ int rowbase[256];
-  __shared__ int64_t grpout[2][64];     // by piece parity (the next piece may overwrite one)
+  __shared__ int64_t grpout[64];
   const bool grp_ok = !a.cols && (a.pool || a.P % 4 == 0);
   constexpr int TN = BN / 16;
   // per column of this lane: bias, output slot, channel offset and stride
@@ -266,14 +266,14 @@ __global__ __launch_bounds__(256, BN == 16 ? 5 : BN == 32 ? 3 : 2) void conv_lds
   };
 
   v4f acc[4][TN];
-  auto epilogue = [&](int m0, int par) {
+  auto epilogue = [&](int m0) {
     const int mw = m0 + wave * 64;
     if (grp_ok) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int mb = mw + i * 16 + (lane >> 4) * 4;
         if (mb >= Mslot) continue;
-        const int64_t go = grpout[par][(wave * 64 + i * 16 + (lane >> 4) * 4) >> 2];
+        const int64_t go = grpout[(wave * 64 + i * 16 + (lane >> 4) * 4) >> 2];
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
           const int n = n0 + j * 16 + (lane & 15);
@@ -358,7 +358,7 @@ __global__ __launch_bounds__(256, BN == 16 ? 5 : BN == 32 ? 3 : 2) void conv_lds
         b = (xi - xi_first) * img + (oy * a.stride * Wp2 + ox * a.stride) * a.C;
         if (grp_ok && (tid & 3) == 0) {
           const int64_t ro = a.out_mode == MODE_BUF ? (int64_t)slot * a.nx + xi : (int64_t)a.x0 + xi;
-          grpout[it & 1][tid >> 2] = ro * a.out_row + (int64_t)(a.pool ? (p >> 2) : p) * a.Cout;
+          grpout[tid >> 2] = ro * a.out_row + (int64_t)(a.pool ? (p >> 2) : p) * a.Cout;
         }
       }
       rowbase[tid] = b;
@@ -450,7 +450,7 @@ __global__ __launch_bounds__(256, BN == 16 ? 5 : BN == 32 ? 3 : 2) void conv_lds
 #undef MURE_LDS_READ
 #undef MURE_LDS_MFMA
     }
-    epilogue(m0, it & 1);
+    epilogue(m0);
   }
 }
 

@@ -102,17 +102,22 @@ inline int64_t valu_lds_bytes(int inH, int inW, int inC, int pad, int Q, int c_o
   return (int64_t)valu_rows(Q) * (inH + 2 * pad) * (inW + 2 * pad) * inC * 4 + (int64_t)c_out * K * 4;
 }
 // LDS convolution: images a block may touch for 256 GEMM rows of P per input.
-inline int conv_lds_nimg_cap(int P) { return P >= 256 ? 2 : (256 + P - 1) / P + 1; }
+// images a 256-row piece spans: exactly 256 / P when P divides 256 (pieces
+// then start at image boundaries), else at most ceil(256 / P) + 1
+inline int conv_lds_nimg_cap(int P) {
+  return P >= 256 ? 2 : 256 % P == 0 ? 256 / P : (256 + P - 1) / P + 1;
+}
 inline int conv_lds_bn(int c_out) { return c_out <= 16 ? 16 : c_out <= 32 ? 32 : 64; }
 // floats per k row of the LDS weight tile [kpad][kst]: the 4 k rows one MFMA
 // reads land in distinct bank quarters
 inline int conv_lds_kst(int bn) { return bn == 16 ? 16 : bn + 16; }
 inline int64_t conv_lds_bytes(int inH, int inW, int inC, int pad, int P, int c_out, int64_t K) {
-  // weights and offsets carry 16 and 32 rows of zero padding past kpad for
-  // the software-pipelined k loop
+  // weights and offsets carry 8 and 16 rows of zero padding past kpad: the
+  // software-pipelined k loop reads up to weight row kpad + 7 and offset
+  // kpad + 15
   const int64_t kpad = (K + 7) / 8 * 8;
   return ((int64_t)conv_lds_nimg_cap(P) * (inH + 2 * pad) * (inW + 2 * pad) * inC +
-          (int64_t)conv_lds_kst(conv_lds_bn(c_out)) * (kpad + 16)) * 4 + (kpad + 32) * 4 +
+          (int64_t)conv_lds_kst(conv_lds_bn(c_out)) * (kpad + 8)) * 4 + (kpad + 16) * 4 +
          (int64_t)inC * 4;
 }
 
