@@ -211,3 +211,40 @@ def test_fused_paths_equal_separate_kernels(cfg):
     assert np.array_equal(w1, w2) and np.array_equal(k1, k2) and s1 == s2
     for mid in sample_mutants(m1, wl):
         assert np.array_equal(m1.get_logits(mid).cpu().numpy(), m2.get_logits(mid).cpu().numpy()), mid
+
+
+def _fp32_cnn():
+    """A small fp32 CNN whose convolutions take the LDS kernel's other
+    instances and the fp32 im2col kernel:
+      C1  20x20x1 -> 5x5 -> pool -> 8x8x16   LDS, C_in odd (4 consecutive k per MFMA)
+      C2  1x1, 16 -> 32                      LDS, 32-column tiles, k pairs
+      C3  1x1, 32 -> 48, pool -> 4x4x48      LDS, 64-column tiles, k pairs
+      C4  3x3 pad 1, 48 -> 24                im2col (its images exceed the LDS budget)
+    C1 and C2 feed LDS convolutions, so their clusters read mmi's output
+    virtually."""
+    b = W.configs._Builder((20, 20, 1))
+    x = b.conv(0, 16, 5, relu=True, pool=2, name="C1")
+    x = b.conv(x, 32, 1, relu=True, name="C2")
+    x = b.conv(x, 48, 1, relu=True, pool=2, name="C3")
+    x = b.conv(x, 24, 3, pad=1, relu=True, name="C4")
+    x = b.dense(x, 20, True, "F1")
+    b.dense(x, 10, False, "F2")
+    w, bb = W.configs._draw_weights(b.nodes, "f32", 0.1, seed=7)
+    model = W.Model("cnn_f32", "f32", b.nodes, w, bb)
+    x = W.make_inputs(model, 150, "uniform")
+    mu = W.make_mutants(model, 48, 2, "layer_first", variant=3, ops=(W.GF, W.NEB, W.NAI, W.NS, W.WS))
+    return W.Workload("cnn_f32", model, x, mu)
+
+
+def test_fp32_cnn_lds_instances_and_im2col():
+    """Parity with the oracle on the fp32 CNN above, the kernel families it is
+    meant to reach, and memoized equal to vanilla bit for bit."""
+    wl = _fp32_cnn()
+    m, _, _ = _parity(wl, kernel_timing=1)
+    launches = m.stats()["kernel_launches"]
+    assert launches[2] > 0 and launches[3] > 0, launches      # LDS and im2col families ran
+    m1, w1, k1, s1 = run_gpu(wl)
+    m2, w2, k2, s2 = run_gpu(wl, vanilla=1)
+    assert np.array_equal(w1, w2) and np.array_equal(k1, k2) and s1 == s2
+    for mid in sample_mutants(m1, wl):
+        assert np.array_equal(m1.get_logits(mid).cpu().numpy(), m2.get_logits(mid).cpu().numpy()), mid
