@@ -163,6 +163,29 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
     }
   };
 
+  // output slot, channel and bias of each of the lane's columns, loaded
+  // before the k loop and completed there: left pending into the branchy
+  // epilogue, each store would wait for every outstanding memory operation
+  const float* __restrict__ bias = a.btab[slot];
+  int cslot[TN], cchan[TN];
+  float cbias[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int n = n0 + wn * WN + j * 16 + (lane & 15);
+    cslot[j] = slot; cchan[j] = n; cbias[j] = 0.f;
+    if (n < ncol) {
+      if (a.cols) {
+        const DeltaCol cd = a.cols[n];
+        cslot[j] = a.slot0 + cd.slot - a.col_slot0;
+        cchan[j] = a.delta_T > 0 ? cd.t : cd.c;
+        cbias[j] = a.btab[cslot[j]][cd.c];
+      } else {
+        cbias[j] = bias[n];
+      }
+    }
+    asm volatile("" ::"v"(cslot[j]), "v"(cchan[j]), "v"(cbias[j]));
+  }
+
   v4f acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
@@ -208,35 +231,23 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
     __syncthreads();
   }
 
-  const float* __restrict__ bias = a.btab[slot];
   const int orow = a.cols && a.delta_T > 0 ? a.delta_T : a.Cout;   // elements per output row
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const int nl = wn * WN + j * 16 + (lane & 15);
     const int n = n0 + nl;
-    // output slot and channel of this column
-    int os = slot, oc = n;
-    float bv = 0.f;
-    if (n < ncol) {
-      if (a.cols) {
-        const DeltaCol cd = a.cols[n];
-        os = a.slot0 + cd.slot - a.col_slot0;
-        oc = a.delta_T > 0 ? cd.t : cd.c;
-        bv = a.btab[os][cd.c];
-      } else {
-        bv = bias[n];
-      }
-    }
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int rl = wm * WM + i * 16 + (lane >> 4) * 4 + e;
-        float v = acc[i][j][e] + bv;
+        float v = acc[i][j][e] + cbias[j];
         v = act(v, a.relu);
         if (a.write_out && n < ncol && m0 + rl < a.nx) {
-          const int64_t ro = row_index(a.out_mode, (int64_t)os * a.nx + m0 + rl, a.nx, a.x0);
-          store_out<T>(a.out, a.out_f32, ro * orow + oc, v);
+          // row r = slot * nx + xi of the chunk: buffer row r, or cache row x0 + xi
+          const int xo = m0 + rl;
+          const int64_t ro = a.out_mode == MODE_BUF ? (int64_t)cslot[j] * a.nx + xo : (int64_t)a.x0 + xo;
+          store_out<T>(a.out, a.out_f32, ro * orow + cchan[j], v);
         }
         if constexpr (LSN > 1) {
           if (a.do_kill) Ls[rl * (BN + 1) + nl] = v;
