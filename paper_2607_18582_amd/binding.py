@@ -8,6 +8,8 @@ built the import of this module succeeds but constructing ``Mure`` raises.
 from __future__ import annotations
 
 import ctypes as C
+import itertools
+import operator
 import os
 from typing import Dict, Optional, Sequence
 
@@ -63,6 +65,26 @@ class mure_stats(C.Structure):
                 ("gemm_macs_executed", C.c_int64), ("kernel_launches", C.c_int64 * N_KERNELS),
                 ("kernel_ms", C.c_double * N_KERNELS), ("kernel_macs_algorithmic", C.c_int64 * N_KERNELS),
                 ("kernel_bytes_algorithmic", C.c_double * N_KERNELS)]
+
+
+def _pack(arrays, R: int, dtype):
+    """Pack the non-None entries of ``arrays`` (length R, or None) into one
+    contiguous pool; returns (pool, address of each record's entry or 0,
+    length of each record's entry or 0).  The per-record iteration runs in
+    C (map, itemgetter) rather than in Python loops."""
+    addr = np.zeros(R, np.uint64)
+    lens = np.zeros(R, np.int64)
+    if arrays is None or len(arrays) == 0:
+        return np.zeros(1, dtype), addr, lens
+    idx = np.flatnonzero(np.fromiter(map(operator.is_not, arrays, itertools.repeat(None)), bool, R))
+    if idx.size == 0:
+        return np.zeros(1, dtype), addr, lens
+    parts = operator.itemgetter(*idx.tolist())(arrays) if idx.size > 1 else (arrays[int(idx[0])],)
+    ln = np.fromiter(map(len, parts), np.int64, idx.size)
+    pool = np.concatenate(parts).astype(dtype, copy=False)
+    addr[idx] = np.where(ln > 0, pool.ctypes.data + pool.itemsize * (np.cumsum(ln) - ln), 0).astype(np.uint64)
+    lens[idx] = ln
+    return pool, addr, lens
 
 
 class MureError(RuntimeError):
@@ -201,20 +223,14 @@ class Mure:
         recs["layer"][:R] = layer
         recs["neuron"][:R] = neuron
         recs["partner"][:R] = partner
-        lens = np.array([0 if e is None else len(e) for e in noise], np.int64)
-        pool = np.concatenate([np.asarray(e, np.float32) for e in noise if e is not None] or
-                              [np.zeros(1, np.float32)])
-        offs = np.concatenate([[0], np.cumsum(lens)[:-1]]) if R else np.zeros(0, np.int64)
-        recs["noise"][:R] = np.where(lens > 0, pool.ctypes.data + 4 * offs, 0)
-        recs["noise_len"][:R] = lens
-        if perm is None or len(perm) == 0:
-            perm = [None] * R
-        plens = np.array([0 if q is None else len(q) for q in perm], np.int64)
-        ppool = np.concatenate([np.asarray(q, np.int32) for q in perm if q is not None] or
-                               [np.zeros(1, np.int32)])
-        poffs = np.concatenate([[0], np.cumsum(plens)[:-1]]) if R else np.zeros(0, np.int64)
-        recs["perm"][:R] = np.where(plens > 0, ppool.ctypes.data + 4 * poffs, 0)
-        recs["noise_len"][:R] = np.where(plens > 0, plens, recs["noise_len"][:R])
+        # per-record arrays (GF noise, WS permutation) are packed into one pool
+        # each and referenced by address and length; one Python pass per list
+        pool, ppool = _pack(noise, R, np.float32), _pack(perm, R, np.int32)
+        recs["noise"][:R], recs["noise_len"][:R] = pool[1], pool[2]
+        wsr = ppool[2] > 0
+        recs["perm"][:R] = ppool[1]
+        recs["noise_len"][:R][wsr] = ppool[2][wsr]
+        pool, ppool = pool[0], ppool[0]
         assert self.RECORD_DTYPE.itemsize == C.sizeof(mure_record)
         ptr = recs.ctypes.data_as(C.POINTER(mure_record))
         self._keep_params = (pool, ppool)
