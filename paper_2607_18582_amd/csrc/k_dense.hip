@@ -121,8 +121,21 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
       const int k = kc + kv * VEC;
       v4u v = v4u{0u, 0u, 0u, 0u};
       if constexpr (VIRT) {
-        if (crow[j] && k < a.K && kdirect[k / VEC]) {
-          v = *reinterpret_cast<const v4u*>(crow[j] + k);   // unchanged channels: one vector
+        if (crow[j] && k + VEC <= a.K) {
+          // the cached original vector, then only the elements the mutant's
+          // channel map changes (another cached channel, zero, or a delta entry)
+          v = *reinterpret_cast<const v4u*>(crow[j] + k);
+          if (!kdirect[k / VEC]) {
+            T e8[VEC];
+            __builtin_memcpy(e8, &v, 16);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+              const int code = kmap[k + e];
+              if (code != k + e)
+                e8[e] = code >= 0 ? crow[j][code] : code != INT_MIN ? drow[j][-1 - code] : T(0);
+            }
+            __builtin_memcpy(&v, e8, 16);
+          }
         } else if (crow[j]) {
           T e8[VEC];
 #pragma unroll
