@@ -51,6 +51,29 @@ struct DevBuf {
   template <typename T> T* as() const { return reinterpret_cast<T*>(p); }
 };
 
+// Page-locked host staging (hipHostMalloc), grow-only: uploads from it are
+// plain DMA transfers instead of the runtime's pageable-copy path.
+struct PinnedBuf {
+  void* p = nullptr;
+  size_t bytes = 0;
+  PinnedBuf() = default;
+  PinnedBuf(const PinnedBuf&) = delete;
+  PinnedBuf& operator=(const PinnedBuf&) = delete;
+  ~PinnedBuf() {
+    if (p) (void)hipHostFree(p);
+  }
+  hipError_t ensure(size_t n) {
+    if (n <= bytes && p) return hipSuccess;
+    if (p) (void)hipHostFree(p);
+    p = nullptr;
+    bytes = 0;
+    hipError_t e = hipHostMalloc(&p, n < 4096 ? 4096 : n, hipHostMallocDefault);
+    if (e == hipSuccess) bytes = n < 4096 ? 4096 : n;
+    else p = nullptr;
+    return e;
+  }
+};
+
 // Liveness-based placement of per-row activation buffers: offsets in bytes
 // per row; a buffer is reused once every reader of its previous owner ran.
 struct Placement {
@@ -123,21 +146,28 @@ struct mure_ctx {
   Plan plan;
   std::vector<Record> recs;
   DevBuf d_cow;                                       // copy-on-write parameters
-  DevBuf d_tables;                                    // pointer tables
+  // the applied mutants' device tables, uploaded as one block: pointer
+  // tables, slot/touched-list ints, channel maps, delta columns, copy-on-write
+  // arguments, device records and noise
+  DevBuf d_apply;
+  PinnedBuf h_apply;
+  const void** tables = nullptr;
+  int32_t* slotv = nullptr;
+  int32_t* chmapv = nullptr;
+  DeltaCol* colv = nullptr;
   struct GroupTabs {
-    std::map<int, int64_t> w, b;                      // node -> offset (in pointers) into d_tables
-    int64_t slot_mutant = 0;                          // offset (int32) into d_slots
-    int64_t chmap = 0;                                // offset (int32) into d_chmap: [slots][C]
-    int64_t choff = 0;                                // offset (int32) into d_slots: touched-list
+    std::map<int, int64_t> w, b;                      // node -> offset (in pointers) into tables
+    int64_t slot_mutant = 0;                          // offset (int32) into slotv
+    int64_t chmap = 0;                                // offset (int32) into chmapv: [slots][C]
+    int64_t choff = 0;                                // offset (int32) into slotv: touched-list
                                                       // offsets of the recompute slots (+1)
-    int64_t vchmap = 0;                               // offset (int32) into d_chmap: virtual maps
-    int64_t cols = 0;                                 // offset (DeltaCol) into d_cols
+    int64_t vchmap = 0;                               // offset (int32) into chmapv: virtual maps
+    int64_t cols = 0;                                 // offset (DeltaCol) into colv
     std::vector<int64_t> colbeg;                      // first column of each recompute slot (+1)
   };
   std::vector<GroupTabs> gtabs;
   std::map<int, int64_t> orig_w, orig_b;              // node -> offset of 1-entry original tables
-  DevBuf d_slots, d_chmap, d_cols;
-  DevBuf d_cargs, d_drecs, d_noise, d_given;          // upload staging
+  DevBuf d_given;                                     // ground-truth labels
   // prefix cache and original results
   int64_t N = 0;
   std::map<int, std::unique_ptr<DevBuf>> cache;
@@ -715,25 +745,44 @@ mure_status mure_apply_mutants(mure_ctx* ctx, int32_t n_mutants, const mure_reco
         gt.colbeg.push_back((int64_t)cols.size() - gt.cols);
       }
     }
-    HIPTRY(ctx->d_cols.ensure(std::max<size_t>(1, cols.size()) * sizeof(DeltaCol)));
-    HIPTRY(ctx->d_tables.ensure(tabs.size() * sizeof(void*)));
-    HIPTRY(ctx->d_slots.ensure(slots.size() * 4));
-    HIPTRY(ctx->d_chmap.ensure(chmaps.size() * 4));
+    // one upload: every table at a 256-byte aligned offset of one block
+    size_t total = 0;
+    auto section = [&](size_t bytes) {
+      const size_t o = total;
+      total += (bytes + 255) / 256 * 256;
+      return o;
+    };
+    const size_t o_tabs = section(tabs.size() * sizeof(void*));
+    const size_t o_slots = section(slots.size() * 4);
+    const size_t o_chmap = section(chmaps.size() * 4);
+    const size_t o_cols = section(cols.size() * sizeof(DeltaCol));
+    const size_t o_cargs = section(cargs.size() * sizeof(CowArgs));
+    const size_t o_drecs = section(drecs.size() * sizeof(DevRecord));
+    const size_t o_noise = section(noise.size() * 4);
+    HIPTRY(ctx->h_apply.ensure(std::max<size_t>(total, 256)));
+    HIPTRY(ctx->d_apply.ensure(std::max<size_t>(total, 256)));
+    char* h = static_cast<char*>(ctx->h_apply.p);
+    auto put = [&](size_t off, const void* src, size_t bytes) {
+      if (bytes) std::memcpy(h + off, src, bytes);
+    };
+    put(o_tabs, tabs.data(), tabs.size() * sizeof(void*));
+    put(o_slots, slots.data(), slots.size() * 4);
+    put(o_chmap, chmaps.data(), chmaps.size() * 4);
+    put(o_cols, cols.data(), cols.size() * sizeof(DeltaCol));
+    put(o_cargs, cargs.data(), cargs.size() * sizeof(CowArgs));
+    put(o_drecs, drecs.data(), drecs.size() * sizeof(DevRecord));
+    put(o_noise, noise.data(), noise.size() * 4);
     hipStream_t st = ctx->stream;
-    if (!tabs.empty()) HIPTRY(hipMemcpyAsync(ctx->d_tables.p, tabs.data(), tabs.size() * sizeof(void*), hipMemcpyHostToDevice, st));
-    if (!slots.empty()) HIPTRY(hipMemcpyAsync(ctx->d_slots.p, slots.data(), slots.size() * 4, hipMemcpyHostToDevice, st));
-    if (!chmaps.empty()) HIPTRY(hipMemcpyAsync(ctx->d_chmap.p, chmaps.data(), chmaps.size() * 4, hipMemcpyHostToDevice, st));
-    if (!cols.empty()) HIPTRY(hipMemcpyAsync(ctx->d_cols.p, cols.data(), cols.size() * sizeof(DeltaCol), hipMemcpyHostToDevice, st));
-    if (!cargs.empty()) {
-      HIPTRY(ctx->d_cargs.ensure(cargs.size() * sizeof(CowArgs)));
-      HIPTRY(ctx->d_drecs.ensure(drecs.size() * sizeof(DevRecord)));
-      HIPTRY(ctx->d_noise.ensure(noise.size() * 4));
-      HIPTRY(hipMemcpyAsync(ctx->d_cargs.p, cargs.data(), cargs.size() * sizeof(CowArgs), hipMemcpyHostToDevice, st));
-      if (!drecs.empty()) HIPTRY(hipMemcpyAsync(ctx->d_drecs.p, drecs.data(), drecs.size() * sizeof(DevRecord), hipMemcpyHostToDevice, st));
-      if (!noise.empty()) HIPTRY(hipMemcpyAsync(ctx->d_noise.p, noise.data(), noise.size() * 4, hipMemcpyHostToDevice, st));
-      HIPTRY(launch_cow(ctx->d_cargs.as<CowArgs>(), (int)cargs.size(), ctx->d_drecs.as<DevRecord>(),
-                        ctx->d_noise.as<float>(), g.dtype, st));
-    }
+    char* d = ctx->d_apply.as<char>();
+    if (total) HIPTRY(hipMemcpyAsync(d, h, total, hipMemcpyHostToDevice, st));
+    ctx->tables = reinterpret_cast<const void**>(d + o_tabs);
+    ctx->slotv = reinterpret_cast<int32_t*>(d + o_slots);
+    ctx->chmapv = reinterpret_cast<int32_t*>(d + o_chmap);
+    ctx->colv = reinterpret_cast<DeltaCol*>(d + o_cols);
+    if (!cargs.empty())
+      HIPTRY(launch_cow(reinterpret_cast<const CowArgs*>(d + o_cargs), (int)cargs.size(),
+                        reinterpret_cast<const DevRecord*>(d + o_drecs), reinterpret_cast<const float*>(d + o_noise),
+                        g.dtype, st));
     HIPTRY(hipEventRecord(ctx->ev1, ctx->stream));
     HIPTRY(hipEventSynchronize(ctx->ev1));
     float ms = 0.f;
@@ -818,7 +867,7 @@ mure_status mure_run_original(mure_ctx* ctx, const void* inputs_dev, int64_t n_i
   if (cached.count(0))
     HIPTRY(hipMemcpyAsync(ctx->cache[0]->p, inputs_dev, (size_t)(n * g.act_bytes(0)),
                           hipMemcpyDeviceToDevice, ctx->stream));
-  const void* const* tabs = ctx->d_tables.as<const void*>();
+  const void* const* tabs = ctx->tables;
   ctx->stats.launches = 0;
   for (int64_t x0 = 0; x0 < n; x0 += nx) {
     const int cnt = (int)std::min<int64_t>(nx, n - x0);
@@ -906,8 +955,8 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
   HIPTRY(ctx->d_ws.ensure((size_t)(pl.peak * cap_rows)));
   ctx->stats.workspace_bytes = std::max<int64_t>(ctx->stats.workspace_bytes, (int64_t)ctx->d_ws.bytes);
   char* ws = ctx->d_ws.as<char>();
-  const void* const* tabs = ctx->d_tables.as<const void*>();
-  const int32_t* slot_mut = ctx->d_slots.as<int32_t>() + gt.slot_mutant;
+  const void* const* tabs = ctx->tables;
+  const int32_t* slot_mut = ctx->slotv + gt.slot_mutant;
   const Node& nm = g.nodes[mmi];
   const void* mmi_cache = mmi == L ? ctx->d_logits.p : (ctx->cache.count(mmi) ? ctx->cache[mmi]->p : nullptr);
   for (int cs0 = s_begin; cs0 < s_end; cs0 += (int)spc) {
@@ -948,7 +997,7 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
           PatchArgs a;
           a.cache = mmi_cache;
           a.out = out;
-          a.chmap = ctx->d_chmap.as<int32_t>() + gt.chmap;
+          a.chmap = ctx->chmapv + gt.chmap;
           a.slot0 = pa - cs0;
           a.chmap_slot0 = pa;
           a.nx = cnt; a.x0 = (int)x0; a.nslots = cs1 - pa;
@@ -970,10 +1019,10 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
             ex.exec_macs = tl * per_ch * cnt;
             ex.delta_channels = tl;
             if (node_family(g, mmi) == FAM_VALU || node_family(g, mmi) == FAM_DW) {
-              ex.ch_off = ctx->d_slots.as<int32_t>() + gt.choff + cs0;
-              ex.ch_list = ctx->d_slots.as<int32_t>();
+              ex.ch_off = ctx->slotv + gt.choff + cs0;
+              ex.ch_list = ctx->slotv;
             } else {
-              ex.cols = ctx->d_cols.as<DeltaCol>() + gt.cols + gt.colbeg[cs0];
+              ex.cols = ctx->colv + gt.cols + gt.colbeg[cs0];
               ex.ncols = (int)(gt.colbeg[rec_end] - gt.colbeg[cs0]);
               ex.col_slot0 = cs0;
               launch_slots = ex.ncols > 0 ? 1 : 0;
@@ -994,7 +1043,7 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
       VirtualIn vin;
       if (gr.virt) {
         vin.cache = mmi_cache;
-        vin.chmap = ctx->d_chmap.as<int32_t>() + gt.vchmap + (int64_t)cs0 * nm.C;
+        vin.chmap = ctx->chmapv + gt.vchmap + (int64_t)cs0 * nm.C;
         vin.delta = where(mmi).p;
         vin.C = nm.C;
         vin.HW = nm.H * nm.W;
