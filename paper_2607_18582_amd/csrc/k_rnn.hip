@@ -4,7 +4,7 @@
 // blocks of one launch row split over the slots.
 //
 // lstm_kernel: a block owns 64 rows (inputs) of one mutant slot and runs all T
-// steps.  The slot's weights sit in LDS k-major ([D + H + 1][4H]); each wave
+// steps; its waves run independently (each owns 16 rows).  The slot's weights sit in LDS k-major ([D + H + 1][4H]); each wave
 // keeps its 16 rows' step input [x_t, h_{t-1}, 1] in LDS and per step computes
 // the 4H gate pre-activations as one 16 x 4H GEMM on MFMA
 // (v_mfma_f32_16x16x4_f32).  Gate q of unit j is column q*H + j, so with H a
@@ -67,26 +67,78 @@ __global__ __launch_bounds__(256) void lstm_kernel(SeqArgs a) {
 
   const int xi0 = (int)blockIdx.x * 64 + wave * 16;    // this wave's 16 rows
   const float* __restrict__ X = reinterpret_cast<const float*>(a.in.p);
+  float* __restrict__ Y = reinterpret_cast<float*>(a.out);
   float* A = As + wave * 16 * KA;
   float cst[HT][4];
 #pragma unroll
   for (int jj = 0; jj < HT; ++jj)
 #pragma unroll
     for (int e = 0; e < 4; ++e) cst[jj][e] = 0.f;
+  // row r = slot * nx + xi of the chunk: buffer row r, or cache row x0 + xi
+  auto in_row = [&](int xi) {
+    return a.in.mode == MODE_BUF ? (int64_t)sl * a.nx + xi : (int64_t)a.x0 + xi;
+  };
+  auto out_row = [&](int xi) {
+    return a.out_mode == MODE_BUF ? (int64_t)sl * a.nx + xi : (int64_t)a.x0 + xi;
+  };
+
+  // x_t as 16-byte vectors (D % 4 == 0, at most NXV per lane): the vectors of
+  // step t + 1 are loaded during step t, ahead of that step's stores, so
+  // their wait does not include the stores; otherwise one element at a time
+  constexpr int NXV = 4;
+  const int DV = D / 4;
+  const bool xvec = D % 4 == 0 && a.in.row_elems % 4 == 0 && 16 * DV <= 64 * NXV;
+  int64_t xg[NXV];                                     // element offset of the vector at t = 0, or -1
+  int xa[NXV];                                         // its place in A, or -1
+  v4f xr[NXV];
+#pragma unroll
+  for (int u = 0; u < NXV; ++u) {
+    const int e4 = lane + 64 * u;
+    xg[u] = -1;
+    xa[u] = -1;
+    if (xvec && e4 < 16 * DV) {
+      const int rr = e4 / DV, d4 = e4 - rr * DV;
+      xa[u] = rr * KA + d4 * 4;
+      if (xi0 + rr < a.nx) xg[u] = in_row(xi0 + rr) * a.in.row_elems + d4 * 4;
+    }
+  }
+  auto load_x = [&](int t) {
+#pragma unroll
+    for (int u = 0; u < NXV; ++u)
+      if (xg[u] >= 0) xr[u] = *reinterpret_cast<const v4f*>(X + xg[u] + (int64_t)t * D);
+  };
+  if (xvec) load_x(0);
+  // h of the previous step, stored to the output during the next step
+  float hp[HT][4];
+  auto store_h = [&](int t) {
+#pragma unroll
+    for (int jj = 0; jj < HT; ++jj)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int xi = xi0 + (lane >> 4) * 4 + e;
+        if (xi < a.nx)
+          Y[out_row(xi) * a.out_row + (int64_t)(a.seq ? t : 0) * H + jj * 16 + (lane & 15)] = hp[jj][e];
+      }
+  };
 
   for (int t = 0; t < a.T; ++t) {
-    // x_t of the wave's rows
-    for (int e = lane; e < 16 * D; e += 64) {
-      const int rr = e / D, d = e - rr * D;
-      const int xi = xi0 + rr;
-      float v = 0.f;
-      if (xi < a.nx) {
-        const int64_t r = (int64_t)sl * a.nx + xi;
-        v = X[row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems + (int64_t)t * D + d];
+    // x_t of the wave's rows (rows past nx read zeros)
+    if (xvec) {
+#pragma unroll
+      for (int u = 0; u < NXV; ++u)
+        if (xa[u] >= 0) *reinterpret_cast<v4f*>(A + xa[u]) = xg[u] >= 0 ? xr[u] : v4f{0.f, 0.f, 0.f, 0.f};
+      if (t + 1 < a.T) load_x(t + 1);
+    } else {
+      for (int e = lane; e < 16 * D; e += 64) {
+        const int rr = e / D, d = e - rr * D;
+        const int xi = xi0 + rr;
+        float v = 0.f;
+        if (xi < a.nx) v = X[in_row(xi) * a.in.row_elems + (int64_t)t * D + d];
+        A[rr * KA + d] = v;
       }
-      A[rr * KA + d] = v;
     }
-    __syncthreads();
+    // a wave reads and writes only its own 16 rows of A, and one wave's LDS
+    // operations complete in the order they are issued: no block barrier
     v4f acc[NT];
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[j] = v4f{0.f, 0.f, 0.f, 0.f};
@@ -97,7 +149,7 @@ __global__ __launch_bounds__(256) void lstm_kernel(SeqArgs a) {
       for (int j = 0; j < NT; ++j)
         acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, Ws[k * NS + j * 16 + (lane & 15)], acc[j], 0, 0, 0);
     }
-    __syncthreads();                                   // every lane done reading h_{t-1}
+    if (a.seq && t > 0) store_h(t - 1);
     // gates: unit u = 16*jj + (lane & 15), rows 4*(lane >> 4) + e of the wave
 #pragma unroll
     for (int jj = 0; jj < HT; ++jj) {
@@ -111,17 +163,12 @@ __global__ __launch_bounds__(256) void lstm_kernel(SeqArgs a) {
         const float c = fmaf(fg, cst[jj][e], ig * gg);
         cst[jj][e] = c;
         const float h = og * tanhf_(c);
-        const int rr = (lane >> 4) * 4 + e;
-        A[rr * KA + D + u] = h;
-        const int xi = xi0 + rr;
-        if (xi < a.nx && (a.seq || t == a.T - 1)) {
-          const int64_t r = (int64_t)sl * a.nx + xi;
-          const int64_t o = row_index(a.out_mode, r, a.nx, a.x0) * a.out_row + (int64_t)(a.seq ? t : 0) * H + u;
-          reinterpret_cast<float*>(a.out)[o] = h;
-        }
+        A[((lane >> 4) * 4 + e) * KA + D + u] = h;
+        hp[jj][e] = h;
       }
     }
   }
+  if (a.T > 0) store_h(a.T - 1);
 }
 
 hipError_t launch_embed(const SeqArgs& a, hipStream_t s) {
