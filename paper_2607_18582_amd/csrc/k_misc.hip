@@ -43,8 +43,17 @@ __global__ void gap_kernel(GapArgs a) {
     const int64_t r = i / a.C;
     const int c = (int)(i % a.C);
     const T* ip = reinterpret_cast<const T*>(a.in.p) + row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems;
+    // eight loads in flight, then their sums in pixel order
     float s = 0.f;
-    for (int p = 0; p < a.P; ++p) s += to_f<T>(ip[(int64_t)p * a.C + c]);
+    int p = 0;
+    for (; p + 8 <= a.P; p += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = to_f<T>(ip[(int64_t)(p + u) * a.C + c]);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; p < a.P; ++p) s += to_f<T>(ip[(int64_t)p * a.C + c]);
     store_out<T>(a.out, a.out_f32, row_index(a.out_mode, r, a.nx, a.x0) * a.C + c, s * (1.0f / (float)a.P));
   }
 }
@@ -85,22 +94,34 @@ __global__ __launch_bounds__(256) void patch_kernel(PatchArgs a, int rows, DivU3
   const E* src = reinterpret_cast<const E*>(a.cache) + ((int64_t)a.x0 + xi0) * per;
   E* dst = reinterpret_cast<E*>(a.out) + ((int64_t)(a.slot0 + sl) * a.nx + xi0) * per;
   if (vec) {
+    // PB vectors per thread and batch: all loads, then all stores, so a
+    // batch waits once for its loads (and the previous batch's stores)
+    constexpr int PB = 8;
     const int nv = nr * (per / VEC);
-    for (int v = tid; v < nv; v += 256) {
-      const int cv = (int)(v - divu(dcv, (uint32_t)v) * CV);
-      if (keep[cv]) {
-        reinterpret_cast<v4u*>(dst)[v] = reinterpret_cast<const v4u*>(src)[v];
-      } else {
-        const int e0 = v * VEC, pix0 = e0 - cv * VEC;
-        E t[VEC];
+    for (int v0 = tid; v0 < nv; v0 += 256 * PB) {
+      v4u o[PB];
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) {
-          const int m = map[cv * VEC + j];
-          t[j] = m < 0 ? E(0) : src[pix0 + m];
+      for (int u = 0; u < PB; ++u) {
+        const int v = v0 + 256 * u;
+        if (v >= nv) continue;
+        const int cv = (int)(v - divu(dcv, (uint32_t)v) * CV);
+        if (keep[cv]) {
+          o[u] = reinterpret_cast<const v4u*>(src)[v];
+        } else {
+          const int e0 = v * VEC, pix0 = e0 - cv * VEC;
+          E t[VEC];
+#pragma unroll
+          for (int j = 0; j < VEC; ++j) {
+            const int m = map[cv * VEC + j];
+            t[j] = m < 0 ? E(0) : src[pix0 + m];
+          }
+          __builtin_memcpy(&o[u], t, 16);
         }
-        v4u o;
-        __builtin_memcpy(&o, t, 16);
-        reinterpret_cast<v4u*>(dst)[v] = o;
+      }
+#pragma unroll
+      for (int u = 0; u < PB; ++u) {
+        const int v = v0 + 256 * u;
+        if (v < nv) reinterpret_cast<v4u*>(dst)[v] = o[u];
       }
     }
   } else {
