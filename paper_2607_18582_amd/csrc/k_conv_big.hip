@@ -216,7 +216,6 @@ void conv_big_kernel(ConvArgs a) {
         }
       }
       __syncthreads();                                   // the staged tiles are complete
-      const int Pout = a.pool ? a.P / 4 : a.P;
       const int Mout = a.pool ? Mslot / 4 : Mslot;
       const int g0 = (m0 + wm * WM) / (a.pool ? 4 : 1);
       const DivU32 dpo = a.pool ? a.dPq : a.dP;

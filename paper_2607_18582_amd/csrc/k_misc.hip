@@ -209,7 +209,7 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   atomicAdd(&count, cnt);
   __syncthreads();
   if (threadIdx.x == 0) a.kills[m] = (int64_t)count;
-  if (threadIdx.x < a.mask_words) a.masks[m * a.mask_words + threadIdx.x] = mask[threadIdx.x];
+  if ((int)threadIdx.x < a.mask_words) a.masks[m * a.mask_words + threadIdx.x] = mask[threadIdx.x];
 }
 
 // ---------------------------------------------------------------- copy-on-write mutation
