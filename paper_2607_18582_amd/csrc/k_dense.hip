@@ -245,6 +245,39 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs a) {
   }
 
   const int orow = a.cols && a.delta_T > 0 ? a.delta_T : a.Cout;   // elements per output row
+  // fp32 outputs of whole layers (no gathered columns, no fused kill) with
+  // 16-byte aligned rows: each wave stages one 16-column slice of its
+  // tile at a time in the (now idle) weight tile and writes it back as
+  // 16-byte vectors, a quarter of the store instructions of one element per lane
+  constexpr int SST = 20;                                    // floats per staged row
+  if constexpr (sizeof(T) == 4 && LSN == 1 && BN * LD >= 4 * WM * SST) {
+    if (a.write_out && !a.cols && (a.Cout & 3) == 0 && ((uintptr_t)a.out & 15) == 0) {
+      float* const st = reinterpret_cast<float*>(Bs) + wave * WM * SST;
+      float* const out = reinterpret_cast<float*>(a.out);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            st[(i * 16 + (lane >> 4) * 4 + e) * SST + (lane & 15)] = act(acc[i][j][e] + cbias[j], a.relu);
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int p = 0; p < WM * 4 / 64; ++p) {
+          const int idx = p * 64 + lane, r = idx >> 2, q = idx & 3;
+          const v4f v = *reinterpret_cast<const v4f*>(&st[r * SST + q * 4]);
+          const int xo = m0 + wm * WM + r;
+          const int n = n0 + wn * WN + j * 16 + q * 4;
+          if (xo < a.nx && n < a.Cout) {
+            const int64_t ro = a.out_mode == MODE_BUF ? (int64_t)slot * a.nx + xo : (int64_t)a.x0 + xo;
+            *reinterpret_cast<v4f*>(out + ro * a.Cout + n) = v;
+          }
+        }
+        __builtin_amdgcn_wave_barrier();
+      }
+      return;
+    }
+  }
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const int nl = wn * WN + j * 16 + (lane & 15);

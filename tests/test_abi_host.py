@@ -211,3 +211,30 @@ def test_sequence_layer_validation():
     with pytest.raises(B.MureError, match="units"):
         ctx.load_model(bad, m.in_hwc, "f32", m.weights, m.biases)
     ctx.close()
+
+
+def test_record_parameter_packing():
+    """Each record's noise/permutation entry is found at its address with its
+    length; records without one get address 0 and length 0, and an empty
+    entry gets length 0 (the library reads nothing there)."""
+    import ctypes
+    arrays = [np.array([1.5, -2.0], np.float32), None, np.arange(5, dtype=np.float64),
+              np.zeros(0, np.float32), None, np.array([7.0], np.float32)]
+    pool, addr, lens = B._pack(arrays, len(arrays), np.float32)
+    assert pool.dtype == np.float32 and pool.size == 8
+    assert lens.tolist() == [2, 0, 5, 0, 0, 1]
+    assert addr[1] == 0 and addr[3] == 0 and addr[4] == 0
+    for r, a in enumerate(arrays):
+        if a is None or len(a) == 0:
+            continue
+        got = np.ctypeslib.as_array((ctypes.c_float * int(lens[r])).from_address(int(addr[r])))
+        assert np.array_equal(got, a.astype(np.float32)), r
+    pool, addr, lens = B._pack([None, None], 2, np.int32)
+    assert not addr.any() and not lens.any()
+    pool, addr, lens = B._pack(None, 3, np.int32)
+    assert addr.shape == (3,) and not addr.any() and not lens.any()
+    # a single non-empty entry (the itemgetter path for one index)
+    arr = [None, np.array([3, 1, 2], np.int64)]
+    pool, addr, lens = B._pack(arr, 2, np.int32)
+    got = np.ctypeslib.as_array((ctypes.c_int32 * 3).from_address(int(addr[1])))
+    assert got.tolist() == [3, 1, 2] and lens.tolist() == [0, 3]

@@ -248,3 +248,26 @@ def test_fp32_cnn_lds_instances_and_im2col():
     assert np.array_equal(w1, w2) and np.array_equal(k1, k2) and s1 == s2
     for mid in sample_mutants(m1, wl):
         assert np.array_equal(m1.get_logits(mid).cpu().numpy(), m2.get_logits(mid).cpu().numpy()), mid
+
+
+def test_reapply_in_one_context_matches_fresh_contexts():
+    """One context, three mutant sets in turn (larger, smaller with fewer
+    inputs, the first again): each run equals a fresh context's bit for bit,
+    so nothing left over from an earlier apply or input set leaks in."""
+    a = W.make_workload("lenet5", n_inputs=300, n_mutants=40, ops=(W.GF, W.NEB, W.NAI, W.NS, W.WS))
+    b = W.make_workload("lenet5", n_inputs=130, n_mutants=12, ops=(W.GF, W.NAI))
+    fresh = {}
+    for wl in (a, b):
+        fm, fw, fk, fs = run_gpu(wl)
+        fresh[wl.mutants.n_mutants] = (fw, fk, fs, [fm.get_logits(i).cpu().numpy() for i in (0, 5, -1)])
+    m = gpu_context(a)
+    for wl in (a, b, a):
+        log(f"[reapply] M={wl.mutants.n_mutants} N={wl.n_inputs}")
+        m.apply(wl.mutants)
+        m.run_original(device_inputs(wl))
+        kb, kills, score = m.run_mutants()
+        fw, fk, fs, fz = fresh[wl.mutants.n_mutants]
+        assert np.array_equal(kb.cpu().numpy().view(np.uint64), fw)
+        assert np.array_equal(kills, fk) and score == fs
+        for i, z in zip((0, 5, -1), fz):
+            assert np.array_equal(m.get_logits(i).cpu().numpy(), z), i
