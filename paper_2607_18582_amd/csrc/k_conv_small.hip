@@ -721,12 +721,19 @@ hipError_t launch_valu(const ValuArgs& a, int dtype, hipStream_t s) {
   const bool spec = a.kh == 5 && a.kw == 5 && a.C == 1 && a.stride == 1 && a.pool;
   if (spec && a.ch_off && a.ch_list && a.in.mode == MODE_CACHE && a.pad == 0 && a.in.row_elems == a.H * a.W &&
       !a.out_f32) {
-    // channel lists over the shared cached input: slot groups share staged images
-    const size_t lds2 = ((size_t)R * a.H * a.W + (size_t)VALU_SPB * a.Cout * 25) * sizeof(float);
+    // channel lists over the shared cached input: slot groups share staged
+    // images.  A slot lists at most delta_T channels when it writes compact
+    // delta rows, so the weight section holds VALU_SPB * min(C_out, delta_T)
+    // channels; with at most 4 images per block the LDS stays near 22 KB
+    // and seven blocks share a CU (the FMA chains wait on LDS and global
+    // latency, which more resident waves hide)
+    const int cmax = a.delta_T > 0 ? std::min(a.Cout, a.delta_T) : a.Cout;
+    const int R2 = std::min(R, 4);
+    const size_t lds2 = ((size_t)R2 * a.H * a.W + (size_t)VALU_SPB * cmax * 25) * sizeof(float);
     if (lds2 <= 64 * 1024) {
-      dim3 g2((unsigned)((a.nx + R - 1) / R), (unsigned)((a.nslots + VALU_SPB - 1) / VALU_SPB));
-      if (dtype == 0) hipLaunchKernelGGL(conv_valu_slots_kernel<float>, g2, dim3(256), lds2, s, a, R);
-      else hipLaunchKernelGGL(conv_valu_slots_kernel<bf16_t>, g2, dim3(256), lds2, s, a, R);
+      dim3 g2((unsigned)((a.nx + R2 - 1) / R2), (unsigned)((a.nslots + VALU_SPB - 1) / VALU_SPB));
+      if (dtype == 0) hipLaunchKernelGGL(conv_valu_slots_kernel<float>, g2, dim3(256), lds2, s, a, R2);
+      else hipLaunchKernelGGL(conv_valu_slots_kernel<bf16_t>, g2, dim3(256), lds2, s, a, R2);
       return hipGetLastError();
     }
   }
