@@ -30,8 +30,12 @@ typedef __attribute__((address_space(1))) const v4u gv4u;
 // The tap of each group is the same for the whole wavefront, so its index
 // math runs once per wave on the scalar unit and each row needs one bounds
 // check and one address per group.
+//
+// The 128-row tiles are compiled for three (BN = 128: 138 VGPRs instead of
+// 172) and five (BN = 64: 92 instead of 116) resident waves per SIMD, without
+// spills; their LDS (37 and 28 KB per block) admits that many blocks.
 template <int BM, int BN, int WAVES_M, int WAVES_N, int G>
-__global__ __launch_bounds__(64 * WAVES_M * WAVES_N)
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N, BM == 128 && BN == 128 ? 3 : BM == 128 && BN == 64 ? 5 : 1)
 void conv_big_kernel(ConvArgs a) {
   constexpr int THREADS = 64 * WAVES_M * WAVES_N;
   constexpr int BK = BIG_BK, LD = BIG_LD;
