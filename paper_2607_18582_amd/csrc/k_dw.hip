@@ -142,9 +142,11 @@ __global__ __launch_bounds__(256) void dw_full_kernel(DwArgs a, int rows, DivU32
 // the previous one (one for stride 1, two for stride 2), requested before the
 // current row's arithmetic.  The chains are the full kernel's: taps in (dy, dx)
 // order from 0, then the bias.  No LDS: a thread's filters come from global
-// memory once.
+// memory once.  In bf16 they stay packed in registers and are widened at
+// each use (127 and 151 VGPRs for stride 1 and 2, four and three waves per
+// SIMD, against 176 and 200 with the widened filters held: two).
 template <typename T, int S>
-__global__ __launch_bounds__(256) void dw_col_kernel(DwArgs a, int tasks, DivU32 dcv, DivU32 dwo) {
+__global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 1) void dw_col_kernel(DwArgs a, int tasks, DivU32 dcv, DivU32 dwo) {
   constexpr int VEC = 16 / sizeof(T);
   constexpr int NNEW = S == 1 ? 1 : 2;                 // new input rows per output row
   const int sl = a.slot0 + (int)blockIdx.y;
@@ -160,15 +162,12 @@ __global__ __launch_bounds__(256) void dw_col_kernel(DwArgs a, int tasks, DivU32
   // the thread's channels' filters ([C][3][3]: VEC * 9 consecutive elements),
   // kept in the node type and widened at each use, and biases, straight from
   // global memory (L2-resident, shared by every column of the slot)
-  T wv[VEC * 9];
+  v4u wraw[9];
   float b[VEC];
   {
     const T* __restrict__ wsrc = reinterpret_cast<const T*>(a.wtab[sl]) + (int64_t)cv * VEC * 9;
 #pragma unroll
-    for (int q = 0; q < 9; ++q) {
-      const v4u raw = reinterpret_cast<const v4u*>(wsrc)[q];
-      __builtin_memcpy(&wv[q * VEC], &raw, 16);
-    }
+    for (int q = 0; q < 9; ++q) wraw[q] = reinterpret_cast<const v4u*>(wsrc)[q];
     const float* __restrict__ bsrc = a.btab[sl] + cv * VEC;
 #pragma unroll
     for (int j = 0; j < VEC; ++j) b[j] = bsrc[j];
@@ -198,6 +197,14 @@ __global__ __launch_bounds__(256) void dw_col_kernel(DwArgs a, int tasks, DivU32
     const int iy2 = (oy + 2) * S - a.pad + 3 - NNEW;  // first new row of output row oy + 2
 #pragma unroll
     for (int k = 0; k < NNEW; ++k) load_row(iy2 + k, nr2[k]);
+    // the filters stay packed across rows: hoisting their widening out of
+    // the row loop would hold them as VEC * 9 floats
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int q = 0; q < 9; ++q) asm volatile("" : "+v"(wraw[q]));
+    }
+    T wv[VEC * 9];
+    __builtin_memcpy(wv, wraw, sizeof(wv));
     float acc[VEC];
 #pragma unroll
     for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
