@@ -40,6 +40,8 @@ extern "C" {
 
 #define MURE_VERSION 3
 #define MURE_N_KERNELS 9   /* kernel families in mure_stats */
+/* Device scratch of mure_run_mutants_noalloc: a fixed array per GPU. */
+#define MURE_NOALLOC_SCRATCH_BYTES (256u << 20)
 
 typedef struct mure_ctx mure_ctx;
 
@@ -247,6 +249,26 @@ mure_status mure_run_original(mure_ctx* ctx, const void* inputs_dev, int64_t n_i
  * Errors: MURE_E_STATE unless run_original ran after the last apply_mutants. */
 mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* kills_host,
                              mure_score* score);
+
+/* mure_run_mutants for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels, outputs and errors, but the call allocates
+ * nothing.  Its chunk activation workspace and the per-mutant kill counts and
+ * label masks live in one file-scope device array of
+ * MURE_NOALLOC_SCRATCH_BYTES per GPU, set up by mure_create and held until
+ * the process ends; chunks of inputs and mutants are sized to fit it.
+ * Differences from mure_run_mutants:
+ *   - kill_bits_dev is required (the caller's output buffer);
+ *   - per-launch timing (option "kernel_timing") is skipped;
+ *   - every call on one GPU shares that GPU's array, so calls that overlap
+ *     on one GPU (contexts on different host threads or streams) race:
+ *     serialise them.
+ * Errors: as mure_run_mutants; MURE_E_INVALID for kill_bits_dev == NULL;
+ * MURE_E_NOMEM, before any device work, when the smallest chunk of some
+ * cluster (one mutant x min(64, n) inputs) or the counters need more than
+ * MURE_NOALLOC_SCRATCH_BYTES. */
+mure_status mure_run_mutants_noalloc(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* kills_host,
+                                     mure_score* score);
 
 /* Logits of one mutant (or of the original for mutant_id = -1) over all
  * inputs: device float32 [n][classes].  Runs that mutant's suffix alone with

@@ -29,7 +29,8 @@ OP_GAUSS_FUZZ, OP_EFFECT_BLOCK, OP_ACT_INVERSE, OP_NEURON_SWITCH, OP_WEIGHT_SHUF
 INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV, EMBED, LSTM = 0, 1, 2, 3, 4, 5, 6, 7, 8
 
 EXPORTED = ["mure_version", "mure_create", "mure_load_model", "mure_apply_mutants",
-            "mure_run_original", "mure_run_mutants", "mure_get_logits", "mure_mutant_plan",
+            "mure_run_original", "mure_run_mutants", "mure_run_mutants_noalloc",
+            "mure_get_logits", "mure_mutant_plan",
             "mure_get_stats", "mure_set_option", "mure_last_error", "mure_destroy"]
 
 
@@ -121,6 +122,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
         "mure_apply_mutants": (C.c_int, [P, C.c_int32, C.POINTER(mure_record), C.c_int64]),
         "mure_run_original": (C.c_int, [P, P, C.c_int64, C.POINTER(C.c_int32)]),
         "mure_run_mutants": (C.c_int, [P, P, C.POINTER(C.c_int64), C.POINTER(mure_score)]),
+        "mure_run_mutants_noalloc": (C.c_int, [P, P, C.POINTER(C.c_int64), C.POINTER(mure_score)]),
         "mure_get_logits": (C.c_int, [P, C.c_int32, P]),
         "mure_mutant_plan": (C.c_int, [P, C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_int32),
                                        C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_int32)]),
@@ -256,9 +258,10 @@ class Mure:
         self._check(self.lib.mure_run_original(self.ctx, C.c_void_p(inputs.data_ptr()), n, lp))
         self.n_inputs = n
 
-    def run_mutants(self, kill_bits=None):
+    def run_mutants(self, kill_bits=None, noalloc: bool = False):
         """Returns (kill_bits [M][ceil(N/64)] int64 CUDA tensor holding the uint64
-        words, kills per mutant (numpy int64), score dict)."""
+        words, kills per mutant (numpy int64), score dict).  noalloc: call
+        mure_run_mutants_noalloc (the library allocates no device memory)."""
         import torch
         nw = (self.n_inputs + 63) // 64
         if kill_bits is None:
@@ -266,9 +269,9 @@ class Mure:
                                     device=f"cuda:{self.device}")
         kills = np.zeros(max(self.n_mutants, 1), np.int64)
         sc = mure_score()
-        self._check(self.lib.mure_run_mutants(self.ctx, C.c_void_p(kill_bits.data_ptr()),
-                                              kills.ctypes.data_as(C.POINTER(C.c_int64)),
-                                              C.byref(sc)))
+        fn = self.lib.mure_run_mutants_noalloc if noalloc else self.lib.mure_run_mutants
+        self._check(fn(self.ctx, C.c_void_p(kill_bits.data_ptr()),
+                       kills.ctypes.data_as(C.POINTER(C.c_int64)), C.byref(sc)))
         score = {k: getattr(sc, k) for k, _ in mure_score._fields_}
         return kill_bits[: self.n_mutants], kills[: self.n_mutants], score
 

@@ -351,4 +351,16 @@ hipError_t launch_copy_rows(const TensorArg& src, void* dst, int64_t rows, int n
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- zero fill
+__global__ __launch_bounds__(256) void zero_u64_kernel(uint64_t* p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = 0;
+}
+
+hipError_t launch_zero_u64(uint64_t* p, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(zero_u64_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, n);
+  return hipGetLastError();
+}
+
 }  // namespace mure

@@ -270,5 +270,11 @@ hipError_t launch_cow(const CowArgs* d_args, int n_copies, const DevRecord* d_re
                       const float* d_noise, int dtype, hipStream_t s);
 hipError_t launch_copy_rows(const TensorArg& src, void* dst, int64_t rows, int nx, int x0,
                             int esize, hipStream_t s);
+hipError_t launch_zero_u64(uint64_t* p, int64_t n, hipStream_t s);   // p[0 .. n) = 0
+
+// Device address of this GPU's scratch array of MURE_NOALLOC_SCRATCH_BYTES
+// (the allocation-free run_mutants); looked up once per device, which must be
+// current.
+hipError_t noalloc_scratch(int device, void** out);
 
 }  // namespace mure

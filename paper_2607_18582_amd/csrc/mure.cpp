@@ -175,6 +175,7 @@ struct mure_ctx {
   int64_t n_labels = 0;
   // run_mutants scratch
   DevBuf d_ws, d_kill, d_kills, d_masks;
+  void* scratch = nullptr;                            // this GPU's scratch array (noalloc entry)
   // options
   int64_t max_ws_mb = 16384;
   int64_t chunk_inputs = 0;
@@ -474,6 +475,8 @@ mure_status mure_create(mure_ctx** out, int32_t device, void* hip_stream) {
     if (e != hipSuccess) { g_create_error = std::string("hipSetDevice: ") + hipGetErrorString(e); return MURE_E_DEVICE; }
     ctx->device = device;
     ctx->stream = reinterpret_cast<hipStream_t>(hip_stream);
+    e = noalloc_scratch(device, &ctx->scratch);
+    if (e != hipSuccess) { g_create_error = std::string("scratch address: ") + hipGetErrorString(e); return MURE_E_DEVICE; }
     if (hipEventCreate(&ctx->ev0) != hipSuccess || hipEventCreate(&ctx->ev1) != hipSuccess) {
       g_create_error = "hipEventCreate failed";
       return MURE_E_DEVICE;
@@ -927,34 +930,71 @@ mure_status mure_run_original(mure_ctx* ctx, const void* inputs_dev, int64_t n_i
 }
 
 // -------------------------------------------------------------------------
+// Chunking of group gi's suffix: per-row buffer placement, inputs per chunk
+// (nx) and mutant slots per chunk (spc) for a workspace budget in bytes.  The
+// budget is a soft cap: the smallest chunk (one slot x min(64, N) inputs) is
+// used even when it needs more (need_bytes tells).
+}  // extern "C"
+namespace {
+struct ChunkGeom {
+  Placement pl;
+  std::map<int, int> fused_adds;                     // conv_b -> ADD run as one launch
+  int64_t nx = 0, spc = 0, cap_rows = 0, need_bytes = 0;
+};
+
+ChunkGeom group_geometry(const mure_ctx* ctx, int gi, int nslots, int64_t budget) {
+  const Graph& g = ctx->g;
+  const Group& gr = ctx->plan.groups[gi];
+  const int L = g.out(), mmi = gr.mmi;
+  const int64_t N = ctx->N;
+  ChunkGeom cg;
+  std::vector<int> nodes;
+  for (int v = mmi; v <= L; ++v) nodes.push_back(v);
+  for (int v = mmi + 1; v <= L; ++v) {
+    const int fa = ctx->fused ? fused_add_of(g, v) : -1;
+    if (fa >= 0) cg.fused_adds[v] = fa;
+  }
+  cg.pl = place_buffers(g, nodes, {}, cg.fused_adds);
+  const int64_t peak = std::max<int64_t>(cg.pl.peak, 1);
+  int64_t nx = N;
+  if (ctx->chunk_inputs) nx = std::min<int64_t>(nx, ctx->chunk_inputs);
+  if (peak * nx > budget) nx = std::max<int64_t>(64, budget / peak / 64 * 64);
+  if (nx > N) nx = N;
+  int64_t spc = std::max<int64_t>(1, budget / (peak * nx));
+  spc = std::min<int64_t>(spc, std::min<int64_t>(65535, std::max(nslots, 1)));
+  spc = std::min<int64_t>(spc, std::max<int64_t>(1, ((int64_t)1 << 31) / nx / 64));
+  cg.nx = nx;
+  cg.spc = spc;
+  cg.cap_rows = spc * nx;
+  cg.need_bytes = cg.pl.peak * cg.cap_rows;
+  return cg;
+}
+}  // namespace
+extern "C" {
+
 // The suffix of group gi for its slots [s_begin, s_end), over all inputs.
+// ws == nullptr: the context's workspace, grown as needed; otherwise ws holds
+// ws_bytes and the chunks are sized to fit it (MURE_E_NOMEM if they cannot).
 static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint64_t* kill_words,
-                             float* logits_out) {
+                             float* logits_out, char* ws = nullptr, int64_t ws_bytes = 0) {
   const Graph& g = ctx->g;
   const Group& gr = ctx->plan.groups[gi];
   const mure_ctx::GroupTabs& gt = ctx->gtabs[gi];
   const int L = g.out(), mmi = gr.mmi;
   const int64_t N = ctx->N;
-  std::vector<int> nodes;
-  for (int v = mmi; v <= L; ++v) nodes.push_back(v);
-  std::map<int, int> fused_adds;                       // conv_b -> ADD run as one launch
-  for (int v = mmi + 1; v <= L; ++v) {
-    const int fa = ctx->fused ? fused_add_of(g, v) : -1;
-    if (fa >= 0) fused_adds[v] = fa;
+  int64_t budget = ctx->max_ws_mb << 20;
+  if (ws) budget = std::min(budget, ws_bytes);
+  const ChunkGeom cg = group_geometry(ctx, gi, s_end - s_begin, budget);
+  const Placement& pl = cg.pl;
+  const std::map<int, int>& fused_adds = cg.fused_adds;
+  const int64_t nx = cg.nx, spc = cg.spc, cap_rows = cg.cap_rows;
+  if (ws) {
+    if (cg.need_bytes > ws_bytes) return ctx->fail(MURE_E_NOMEM, "chunk workspace exceeds the scratch array");
+  } else {
+    HIPTRY(ctx->d_ws.ensure((size_t)cg.need_bytes));
+    ctx->stats.workspace_bytes = std::max<int64_t>(ctx->stats.workspace_bytes, (int64_t)ctx->d_ws.bytes);
+    ws = ctx->d_ws.as<char>();
   }
-  Placement pl = place_buffers(g, nodes, {}, fused_adds);
-  const int64_t budget = ctx->max_ws_mb << 20;
-  int64_t nx = N;
-  if (ctx->chunk_inputs) nx = std::min<int64_t>(nx, ctx->chunk_inputs);
-  if (pl.peak * nx > budget) nx = std::max<int64_t>(64, budget / pl.peak / 64 * 64);
-  if (nx > N) nx = N;
-  int64_t spc = std::max<int64_t>(1, budget / (pl.peak * nx));
-  spc = std::min<int64_t>(spc, std::min<int64_t>(65535, s_end - s_begin));
-  spc = std::min<int64_t>(spc, std::max<int64_t>(1, ((int64_t)1 << 31) / nx / 64));
-  const int64_t cap_rows = spc * nx;
-  HIPTRY(ctx->d_ws.ensure((size_t)(pl.peak * cap_rows)));
-  ctx->stats.workspace_bytes = std::max<int64_t>(ctx->stats.workspace_bytes, (int64_t)ctx->d_ws.bytes);
-  char* ws = ctx->d_ws.as<char>();
   const void* const* tabs = ctx->tables;
   const int32_t* slot_mut = ctx->slotv + gt.slot_mutant;
   const Node& nm = g.nodes[mmi];
@@ -1108,21 +1148,62 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
   return MURE_OK;
 }
 
-mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* kills_host, mure_score* score) {
+}  // extern "C"
+
+// Both run_mutants entry points.  noalloc: the kill words are the caller's,
+// and the workspace, kill counts and label masks live in this GPU's scratch
+// array; no device memory is allocated and no launch is timed.
+static mure_status run_mutants_impl(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* kills_host,
+                                    mure_score* score, bool noalloc) {
   if (!ctx) return MURE_E_INVALID;
   if (ctx->plan_only) return ctx->fail(MURE_E_UNSUPPORTED, "planning-only context");
   if (ctx->state != 3) return ctx->fail(MURE_E_STATE, "run_original must run after the last apply_mutants");
+  if (noalloc && !kill_bits_dev) return ctx->fail(MURE_E_INVALID, "kill_bits_dev is NULL");
   HIPTRY(hipSetDevice(ctx->device));
   const int64_t M = ctx->plan.n_mutants, N = ctx->N, nwords = (N + 63) / 64;
   const int C = ctx->g.classes();
   const int mw = (C + 63) / 64;
   uint64_t* kw = kill_bits_dev;
-  if (!kw) {
-    if ((size_t)(M * nwords * 8) > ctx->d_kill.bytes) HIPTRY(ctx->d_kill.alloc((size_t)std::max<int64_t>(M * nwords * 8, 8)));
-    kw = ctx->d_kill.as<uint64_t>();
+  int64_t* d_kills = nullptr;
+  unsigned long long* d_masks = nullptr;
+  char* ws = nullptr;
+  int64_t ws_bytes = 0;
+  if (noalloc) {
+    // [kill counts | label masks | chunk workspace], 256-byte aligned parts
+    if (!ctx->scratch) return ctx->fail(MURE_E_DEVICE, "no scratch array on this device");
+    const int64_t kb = (M * 8 + 255) / 256 * 256, mb = (M * mw * 8 + 255) / 256 * 256;
+    const int64_t total = (int64_t)MURE_NOALLOC_SCRATCH_BYTES;
+    if (kb + mb >= total) return ctx->fail(MURE_E_NOMEM, "kill counters exceed the scratch array");
+    char* base = static_cast<char*>(ctx->scratch);
+    d_kills = reinterpret_cast<int64_t*>(base);
+    d_masks = reinterpret_cast<unsigned long long*>(base + kb);
+    ws = base + kb + mb;
+    ws_bytes = total - kb - mb;
+    // refuse before any device work if some cluster's smallest chunk does not fit
+    for (int gi = 0; gi < (int)ctx->plan.groups.size(); ++gi) {
+      const int ns = (int)ctx->plan.groups[gi].mutants.size();
+      const ChunkGeom cg = group_geometry(ctx, gi, ns, std::min(ws_bytes, ctx->max_ws_mb << 20));
+      if (cg.need_bytes > ws_bytes)
+        return ctx->fail(MURE_E_NOMEM, "cluster " + std::to_string(gi) + " needs " + std::to_string(cg.need_bytes) +
+                                           " bytes of workspace per chunk; the scratch array holds " +
+                                           std::to_string(ws_bytes));
+    }
+  } else {
+    if (!kw) {
+      if ((size_t)(M * nwords * 8) > ctx->d_kill.bytes) HIPTRY(ctx->d_kill.alloc((size_t)std::max<int64_t>(M * nwords * 8, 8)));
+      kw = ctx->d_kill.as<uint64_t>();
+    }
+    if ((size_t)(M * 8) > ctx->d_kills.bytes) HIPTRY(ctx->d_kills.alloc((size_t)std::max<int64_t>(M * 8, 8)));
+    if ((size_t)(M * mw * 8) > ctx->d_masks.bytes) HIPTRY(ctx->d_masks.alloc((size_t)std::max<int64_t>(M * mw * 8, 8)));
+    d_kills = ctx->d_kills.as<int64_t>();
+    d_masks = ctx->d_masks.as<unsigned long long>();
   }
-  if ((size_t)(M * 8) > ctx->d_kills.bytes) HIPTRY(ctx->d_kills.alloc((size_t)std::max<int64_t>(M * 8, 8)));
-  if ((size_t)(M * mw * 8) > ctx->d_masks.bytes) HIPTRY(ctx->d_masks.alloc((size_t)std::max<int64_t>(M * mw * 8, 8)));
+  const int64_t timing = ctx->kernel_timing;
+  if (noalloc) ctx->kernel_timing = 0;
+  struct Restore {
+    mure_ctx* c; int64_t t;
+    ~Restore() { c->kernel_timing = t; }
+  } restore{ctx, timing};
   ctx->stats.launches = 0;
   ctx->stats.gemm_launches = 0;
   ctx->stats.ms_gemm = 0;
@@ -1137,10 +1218,16 @@ mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* ki
   ctx->tevents_used = 0;
   ctx->tevent_family.clear();
   HIPTRY(hipEventRecord(ctx->ev0, ctx->stream));
-  HIPTRY(hipMemsetAsync(ctx->d_nonfinite.p, 0, 8, ctx->stream));
-  if (M > 0) HIPTRY(hipMemsetAsync(kw, 0, (size_t)(M * nwords * 8), ctx->stream));
+  if (noalloc) {
+    // zero fills as kernels (no memset nodes in work a caller may capture)
+    HIPTRY(launch_zero_u64(reinterpret_cast<uint64_t*>(ctx->d_nonfinite.p), 1, ctx->stream));
+    if (M > 0) HIPTRY(launch_zero_u64(kw, M * nwords, ctx->stream));
+  } else {
+    HIPTRY(hipMemsetAsync(ctx->d_nonfinite.p, 0, 8, ctx->stream));
+    if (M > 0) HIPTRY(hipMemsetAsync(kw, 0, (size_t)(M * nwords * 8), ctx->stream));
+  }
   for (int gi = 0; gi < (int)ctx->plan.groups.size(); ++gi) {
-    mure_status st = run_group(ctx, gi, 0, (int)ctx->plan.groups[gi].mutants.size(), kw, nullptr);
+    mure_status st = run_group(ctx, gi, 0, (int)ctx->plan.groups[gi].mutants.size(), kw, nullptr, ws, ws_bytes);
     if (st != MURE_OK) return st;
   }
   ScoreArgs sa;
@@ -1149,8 +1236,8 @@ mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* ki
   sa.N = N;
   sa.label = ctx->d_label.as<int32_t>();
   sa.mask_words = mw;
-  sa.kills = ctx->d_kills.as<int64_t>();
-  sa.masks = ctx->d_masks.as<unsigned long long>();
+  sa.kills = d_kills;
+  sa.masks = d_masks;
   HIPTRY(launch_score(sa, (int)M, ctx->stream));
   HIPTRY(hipEventRecord(ctx->ev1, ctx->stream));
   HIPTRY(hipEventSynchronize(ctx->ev1));
@@ -1168,8 +1255,8 @@ mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* ki
   std::vector<unsigned long long> masks(M * mw);
   unsigned long long nonfinite = 0;
   if (M > 0) {
-    HIPTRY(hipMemcpy(kills.data(), ctx->d_kills.p, (size_t)(M * 8), hipMemcpyDeviceToHost));
-    HIPTRY(hipMemcpy(masks.data(), ctx->d_masks.p, (size_t)(M * mw * 8), hipMemcpyDeviceToHost));
+    HIPTRY(hipMemcpy(kills.data(), d_kills, (size_t)(M * 8), hipMemcpyDeviceToHost));
+    HIPTRY(hipMemcpy(masks.data(), d_masks, (size_t)(M * mw * 8), hipMemcpyDeviceToHost));
   }
   HIPTRY(hipMemcpy(&nonfinite, ctx->d_nonfinite.p, 8, hipMemcpyDeviceToHost));
   int64_t num = 0, killed = 0;
@@ -1194,6 +1281,17 @@ mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* ki
   ctx->stats.macs_algorithmic = ctx->plan.macs_algorithmic * N;
   ctx->stats.macs_executed = ctx->plan.macs_executed * N;
   return MURE_OK;
+}
+
+extern "C" {
+
+mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* kills_host, mure_score* score) {
+  return run_mutants_impl(ctx, kill_bits_dev, kills_host, score, false);
+}
+
+mure_status mure_run_mutants_noalloc(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* kills_host,
+                                     mure_score* score) {
+  return run_mutants_impl(ctx, kill_bits_dev, kills_host, score, true);
 }
 
 mure_status mure_get_logits(mure_ctx* ctx, int32_t mutant_id, float* out_dev) {
