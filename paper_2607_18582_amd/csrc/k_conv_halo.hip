@@ -1,267 +1,385 @@
-// bf16 3x3 convolutions with stride 1 and padding 1 (C_in % 16 == 0, image
-// width 8, 16, 32 or 64) as an implicit GEMM on MFMA whose operands both come
-// from LDS (v_mfma_f32_16x16x32_bf16).
+// bf16 3x3 convolutions with stride 1 and padding 1 (C_in % 16 == 0, square
+// images of width 8, 16, 32 or 64) as an implicit GEMM on MFMA
+// (v_mfma_f32_32x32x16_bf16) whose operands both come from LDS.
 //
-// Block tile: 512 output pixels x BN output channels, eight waves of 64 rows
-// (one block per CU: the LDS stages below take most of it).  The pixels are
-// TR = 512 / W consecutive image rows -- a band of one image, or 512 / (H W)
-// whole images -- so a tile never mixes two images' borders.
+// Tile: 512 output pixels x BN = 32 TN output channels, four waves of 128
+// pixels x BN channels (4 x TN accumulator tiles of 32 x 32), two blocks per
+// CU (one wave per SIMD each).  The pixels are TR = 512 / W consecutive image
+// rows -- a band of one image, or 512 / (H W) whole images -- so a tile never
+// mixes two images' borders.
+//
 // The input channels go in chunks of 16.  Per chunk the block stages in LDS
 // (a) the band's input rows plus a one-pixel border (the halo, zero outside
-// the image): every input element crosses the memory pipeline once per block
-// and chunk instead of once per tap as an im2col gather would; and (b) the
-// chunk's weights for the tile's columns.  One MFMA k-step of 32 covers two
-// taps of the chunk (taps 2p and 2p+1; a tenth, all-zero tap pads the
-// ninth), so a chunk is five k-steps.  The stages are double-buffered in LDS
-// and fetched into registers two chunks ahead: the k loop has one barrier per
-// chunk and no global loads of its own.
+// the image), stored as two halves of 8 channels, [half][halo pixel][8]: every
+// input element crosses the memory pipeline once per block and chunk instead
+// of once per tap as an im2col gather would; and (b) the chunk's weights for
+// the tile's columns, [tap][half][column][8].  One MFMA k-step of 16 is one
+// tap of the chunk, so a chunk is nine k-steps, and the A fragment of a tap is
+// the lane's halo entry at a constant offset: the operand reads take
+// immediate offsets.  Both fragments of a k-step are 32 consecutive 16-byte
+// entries per half wave (conflict-free LDS reads).  Within a chunk the
+// fragments of tap t + 1 are read before the MFMAs of tap t are issued.
 //
-// Reduction order: k = (chunk of 16 channels, tap pair, tap, channel), fixed
-// for a node shape; every launch of a node (full rows or gathered delta
-// columns) uses it.
+// The stages are fetched with direct global-to-LDS loads (16 bytes per lane,
+// landing at consecutive LDS addresses per instruction), so staging takes no
+// registers; they are double-buffered: the loads of chunk c + 1 are issued
+// before the MFMAs of chunk c and waited for after them, one barrier per
+// chunk.
+//
+// One tile per block.  The epilogue (bias, activation, bf16 rounding) stages
+// the tile in LDS and stores whole output rows as 16-byte vectors, with a
+// fused ADD (identity or option-A shortcut) or a fused 2x2 max-pool, or the
+// gathered delta columns.
+//
+// Reduction order: k = (chunk of 16 channels, tap, channel), fixed for a node
+// shape; every launch of a node (full rows or gathered delta columns) uses it.
 #include "dev.hpp"
 #include "plan.hpp"
 
 namespace mure {
 
 namespace {
-constexpr int HALO_PS = 24;                            // LDS pixel stride: 16 channels + 8 (bf16)
-constexpr int HALO_ELEMS = HALO_MAXPX * HALO_PS;       // halo part of a stage (elements)
-typedef __attribute__((address_space(1))) const v4u gv4u;
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Compile-time geometry of an instance (image width W, TN column tiles).
+template <int W, int TN>
+struct HaloGeo {
+  static constexpr int NT = 256, BM = 512, TR = BM / W, W2 = W + 2, BN = 32 * TN;
+  static constexpr int NPX = conv_halo_cap(W);          // halo pixels a stage holds
+  static constexpr int HSTR = NPX * 16;                 // bytes of one channel half of the halo
+  static constexpr int HALO_B = 2 * HSTR;
+  static constexpr int B_B = 9 * 2 * BN * 16;           // weights: [tap][half][column][8]
+  static constexpr int STAGE = HALO_B + B_B;
+  static constexpr int NQH = (NPX + 63) / 64;           // load instructions per halo half
+  static constexpr int NQ_HALO = 2 * NQH;
+  static constexpr int NQ = NQ_HALO + 9 * 2 * BN / 64;  // load instructions per chunk
+  static constexpr int QPW = (NQ + 3) / 4;              // ... per wave
+  static constexpr int OLD = BN + 8;                    // staged output row (bf16)
+  static constexpr int VPR = BN / 8;                    // 16-byte vectors per output row
+};
+
+struct HaloTile {
+  int slot, n0, xi0, y0;
+};
+
+// Tile t -> (slot, band, column block).  Consecutive tiles go round-robin to
+// the 8 XCDs (block b runs on XCD b % 8); on one XCD the column blocks of a
+// band take consecutive turns and share its L2 copy of the band's input.
+// false: t is padding of that order.
+template <int W, int TN>
+__device__ __forceinline__ bool halo_decode(const ConvArgs& a, int t, HaloTile& tl) {
+  using G = HaloGeo<W, TN>;
+  const int bgroups = (a.bands + 7) / 8;
+  const int xcd = t & 7, turn = t >> 3, per_slot = bgroups * a.zblocks;
+  const int si = turn / per_slot, rem = turn % per_slot;
+  const int band = (rem / a.zblocks) * 8 + xcd;
+  if (band >= a.bands) return false;
+  tl.slot = a.slot0 + si;
+  tl.n0 = (rem % a.zblocks) * G::BN;
+  const int64_t r0 = (int64_t)band * G::TR;             // first row of the flattened (input, row) axis
+  tl.xi0 = (int)(r0 / a.H);
+  tl.y0 = (int)(r0 % a.H);
+  return true;
 }
 
-// Zero bytes that out-of-image halo pixels and the padding tap read.
-static __device__ __attribute__((aligned(16))) v4u g_halo_zero[4] = {};
-
-template <int W, int BN>
-__global__ __launch_bounds__(512)
-void conv_halo_kernel(ConvArgs a) {
-  constexpr int NT = 512, BM = 512, TR = BM / W, W2 = W + 2;
-  constexpr int TM = 4, TN = BN / 16;                  // a wave: 64 rows x BN columns
-  constexpr int B_ELEMS = 5 * BN * 32;                 // weight part of a stage: [pair][column][32]
-  constexpr int STAGE = HALO_ELEMS + B_ELEMS;
-  constexpr int OLD = BN + 8;                          // staged output row (bf16)
-  constexpr int LDS_ELEMS = 2 * STAGE > BM * OLD ? 2 * STAGE : BM * OLD;
-  constexpr int HV = (HALO_MAXPX * 2 + NT - 1) / NT;   // halo vectors per thread and chunk
-  constexpr int BV = (5 * BN * 4 + NT - 1) / NT;       // weight vectors per thread and chunk
-  __shared__ __attribute__((aligned(16))) bf16_t smem[LDS_ELEMS];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int slot = a.slot0 + (int)blockIdx.y;
-  // XCD-aware order: consecutive blocks go round-robin to the 8 XCDs, so block
-  // b runs on XCD b % 8; the column blocks of one band take consecutive turns
-  // on the same XCD and share its L2 copy of the band's input
-  const int bx = (int)blockIdx.x, xcd = bx & 7, turn = bx >> 3;
-  const int band = (turn / a.zblocks) * 8 + xcd;
-  if (band >= a.bands) return;                           // padding of the order (whole block)
-  const int n0 = (turn % a.zblocks) * BN;
+// The lane's sources for this wave's load instructions q = wave + 4 s of a
+// tile, at chunk 0 (nullptr: zeros).  q < NQ_HALO fills halo half q / NQH,
+// pixels 64 (q % NQH) + lane; the others fill 64 consecutive
+// [tap][half][column] weight entries.
+template <int W, int TN>
+__device__ __forceinline__ void halo_sources(const ConvArgs& a, const HaloTile& tl, int RI, int npx, int wave,
+                                             int lane, const bf16_t* (&src)[HaloGeo<W, TN>::QPW]) {
+  using G = HaloGeo<W, TN>;
   const int ncol = a.cols ? a.ncols : a.Cout;
-  // the band: image rows [r0, r0 + TR) of the flattened (input, row) axis;
-  // RI rows of each of IMGS images (RI = H when whole images are packed)
-  const int RI = a.H < TR ? a.H : TR;
-  const int IMGS = TR / RI;
-  const int64_t r0 = (int64_t)band * TR;
-  const int xi0 = (int)(r0 / a.H), y0 = (int)(r0 % a.H);
-  const int npx = IMGS * (RI + 2) * W2;                // halo pixels (<= HALO_MAXPX, checked by the launcher)
-  const bf16_t* const zp = reinterpret_cast<const bf16_t*>(g_halo_zero);
-
-  // halo vectors of this thread: vector v = tid + NT j is pixel v / 2,
-  // channels (v % 2) * 8 .. + 8 of the chunk, at element offset hoff[j] from
-  // the band's first input row (consecutive inputs are consecutive rows in
-  // both tensor modes); -1 reads zeros, -2 is past the halo (not stored)
-  const bf16_t* const in0 = reinterpret_cast<const bf16_t*>(a.in.p) +
-                            row_index(a.in.mode, (int64_t)slot * a.nx + (xi0 < a.nx ? xi0 : 0), a.nx, a.x0) *
-                                a.in.row_elems;
-  int hoff[HV];
+  const bf16_t* in0 = reinterpret_cast<const bf16_t*>(a.in.p) +
+                      row_index(a.in.mode, (int64_t)tl.slot * a.nx + (tl.xi0 < a.nx ? tl.xi0 : 0), a.nx, a.x0) *
+                          a.in.row_elems;
 #pragma unroll
-  for (int j = 0; j < HV; ++j) {
-    const int v = tid + NT * j;
-    const int px = v >> 1, h = v & 1;
-    hoff[j] = -2;
-    if (px < npx) {
-      hoff[j] = -1;
-      const int im = px / ((RI + 2) * W2), rem = px % ((RI + 2) * W2);
-      const int hy = rem / W2, hx = rem % W2;
-      const int y = y0 + hy - 1, x = hx - 1;
-      if (xi0 + im < a.nx && (unsigned)y < (unsigned)a.H && (unsigned)x < (unsigned)W)
-        hoff[j] = (int)(im * a.in.row_elems) + (y * W + x) * a.C + h * 8;
-    }
-  }
-  // weight vectors of this thread: vector v = tid + NT j is tap pair p,
-  // column n, quarter q (8 of the pair's 32 k: tap 2p + q / 2, channels
-  // (q % 2) * 8 ..); bsrc is its source at chunk 0 (nullptr: zeros), bdst its
-  // LDS slot, the quarter rotated by (n / 4) % 4 so that the 16 lanes reading
-  // one quarter of 16 consecutive columns hit distinct banks
-  const bf16_t* bsrc[BV];
-  int bdst[BV];
-#pragma unroll
-  for (int j = 0; j < BV; ++j) {
-    const int v = tid + NT * j;
-    const int p = v / (BN * 4), rem = v % (BN * 4);
-    const int n = rem >> 2, q = rem & 3;
-    const int tap = 2 * p + (q >> 1);
-    bsrc[j] = nullptr;
-    bdst[j] = -1;
-    if (p < 5) {
-      bdst[j] = ((p * BN + n) * 4 + (q ^ ((n >> 2) & 3))) * 8;
-      const int nc = n0 + n;
-      if (tap < 9 && nc < ncol) {
+  for (int s = 0; s < G::QPW; ++s) {
+    const int q = wave + 4 * s;
+    src[s] = nullptr;
+    if (q < G::NQ_HALO) {
+      const int hh = q / G::NQH, px = (q % G::NQH) * 64 + lane;
+      const int im = px / ((RI + 2) * G::W2), rem = px % ((RI + 2) * G::W2);
+      const int y = tl.y0 + rem / G::W2 - 1, x = rem % G::W2 - 1;
+      if (px < npx && tl.xi0 + im < a.nx && (unsigned)y < (unsigned)a.H && (unsigned)x < (unsigned)W)
+        src[s] = in0 + im * a.in.row_elems + (y * W + x) * a.C + hh * 8;
+    } else if (q < G::NQ) {
+      const int e = (q - G::NQ_HALO) * 64 + lane;
+      const int tap = e / (2 * G::BN), hh = (e / G::BN) & 1, nc = tl.n0 + e % G::BN;
+      if (nc < ncol) {
         const bf16_t* row;
         if (a.cols) {
           const DeltaCol cd = a.cols[nc];
           row = reinterpret_cast<const bf16_t*>(a.wtab[a.slot0 + cd.slot - a.col_slot0]) + (int64_t)cd.c * a.K;
         } else {
-          row = reinterpret_cast<const bf16_t*>(a.wtab[slot]) + (int64_t)nc * a.K;
+          row = reinterpret_cast<const bf16_t*>(a.wtab[tl.slot]) + (int64_t)nc * a.K;
         }
-        bsrc[j] = row + tap * a.C + (q & 1) * 8;
+        src[s] = row + tap * a.C + hh * 8;
       }
     }
   }
-  // one chunk's staging registers
-  struct Regs { v4u h[HV], b[BV]; };
-  auto fetch = [&](Regs& r, int c0) {
-#pragma unroll
-    for (int j = 0; j < HV; ++j) r.h[j] = *(const gv4u*)(hoff[j] >= 0 ? in0 + hoff[j] + c0 : zp);
-#pragma unroll
-    for (int j = 0; j < BV; ++j) r.b[j] = *(const gv4u*)(bsrc[j] ? bsrc[j] + c0 : zp);
-  };
-  auto stage = [&](const Regs& r, int buf) {
-    bf16_t* st = smem + buf * STAGE;
-#pragma unroll
-    for (int j = 0; j < HV; ++j) {
-      const int v = tid + NT * j;
-      if (hoff[j] != -2) *reinterpret_cast<v4u*>(&st[(v >> 1) * HALO_PS + (v & 1) * 8]) = r.h[j];
-    }
-#pragma unroll
-    for (int j = 0; j < BV; ++j)
-      if (bdst[j] >= 0) *reinterpret_cast<v4u*>(&st[HALO_ELEMS + bdst[j]]) = r.b[j];
-  };
+}
 
-  // A fragment bases: lane row (lane & 15) of M tile i is band pixel m; the
-  // lane's 8 k are channels (q % 2) * 8 of tap 2p + q / 2 (q = lane >> 4), so
-  // its halo pixel is the pair's first tap shifted by 0 or by the distance to
-  // the second tap: 1 pixel (pairs 0, 2, 3), W + 2 - 2 pixels (pair 1: taps
-  // 2 and 3 change row), 0 (pair 4: the zero tap, any finite value)
-  const int q = lane >> 4;
-  int abase0[TM], abase1[TM], abase2[TM];
+// Issue the loads of the chunk at channel c0 into the stage at st.  Lanes
+// past the halo load nothing.
+template <int W, int TN>
+__device__ __forceinline__ void halo_fetch(unsigned char* st, const bf16_t* const (&src)[HaloGeo<W, TN>::QPW],
+                                           int npx, int wave, int lane, int c0, const bf16_t* zp) {
+  using G = HaloGeo<W, TN>;
 #pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int m = wave * 64 + i * 16 + (lane & 15);
+  for (int s = 0; s < G::QPW; ++s) {
+    const int q = wave + 4 * s;
+    if (q >= G::NQ) continue;
+    const bool halo = q < G::NQ_HALO;
+    const int off = halo ? (q / G::NQH) * G::HSTR + (q % G::NQH) * 1024 : G::HALO_B + (q - G::NQ_HALO) * 1024;
+    if (!halo || (q % G::NQH) * 64 + lane < npx)
+      __builtin_amdgcn_global_load_lds((const void*)(src[s] ? src[s] + c0 : zp), (lds_void*)(st + off), 16, 0, 0);
+  }
+}
+
+// Fragment bases: lane row (lane & 31) of M tile i is band pixel m, its 8 k
+// are channels 8 h of the chunk (h = lane >> 5); tap (dy, dx) adds the
+// constant (dy W2 + dx) entries.
+template <int W, int TN>
+__device__ __forceinline__ void halo_abase(int wave, int lane, int RI, int (&abase)[4]) {
+  using G = HaloGeo<W, TN>;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = wave * 128 + i * 32 + (lane & 31);
     const int row = m / W, x = m % W;
-    const int im = row / RI, y = row % RI;
-    abase0[i] = ((im * (RI + 2) + y) * W2 + x) * HALO_PS + (q & 1) * 8;
-    abase1[i] = abase0[i] + (q >> 1) * HALO_PS;
-    abase2[i] = abase0[i] + (q >> 1) * (W2 - 2) * HALO_PS;
+    abase[i] = (lane >> 5) * G::HSTR + (((row / RI) * (RI + 2) + row % RI) * G::W2 + x) * 16;
   }
-  // B fragment: column j * 16 + (lane & 15), quarter q, rotated as stored
-  const int bbase = ((lane & 15) * 4 + (q ^ ((lane >> 2) & 3))) * 8;
+}
 
-  v4f acc[TM][TN];
+// The nine k-steps of the chunk staged at st (B: column j 32 + (lane & 31),
+// half h).
+template <int W, int TN>
+__device__ __forceinline__ void halo_mma(const unsigned char* st, const int (&abase)[4], int bbase,
+                                         v16f (&acc)[4][TN]) {
+  using G = HaloGeo<W, TN>;
+  v8bf fa[2][4], fb[2][TN];
+  auto load = [&](int t, int p) {
+    const int toff = ((t / 3) * G::W2 + t % 3) * 16;
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < 4; ++i) fa[p][i] = *reinterpret_cast<const v8bf*>(st + abase[i] + toff);
 #pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
-
-  auto compute = [&](int buf) {
-    const bf16_t* st = smem + buf * STAGE;
+    for (int j = 0; j < TN; ++j) fb[p][j] = *reinterpret_cast<const v8bf*>(st + bbase + (t * 2 * G::BN + j * 32) * 16);
+  };
+  load(0, 0);
 #pragma unroll
-    for (int p = 0; p < 5; ++p) {
-      const int t0 = 2 * p;
-      const int toff = ((t0 / 3) * W2 + (t0 % 3)) * HALO_PS;
-      v8bf av[TM], bv[TN];
+  for (int t = 0; t < 9; ++t) {
+    if (t < 8) load(t + 1, (t + 1) & 1);
+    __builtin_amdgcn_sched_barrier(0);                 // keep those reads ahead of the MFMAs
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int base = p == 1 ? abase2[i] : p == 4 ? abase0[i] : abase1[i];
-        av[i] = *reinterpret_cast<const v8bf*>(&st[base + toff]);
-      }
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        bv[j] = *reinterpret_cast<const v8bf*>(&st[HALO_ELEMS + (p * BN + j * 16) * 32 + bbase]);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
-    }
-  };
-
-  // chunks c = 0 .. nch-1 through buffers c % 2; registers RA / RB hold the
-  // chunks two ahead (fetches past the last chunk reload it, unused, so that
-  // every path keeps the same requests in flight)
-  const int nch = a.C / 16;
-  auto cidx = [&](int c) { return (c < nch ? c : nch - 1) * 16; };
-  Regs RA, RB;
-  fetch(RA, 0);
-  stage(RA, 0);
-  fetch(RA, cidx(1));
-  fetch(RB, cidx(2));
-  __syncthreads();
-  // pairs of chunks, straight-line (the same requests in flight on every
-  // path); past the last chunk the stores write a reloaded chunk nobody reads
-  int c = 0;
-  for (; c + 1 < nch; c += 2) {
-    compute(0);
-    stage(RA, 1);
-    fetch(RA, cidx(c + 3));
-    __syncthreads();
-    compute(1);
-    stage(RB, 0);
-    fetch(RB, cidx(c + 4));
-    __syncthreads();
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[t & 1][i], fb[t & 1][j], acc[i][j], 0, 0, 0);
   }
-  if (c < nch) compute(0);                             // odd chunk count: the last one
-  __syncthreads();
+}
 
-  // ---- epilogue: bias, activation, bf16 rounding, staged in LDS ----
-  bf16_t* Os = smem;                                   // [BM][OLD]
+// Bias, activation and bf16 rounding of a wave's accumulators, packed in
+// pairs of rows (e, e + 1).
+template <int TN>
+__device__ __forceinline__ void halo_round(const ConvArgs& a, const HaloTile& tl, int lane,
+                                           const v16f (&acc)[4][TN], uint32_t (&ob)[4][TN][8]) {
+  const int ncol = a.cols ? a.ncols : a.Cout;
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
-    const int nl = j * 16 + (lane & 15);
-    const int nc = n0 + nl;
+    const int nc = tl.n0 + j * 32 + (lane & 31);
     float bv = 0.f;
     if (nc < ncol) {
       if (a.cols) {
         const DeltaCol cd = a.cols[nc];
         bv = a.btab[a.slot0 + cd.slot - a.col_slot0][cd.c];
       } else {
-        bv = a.btab[slot][nc];
+        bv = a.btab[tl.slot][nc];
       }
     }
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        Os[(wave * 64 + i * 16 + (lane >> 4) * 4 + e) * OLD + nl] = f2bf(act(acc[i][j][e] + bv, a.relu));
+      for (int e = 0; e < 16; e += 2)
+        ob[i][j][e >> 1] = f2bf2(act(acc[i][j][e] + bv, a.relu), act(acc[i][j][e + 1] + bv, a.relu));
+  }
+}
+
+// A wave's 128 rounded pixels into the staging tile Os ([pixel][OLD]) from
+// row r0 on.
+template <int W, int TN>
+__device__ __forceinline__ void halo_stage(bf16_t* Os, int r0, int lane, const uint32_t (&ob)[4][TN][8]) {
+  using G = HaloGeo<W, TN>;
+  const int h = lane >> 5;
+#pragma unroll
+  for (int j = 0; j < TN; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; e += 2) {
+        const int r = r0 + i * 32 + (e >> 2) * 8 + h * 4 + (e & 3);
+        const uint32_t v = ob[i][j][e >> 1];
+        Os[r * G::OLD + j * 32 + (lane & 31)] = (bf16_t)v;
+        Os[(r + 1) * G::OLD + j * 32 + (lane & 31)] = (bf16_t)(v >> 16);
+      }
+}
+
+// band pixel m -> (input xi, image row y, column x)
+template <int W>
+__device__ __forceinline__ void halo_pixel(const HaloTile& tl, int RI, int m, int& xi, int& y, int& x) {
+  const int row = m / W;
+  x = m % W;
+  xi = tl.xi0 + row / RI;
+  y = tl.y0 + row % RI;
+}
+
+// A fused ADD's shortcut vectors for the output vectors idx = tid + NT k of
+// the pixels [m0, m0 + PB) (pixel idx / VPR, channels 8 (idx % VPR)),
+// requested before the staging so that their latency overlaps it.
+template <int W, int TN, int PB>
+__device__ __forceinline__ void halo_skip(const ConvArgs& a, const HaloTile& tl, int RI, int m0, int tid,
+                                          v4u (&skipv)[PB * HaloGeo<W, TN>::VPR / HaloGeo<W, TN>::NT]) {
+  using G = HaloGeo<W, TN>;
+  constexpr int NV = PB * G::VPR / G::NT;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int idx = tid + G::NT * k, m = m0 + idx / G::VPR, n = tl.n0 + (idx % G::VPR) * 8;
+    int xi, y, x;
+    halo_pixel<W>(tl, RI, m, xi, y, x);
+    skipv[k] = v4u{0u, 0u, 0u, 0u};
+    if (n >= a.Cout || xi >= a.nx) continue;
+    const bf16_t* sp = reinterpret_cast<const bf16_t*>(a.skip.p) +
+                       row_index(a.skip.mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0) * a.skip.row_elems;
+    if (a.add_mode == 1) {
+      skipv[k] = *reinterpret_cast<const v4u*>(sp + ((int64_t)y * W + x) * a.Cout + n);
+    } else {
+      // option A: the skip subsampled by 2 and zero-padded in channels; with
+      // the padding and C_s multiples of 8 a vector is wholly inside or out
+      const int cs0 = n - (a.Cout - a.Cs) / 2;
+      const bf16_t* px = sp + ((int64_t)(2 * y) * a.Ws + 2 * x) * a.Cs;
+      if (((a.Cout - a.Cs) / 2) % 8 == 0 && a.Cs % 8 == 0) {
+        if (cs0 >= 0 && cs0 < a.Cs) skipv[k] = *reinterpret_cast<const v4u*>(px + cs0);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int cs = cs0 + e;
+          if (cs >= 0 && cs < a.Cs) skipv[k][e >> 1] |= (uint32_t)px[cs] << (16 * (e & 1));
+        }
+      }
+    }
+  }
+}
+
+// Whole output rows of the pixels [m0, m0 + PB) staged in Os (local row
+// m - m0), with the ADD's shortcut (add_mode 1 or 2) added in float32 before
+// its activation: thread tid stores the vectors idx = tid + NT k.
+template <int W, int TN, int PB>
+__device__ __forceinline__ void halo_store_rows(const ConvArgs& a, const HaloTile& tl, int RI, int m0, int tid,
+                                                const bf16_t* Os, int add_mode,
+                                                const v4u (&skipv)[PB * HaloGeo<W, TN>::VPR / HaloGeo<W, TN>::NT]) {
+  using G = HaloGeo<W, TN>;
+  constexpr int NV = PB * G::VPR / G::NT;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int idx = tid + G::NT * k, ml = idx / G::VPR, vc = idx % G::VPR;
+    const int n = tl.n0 + vc * 8;
+    if (n >= a.Cout) continue;
+    int xi, y, x;
+    halo_pixel<W>(tl, RI, m0 + ml, xi, y, x);
+    if (xi >= a.nx) continue;
+    v4u val = *reinterpret_cast<const v4u*>(&Os[ml * G::OLD + vc * 8]);
+    if (add_mode) {
+      const v4u sv = skipv[k];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float t0 = act(bf2f((bf16_t)val[w]) + bf2f((bf16_t)sv[w]), a.add_relu);
+        const float t1 = act(bf2f((bf16_t)(val[w] >> 16)) + bf2f((bf16_t)(sv[w] >> 16)), a.add_relu);
+        val[w] = f2bf2(t0, t1);
+      }
+    }
+    const int64_t ro = row_index(a.out_mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0);
+    *reinterpret_cast<v4u*>(reinterpret_cast<bf16_t*>(a.out) + ro * a.out_row + ((int64_t)y * W + x) * a.Cout + n) =
+        val;
+  }
+}
+}  // namespace
+
+// Zero bytes that out-of-image halo pixels and columns past the last read.
+static __device__ __attribute__((aligned(16))) v4u g_halo_zero[4] = {};
+
+// Two blocks per CU fit in LDS except for width 8 with 64 columns (88 KB).
+template <int W, int TN>
+__global__ __launch_bounds__(256, W == 8 && TN == 2 ? 1 : 2)
+void conv_halo_kernel(ConvArgs a) {
+  using G = HaloGeo<W, TN>;
+  constexpr int BM = G::BM, NT = G::NT, BN = G::BN, OLD = G::OLD, VPR = G::VPR;
+  constexpr int NV = BM * VPR / NT;
+  constexpr int LDS_B = 2 * G::STAGE > BM * OLD * 2 ? 2 * G::STAGE : BM * OLD * 2;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_B];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  HaloTile tl;
+  if (!halo_decode<W, TN>(a, (int)blockIdx.x, tl)) return;   // padding of the order (whole block)
+  const int ncol = a.cols ? a.ncols : a.Cout;
+  const int RI = a.H < G::TR ? a.H : G::TR;
+  const int npx = (G::TR / RI) * (RI + 2) * G::W2;
+  const bf16_t* const zp = reinterpret_cast<const bf16_t*>(g_halo_zero);
+  const int nch = a.C / 16;
+
+  const bf16_t* src[G::QPW];
+  halo_sources<W, TN>(a, tl, RI, npx, wave, lane, src);
+  int abase[4];
+  halo_abase<W, TN>(wave, lane, RI, abase);
+  const int bbase = G::HALO_B + ((lane >> 5) * BN + (lane & 31)) * 16;
+  v16f acc[4][TN];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  halo_fetch<W, TN>(smem, src, npx, wave, lane, 0, zp);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  for (int c = 0; c < nch; ++c) {
+    if (c + 1 < nch) halo_fetch<W, TN>(smem + ((c + 1) & 1) * G::STAGE, src, npx, wave, lane, (c + 1) * 16, zp);
+    halo_mma<W, TN>(smem + (c & 1) * G::STAGE, abase, bbase, acc);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  }
+
+  // ---- epilogue: bias, activation, bf16 rounding, staged in LDS ----
+  v4u skipv[NV];
+  if (!a.cols && !a.pool && a.add_mode) halo_skip<W, TN, BM>(a, tl, RI, 0, tid, skipv);
+  {
+    uint32_t ob[4][TN][8];
+    halo_round<TN>(a, tl, lane, acc, ob);
+    halo_stage<W, TN>(reinterpret_cast<bf16_t*>(smem), wave * 128, lane, ob);
   }
   __syncthreads();
-
-  // band pixel m -> (input xi, image row y, column x)
-  auto pixel = [&](int m, int& xi, int& y, int& x) {
-    const int row = m / W;
-    x = m % W;
-    xi = xi0 + row / RI;
-    y = y0 + row % RI;
-  };
+  const bf16_t* Os = reinterpret_cast<const bf16_t*>(smem);   // [BM][OLD]
+  auto pixel = [&](int m, int& xi, int& y, int& x) { halo_pixel<W>(tl, RI, m, xi, y, x); };
   if (a.cols) {
     // gathered columns: each column has its own slot and channel
     const int PX = a.pool ? BM / 4 : BM;
     for (int idx = tid; idx < PX * BN; idx += NT) {
-      const int nl = idx / PX, p = idx % PX;
-      const int nc = n0 + nl;
+      const int nl = idx / PX, q = idx % PX;
+      const int nc = tl.n0 + nl;
       if (nc >= ncol) continue;
       int xi, y, x;
       float v;
       if (a.pool) {
-        // pooled pixel p: band rows 2 (p / (W/2)) .. +1, columns 2 (p % (W/2)) .. +1
-        const int pr = p / (W / 2), pc = p % (W / 2);
-        const int m = 2 * pr * W + 2 * pc;
+        // pooled pixel q: band rows 2 (q / (W/2)) .. +1, columns 2 (q % (W/2)) .. +1
+        const int m = 2 * (q / (W / 2)) * W + 2 * (q % (W / 2));
         pixel(m, xi, y, x);
         v = fmaxf(fmaxf(bf2f(Os[m * OLD + nl]), bf2f(Os[(m + 1) * OLD + nl])),
                   fmaxf(bf2f(Os[(m + W) * OLD + nl]), bf2f(Os[(m + W + 1) * OLD + nl])));
         y >>= 1; x >>= 1;
       } else {
-        pixel(p, xi, y, x);
-        v = bf2f(Os[p * OLD + nl]);
+        pixel(q, xi, y, x);
+        v = bf2f(Os[q * OLD + nl]);
       }
       if (xi >= a.nx) continue;
       const DeltaCol cd = a.cols[nc];
@@ -274,14 +392,12 @@ void conv_halo_kernel(ConvArgs a) {
     }
     return;
   }
-  constexpr int VPR = BN / 8;                          // 16-byte vectors per staged row
   if (a.pool) {
     for (int idx = tid; idx < (BM / 4) * VPR; idx += NT) {
-      const int p = idx / VPR, vc = idx % VPR;
-      const int n = n0 + vc * 8;
+      const int q = idx / VPR, vc = idx % VPR;
+      const int n = tl.n0 + vc * 8;
       if (n >= a.Cout) continue;
-      const int pr = p / (W / 2), pc = p % (W / 2);
-      const int m = 2 * pr * W + 2 * pc;
+      const int m = 2 * (q / (W / 2)) * W + 2 * (q % (W / 2));
       int xi, y, x;
       pixel(m, xi, y, x);
       if (xi >= a.nx) continue;
@@ -295,69 +411,33 @@ void conv_halo_kernel(ConvArgs a) {
       for (int w = 0; w < 4; ++w) {
         uint32_t r = 0;
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int sh = 16 * h;
+        for (int hh = 0; hh < 2; ++hh) {
+          const int sh = 16 * hh;
           const float f = fmaxf(fmaxf(bf2f((bf16_t)(q0[w] >> sh)), bf2f((bf16_t)(q1[w] >> sh))),
                                 fmaxf(bf2f((bf16_t)(q2[w] >> sh)), bf2f((bf16_t)(q3[w] >> sh))));
           r |= (uint32_t)f2bf(f) << sh;
         }
         o[w] = r;
       }
-      const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xi, a.nx, a.x0);
+      const int64_t ro = row_index(a.out_mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0);
       *reinterpret_cast<v4u*>(reinterpret_cast<bf16_t*>(a.out) + ro * a.out_row +
                               ((int64_t)(y >> 1) * (W / 2) + (x >> 1)) * a.Cout + n) = o;
     }
     return;
   }
-  for (int idx = tid; idx < BM * VPR; idx += NT) {
-    const int m = idx / VPR, vc = idx % VPR;
-    const int n = n0 + vc * 8;
-    if (n >= a.Cout) continue;
-    int xi, y, x;
-    pixel(m, xi, y, x);
-    if (xi >= a.nx) continue;
-    const int64_t q = (int64_t)y * W + x;
-    v4u val = *reinterpret_cast<const v4u*>(&Os[m * OLD + vc * 8]);
-    if (a.add_mode) {
-      // the rounded convolution + the shortcut, in float32, then the ADD's activation
-      const bf16_t* sp = reinterpret_cast<const bf16_t*>(a.skip.p) +
-                         row_index(a.skip.mode, (int64_t)slot * a.nx + xi, a.nx, a.x0) * a.skip.row_elems;
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        uint32_t o = 0;
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int c = n + 2 * w + h;
-          float s = 0.f;
-          if (a.add_mode == 1) {
-            s = bf2f(sp[q * a.Cout + c]);
-          } else {
-            // option A: the skip subsampled by 2 and zero-padded in channels
-            const int cs = c - (a.Cout - a.Cs) / 2;
-            if (cs >= 0 && cs < a.Cs) s = bf2f(sp[((int64_t)(2 * y) * a.Ws + 2 * x) * a.Cs + cs]);
-          }
-          const float t = act(bf2f((bf16_t)(val[w] >> (16 * h))) + s, a.add_relu);
-          o |= (uint32_t)f2bf(t) << (16 * h);
-        }
-        val[w] = o;
-      }
-    }
-    const int64_t ro = row_index(a.out_mode, (int64_t)slot * a.nx + xi, a.nx, a.x0);
-    *reinterpret_cast<v4u*>(reinterpret_cast<bf16_t*>(a.out) + ro * a.out_row + q * a.Cout + n) = val;
-  }
+  halo_store_rows<W, TN, BM>(a, tl, RI, 0, tid, Os, a.add_mode, skipv);
 }
 
-int conv_halo_bn(int cout) { return cout <= 16 ? 16 : cout <= 32 ? 32 : 64; }
+int conv_halo_bn(int cout) { return cout <= 32 ? 32 : 64; }
 
+namespace {
 template <int W>
-static hipError_t launch_halo_w(const ConvArgs& a, dim3 grid, int bn, hipStream_t s) {
-  switch (bn) {
-    case 16: hipLaunchKernelGGL((conv_halo_kernel<W, 16>), grid, dim3(512), 0, s, a); break;
-    case 32: hipLaunchKernelGGL((conv_halo_kernel<W, 32>), grid, dim3(512), 0, s, a); break;
-    default: hipLaunchKernelGGL((conv_halo_kernel<W, 64>), grid, dim3(512), 0, s, a); break;
-  }
+hipError_t launch_halo_w(const ConvArgs& a, int bn, int tiles, hipStream_t s) {
+  if (bn == 32) hipLaunchKernelGGL((conv_halo_kernel<W, 1>), dim3((unsigned)tiles), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((conv_halo_kernel<W, 2>), dim3((unsigned)tiles), dim3(256), 0, s, a);
   return hipGetLastError();
 }
+}  // namespace
 
 hipError_t launch_conv_halo(const ConvArgs& a0, int nslots, hipStream_t s) {
   if (nslots <= 0 || a0.nx <= 0) return hipSuccess;
@@ -372,15 +452,16 @@ hipError_t launch_conv_halo(const ConvArgs& a0, int nslots, hipStream_t s) {
   const int bn = conv_halo_bn(ncol);
   const int64_t bands = ((int64_t)a.nx * a.H + TR - 1) / TR;
   const int zb = (ncol + bn - 1) / bn;
-  if ((bands + 7) / 8 * 8 * zb >= (1 << 30)) return hipErrorInvalidValue;
+  const int64_t tiles = (bands + 7) / 8 * 8 * zb * nslots;
+  if (tiles >= (1 << 30)) return hipErrorInvalidValue;
   a.bands = (int)bands;
   a.zblocks = zb;
-  dim3 grid((unsigned)((bands + 7) / 8 * 8 * zb), (unsigned)nslots, 1);
+  a.halo_slots = nslots;
   switch (a.W) {
-    case 8: return launch_halo_w<8>(a, grid, bn, s);
-    case 16: return launch_halo_w<16>(a, grid, bn, s);
-    case 32: return launch_halo_w<32>(a, grid, bn, s);
-    default: return launch_halo_w<64>(a, grid, bn, s);
+    case 8: return launch_halo_w<8>(a, bn, (int)tiles, s);
+    case 16: return launch_halo_w<16>(a, bn, (int)tiles, s);
+    case 32: return launch_halo_w<32>(a, bn, (int)tiles, s);
+    default: return launch_halo_w<64>(a, bn, (int)tiles, s);
   }
 }
 

@@ -98,7 +98,7 @@ struct ConvArgs {
   // padded image size; the halo kernel's band count and column blocks per
   // band (XCD-aware order)
   DivU32 dP, dPq, dWp, dWc, dHW, dC, dKW, dImg;
-  int bands = 0, zblocks = 1;
+  int bands = 0, zblocks = 1, halo_slots = 1;
 };
 
 // DENSE on MFMA: out[r][n] = sum_k in[r][k] * W[n][k] + b[n] (k in increasing
