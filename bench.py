@@ -363,7 +363,7 @@ def main():
                  "launches_run_mutants": st["launches"]},
     }
     if args.gain if args.gain is not None else args.config in ("mlp", "lenet5"):
-        # the paper's measure (Section 6.2): gain = (t_v - t) / t_v with every
+        # the paper's measure (Section 5.2): gain = (t_v - t) / t_v with every
         # overhead in both times; vanilla = the same library with memoization off
         m.set_option("vanilla", 1)
         for _ in range(args.warmup):

@@ -5,12 +5,12 @@
  * set, running each mutant only from its earliest mutated layer (mmi) onward
  * on activations of the original model cached in device memory, and reduces
  * the outputs to a kill matrix and a mutation score.  By the paper's
- * soundness theorem (Section 5.1, Theorem 1) this equals running every mutant
+ * soundness theorem (Section 4.1, Theorem 1) this equals running every mutant
  * from the raw input ("vanilla" mutation testing).
  *
  * The calls follow the problem statement of Algorithm 1 (inputs: a model M,
  * a test set X and a mapping from mutant ids to mutants; output: every
- * mutant's outputs on X) and the measures of Section 6.2 (kill predicate,
+ * mutant's outputs on X) and the measures of Section 5.2 (kill predicate,
  * killingLabels, mutation score):
  *
  *   mure_create -> mure_load_model -> mure_apply_mutants -> mure_run_original
@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define MURE_VERSION 3
+#define MURE_VERSION 4
 #define MURE_N_KERNELS 9   /* kernel families in mure_stats */
 /* Device scratch of mure_run_mutants_noalloc: a fixed array per GPU. */
 #define MURE_NOALLOC_SCRATCH_BYTES (256u << 20)
@@ -140,7 +140,7 @@ typedef struct {
   const int32_t* perm;  /* WEIGHT_SHUFFLE: host, a permutation of 0..fan_in-1; else NULL */
 } mure_record;
 
-/* Mutation score (Section 6.2): MS = ms_num / ms_den with
+/* Mutation score (Section 5.2): MS = ms_num / ms_den with
  * ms_num = sum over mutants of |killingLabels(mutant)| and
  * ms_den = n_mutants * n_labels. */
 typedef struct {
@@ -185,6 +185,11 @@ typedef struct {
    * prefix-cache tensor once for all mutants), every output element written
    * once, every mutant's weights read once. */
   double kernel_bytes_algorithmic[MURE_N_KERNELS];
+  /* Shapes the caller's buffers must match: classes of the loaded model,
+   * inputs of the last run_original (0 before), registered mutants.
+   * get_logits writes n_inputs * n_classes floats; run_mutants writes
+   * n_mutants * ceil(n_inputs / 64) kill words. */
+  int64_t n_classes, n_inputs, n_mutants;
 } mure_stats;
 
 /* Version of this interface (MURE_VERSION). */
@@ -239,7 +244,7 @@ mure_status mure_run_original(mure_ctx* ctx, const void* inputs_dev, int64_t n_i
 /* Run every mutant's suffix over every input and classify each (mutant,
  * input) pair: kill(mutant, x) holds when argmax of the original's logits at
  * x equals label(x) and argmax of the mutant's logits differs from label(x)
- * (Section 6.2).  Outputs (each may be NULL):
+ * (Section 5.2).  Outputs (each may be NULL):
  *   kill_bits_dev     device uint64 [n_mutants][ceil(n/64)]; the bit for
  *                     (m, x) is bit (x & 63) of word m*ceil(n/64) + (x >> 6);
  *                     padding bits are 0;
@@ -287,6 +292,10 @@ mure_status mure_get_stats(const mure_ctx* ctx, mure_stats* out);
 
 /* Tuning and testing knobs (name, integer value).  Known names:
  *   "max_workspace_mb"  cap on per-chunk activation buffers (default 16384)
+ *   "max_device_mb"     cap on the device memory of the model, the mutants'
+ *                       copy-on-write layers and the prefix cache (0 = none,
+ *                       the default): apply_mutants and run_original refuse a
+ *                       plan above it with MURE_E_NOMEM and change nothing
  *   "chunk_inputs"      inputs per chunk, multiple of 64 (0 = automatic)
  *   "fused_paths"       1 (default) fuse a residual block's ADD into its second
  *                       convolution and the kill into the output layer where

@@ -10,12 +10,12 @@ Contents
                 (Section 4) with float64 accumulation
   mutate     -- the four neuron-level operators (Section 3.1)
   vanilla    -- exhaustive ("vanilla") mutation testing, the kill predicate,
-                killingLabels and the mutation score (Section 6.2), margins
+                killingLabels and the mutation score (Section 5.2), margins
                 and the ambiguous-pair set
   memoized   -- Algorithms 1-4 (dependence graph, memoization boundary,
                 clustering, instrumentation, chopping) taken step by step,
                 used to check the soundness theorem (Theorem 1) by brute force
-  ledger     -- the additive MAC cost model of Section 5.2 (axioms C1-C3,
+  ledger     -- the additive MAC cost model of Section 4.2 (axioms C1-C3,
                 Lemma 4)
 
 Every function is pinned by the CPU tests (tests/test_oracle_*.py) to

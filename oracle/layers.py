@@ -188,14 +188,18 @@ def phi(model: OracleModel, v: int, ins: Sequence[np.ndarray], W=None, b=None,
 
 def forward_all(model: OracleModel, X: np.ndarray, weights=None, biases=None,
                 accumulate: str = "blas", keep: Optional[Sequence[int]] = None,
-                chunk: int = 256) -> Dict[int, np.ndarray]:
+                chunk: int = 256, last: Optional[int] = None) -> Dict[int, np.ndarray]:
     """Activations a_v(x) of every node (or of ``keep``) for all inputs.
 
     a_v(x) = x for the input node, Phi(v)(a_p(x) for p in Pred(v)) otherwise
     (Section 4).  ``weights``/``biases`` override per-node parameters (a
-    mutant's Phi')."""
+    mutant's Phi').  ``last``: compute the nodes up to that index only (every
+    node of ``keep`` must be among them)."""
     xs = model.input_values(X)
     keep = set(range(len(model.nodes))) if keep is None else set(keep)
+    n_run = len(model.nodes) if last is None else last + 1
+    if any(v >= n_run for v in keep):
+        raise ValueError("a kept node lies after the last computed node")
     parts: Dict[int, List[np.ndarray]] = {v: [] for v in keep}
     last_use = {}
     for v, node in enumerate(model.nodes):
@@ -203,7 +207,7 @@ def forward_all(model: OracleModel, X: np.ndarray, weights=None, biases=None,
             last_use[p] = v
     for s in range(0, xs.shape[0], chunk):
         acts: Dict[int, np.ndarray] = {0: xs[s:s + chunk]}
-        for v in range(1, len(model.nodes)):
+        for v in range(1, n_run):
             node = model.nodes[v]
             W = weights[v] if weights is not None else None
             b = biases[v] if biases is not None else None

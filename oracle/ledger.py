@@ -1,4 +1,4 @@
-"""The additive cost model of Section 5.2, counted in multiply-accumulates.
+"""The additive cost model of Section 4.2, counted in multiply-accumulates.
 
 cost(v) per input = MACs of node v (CONV2D: pre-pool output pixels * C_out *
 kh*kw*C_in; DWCONV: output pixels * C * kh*kw; DENSE: C_in*C_out; LSTM:

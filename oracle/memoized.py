@@ -47,14 +47,15 @@ def mutated_layers(mutants: Mutants, m: int) -> List[int]:
 def instrument(model: OracleModel, probes: Sequence[int]) -> Callable[[np.ndarray], Dict[int, np.ndarray]]:
     """Algorithm 3: a model returning the original's activations at ``probes``.
 
-    An empty probe list gives the identity on the input."""
+    Its outputs are the probe tensors, so the layers after the last probe are
+    not computed.  An empty probe list gives the identity on the input."""
     probes = sorted(probes)
     for p in probes:
         if not (0 <= p < len(model.nodes)):
             raise KeyError("Probe point not found")
     if not probes:
         return lambda X: {0: model.input_values(X)}
-    return lambda X: forward_all(model, X, keep=probes, accumulate="ordered")
+    return lambda X: forward_all(model, X, keep=probes, accumulate="ordered", last=probes[-1])
 
 
 def chop_mutant(model: OracleModel, weights, biases, mmi: int,

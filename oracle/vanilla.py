@@ -1,4 +1,4 @@
-"""Vanilla (exhaustive) mutation testing and the mutation score (Section 6.2).
+"""Vanilla (exhaustive) mutation testing and the mutation score (Section 5.2).
 
 Every mutant is evaluated from the raw input through every layer -- no
 memoization -- which is the baseline the paper compares against and, by

@@ -23,7 +23,7 @@ MURE_OK, MURE_E_INVALID, MURE_E_STATE, MURE_E_NOMEM, MURE_E_DEVICE, MURE_E_UNSUP
 STATUS_NAMES = {0: "MURE_OK", -1: "MURE_E_INVALID", -2: "MURE_E_STATE", -3: "MURE_E_NOMEM",
                 -4: "MURE_E_DEVICE", -5: "MURE_E_UNSUPPORTED"}
 MURE_F32, MURE_BF16 = 0, 1
-MURE_VERSION = 3
+MURE_VERSION = 4
 N_KERNELS = 9                                   # kernel families in mure_stats (MURE_N_KERNELS)
 OP_GAUSS_FUZZ, OP_EFFECT_BLOCK, OP_ACT_INVERSE, OP_NEURON_SWITCH, OP_WEIGHT_SHUFFLE = 0, 1, 2, 3, 4
 INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV, EMBED, LSTM = 0, 1, 2, 3, 4, 5, 6, 7, 8
@@ -65,7 +65,8 @@ class mure_stats(C.Structure):
                 ("ms_gemm", C.c_double), ("gemm_macs_algorithmic", C.c_int64),
                 ("gemm_macs_executed", C.c_int64), ("kernel_launches", C.c_int64 * N_KERNELS),
                 ("kernel_ms", C.c_double * N_KERNELS), ("kernel_macs_algorithmic", C.c_int64 * N_KERNELS),
-                ("kernel_bytes_algorithmic", C.c_double * N_KERNELS)]
+                ("kernel_bytes_algorithmic", C.c_double * N_KERNELS),
+                ("n_classes", C.c_int64), ("n_inputs", C.c_int64), ("n_mutants", C.c_int64)]
 
 
 def _pack(arrays, R: int, dtype):
@@ -157,7 +158,7 @@ def layer_descriptors(nodes) -> "C.Array":
         elif n.kind in (EMBED, LSTM):
             L.c_in, L.c_out = int(n.c_in), int(n.c_out)
             L.seq = int(getattr(n, "seq", 0)) if n.kind == LSTM else 0
-        elif n.kind in (ADD, GAP):
+        elif n.kind in (ADD, GAP, FLATTEN):
             L.c_in, L.c_out = int(n.c_in), int(n.c_out)
         L.relu = int(n.relu)
         L.shortcut = int(n.shortcut) if n.kind == ADD else 0
@@ -211,7 +212,7 @@ class Mure:
                 bp[i] = b.ctypes.data
         dt = MURE_F32 if dtype == "f32" else MURE_BF16
         self._check(self.lib.mure_load_model(self.ctx, arr, n, hwc, dt, wp, bp))
-        self.classes = int(nodes[-1].out_hwc[2]) if hasattr(nodes[-1], "out_hwc") else 0
+        self.classes = self._shapes()[0]
 
     RECORD_DTYPE = np.dtype([("mutant", "<i4"), ("op", "<i4"), ("layer", "<i4"), ("neuron", "<i4"),
                              ("partner", "<i4"), ("reserved", "<i4"), ("noise", "<u8"),
@@ -258,27 +259,45 @@ class Mure:
         self._check(self.lib.mure_run_original(self.ctx, C.c_void_p(inputs.data_ptr()), n, lp))
         self.n_inputs = n
 
+    def _shapes(self):
+        """(classes, inputs, mutants) as the library holds them."""
+        st = mure_stats()
+        self._check(self.lib.mure_get_stats(self.ctx, C.byref(st)))
+        return int(st.n_classes), int(st.n_inputs), int(st.n_mutants)
+
+    @staticmethod
+    def _check_device_buffer(t, nbytes: int, what: str):
+        if not (t.is_cuda and t.is_contiguous()):
+            raise ValueError(f"{what} must be a contiguous CUDA tensor")
+        if t.numel() * t.element_size() < nbytes:
+            raise ValueError(f"{what} holds {t.numel() * t.element_size()} bytes; the library writes {nbytes}")
+
     def run_mutants(self, kill_bits=None, noalloc: bool = False):
         """Returns (kill_bits [M][ceil(N/64)] int64 CUDA tensor holding the uint64
         words, kills per mutant (numpy int64), score dict).  noalloc: call
         mure_run_mutants_noalloc (the library allocates no device memory)."""
         import torch
-        nw = (self.n_inputs + 63) // 64
+        _, n, mutants = self._shapes()
+        nw = (n + 63) // 64
         if kill_bits is None:
-            kill_bits = torch.empty((max(self.n_mutants, 1), nw), dtype=torch.int64,
+            kill_bits = torch.empty((max(mutants, 1), nw), dtype=torch.int64,
                                     device=f"cuda:{self.device}")
-        kills = np.zeros(max(self.n_mutants, 1), np.int64)
+        self._check_device_buffer(kill_bits, mutants * nw * 8, "kill_bits")
+        kills = np.zeros(max(mutants, 1), np.int64)
         sc = mure_score()
         fn = self.lib.mure_run_mutants_noalloc if noalloc else self.lib.mure_run_mutants
         self._check(fn(self.ctx, C.c_void_p(kill_bits.data_ptr()),
                        kills.ctypes.data_as(C.POINTER(C.c_int64)), C.byref(sc)))
         score = {k: getattr(sc, k) for k, _ in mure_score._fields_}
-        return kill_bits[: self.n_mutants], kills[: self.n_mutants], score
+        return kill_bits[:mutants], kills[:mutants], score
 
-    def get_logits(self, mutant_id: int):
+    def get_logits(self, mutant_id: int, out=None):
+        """float32 logits [N][classes] of one mutant (-1: the original)."""
         import torch
-        out = torch.empty((self.n_inputs, self.classes), dtype=torch.float32,
-                          device=f"cuda:{self.device}")
+        classes, n, _ = self._shapes()
+        if out is None:
+            out = torch.empty((n, classes), dtype=torch.float32, device=f"cuda:{self.device}")
+        self._check_device_buffer(out, n * classes * 4, "out")
         self._check(self.lib.mure_get_logits(self.ctx, int(mutant_id), C.c_void_p(out.data_ptr())))
         return out
 

@@ -11,6 +11,16 @@
 // multiple of 16 one lane holds all four gates of its units in the same
 // accumulator position: the cell state stays in registers and the gates never
 // leave the lane.
+//
+// lstm_wide_kernel: for layers whose weights do not fit in LDS.  A block owns
+// 64 rows of one slot with H / 16 waves; wave w owns units 16w .. 16w + 15, all
+// four gates (64 GEMM columns), and holds its weight columns in registers.
+// The step input [x_t, h_{t-1}, 1] lives in LDS as [k / 4][row][4], so the A
+// fragments of a k-step are 256 contiguous bytes; two such tiles alternate by
+// step: x_{t+1} is fetched into the other tile with direct global-to-LDS
+// loads during step t and the gates write h_t there, so one barrier per step
+// suffices.
+// Both kernels accumulate k in the same order (steps of 4 from k = 0).
 #include "dev.hpp"
 #include "plan.hpp"
 
@@ -40,6 +50,10 @@ __global__ __launch_bounds__(256) void embed_kernel(SeqArgs a, DivU32 dd, DivU32
 // values; every launch of a layer uses the same formulas).
 __device__ __forceinline__ float sigmoidf_(float z) { return __fdividef(1.f, 1.f + __expf(-z)); }
 __device__ __forceinline__ float tanhf_(float z) { return 2.f * sigmoidf_(2.f * z) - 1.f; }
+
+// Zero bytes that the wide kernel's rows past the last input read.
+static __device__ __attribute__((aligned(16))) v4f g_lstm_zero[1] = {};
+__device__ __forceinline__ const float* lstm_zero() { return reinterpret_cast<const float*>(g_lstm_zero); }
 
 template <int HT>                                      // H = 16 * HT units
 __global__ __launch_bounds__(256) void lstm_kernel(SeqArgs a) {
@@ -171,6 +185,122 @@ __global__ __launch_bounds__(256) void lstm_kernel(SeqArgs a) {
   if (a.T > 0) store_h(a.T - 1);
 }
 
+
+// KS k-steps of 4 (K = D + H + 1 padded with zero weights to 4 KS; the
+// launcher rounds the needed steps up to a multiple of 4).
+template <int KS>
+__global__ __launch_bounds__(256, 1) void lstm_wide_kernel(SeqArgs a) {
+  extern __shared__ __attribute__((aligned(16))) float lsm[];
+  typedef __attribute__((address_space(3))) void lds_void;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int NW = (int)blockDim.x / 64;                 // = H / 16
+  const int sl = a.slot0 + (int)blockIdx.y;
+  const int D = a.D, H = a.H, K = D + H + 1, DS = D / 4;
+  // LDS: two step tiles [KS][64][4]: [x_t, h_{t-1}, 1, zeros] of step t in
+  // tile t % 2
+  const float* __restrict__ Wt = reinterpret_cast<const float*>(a.wtab[sl]);
+  const int unit = wave * 16 + (lane & 15);
+  // the wave's weight columns: wreg[s][q] = W[unit][gate q][4 s + (lane >> 4)]
+  float wreg[KS][4];
+#pragma unroll
+  for (int s = 0; s < KS; ++s)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int k = 4 * s + (lane >> 4);
+      wreg[s][q] = k < K ? Wt[((int64_t)unit * 4 + q) * K + k] : 0.f;
+    }
+  // both tiles: h = 0, the bias input 1 (k = D + H), zero padding (x_0 is loaded below)
+  for (int e = tid; e < 2 * (KS - DS) * 256; e += NW * 64) {
+    const int b = e / ((KS - DS) * 256), r = e % ((KS - DS) * 256);
+    const int k = D + (r >> 8) * 4 + (r & 3);
+    lsm[(b * KS + DS) * 256 + r] = k == D + H ? 1.f : 0.f;
+  }
+  const int xi0 = (int)blockIdx.x * 64;
+  const float* __restrict__ X = reinterpret_cast<const float*>(a.in.p);
+  float* __restrict__ Y = reinterpret_cast<float*>(a.out);
+  auto in_row = [&](int xi) {
+    return a.in.mode == MODE_BUF ? (int64_t)sl * a.nx + xi : (int64_t)a.x0 + xi;
+  };
+  auto out_row = [&](int xi) {
+    return a.out_mode == MODE_BUF ? (int64_t)sl * a.nx + xi : (int64_t)a.x0 + xi;
+  };
+  // x_t into tile b: instruction j (channels 4j .. 4j + 3 of the 64 rows),
+  // lane = row; rows past nx read the zero page
+  const float* xsrc = xi0 + lane < a.nx ? X + in_row(xi0 + lane) * a.in.row_elems : nullptr;
+  auto fetch_x = [&](int t, int b) {
+    for (int j = wave; j < DS; j += NW)
+      __builtin_amdgcn_global_load_lds((const void*)(xsrc ? xsrc + (int64_t)t * D + 4 * j : lstm_zero()),
+                                       (lds_void*)(lsm + (b * KS + j) * 256), 16, 0, 0);
+  };
+  fetch_x(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+
+  float cst[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) cst[i][e] = 0.f;
+  for (int t = 0; t < a.T; ++t) {
+    const int b = t & 1;
+    // x_{t+1} and h_t go to the other tile, which no wave reads during step t
+    if (t + 1 < a.T) fetch_x(t + 1, b ^ 1);
+    // z = [x_t, h_{t-1}, 1] W^T for the wave's 64 columns, k in steps of 4;
+    // A fragment: row 16 i + (lane & 15), k = 4 s + (lane >> 4)
+    v4f acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[i][q] = v4f{0.f, 0.f, 0.f, 0.f};
+    const float* at = lsm + b * KS * 256 + (lane & 15) * 4 + (lane >> 4);
+    // the fragments of k-step s + 1 are read before the MFMAs of step s
+    float av[2][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) av[0][i] = at[i * 64];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      if (s + 1 < KS) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) av[(s + 1) & 1][i] = at[(s + 1) * 256 + i * 64];
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          acc[i][q] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s & 1][i], wreg[s][q], acc[i][q], 0, 0, 0);
+    }
+    // gates of unit `unit`, rows 16 i + 4 (lane >> 4) + e
+    float* hn = lsm + ((b ^ 1) * KS + DS + (unit >> 2)) * 256 + (unit & 3);
+    float hv[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float ig = sigmoidf_(acc[i][0][e]);
+        const float fg = sigmoidf_(acc[i][1][e]);
+        const float gg = tanhf_(acc[i][2][e]);
+        const float og = sigmoidf_(acc[i][3][e]);
+        const float c = fmaf(fg, cst[i][e], ig * gg);
+        cst[i][e] = c;
+        const float h = og * tanhf_(c);
+        hn[(i * 16 + (lane >> 4) * 4 + e) * 4] = h;
+        hv[i][e] = h;
+      }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // x_{t+1} has landed
+    if (a.seq || t + 1 == a.T) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int xi = xi0 + i * 16 + (lane >> 4) * 4 + e;
+          if (xi < a.nx) Y[out_row(xi) * a.out_row + (int64_t)(a.seq ? t : 0) * H + unit] = hv[i][e];
+        }
+    }
+    __syncthreads();                                   // h_t and x_{t+1} in place
+  }
+}
+
 hipError_t launch_embed(const SeqArgs& a, hipStream_t s) {
   if (a.nslots <= 0 || a.nx <= 0) return hipSuccess;
   const int64_t per_slot = (int64_t)a.nx * a.T * a.D;
@@ -184,9 +314,24 @@ hipError_t launch_embed(const SeqArgs& a, hipStream_t s) {
 hipError_t launch_lstm(const SeqArgs& a, hipStream_t s) {
   if (a.nslots <= 0 || a.nx <= 0) return hipSuccess;
   if (a.H % 16 || a.H < 16 || a.H > 64 || a.nslots > 65535) return hipErrorInvalidValue;
+  dim3 grid((unsigned)((a.nx + 63) / 64), (unsigned)a.nslots);
+  if (lstm_uses_wide(a.D, a.H)) {
+    if (!lstm_wide_fits(a.D, a.H) || a.in.row_elems % 4) return hipErrorInvalidValue;
+    const int ks = lstm_wide_ks(a.D, a.H);
+    const size_t lds = (size_t)lstm_wide_lds_bytes(a.D, a.H);
+    const dim3 block(64 * (a.H / 16));
+    switch (ks) {
+#define MURE_LSTM_WIDE(n) case n: hipLaunchKernelGGL(lstm_wide_kernel<n>, grid, block, lds, s, a); break;
+      MURE_LSTM_WIDE(8) MURE_LSTM_WIDE(12) MURE_LSTM_WIDE(16) MURE_LSTM_WIDE(20) MURE_LSTM_WIDE(24)
+      MURE_LSTM_WIDE(28) MURE_LSTM_WIDE(32) MURE_LSTM_WIDE(36) MURE_LSTM_WIDE(40) MURE_LSTM_WIDE(44)
+      MURE_LSTM_WIDE(48) MURE_LSTM_WIDE(52)
+#undef MURE_LSTM_WIDE
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   const size_t lds = (size_t)lstm_lds_bytes(a.D, a.H);
   if (lds > 64 * 1024) return hipErrorInvalidValue;
-  dim3 grid((unsigned)((a.nx + 63) / 64), (unsigned)a.nslots);
   switch (a.H / 16) {
     case 1: hipLaunchKernelGGL(lstm_kernel<1>, grid, dim3(256), lds, s, a); break;
     case 2: hipLaunchKernelGGL(lstm_kernel<2>, grid, dim3(256), lds, s, a); break;

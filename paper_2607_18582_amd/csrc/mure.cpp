@@ -8,7 +8,9 @@
 #include <cstring>
 #include <map>
 #include <memory>
+#include <new>
 #include <set>
+#include <stdexcept>
 #include <string>
 #include <vector>
 
@@ -178,6 +180,8 @@ struct mure_ctx {
   void* scratch = nullptr;                            // this GPU's scratch array (noalloc entry)
   // options
   int64_t max_ws_mb = 16384;
+  int64_t max_device_mb = 0;                          // 0: no cap on model + copies + prefix cache
+  int64_t cow_bytes = 0;                              // copy-on-write pool of the applied mutants
   int64_t chunk_inputs = 0;
   int64_t fused = 1;
   int64_t kernel_timing = 0;
@@ -207,6 +211,15 @@ struct mure_ctx {
 namespace {
 
 int64_t esize_of(const Graph& g, int v) { return (v == g.out() || g.dtype == DT_F32) ? 4 : 2; }
+
+// device bytes of the original parameters
+int64_t model_bytes(const Graph& g) {
+  const int64_t es = g.dtype == DT_F32 ? 4 : 2;
+  int64_t b = 0;
+  for (const Node& n : g.nodes)
+    if (n.weighted()) b += n.n_weights() * es + (int64_t)n.c_out * 4;
+  return b;
+}
 
 // The ADD node that reads convolution v as its first input when nothing else
 // reads v (conv_b of a residual block): the pair runs as one launch whose
@@ -434,10 +447,17 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
     a.nx = nx; a.x0 = x0; a.rows = chunk_rows; a.P = n.inH * n.inW; a.C = n.C;
     e = launch_gap(a, g.dtype, ctx->stream);
   } else if (n.kind == K_FLATTEN) {
-    if (out_mode != MODE_BUF) return ctx->fail(MURE_E_UNSUPPORTED, "a cached FLATTEN node");
+    // a view: the rows are copied; a cached output (run_original, one slot)
+    // takes the chunk's rows from input x0 on
     TensorArg src;
     src.p = ins[0].p; src.mode = ins[0].mode; src.row_elems = n.out_elems();
-    e = launch_copy_rows(src, out, chunk_rows, nx, x0, (int)esize_of(g, n.in[0]), ctx->stream);
+    const int es = (int)esize_of(g, n.in[0]);
+    char* dst = static_cast<char*>(out);
+    if (out_mode == MODE_CACHE) {
+      if (chunk_rows != nx) return ctx->fail(MURE_E_INVALID, "internal: cached FLATTEN over several slots");
+      dst += (int64_t)x0 * n.out_elems() * es;
+    }
+    e = launch_copy_rows(src, dst, chunk_rows, nx, x0, es, ctx->stream);
   } else {
     return ctx->fail(MURE_E_INVALID, "node without a layer function");
   }
@@ -456,7 +476,7 @@ extern "C" {
 
 int32_t mure_version(void) { return MURE_VERSION; }
 
-mure_status mure_create(mure_ctx** out, int32_t device, void* hip_stream) {
+static mure_status create_impl(mure_ctx** out, int32_t device, void* hip_stream) {
   if (!out) {
     g_create_error = "out is NULL";
     return MURE_E_INVALID;
@@ -486,7 +506,7 @@ mure_status mure_create(mure_ctx** out, int32_t device, void* hip_stream) {
   return MURE_OK;
 }
 
-void mure_destroy(mure_ctx* ctx) {
+static void destroy_impl(mure_ctx* ctx) {
   if (!ctx) return;
   if (!ctx->plan_only) {
     (void)hipSetDevice(ctx->device);
@@ -503,12 +523,15 @@ const char* mure_last_error(const mure_ctx* ctx) {
   return ctx->err.c_str();
 }
 
-mure_status mure_set_option(mure_ctx* ctx, const char* name, int64_t value) {
+static mure_status set_option_impl(mure_ctx* ctx, const char* name, int64_t value) {
   if (!ctx || !name) return MURE_E_INVALID;
   const std::string n(name);
   if (n == "max_workspace_mb") {
     if (value < 1) return ctx->fail(MURE_E_INVALID, "max_workspace_mb must be >= 1");
     ctx->max_ws_mb = value;
+  } else if (n == "max_device_mb") {
+    if (value < 0) return ctx->fail(MURE_E_INVALID, "max_device_mb must be >= 0");
+    ctx->max_device_mb = value;
   } else if (n == "chunk_inputs") {
     if (value < 0 || value % 64) return ctx->fail(MURE_E_INVALID, "chunk_inputs must be 0 or a multiple of 64");
     ctx->chunk_inputs = value;
@@ -530,7 +553,7 @@ mure_status mure_set_option(mure_ctx* ctx, const char* name, int64_t value) {
   return MURE_OK;
 }
 
-mure_status mure_load_model(mure_ctx* ctx, const mure_layer* layers, int32_t n_layers,
+static mure_status load_model_impl(mure_ctx* ctx, const mure_layer* layers, int32_t n_layers,
                             const int32_t in_hwc[3], int32_t dtype, const void* const* weights,
                             const float* const* biases) {
   if (!ctx) return MURE_E_INVALID;
@@ -585,7 +608,7 @@ mure_status mure_load_model(mure_ctx* ctx, const mure_layer* layers, int32_t n_l
   return MURE_OK;
 }
 
-mure_status mure_apply_mutants(mure_ctx* ctx, int32_t n_mutants, const mure_record* records,
+static mure_status apply_mutants_impl(mure_ctx* ctx, int32_t n_mutants, const mure_record* records,
                                int64_t n_records) {
   if (!ctx) return MURE_E_INVALID;
   if (ctx->state < 1) return ctx->fail(MURE_E_STATE, "load_model first");
@@ -633,21 +656,27 @@ mure_status mure_apply_mutants(mure_ctx* ctx, int32_t n_mutants, const mure_reco
   std::string m = build_plan(g, n_mutants, recs, plan, ctx->vanilla != 0);
   if (!m.empty()) return ctx->fail(MURE_E_INVALID, m);
 
+  // copy-on-write pool: weights (256-byte aligned) then biases
+  const int64_t es = g.dtype == DT_F32 ? 4 : 2;
+  std::vector<int64_t> woff(plan.cows.size()), boff(plan.cows.size());
+  int64_t pos = 0;
+  for (size_t c = 0; c < plan.cows.size(); ++c) {
+    woff[c] = pos;
+    pos += (g.nodes[plan.cows[c].layer].n_weights() * es + 255) / 256 * 256;
+  }
+  for (size_t c = 0; c < plan.cows.size(); ++c) {
+    boff[c] = pos;
+    pos += ((int64_t)g.nodes[plan.cows[c].layer].c_out * 4 + 255) / 256 * 256;
+  }
+  if (ctx->max_device_mb > 0 && model_bytes(g) + pos > (ctx->max_device_mb << 20))
+    return ctx->fail(MURE_E_NOMEM, "the model and the mutants' copy-on-write layers need " +
+                                       std::to_string((model_bytes(g) + pos) >> 20) + " MB, above max_device_mb = " +
+                                       std::to_string(ctx->max_device_mb));
+  ctx->cow_bytes = pos;
+
   if (!ctx->plan_only) {
     HIPTRY(hipSetDevice(ctx->device));
     HIPTRY(hipEventRecord(ctx->ev0, ctx->stream));
-    const int64_t es = g.dtype == DT_F32 ? 4 : 2;
-    // copy-on-write pool: weights (256-byte aligned) then biases
-    std::vector<int64_t> woff(plan.cows.size()), boff(plan.cows.size());
-    int64_t pos = 0;
-    for (size_t c = 0; c < plan.cows.size(); ++c) {
-      woff[c] = pos;
-      pos += (g.nodes[plan.cows[c].layer].n_weights() * es + 255) / 256 * 256;
-    }
-    for (size_t c = 0; c < plan.cows.size(); ++c) {
-      boff[c] = pos;
-      pos += ((int64_t)g.nodes[plan.cows[c].layer].c_out * 4 + 255) / 256 * 256;
-    }
     // from here on a device failure leaves the context without mutants
     ctx->state = 1;
     ctx->plan = Plan();
@@ -807,7 +836,7 @@ mure_status mure_apply_mutants(mure_ctx* ctx, int32_t n_mutants, const mure_reco
 
 // -------------------------------------------------------------------------
 // run_original: the original model once over X; fills the prefix cache.
-mure_status mure_run_original(mure_ctx* ctx, const void* inputs_dev, int64_t n_inputs,
+static mure_status run_original_impl(mure_ctx* ctx, const void* inputs_dev, int64_t n_inputs,
                               const int32_t* labels) {
   if (!ctx) return MURE_E_INVALID;
   if (ctx->plan_only) return ctx->fail(MURE_E_UNSUPPORTED, "planning-only context");
@@ -820,11 +849,19 @@ mure_status mure_run_original(mure_ctx* ctx, const void* inputs_dev, int64_t n_i
   if (labels)
     for (int64_t i = 0; i < n_inputs; ++i)
       if (labels[i] < 0 || labels[i] >= C) return ctx->fail(MURE_E_INVALID, "label out of range");
+  const int64_t n = n_inputs;
+  std::set<int> cached(ctx->plan.cache_nodes.begin(), ctx->plan.cache_nodes.end());
+  if (ctx->max_device_mb > 0) {
+    int64_t need = model_bytes(g) + ctx->cow_bytes + n * C * 4;
+    for (int v : cached)
+      if (v != L) need += n * g.act_bytes(v);
+    if (need > (ctx->max_device_mb << 20))
+      return ctx->fail(MURE_E_NOMEM, "the model, the copies and the prefix cache need " + std::to_string(need >> 20) +
+                                         " MB, above max_device_mb = " + std::to_string(ctx->max_device_mb));
+  }
   HIPTRY(hipSetDevice(ctx->device));
   reset_cache(ctx);
   ctx->state = 2;
-  const int64_t n = n_inputs;
-  std::set<int> cached(ctx->plan.cache_nodes.begin(), ctx->plan.cache_nodes.end());
   int64_t cache_bytes = 0;
   for (auto it = ctx->cache.begin(); it != ctx->cache.end();)     // drop tensors no longer cached
     it = cached.count(it->first) ? std::next(it) : ctx->cache.erase(it);
@@ -1285,16 +1322,8 @@ static mure_status run_mutants_impl(mure_ctx* ctx, uint64_t* kill_bits_dev, int6
 
 extern "C" {
 
-mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* kills_host, mure_score* score) {
-  return run_mutants_impl(ctx, kill_bits_dev, kills_host, score, false);
-}
 
-mure_status mure_run_mutants_noalloc(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* kills_host,
-                                     mure_score* score) {
-  return run_mutants_impl(ctx, kill_bits_dev, kills_host, score, true);
-}
-
-mure_status mure_get_logits(mure_ctx* ctx, int32_t mutant_id, float* out_dev) {
+static mure_status get_logits_impl(mure_ctx* ctx, int32_t mutant_id, float* out_dev) {
   if (!ctx) return MURE_E_INVALID;
   if (ctx->plan_only) return ctx->fail(MURE_E_UNSUPPORTED, "planning-only context");
   if (ctx->state != 3) return ctx->fail(MURE_E_STATE, "run_original must run first");
@@ -1313,7 +1342,7 @@ mure_status mure_get_logits(mure_ctx* ctx, int32_t mutant_id, float* out_dev) {
   return MURE_OK;
 }
 
-mure_status mure_mutant_plan(const mure_ctx* ctx, int32_t mutant_id, int32_t* mmi, int32_t* group,
+static mure_status mutant_plan_impl(const mure_ctx* ctx, int32_t mutant_id, int32_t* mmi, int32_t* group,
                              int32_t* k_nodes, int32_t max_k, int32_t* n_k) {
   if (!ctx) return MURE_E_INVALID;
   if (ctx->state < 2) return const_cast<mure_ctx*>(ctx)->fail(MURE_E_STATE, "apply_mutants first");
@@ -1328,9 +1357,12 @@ mure_status mure_mutant_plan(const mure_ctx* ctx, int32_t mutant_id, int32_t* mm
   return MURE_OK;
 }
 
-mure_status mure_get_stats(const mure_ctx* ctx, mure_stats* out) {
+static mure_status get_stats_impl(const mure_ctx* ctx, mure_stats* out) {
   if (!ctx || !out) return MURE_E_INVALID;
   *out = ctx->stats;
+  out->n_classes = ctx->have_graph ? ctx->g.classes() : 0;
+  out->n_inputs = ctx->state == 3 ? ctx->N : 0;
+  out->n_mutants = ctx->state >= 2 ? ctx->plan.n_mutants : 0;
   out->n_groups = (int64_t)ctx->plan.groups.size();
   out->n_identity_mutants = ctx->plan.n_identity;
   if (ctx->N == 0) {   // before run_original: per-input ledger
@@ -1340,6 +1372,89 @@ mure_status mure_get_stats(const mure_ctx* ctx, mure_stats* out) {
     out->macs_executed = ctx->plan.macs_executed;
   }
   return MURE_OK;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Exported entry points: no C++ exception crosses the interface.  Host
+// allocation failures become MURE_E_NOMEM, anything else MURE_E_INVALID, with
+// the message in mure_last_error (the call may then have done part of its
+// work, as after a device error).
+namespace {
+mure_status guard_fail(const mure_ctx* ctx, mure_status st, const char* what) noexcept {
+  try {
+    if (ctx) const_cast<mure_ctx*>(ctx)->err = what;
+    else g_create_error = what;
+  } catch (...) {
+  }
+  return st;
+}
+
+template <typename F>
+mure_status guarded(const mure_ctx* ctx, F&& f) noexcept {
+  try {
+    return f();
+  } catch (const std::bad_alloc&) {
+    return guard_fail(ctx, MURE_E_NOMEM, "host memory exhausted");
+  } catch (const std::exception& e) {
+    return guard_fail(ctx, MURE_E_INVALID, e.what());
+  } catch (...) {
+    return guard_fail(ctx, MURE_E_INVALID, "unexpected internal error");
+  }
+}
+}  // namespace
+
+extern "C" {
+
+mure_status mure_create(mure_ctx** out, int32_t device, void* hip_stream) {
+  return guarded(nullptr, [&] { return create_impl(out, device, hip_stream); });
+}
+
+void mure_destroy(mure_ctx* ctx) {
+  try {
+    destroy_impl(ctx);
+  } catch (...) {
+  }
+}
+
+mure_status mure_set_option(mure_ctx* ctx, const char* name, int64_t value) {
+  return guarded(ctx, [&] { return set_option_impl(ctx, name, value); });
+}
+
+mure_status mure_load_model(mure_ctx* ctx, const mure_layer* layers, int32_t n_layers, const int32_t in_hwc[3],
+                            int32_t dtype, const void* const* weights, const float* const* biases) {
+  return guarded(ctx, [&] { return load_model_impl(ctx, layers, n_layers, in_hwc, dtype, weights, biases); });
+}
+
+mure_status mure_apply_mutants(mure_ctx* ctx, int32_t n_mutants, const mure_record* records, int64_t n_records) {
+  return guarded(ctx, [&] { return apply_mutants_impl(ctx, n_mutants, records, n_records); });
+}
+
+mure_status mure_run_original(mure_ctx* ctx, const void* inputs_dev, int64_t n_inputs, const int32_t* labels) {
+  return guarded(ctx, [&] { return run_original_impl(ctx, inputs_dev, n_inputs, labels); });
+}
+
+mure_status mure_run_mutants(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* kills_host, mure_score* score) {
+  return guarded(ctx, [&] { return run_mutants_impl(ctx, kill_bits_dev, kills_host, score, false); });
+}
+
+mure_status mure_run_mutants_noalloc(mure_ctx* ctx, uint64_t* kill_bits_dev, int64_t* kills_host,
+                                     mure_score* score) {
+  return guarded(ctx, [&] { return run_mutants_impl(ctx, kill_bits_dev, kills_host, score, true); });
+}
+
+mure_status mure_get_logits(mure_ctx* ctx, int32_t mutant_id, float* out_dev) {
+  return guarded(ctx, [&] { return get_logits_impl(ctx, mutant_id, out_dev); });
+}
+
+mure_status mure_mutant_plan(const mure_ctx* ctx, int32_t mutant_id, int32_t* mmi, int32_t* group,
+                             int32_t* k_nodes, int32_t max_k, int32_t* n_k) {
+  return guarded(ctx, [&] { return mutant_plan_impl(ctx, mutant_id, mmi, group, k_nodes, max_k, n_k); });
+}
+
+mure_status mure_get_stats(const mure_ctx* ctx, mure_stats* out) {
+  return guarded(ctx, [&] { return get_stats_impl(ctx, out); });
 }
 
 }  // extern "C"

@@ -101,7 +101,9 @@ std::string build_graph(Graph& g, int in_h, int in_w, int in_c, int dtype) {
         if (v.c_out < 16 || v.c_out > 64 || v.c_out % 16) return fmt_node(i, "LSTM units must be 16, 32, 48 or 64");
         if (v.seq != 0 && v.seq != 1) return fmt_node(i, "seq must be 0 or 1");
         if (v.relu) return fmt_node(i, "LSTM has its own gate activations (relu must be 0)");
-        if (lstm_lds_bytes(v.c_in, v.c_out) > 64 * 1024) return fmt_node(i, "LSTM too wide for the kernel's LDS");
+        if (lstm_uses_wide(v.c_in, v.c_out) && !lstm_wide_fits(v.c_in, v.c_out))
+          return fmt_node(i, "LSTM too wide: c_in + c_out + 1 must be at most 208, and c_in a multiple of 4 "
+                             "when the layer's weights exceed 64 KB");
         v.kh = v.kw = v.stride = 1; v.pad = 0;
         v.H = 1; v.W = v.seq ? a.W : 1; v.C = v.c_out;
         v.Hc = v.H; v.Wc = v.W;
@@ -149,6 +151,7 @@ std::string build_graph(Graph& g, int in_h, int in_w, int in_c, int dtype) {
     }
   }
   if (g.nodes.back().H != 1 || g.nodes.back().W != 1) return "the output node must be 1x1xC";
+  if (g.nodes.back().kind == K_FLATTEN) return "the output node must compute its logits (not a FLATTEN view)";
   if (g.nodes.back().C < 2 || g.nodes.back().C > 512) return "the output needs 2 to 512 classes";
   // every node but the output must be read by some later node
   std::vector<int> used(n, 0);

@@ -5,7 +5,7 @@
 // earliest mutated layer mmi and memoization boundary K (Algorithm 1;
 // Section 4), the clustering of mutants (grouped by mmi, which determines K),
 // the prefix-cache set, the per-mutant channel patches at mmi, and the MAC
-// ledger of Section 5.2 (Lemma 4).
+// ledger of Section 4.2 (Lemma 4).
 #pragma once
 
 #include <cstdint>
@@ -93,6 +93,16 @@ constexpr int lstm_kpad(int d, int h) { return (d + h + 1 + 3) / 4 * 4; }
 constexpr int lstm_ka(int d, int h) { const int k = lstm_kpad(d, h); return (k / 4) % 2 ? k : k + 4; }
 constexpr int64_t lstm_lds_bytes(int d, int h) {
   return ((int64_t)lstm_kpad(d, h) * (4 * h + 16) + 64LL * lstm_ka(d, h)) * 4;
+}
+// Wide LSTM kernel (layers whose weights do not fit in LDS): per lane the
+// weights of KS k-steps of 4 in registers, KS = ceil((D + H + 1) / 4) rounded
+// up to a multiple of 4 (8 .. 52); LDS for two step tiles [KS][64][4].
+constexpr int LSTM_WIDE_KS = 52;
+constexpr int lstm_wide_ks(int d, int h) { return ((d + h + 1 + 3) / 4 + 3) / 4 * 4 < 8 ? 8 : ((d + h + 1 + 3) / 4 + 3) / 4 * 4; }
+constexpr int64_t lstm_wide_lds_bytes(int d, int h) { return 2LL * lstm_wide_ks(d, h) * 256 * 4; }
+inline bool lstm_uses_wide(int d, int h) { return lstm_lds_bytes(d, h) > 64 * 1024; }
+inline bool lstm_wide_fits(int d, int h) {
+  return d % 4 == 0 && lstm_wide_ks(d, h) <= LSTM_WIDE_KS && lstm_wide_lds_bytes(d, h) <= 160 * 1024;
 }
 int node_family(const Graph& g, int v);
 

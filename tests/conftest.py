@@ -11,3 +11,32 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) and the built HIP library")
     config.addinivalue_line("markers", "slow: CPU test that takes more than a few seconds")
+
+
+def pytest_terminal_summary(terminalreporter, exitstatus, config):
+    """One line per parity comparison against the oracle: pairs compared,
+    |A| (an oracle margin below tau = 1e-3), |A2| (outside A, an oracle
+    margin below the logit tolerance times S), kill disagreements in A, in A2
+    and elsewhere (must be 0), the largest logit error over S, and the
+    mutation score over the retained pairs (outside A and A2), GPU against
+    oracle, with the whole-matrix scores."""
+    try:
+        import harness
+    except ImportError:
+        return
+    rows = getattr(harness, "RECORDS", [])
+    if not rows:
+        return
+    tr = terminalreporter
+    tr.section("parity against the oracle: A = margin < 1e-3, A2 = margin < tol*S outside A")
+    tr.write_line(f"{'comparison':34s} {'dtype':5s} {'pairs':>8s} {'|A|':>6s} {'|A2|':>7s} "
+                  f"{'dis':>5s} {'in A':>5s} {'in A2':>6s} {'else':>5s} {'err/S':>9s}  "
+                  f"{'MS retained gpu | oracle':27s} MS whole gpu | oracle")
+    for r in rows:
+        ms_w = (f"{r['ms_gpu'][0]}/{r['ms_gpu'][1]} | " +
+                (f"{r['ms_oracle'][0]}/{r['ms_oracle'][1]}" if r["ms_oracle"] else "-")) if r["ms_gpu"] else "-"
+        err = f"{r['err']:.2e}" if r["err"] == r["err"] else "-"
+        ret = f"{r['ms_ret_gpu'][0]}/{r['ms_ret_gpu'][1]} | {r['ms_ret_oracle'][0]}/{r['ms_ret_oracle'][1]}"
+        tr.write_line(f"{r['name'][:34]:34s} {r['dtype']:5s} {r['pairs']:8d} {r['A']:6d} {r['A2']:7d} "
+                      f"{r['dis']:5d} {r['dis_A']:5d} {r['dis_A2']:6d} {r['dis_out']:5d} {err:>9s}  "
+                      f"{ret:27s} {ms_w}")

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) == set(B.EXPORTED)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.mure_version() == 3
+    assert lib.mure_version() == 4
 
 
 def _plan_ctx(model):
@@ -36,7 +36,8 @@ def _plan_ctx(model):
     return m
 
 
-@pytest.mark.parametrize("cfg", ["mlp", "lenet5", "vgg", "resnet20", "resnet18w", "mobilenetv2", "lstm"])
+@pytest.mark.parametrize("cfg", ["mlp", "lenet5", "vgg", "resnet20", "resnet18w", "mobilenetv2", "lstm",
+                                 "rnn_imdb"])
 def test_planner_matches_oracle_boundaries_and_ledger(cfg):
     wl = W.make_workload(cfg, n_inputs=1, n_mutants=60)
     m = _plan_ctx(wl.model)
@@ -238,3 +239,48 @@ def test_record_parameter_packing():
     pool, addr, lens = B._pack(arr, 2, np.int32)
     got = np.ctypeslib.as_array((ctypes.c_int32 * 3).from_address(int(addr[1])))
     assert got.tolist() == [3, 1, 2] and lens.tolist() == [0, 3]
+
+
+def test_flatten_boundary_and_flatten_output_rejected():
+    """A FLATTEN between a convolution and a dense layer is the boundary K of
+    the mutants whose first mutated layer is that dense layer; a FLATTEN as
+    the output node (a view, not logits) is refused."""
+    b = W.configs._Builder((8, 8, 4))
+    x = b.conv(0, 8, 3, pad=1, relu=True, pool=2, name="C1")
+    f = b.flatten(x)
+    b.dense(f, 10, False, "F")
+    w, bb = W.configs._draw_weights(b.nodes, "f32", 0.1, seed=2)
+    model = W.Model("flat", "f32", b.nodes, w, bb)
+    mu = W.make_mutants(model, 20, 1, "layer_first", variant=1)
+    m = _plan_ctx(model)
+    m.apply(mu)
+    plans = [m.mutant_plan(i) for i in range(mu.n_mutants)]
+    assert any(p[0] == f + 1 and p[2] == [f] for p in plans)
+    b2 = W.configs._Builder((1, 1, 16))
+    x = b2.dense(0, 10, False, "F")
+    b2.flatten(x)
+    w2, bb2 = W.configs._draw_weights(b2.nodes, "f32", 0.1, seed=2)
+    with pytest.raises(B.MureError) as e:
+        _plan_ctx(W.Model("flat_out", "f32", b2.nodes, w2, bb2))
+    assert e.value.status == B.MURE_E_INVALID and "FLATTEN" in e.value.message
+
+
+def test_device_memory_cap_refuses_plans_with_nomem():
+    """max_device_mb bounds the model plus the mutants' copy-on-write layers:
+    resnet18w (22.5 MB of bf16 weights) with 40 mutants at 5% copies about
+    40 x 22 MB; a 100 MB cap refuses the plan with MURE_E_NOMEM and keeps the
+    previous mutants, a 2 GB cap accepts it."""
+    wl = W.make_workload("resnet18w", n_inputs=1, n_mutants=40)
+    m = _plan_ctx(wl.model)
+    small = W.make_workload("resnet18w", n_inputs=1, n_mutants=1)
+    m.apply(small.mutants)
+    m.set_option("max_device_mb", 100)
+    with pytest.raises(B.MureError) as e:
+        m.apply(wl.mutants)
+    assert e.value.status == B.MURE_E_NOMEM and "max_device_mb" in e.value.message
+    assert m.stats()["n_mutants"] == 1                  # the earlier plan stands
+    m.set_option("max_device_mb", 2048)
+    m.apply(wl.mutants)
+    assert m.stats()["n_mutants"] == 40
+    with pytest.raises(B.MureError):
+        m.set_option("max_device_mb", -1)

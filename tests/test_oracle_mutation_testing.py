@@ -3,7 +3,7 @@
 * operators: hand-computed rows and output-layer closed forms (a switch swaps
   two logits exactly, an inverse negates one, a block zeroes one, a fuzz
   recomputes one from the penultimate activations);
-* kill / killingLabels / MS: a hand-worked fixture (Section 6.2);
+* kill / killingLabels / MS: a hand-worked fixture (Section 5.2);
 * Theorem 1 by brute force: Algorithms 1-4 (memoized) equal vanilla testing
   bit for bit on tiny sequential and residual networks, every neuron x every
   operator plus multi-neuron mutants;
@@ -309,3 +309,49 @@ def test_acceleration_closed_form(cfg):
         total_v += c["vanilla"]; total_m += c["memoized"]
     assert total_m < total_v                                # strict (Theorem 2)
     assert sum(macs) == {"mlp": 109184, "lenet5": 281640, "resnet20": 40551040}[cfg]
+
+
+@pytest.mark.parametrize("builder", ["mlp", "lenet", "resnetA", "resnetP", "mobilenet", "rnn"])
+def test_ledger_counts_the_macs_the_algorithms_perform(builder, monkeypatch):
+    """cluster_costs (the Lemma 4 ledger) against the multiply-accumulates the
+    oracle actually executes: every matrix product [R, K] x [K, C_out] of a
+    layer function counts R K C_out, a depthwise layer n Ho Wo C kh kw.
+    Algorithm 1 (memoized) executes cost(P) once per cluster plus every
+    mutant from its mmi on; vanilla testing executes the whole network per
+    mutant."""
+    import oracle.layers as OL
+    import oracle.memoized as OM
+    m = {"mlp": lambda: W.tiny_mlp(), "lenet": lambda: W.tiny_lenet(),
+         "resnetA": lambda: W.tiny_resnet("f32", shortcut="optionA"),
+         "resnetP": lambda: W.tiny_resnet("f32", shortcut="proj"),
+         "mobilenet": lambda: W.tiny_mobilenet(), "rnn": lambda: W.tiny_rnn()}[builder]()
+    om = O.OracleModel(m)
+    n = 5
+    x = W.make_inputs(m, n, "tokens" if builder == "rnn" else "normal")
+    muts = _all_single_mutants(m)
+    muts = muts.subset(muts.n_mutants - 1)                 # drop the identity mutant
+    count = [0]
+    mm, ph = OL._matmul64, OL.phi
+
+    def matmul(a64, w2, accumulate):
+        count[0] += a64.shape[0] * a64.shape[1] * w2.shape[0]
+        return mm(a64, w2, accumulate)
+
+    def phi(model, v, ins, W_=None, b=None, accumulate="blas"):
+        out = ph(model, v, ins, W_, b, accumulate)
+        nd = model.nodes[v]
+        if nd.kind == W.DWCONV:
+            count[0] += out.size * nd.kh * nd.kw
+        return out
+
+    monkeypatch.setattr(OL, "_matmul64", matmul)
+    monkeypatch.setattr(OL, "phi", phi)
+    monkeypatch.setattr(OM, "phi", phi)
+    cc = O.cluster_costs(om, muts)
+    O.mure(om, x, muts)
+    assert count[0] == n * sum(c["memoized"] for c in cc)
+    count[0] = 0
+    O.run_vanilla(om, x, muts, accumulate="ordered")
+    full = sum(O.node_macs(om))
+    assert count[0] == n * (sum(c["vanilla"] for c in cc) + full)   # + the original's forward
+    assert sum(c["size"] for c in cc) == muts.n_mutants

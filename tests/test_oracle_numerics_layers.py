@@ -188,7 +188,7 @@ def test_table1_parameter_counts():
         assert m.n_params() == r["params"], r["row"]
         # the oracle's layer functions produce the shapes the builder declares
         om = O.OracleModel(m)
-        x = W.make_inputs(m, 2, "uniform")
+        x = W.make_inputs(m, 2, "tokens" if any(n.kind == W.EMBED for n in m.nodes) else "uniform")
         acts = O.forward_all(om, x)
         for v, n in enumerate(m.nodes):
             assert acts[v].shape[1:] == tuple(n.out_hwc), (r["row"], v)

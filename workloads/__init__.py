@@ -1,4 +1,4 @@
-"""Seeded synthetic workloads shaped like the paper's models (Section 6, Table 1).
+"""Seeded synthetic workloads shaped like the paper's models (Section 5, Table 1).
 
 This package only *draws data*: graph descriptors, He-normal weights, test
 inputs and mutation records (with the Gaussian-fuzz noise already drawn).  It

@@ -28,7 +28,7 @@ from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
-from .graph import (INPUT, DENSE, CONV2D, ADD, GAP, DWCONV, EMBED, LSTM, GF, NEB, NAI, NS,
+from .graph import (INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV, EMBED, LSTM, GF, NEB, NAI, NS,
                     WS, Node, Model, Mutants, Workload)
 
 
@@ -83,6 +83,11 @@ class _Builder:
                                relu=int(relu), shortcut=shortcut, out_hwc=ha, name=name))
         return len(self.nodes) - 1
 
+    def flatten(self, src, name="flatten"):
+        h, w, c = self.nodes[src].out_hwc
+        self.nodes.append(Node(FLATTEN, (src,), c, h * w * c, out_hwc=(1, 1, h * w * c), name=name))
+        return len(self.nodes) - 1
+
     def gap(self, src, name="gap"):
         c = self.nodes[src].out_hwc[2]
         self.nodes.append(Node(GAP, (src,), c, c, out_hwc=(1, 1, c), name=name))
@@ -119,6 +124,9 @@ def _inverted_residual(b, src, expand, c_out, stride, name):
 
 
 LSTM_VOCAB, LSTM_STEPS = 2000, 40
+# the paper's RNN (Table 1): a 20,000-token vocabulary embedded in 128
+# features, two 64-unit LSTM layers; sequences of 80 tokens
+RNN_VOCAB, RNN_EMBED, RNN_UNITS, RNN_STEPS = 20000, 128, 64, 80
 
 
 def lstm_bias_positions(node: Node) -> np.ndarray:
@@ -196,6 +204,14 @@ def _graph(name: str, hwc=None, classes: int = 10) -> List[Node]:
         x = b.embed(0, LSTM_VOCAB, 32, name="embed")
         x = b.lstm(x, 32, seq=1, name="lstm1")
         x = b.lstm(x, 32, seq=0, name="lstm2")
+        b.dense(x, 2 if classes == 10 else classes, False, "out")
+    elif name == "rnn":
+        # Table 1's RNN: embedding 20,000 x 128, LSTM 64 (sequence), LSTM 64,
+        # dense output (2 classes for IMDB, 90 for Reuters)
+        b = _Builder(hwc or (1, RNN_STEPS, 1))
+        x = b.embed(0, RNN_VOCAB, RNN_EMBED, name="embed")
+        x = b.lstm(x, RNN_UNITS, seq=1, name="lstm1")
+        x = b.lstm(x, RNN_UNITS, seq=0, name="lstm2")
         b.dense(x, 2 if classes == 10 else classes, False, "out")
     else:
         raise KeyError(name)
@@ -373,6 +389,11 @@ CONFIGS: Dict[str, dict] = {
                  desc="RNN: embedding 2000x32, LSTM 32 (sequence), LSTM 32, dense 2, fp32, "
                       "40-token sequences uniform over the vocabulary, 10,000 inputs, "
                       "1,000 mutants at 1%"),
+    "rnn_imdb": dict(graph="rnn", dtype="f32", bias_std=0.0, n_inputs=25000, dist="tokens",
+                     n_mutants=1000, ratio=0.01, mode="layer_first", variant=0,
+                     desc="RNN of Table 1 (IMDB): embedding 20,000x128, LSTM 64 (sequence), LSTM 64, "
+                          "dense 2 (2,642,562 parameters), fp32, 80-token sequences uniform over the "
+                          "vocabulary, 25,000 inputs, 1,000 mutants at 1%"),
     "resnet18w": dict(graph="resnet18w", dtype="bf16", bias_std=0.01, n_inputs=5000, dist="normal",
                       n_mutants=500, ratio=0.05, mode="uniform", variant=0,
                       desc="ResNet-18-style 64x64x3 bf16 FC200, 5,000 inputs N(0,1), "

@@ -97,8 +97,12 @@ class Model:
         return self.nodes[-1].out_hwc[2]
 
     def n_params(self) -> int:
+        """Trainable parameters: every weight array, and the bias arrays of the
+        kinds that use theirs (an embedding has none, an LSTM keeps its gate
+        biases inside its weight rows)."""
         return int(sum(w.size for w in self.weights if w is not None)
-                   + sum(b.size for b in self.biases if b is not None))
+                   + sum(b.size for b, n in zip(self.biases, self.nodes)
+                         if b is not None and n.kind not in (EMBED, LSTM)))
 
     def weighted_nodes(self) -> List[int]:
         return [i for i, n in enumerate(self.nodes) if n.weighted]
