@@ -1,18 +1,22 @@
 """Throughput of memoized mutation testing on one MI355X.
 
-One step = the whole hot path over one batch: load the model (a1), apply the
-mutants (a2: clusters, copy-on-write layers), run the original once and fill
-the prefix cache (a3), run every mutant's suffix (a4 delta at the first
-mutated layer, a5 layers after it) and reduce to kill bits and the mutation
-score (a6).  Inputs are resident in device memory before the timed region.
+One step = the whole hot path over one batch of inputs: load the model (a1),
+apply the mutants (a2: clusters, copy-on-write layers), run the original once
+over the batch and fill the prefix cache (a3), run every mutant's suffix over
+the batch (a4 delta at the first mutated layer, a5 layers after it) and
+reduce to kill bits and the mutation score (a6).  The workload's inputs are
+resident in device memory before the timed region; consecutive steps take
+consecutive batches of them (resnet18w: batches of 1,000 of its 5,000
+inputs, so five steps cover the test set; the other workloads: the whole set
+per step).
 
-value = (mutants x inputs) / step time: (mutant, input) evaluations per
-second of the whole job.  The line also carries the suffix-only rate
-(run_mutants alone), the implicit-GEMM kernel's achieved rate against the
-MFMA peak of its dtype (per-launch HIP events on the library's stream), and
-the CPU oracle timed on a bounded sample.
+value = (mutants x inputs per step) / step time: (mutant, input)
+evaluations per second of the whole job.  The line also carries the
+suffix-only rate (run_mutants alone), the dominant kernel's achieved rate
+against its roofline (per-launch HIP events on the library's stream), and the
+CPU oracle timed on a bounded sample.
 
-    python bench.py [--steps K] [--warmup W] [--config lenet5] [--gpus 1]
+    python bench.py [--steps K] [--warmup W] [--config resnet18w] [--gpus 1]
 """
 from __future__ import annotations
 
@@ -47,7 +51,8 @@ PEAK_VALU_TFLOPS = 78.6                          # fp32 FMA without packed-fp32 
 PEAK_HBM_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
 ORACLE_SAMPLE = {"mlp": (100, 500), "lenet5": (24, 6000), "vgg": (3, 64), "resnet20": (8, 256),
-                 "resnet18w": (2, 16), "mobilenetv2": (8, 256), "lstm": (8, 500)}
+                 "resnet18w": (6, 64), "mobilenetv2": (8, 256), "lstm": (8, 500), "rnn_imdb": (8, 500)}
+INPUTS_PER_STEP = {"resnet18w": 1000}             # others: the whole input set per step
 
 
 def cpu_baseline(wl, n_mut: int, n_in: int):
@@ -200,9 +205,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--config", default="lenet5")
+    ap.add_argument("--config", default="resnet18w")
     ap.add_argument("--ratio-index", type=int, default=1)
     ap.add_argument("--inputs", type=int, default=None)
+    ap.add_argument("--inputs-per-step", type=int, default=None,
+                    help="inputs of one step's batch (default: 1,000 for resnet18w, else all)")
     ap.add_argument("--mutants", type=int, default=None)
     ap.add_argument("--oracle-mutants", type=int, default=None)
     ap.add_argument("--oracle-inputs", type=int, default=None)
@@ -224,9 +231,11 @@ def main():
                     help="print the kernel-trace summary of a rocprofv3 run and exit")
     ap.add_argument("--kernel", default="conv_lds_kernel", help="kernel the summaries follow")
     args = ap.parse_args()
+    cfgd = W.CONFIGS[args.config]
+    n_all = args.inputs or cfgd["n_inputs"]
+    ips = min(args.inputs_per_step or INPUTS_PER_STEP.get(args.config, n_all), n_all)
     if args.summarize_pmc or args.summarize_trace:
-        cfgd = W.CONFIGS[args.config]
-        args.n_inputs_resolved = args.inputs or cfgd["n_inputs"]
+        args.n_inputs_resolved = ips
         args.n_mutants_resolved = args.mutants or cfgd["n_mutants"]
         if args.summarize_pmc:
             print(summarize_pmc(*args.summarize_pmc, args.kernel, args), end="")
@@ -254,11 +263,14 @@ def main():
     wl = W.make_workload(args.config, n_inputs=args.inputs, n_mutants=args.mutants,
                          ratio_index=args.ratio_index)
     md = wl.model
-    M, N = wl.mutants.n_mutants, wl.n_inputs
+    M, N_all = wl.mutants.n_mutants, wl.n_inputs
+    N = ips                                            # inputs per step
+    n_batches = N_all // N
     dev = torch.device("cuda:0")
     x = wl.inputs
     xt = torch.from_numpy(x.view(np.int16).copy() if x.dtype == np.uint16 else x).to(dev)
     kill = torch.empty((M, (N + 63) // 64), dtype=torch.int64, device=dev)
+    batch = [0]
     m = Mure(device=0)
     m.set_option("kernel_timing", 1)
     m.set_option("fused_paths", args.fused)
@@ -267,9 +279,11 @@ def main():
         m.set_option("max_workspace_mb", args.workspace_mb)
 
     def step():
+        b0 = (batch[0] % n_batches) * N                # the next batch of the input set
+        batch[0] += 1
         m.load_model(md.nodes, md.in_hwc, md.dtype, md.weights, md.biases)
         m.apply(wl.mutants)
-        m.run_original(xt)
+        m.run_original(xt[b0:b0 + N])
         return m.run_mutants(kill)
 
     for _ in range(args.warmup):
@@ -337,8 +351,8 @@ def main():
         "vs_baseline": None,
         "dtype": md.dtype,
         "data": "synthetic",
-        "config": {"workload": f"{wl.name}: {wl.description}", "n_inputs": N, "n_mutants": M,
-                   "parallelism": "single GPU"},
+        "config": {"workload": f"{wl.name}: {wl.description}", "n_inputs": N_all, "n_mutants": M,
+                   "inputs_per_step": N, "parallelism": "single GPU"},
         "suffix_evals_per_s": M * N / (ms_mut * 1e-3),
         "ms_run_mutants": ms_mut,
         "ms_run_original": float(np.median([s["ms_run_original"] for s in stats])),
@@ -387,7 +401,7 @@ def main():
         om, oi = ORACLE_SAMPLE[args.config]
         om = args.oracle_mutants or om
         oi = args.oracle_inputs or oi
-        line["cpu_baseline"] = cpu_baseline(wl, min(om, M), min(oi, N))
+        line["cpu_baseline"] = cpu_baseline(wl, min(om, M), min(oi, N_all))
     print(json.dumps(line), flush=True)
 
 
