@@ -9,16 +9,20 @@
 // mixes two images' borders.
 //
 // The input channels go in chunks of 16.  Per chunk the block stages in LDS
-// (a) the band's input rows plus a one-pixel border (the halo, zero outside
-// the image), stored as two halves of 8 channels, [half][halo pixel][8]: every
-// input element crosses the memory pipeline once per block and chunk instead
-// of once per tap as an im2col gather would; and (b) the chunk's weights for
-// the tile's columns, [tap][half][column][8].  One MFMA k-step of 16 is one
-// tap of the chunk, so a chunk is nine k-steps, and the A fragment of a tap is
-// the lane's halo entry at a constant offset: the operand reads take
-// immediate offsets.  Both fragments of a k-step are 32 consecutive 16-byte
-// entries per half wave (conflict-free LDS reads).  Within a chunk the
-// fragments of tap t + 1 are read before the MFMAs of tap t are issued.
+// (a) the band's input rows plus the row above and below each packed image's
+// rows (the halo, zero outside the image), W pixels a row, stored as two
+// halves of 8 channels, [half][halo pixel][8]: every input element crosses
+// the memory pipeline once per block and chunk instead of once per tap as an
+// im2col gather would; and (b) the chunk's weights for the tile's columns,
+// [tap][half][column][8].  One MFMA k-step of 16 is one tap of the chunk, so a
+// chunk is nine k-steps, and the A fragment of a tap is the lane's halo entry
+// at a constant offset: the operand reads take immediate offsets.  A tap that
+// would read column -1 or W reads a zero entry kept after each half instead
+// (a per-lane select), so the halo has no border columns.  Both fragments of a
+// k-step are 32 consecutive 16-byte entries per half wave (32 pixels of whole
+// image rows), which ds_read_b128 serves without bank conflicts.  Within a
+// chunk the fragments of tap t + 1 are read before the MFMAs of tap t are
+// issued.
 //
 // The stages are fetched with direct global-to-LDS loads (16 bytes per lane,
 // landing at consecutive LDS addresses per instruction), so staging takes no
@@ -45,9 +49,9 @@ typedef __attribute__((address_space(3))) void lds_void;
 // Compile-time geometry of an instance (image width W, TN column tiles).
 template <int W, int TN>
 struct HaloGeo {
-  static constexpr int NT = 256, BM = 512, TR = BM / W, W2 = W + 2, BN = 32 * TN;
+  static constexpr int NT = 256, BM = 512, TR = BM / W, BN = 32 * TN;
   static constexpr int NPX = conv_halo_cap(W);          // halo pixels a stage holds
-  static constexpr int HSTR = NPX * 16;                 // bytes of one channel half of the halo
+  static constexpr int HSTR = (NPX + 1) * 16;           // bytes of one channel half: pixels, zero entry
   static constexpr int HALO_B = 2 * HSTR;
   static constexpr int B_B = 9 * 2 * BN * 16;           // weights: [tap][half][column][8]
   static constexpr int STAGE = HALO_B + B_B;
@@ -101,9 +105,9 @@ __device__ __forceinline__ void halo_sources(const ConvArgs& a, const HaloTile& 
     src[s] = nullptr;
     if (q < G::NQ_HALO) {
       const int hh = q / G::NQH, px = (q % G::NQH) * 64 + lane;
-      const int im = px / ((RI + 2) * G::W2), rem = px % ((RI + 2) * G::W2);
-      const int y = tl.y0 + rem / G::W2 - 1, x = rem % G::W2 - 1;
-      if (px < npx && tl.xi0 + im < a.nx && (unsigned)y < (unsigned)a.H && (unsigned)x < (unsigned)W)
+      const int im = px / ((RI + 2) * W), rem = px % ((RI + 2) * W);
+      const int y = tl.y0 + rem / W - 1, x = rem % W;
+      if (px < npx && tl.xi0 + im < a.nx && (unsigned)y < (unsigned)a.H)
         src[s] = in0 + im * a.in.row_elems + (y * W + x) * a.C + hh * 8;
     } else if (q < G::NQ) {
       const int e = (q - G::NQ_HALO) * 64 + lane;
@@ -140,30 +144,40 @@ __device__ __forceinline__ void halo_fetch(unsigned char* st, const bf16_t* cons
 }
 
 // Fragment bases: lane row (lane & 31) of M tile i is band pixel m, its 8 k
-// are channels 8 h of the chunk (h = lane >> 5); tap (dy, dx) adds the
-// constant (dy W2 + dx) entries.
+// are channels 8 h of the chunk (h = lane >> 5).  abase[i] is the entry of
+// the pixel's column in the halo row above it; tap (dy, dx) adds the constant
+// ((dy + 1) W + dx) entries.  edge bit i: the pixel is in column 0, bit 4 + i:
+// in column W - 1.
 template <int W, int TN>
-__device__ __forceinline__ void halo_abase(int wave, int lane, int RI, int (&abase)[4]) {
+__device__ __forceinline__ void halo_abase(int wave, int lane, int RI, int (&abase)[4], int& zoff, int& edge) {
   using G = HaloGeo<W, TN>;
+  edge = 0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int m = wave * 128 + i * 32 + (lane & 31);
     const int row = m / W, x = m % W;
-    abase[i] = (lane >> 5) * G::HSTR + (((row / RI) * (RI + 2) + row % RI) * G::W2 + x) * 16;
+    abase[i] = (lane >> 5) * G::HSTR + (((row / RI) * (RI + 2) + row % RI) * W + x) * 16;
+    edge |= (x == 0 ? 1 : 0) << i;
+    edge |= (x == W - 1 ? 1 : 0) << (4 + i);
   }
+  zoff = (lane >> 5) * G::HSTR + G::NPX * 16;
 }
 
 // The nine k-steps of the chunk staged at st (B: column j 32 + (lane & 31),
 // half h).
 template <int W, int TN>
-__device__ __forceinline__ void halo_mma(const unsigned char* st, const int (&abase)[4], int bbase,
-                                         v16f (&acc)[4][TN]) {
+__device__ __forceinline__ void halo_mma(const unsigned char* st, const int (&abase)[4], int zoff, int edge,
+                                         int bbase, v16f (&acc)[4][TN]) {
   using G = HaloGeo<W, TN>;
   v8bf fa[2][4], fb[2][TN];
   auto load = [&](int t, int p) {
-    const int toff = ((t / 3) * G::W2 + t % 3) * 16;
+    const int dx = t % 3 - 1, toff = ((t / 3) * W + dx) * 16;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) fa[p][i] = *reinterpret_cast<const v8bf*>(st + abase[i] + toff);
+    for (int i = 0; i < 4; ++i) {
+      int off = abase[i] + toff;
+      if (dx != 0 && ((edge >> (i + (dx > 0 ? 4 : 0))) & 1)) off = zoff;
+      fa[p][i] = *reinterpret_cast<const v8bf*>(st + off);
+    }
 #pragma unroll
     for (int j = 0; j < TN; ++j) fb[p][j] = *reinterpret_cast<const v8bf*>(st + bbase + (t * 2 * G::BN + j * 32) * 16);
   };
@@ -308,9 +322,9 @@ __device__ __forceinline__ void halo_store_rows(const ConvArgs& a, const HaloTil
 // Zero bytes that out-of-image halo pixels and columns past the last read.
 static __device__ __attribute__((aligned(16))) v4u g_halo_zero[4] = {};
 
-// Two blocks per CU fit in LDS except for width 8 with 64 columns (88 KB).
+// Two blocks per CU (at most 78 KB of LDS each).
 template <int W, int TN>
-__global__ __launch_bounds__(256, W == 8 && TN == 2 ? 1 : 2)
+__global__ __launch_bounds__(256, 2)
 void conv_halo_kernel(ConvArgs a) {
   using G = HaloGeo<W, TN>;
   constexpr int BM = G::BM, NT = G::NT, BN = G::BN, OLD = G::OLD, VPR = G::VPR;
@@ -323,14 +337,17 @@ void conv_halo_kernel(ConvArgs a) {
   if (!halo_decode<W, TN>(a, (int)blockIdx.x, tl)) return;   // padding of the order (whole block)
   const int ncol = a.cols ? a.ncols : a.Cout;
   const int RI = a.H < G::TR ? a.H : G::TR;
-  const int npx = (G::TR / RI) * (RI + 2) * G::W2;
+  const int npx = (G::TR / RI) * (RI + 2) * W;
   const bf16_t* const zp = reinterpret_cast<const bf16_t*>(g_halo_zero);
   const int nch = a.C / 16;
 
   const bf16_t* src[G::QPW];
   halo_sources<W, TN>(a, tl, RI, npx, wave, lane, src);
-  int abase[4];
-  halo_abase<W, TN>(wave, lane, RI, abase);
+  int abase[4], zoff, edge;
+  halo_abase<W, TN>(wave, lane, RI, abase, zoff, edge);
+  // the zero entries after each half of both stages (no load writes them)
+  if (tid < 4)
+    *reinterpret_cast<v4u*>(smem + (tid >> 1) * G::STAGE + (tid & 1) * G::HSTR + G::NPX * 16) = v4u{0u, 0u, 0u, 0u};
   const int bbase = G::HALO_B + ((lane >> 5) * BN + (lane & 31)) * 16;
   v16f acc[4][TN];
 #pragma unroll
@@ -345,7 +362,7 @@ void conv_halo_kernel(ConvArgs a) {
   __syncthreads();
   for (int c = 0; c < nch; ++c) {
     if (c + 1 < nch) halo_fetch<W, TN>(smem + ((c + 1) & 1) * G::STAGE, src, npx, wave, lane, (c + 1) * 16, zp);
-    halo_mma<W, TN>(smem + (c & 1) * G::STAGE, abase, bbase, acc);
+    halo_mma<W, TN>(smem + (c & 1) * G::STAGE, abase, zoff, edge, bbase, acc);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }

@@ -75,17 +75,17 @@ enum Family {
 };
 constexpr int N_FAMILIES = 9;
 // Halo convolution: 512-pixel bands of TR = 512 / W image rows (the bands
-// never straddle two images); a band's halo -- its rows plus a one-pixel
-// border, per packed image -- holds at most conv_halo_cap(W) pixels, the halo
-// of square images of that width.
-constexpr int conv_halo_cap(int W) { return W == 64 ? 660 : W == 32 ? 612 : W == 16 ? 648 : 800; }
+// never straddle two images); a band's halo -- its rows plus the row above
+// and below, per packed image -- holds at most conv_halo_cap(W) pixels, the
+// halo of square images of that width.
+constexpr int conv_halo_cap(int W) { return W == 64 ? 640 : W == 32 ? 576 : W == 16 ? 576 : 640; }
 inline bool conv_halo_fits(int H, int W, int C, int kh, int kw, int stride, int pad) {
   if (kh != 3 || kw != 3 || stride != 1 || pad != 1 || C % 16 || C <= 0 || H % 2) return false;
   if (W != 8 && W != 16 && W != 32 && W != 64) return false;
   const int TR = 512 / W;
   if (H % TR && TR % H) return false;
   const int RI = H < TR ? H : TR, IMGS = TR / RI;
-  return IMGS * (RI + 2) * (W + 2) <= conv_halo_cap(W) && (int64_t)9 * C <= (1 << 20);
+  return IMGS * (RI + 2) * W <= conv_halo_cap(W) && (int64_t)9 * C <= (1 << 20);
 }
 // LSTM kernel: units a multiple of 16, at most 64; LDS for the weights
 // (k-major, row stride 4H + 16) and a 64-row step tile
