@@ -214,7 +214,8 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
 
 // ---------------------------------------------------------------- copy-on-write mutation
 // One block per (mutant, layer) copy: copy the original parameters, then
-// apply that mutant's records on this layer in order.
+// apply that mutant's records on this layer in order.  Weight (neuron n, k)
+// is element n rs + k ks of the layer's array.
 template <typename T>
 __global__ __launch_bounds__(256) void cow_kernel(const CowArgs* args, const DevRecord* recs,
                                                   const float* noise) {
@@ -227,30 +228,31 @@ __global__ __launch_bounds__(256) void cow_kernel(const CowArgs* args, const Dev
   __syncthreads();
   for (int ri = c.rec0; ri < c.rec1; ++ri) {
     const DevRecord r = recs[ri];
-    T* row = wd + (int64_t)r.neuron * c.fan_in;
+    T* row = wd + (int64_t)r.neuron * c.rs;
+    const int64_t ks = c.ks;
     if (r.op == 0) {                      // Gaussian fuzz: float32 add, then round
       const float* eps = noise + r.noise_off;
       for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x)
-        row[k] = from_f<T>(to_f<T>(row[k]) + eps[k]);
+        row[k * ks] = from_f<T>(to_f<T>(row[k * ks]) + eps[k]);
     } else if (r.op == 1) {               // effect block
-      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) row[k] = T(0);
+      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) row[k * ks] = T(0);
       if (threadIdx.x == 0) c.b_dst[r.neuron] = 0.f;
     } else if (r.op == 2) {               // activation inverse (exact sign flip)
       for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) {
-        if constexpr (sizeof(T) == 2) row[k] = (T)(row[k] ^ 0x8000u);
-        else row[k] = -row[k];
+        if constexpr (sizeof(T) == 2) row[k * ks] = (T)(row[k * ks] ^ 0x8000u);
+        else row[k * ks] = -row[k * ks];
       }
       if (threadIdx.x == 0) c.b_dst[r.neuron] = -c.b_dst[r.neuron];
     } else if (r.op == 4) {               // weight shuffle: row[k] <- old row[perm[k]]
       float* scratch = const_cast<float*>(noise) + r.scratch_off;
       const int32_t* perm = reinterpret_cast<const int32_t*>(noise + r.noise_off);
-      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) scratch[k] = to_f<T>(row[k]);
+      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) scratch[k] = to_f<T>(row[k * ks]);
       __syncthreads();
-      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) row[k] = from_f<T>(scratch[perm[k]]);
+      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) row[k * ks] = from_f<T>(scratch[perm[k]]);
     } else {                              // neuron switch
-      T* other = wd + (int64_t)r.partner * c.fan_in;
+      T* other = wd + (int64_t)r.partner * c.rs;
       for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) {
-        const T t = row[k]; row[k] = other[k]; other[k] = t;
+        const T t = row[k * ks]; row[k * ks] = other[k * ks]; other[k * ks] = t;
       }
       if (threadIdx.x == 0) {
         const float t = c.b_dst[r.neuron]; c.b_dst[r.neuron] = c.b_dst[r.partner]; c.b_dst[r.partner] = t;

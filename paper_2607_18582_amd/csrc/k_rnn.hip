@@ -1,7 +1,8 @@
 // Sequence layers of the RNN family (float32 models).
 //
-// embed_kernel: one thread per (row, step, feature) gathers W[d][token];
-// blocks of one launch row split over the slots.
+// embed_kernel: one thread per (row, step, feature) gathers W[token][d] (the
+// library keeps embedding tables token-major, so a token's D values are one
+// contiguous row); blocks of one launch row split over the slots.
 //
 // lstm_kernel: a block owns 64 rows (inputs) of one mutant slot and runs all T
 // steps; its waves run independently (each owns 16 rows).  The slot's weights sit in LDS k-major ([D + H + 1][4H]); each wave
@@ -26,22 +27,27 @@
 
 namespace mure {
 
+// VEC features per thread (4: D % 4 == 0, 16-byte loads and stores).
+template <int VEC>
 __global__ __launch_bounds__(256) void embed_kernel(SeqArgs a, DivU32 dd, DivU32 dt) {
+  typedef float vf __attribute__((ext_vector_type(VEC)));
   const int sl = a.slot0 + (int)blockIdx.y;
-  const int total = a.nx * a.T * a.D;                  // < 2^31 (checked by the launcher)
+  const int DV = a.D / VEC;
+  const int total = a.nx * a.T * DV;                   // < 2^31 (checked by the launcher)
   const float* __restrict__ X = reinterpret_cast<const float*>(a.in.p);
   const float* __restrict__ Wt = reinterpret_cast<const float*>(a.wtab[sl]);
   for (int i = (int)blockIdx.x * 256 + threadIdx.x; i < total; i += (int)gridDim.x * 256) {
-    int rt, d, xi, t;
-    divmodu(dd, (uint32_t)i, rt, d);                   // rt = xi * T + t
+    int rt, dv, xi, t;
+    divmodu(dd, (uint32_t)i, rt, dv);                  // rt = xi * T + t
     divmodu(dt, (uint32_t)rt, xi, t);
     const int64_t r = (int64_t)sl * a.nx + xi;
     const float tokf = X[row_index(a.in.mode, r, a.nx, a.x0) * a.in.row_elems + t];
     const int tok = (int)tokf;
     // an id outside the vocabulary (or not an integer) embeds to zeros
-    float v = 0.f;
-    if ((float)tok == tokf && tok >= 0 && tok < a.V) v = Wt[(int64_t)d * a.V + tok];
-    reinterpret_cast<float*>(a.out)[row_index(a.out_mode, r, a.nx, a.x0) * a.out_row + (int64_t)t * a.D + d] = v;
+    vf v = {};
+    if ((float)tok == tokf && tok >= 0 && tok < a.V) v = *reinterpret_cast<const vf*>(Wt + (int64_t)tok * a.D + dv * VEC);
+    *reinterpret_cast<vf*>(reinterpret_cast<float*>(a.out) + row_index(a.out_mode, r, a.nx, a.x0) * a.out_row +
+                           (int64_t)t * a.D + dv * VEC) = v;
   }
 }
 
@@ -303,11 +309,15 @@ __global__ __launch_bounds__(256, 1) void lstm_wide_kernel(SeqArgs a) {
 
 hipError_t launch_embed(const SeqArgs& a, hipStream_t s) {
   if (a.nslots <= 0 || a.nx <= 0) return hipSuccess;
-  const int64_t per_slot = (int64_t)a.nx * a.T * a.D;
-  if (per_slot >= INT32_MAX || a.nslots > 65535) return hipErrorInvalidValue;
+  const int vec = a.D % 4 == 0 && a.out_row % 4 == 0 ? 4 : 1;
+  const int64_t per_slot = (int64_t)a.nx * a.T * (a.D / vec);
+  if ((int64_t)a.nx * a.T * a.D >= INT32_MAX || a.nslots > 65535) return hipErrorInvalidValue;
   const int64_t blocks = std::min<int64_t>((per_slot + 255) / 256, 4096);
-  hipLaunchKernelGGL(embed_kernel, dim3((unsigned)blocks, (unsigned)a.nslots), dim3(256), 0, s, a,
-                     make_divu32((uint32_t)a.D), make_divu32((uint32_t)a.T));
+  const dim3 grid((unsigned)blocks, (unsigned)a.nslots);
+  if (vec == 4)
+    hipLaunchKernelGGL(embed_kernel<4>, grid, dim3(256), 0, s, a, make_divu32((uint32_t)(a.D / 4)), make_divu32((uint32_t)a.T));
+  else
+    hipLaunchKernelGGL(embed_kernel<1>, grid, dim3(256), 0, s, a, make_divu32((uint32_t)a.D), make_divu32((uint32_t)a.T));
   return hipGetLastError();
 }
 

@@ -245,6 +245,7 @@ struct CowArgs {                           // one copy-on-write parameter copy
   const void* w_src; void* w_dst;
   const float* b_src; float* b_dst;
   int c_out; int64_t fan_in;
+  int64_t rs, ks;                          // element strides of a neuron's row and of k (EMBED: 1, c_out)
   int rec0, rec1;                          // records [rec0, rec1) in the device record table
 };
 

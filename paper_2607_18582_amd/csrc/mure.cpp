@@ -593,7 +593,20 @@ static mure_status load_model_impl(mure_ctx* ctx, const mure_layer* layers, int3
       const size_t wb = (size_t)g.nodes[i].n_weights() * es, bb = (size_t)g.nodes[i].c_out * 4;
       HIPTRY(ctx->d_w[i]->ensure(wb));
       HIPTRY(ctx->d_b[i]->ensure(bb));
-      HIPTRY(hipMemcpyAsync(ctx->d_w[i]->p, weights[i], wb, hipMemcpyHostToDevice, ctx->stream));
+      if (g.nodes[i].kind == K_EMBED) {
+        // token-major on the device ([V][D]): a token's D values are one
+        // contiguous row for the gather
+        const Node& e = g.nodes[i];
+        std::vector<unsigned char> t(wb);
+        const unsigned char* src = static_cast<const unsigned char*>(weights[i]);
+        for (int64_t d = 0; d < e.c_out; ++d)
+          for (int64_t v = 0; v < e.c_in; ++v)
+            std::memcpy(&t[(size_t)((v * e.c_out + d) * es)], src + (size_t)((d * e.c_in + v) * es), (size_t)es);
+        HIPTRY(hipMemcpyAsync(ctx->d_w[i]->p, t.data(), wb, hipMemcpyHostToDevice, ctx->stream));
+        HIPTRY(hipStreamSynchronize(ctx->stream));
+      } else {
+        HIPTRY(hipMemcpyAsync(ctx->d_w[i]->p, weights[i], wb, hipMemcpyHostToDevice, ctx->stream));
+      }
       HIPTRY(hipMemcpyAsync(ctx->d_b[i]->p, biases[i], bb, hipMemcpyHostToDevice, ctx->stream));
     }
     HIPTRY(hipStreamSynchronize(ctx->stream));
@@ -694,6 +707,9 @@ static mure_status apply_mutants_impl(mure_ctx* ctx, int32_t n_mutants, const mu
       a.b_dst = reinterpret_cast<float*>(base + boff[c]);
       a.c_out = g.nodes[cc.layer].c_out;
       a.fan_in = g.nodes[cc.layer].fan_in;
+      const bool tok_major = g.nodes[cc.layer].kind == K_EMBED;      // stored [V][D]
+      a.rs = tok_major ? 1 : a.fan_in;
+      a.ks = tok_major ? a.c_out : 1;
       a.rec0 = (int)drecs.size();
       for (int r : cc.records) {
         DevRecord d;
