@@ -178,7 +178,9 @@ int node_family(const Graph& g, int v) {
   if (g.dtype == DT_F32 && n.c_out <= 64 &&
       conv_lds_bytes(n.inH, n.inW, n.inC, n.pad, P, n.c_out, n.fan_in) <= 48 * 1024)
     return FAM_LDS;
-  if (g.dtype == DT_BF16 && v != g.out() && n.c_out % 64 == 0 &&
+  // halo tiles are 32 or 64 columns wide: 16-column outputs stay on the
+  // gather kernel, which wastes no MFMA columns on them
+  if (g.dtype == DT_BF16 && v != g.out() && n.c_out % 32 == 0 &&
       conv_halo_fits(n.inH, n.inW, n.inC, n.kh, n.kw, n.stride, n.pad))
     return FAM_HALO;
   if (g.dtype == DT_BF16 && n.inC % 8 == 0 && n.kh <= 15 && n.kw <= 15 && n.fan_in <= 8192 &&
