@@ -218,6 +218,8 @@ def main():
     ap.add_argument("--conv-tile", type=int, default=0)
     ap.add_argument("--workspace-mb", type=int, default=0,
                     help="cap the per-chunk activation workspace (0: the library default)")
+    ap.add_argument("--set", action="append", metavar="NAME=VALUE",
+                    help="a library option (mure_set_option), e.g. group_reads=0; repeatable")
     ap.add_argument("--gain", type=int, default=None,
                     help="also time vanilla mutation testing (every mutant from the raw "
                          "input) and report the paper's gain (t_v - t) / t_v (default: on "
@@ -277,6 +279,9 @@ def main():
     m.set_option("conv_tile", args.conv_tile)
     if args.workspace_mb:
         m.set_option("max_workspace_mb", args.workspace_mb)
+    for kv in args.set or []:
+        k, v = kv.split("=", 1)
+        m.set_option(k, int(v))
 
     def step():
         b0 = (batch[0] % n_batches) * N                # the next batch of the input set

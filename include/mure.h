@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define MURE_VERSION 4
+#define MURE_VERSION 5
 #define MURE_N_KERNELS 9   /* kernel families in mure_stats */
 /* Device scratch of mure_run_mutants_noalloc: a fixed array per GPU. */
 #define MURE_NOALLOC_SCRATCH_BYTES (256u << 20)
@@ -190,6 +190,11 @@ typedef struct {
    * get_logits writes n_inputs * n_classes floats; run_mutants writes
    * n_mutants * ceil(n_inputs / 64) kill words. */
   int64_t n_classes, n_inputs, n_mutants;
+  /* Side planes (one mutant's changed 8-channel group of the first mutated
+   * node's output, over a chunk's inputs) built by the last run_mutants for
+   * halo convolutions that read that output in channel groups (option
+   * "group_reads"); 0 when every consumer read per-mutant copies. */
+  int64_t group_planes;
 } mure_stats;
 
 /* Version of this interface (MURE_VERSION). */
@@ -307,6 +312,14 @@ mure_status mure_get_stats(const mure_ctx* ctx, mure_stats* out);
  *                       the next apply_mutants.  0 (default) memoized
  *   "conv_tile"         block shape of the tiled bf16 convolution: 0 automatic,
  *                       1 = 128 output pixels per block, 2 = 256
+ *   "group_reads"       1 (default): where every consumer of a cluster's first
+ *                       mutated node is a bf16 halo convolution (or an
+ *                       identity-shortcut ADD fused into one), the consumers
+ *                       read that output in 8-channel groups: the cached
+ *                       groups for all mutants, only each mutant's changed
+ *                       groups copied.  0: a full copy per mutant (the same
+ *                       results, bit for bit).  Not used by
+ *                       mure_run_mutants_noalloc.
  *   "kernel_timing"     1: time each implicit-GEMM launch of run_mutants (see
  *                       mure_stats); 0 (default) off
  * Errors: MURE_E_INVALID for an unknown name or value. */

@@ -90,8 +90,10 @@ __device__ __forceinline__ bool halo_decode(const ConvArgs& a, int t, HaloTile& 
 // The lane's sources for this wave's load instructions q = wave + 4 s of a
 // tile, at chunk 0 (nullptr: zeros).  q < NQ_HALO fills halo half q / NQH,
 // pixels 64 (q % NQH) + lane; the others fill 64 consecutive
-// [tap][half][column] weight entries.
-template <int W, int TN>
+// [tap][half][column] weight entries.  VIN (input read in channel groups):
+// a halo source holds the pixel's index in the launch's rows plus one
+// instead of an address (0: zeros); the group's base comes per chunk.
+template <int W, int TN, bool VIN>
 __device__ __forceinline__ void halo_sources(const ConvArgs& a, const HaloTile& tl, int RI, int npx, int wave,
                                              int lane, const bf16_t* (&src)[HaloGeo<W, TN>::QPW]) {
   using G = HaloGeo<W, TN>;
@@ -107,8 +109,12 @@ __device__ __forceinline__ void halo_sources(const ConvArgs& a, const HaloTile& 
       const int hh = q / G::NQH, px = (q % G::NQH) * 64 + lane;
       const int im = px / ((RI + 2) * W), rem = px % ((RI + 2) * W);
       const int y = tl.y0 + rem / W - 1, x = rem % W;
-      if (px < npx && tl.xi0 + im < a.nx && (unsigned)y < (unsigned)a.H)
-        src[s] = in0 + im * a.in.row_elems + (y * W + x) * a.C + hh * 8;
+      if (px < npx && tl.xi0 + im < a.nx && (unsigned)y < (unsigned)a.H) {
+        if constexpr (VIN)
+          src[s] = reinterpret_cast<const bf16_t*>((uintptr_t)((tl.xi0 + im) * a.H * W + y * W + x + 1));
+        else
+          src[s] = in0 + im * a.in.row_elems + (y * W + x) * a.C + hh * 8;
+      }
     } else if (q < G::NQ) {
       const int e = (q - G::NQ_HALO) * 64 + lane;
       const int tap = e / (2 * G::BN), hh = (e / G::BN) & 1, nc = tl.n0 + e % G::BN;
@@ -126,11 +132,31 @@ __device__ __forceinline__ void halo_sources(const ConvArgs& a, const HaloTile& 
   }
 }
 
+// The chunk at channel c0 of a VIN input: per channel half, the base of its
+// 8-channel group (the cache or the group's side plane) and the pixel stride.
+__device__ __forceinline__ void halo_group_bases(const GroupIn& gi, int slot, int nx, int c0,
+                                                 const bf16_t* (&gb)[2], int (&gst)[2]) {
+  const int64_t plane = (int64_t)nx * gi.P * 8;
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const int g = c0 / 8 + hh;
+    const int e = gi.src[slot * (gi.C / 8) + g];
+    if (e < 0) {
+      gb[hh] = reinterpret_cast<const bf16_t*>(gi.cache) + 8 * g;
+      gst[hh] = gi.C;
+    } else {
+      gb[hh] = reinterpret_cast<const bf16_t*>(gi.side) + (int64_t)(e - gi.g0) * plane;
+      gst[hh] = 8;
+    }
+  }
+}
+
 // Issue the loads of the chunk at channel c0 into the stage at st.  Lanes
 // past the halo load nothing.
-template <int W, int TN>
+template <int W, int TN, bool VIN>
 __device__ __forceinline__ void halo_fetch(unsigned char* st, const bf16_t* const (&src)[HaloGeo<W, TN>::QPW],
-                                           int npx, int wave, int lane, int c0, const bf16_t* zp) {
+                                           int npx, int wave, int lane, int c0, const bf16_t* zp,
+                                           const bf16_t* const (&gb)[2], const int (&gst)[2]) {
   using G = HaloGeo<W, TN>;
 #pragma unroll
   for (int s = 0; s < G::QPW; ++s) {
@@ -138,8 +164,16 @@ __device__ __forceinline__ void halo_fetch(unsigned char* st, const bf16_t* cons
     if (q >= G::NQ) continue;
     const bool halo = q < G::NQ_HALO;
     const int off = halo ? (q / G::NQH) * G::HSTR + (q % G::NQH) * 1024 : G::HALO_B + (q - G::NQ_HALO) * 1024;
-    if (!halo || (q % G::NQH) * 64 + lane < npx)
-      __builtin_amdgcn_global_load_lds((const void*)(src[s] ? src[s] + c0 : zp), (lds_void*)(st + off), 16, 0, 0);
+    if (!halo || (q % G::NQH) * 64 + lane < npx) {
+      const bf16_t* p;
+      if (VIN && halo) {
+        const int hh = q / G::NQH, pix = (int)(uintptr_t)src[s] - 1;
+        p = pix < 0 ? zp : gb[hh] + (int64_t)pix * gst[hh];
+      } else {
+        p = src[s] ? src[s] + c0 : zp;
+      }
+      __builtin_amdgcn_global_load_lds((const void*)p, (lds_void*)(st + off), 16, 0, 0);
+    }
   }
 }
 
@@ -251,9 +285,9 @@ __device__ __forceinline__ void halo_pixel(const HaloTile& tl, int RI, int m, in
 // A fused ADD's shortcut vectors for the output vectors idx = tid + NT k of
 // the pixels [m0, m0 + PB) (pixel idx / VPR, channels 8 (idx % VPR)),
 // requested before the staging so that their latency overlaps it.
-template <int W, int TN, int PB>
+template <int W, int TN, int PB, bool VSKIP>
 __device__ __forceinline__ void halo_skip(const ConvArgs& a, const HaloTile& tl, int RI, int m0, int tid,
-                                          v4u (&skipv)[PB * HaloGeo<W, TN>::VPR / HaloGeo<W, TN>::NT]) {
+                                          v4u (&skipv)[PB * HaloGeo<W, TN>::VPR / HaloGeo<W, TN>::NT], int skip_e) {
   using G = HaloGeo<W, TN>;
   constexpr int NV = PB * G::VPR / G::NT;
 #pragma unroll
@@ -263,6 +297,18 @@ __device__ __forceinline__ void halo_skip(const ConvArgs& a, const HaloTile& tl,
     halo_pixel<W>(tl, RI, m, xi, y, x);
     skipv[k] = v4u{0u, 0u, 0u, 0u};
     if (n >= a.Cout || xi >= a.nx) continue;
+    if constexpr (VSKIP) {
+      // identity shortcut read in channel groups; skip_e is the side plane of
+      // this thread's group (its n is the same for every k), looked up before
+      // the k loop
+      const GroupIn& gs = a.gskip;
+      const int e = skip_e;
+      const int64_t pix = (int64_t)xi * gs.P + y * W + x;
+      const bf16_t* p = e < 0 ? reinterpret_cast<const bf16_t*>(gs.cache) + pix * gs.C + n
+                              : reinterpret_cast<const bf16_t*>(gs.side) + (int64_t)(e - gs.g0) * a.nx * gs.P * 8 + pix * 8;
+      skipv[k] = *reinterpret_cast<const v4u*>(p);
+      continue;
+    }
     const bf16_t* sp = reinterpret_cast<const bf16_t*>(a.skip.p) +
                        row_index(a.skip.mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0) * a.skip.row_elems;
     if (a.add_mode == 1) {
@@ -323,9 +369,12 @@ __device__ __forceinline__ void halo_store_rows(const ConvArgs& a, const HaloTil
 static __device__ __attribute__((aligned(16))) v4u g_halo_zero[4] = {};
 
 // Two blocks per CU (at most 78 KB of LDS each).
-template <int W, int TN>
+// V bit 0: the input is read in channel groups (a.gin); bit 1: the identity
+// shortcut is (a.gskip).
+template <int W, int TN, int V>
 __global__ __launch_bounds__(256, 2)
 void conv_halo_kernel(ConvArgs a) {
+  constexpr bool VIN = (V & 1) != 0, VSKIP = (V & 2) != 0;
   using G = HaloGeo<W, TN>;
   constexpr int BM = G::BM, NT = G::NT, BN = G::BN, OLD = G::OLD, VPR = G::VPR;
   constexpr int NV = BM * VPR / NT;
@@ -342,7 +391,14 @@ void conv_halo_kernel(ConvArgs a) {
   const int nch = a.C / 16;
 
   const bf16_t* src[G::QPW];
-  halo_sources<W, TN>(a, tl, RI, npx, wave, lane, src);
+  halo_sources<W, TN, VIN>(a, tl, RI, npx, wave, lane, src);
+  const bf16_t* gb[2] = {nullptr, nullptr};
+  int gst[2] = {0, 0};
+  int skip_e = -1;
+  if constexpr (VSKIP) {
+    const int n = tl.n0 + (tid % VPR) * 8;            // the shortcut columns of this thread
+    if (n < a.Cout) skip_e = a.gskip.src[tl.slot * (a.gskip.C / 8) + n / 8];
+  }
   int abase[4], zoff, edge;
   halo_abase<W, TN>(wave, lane, RI, abase, zoff, edge);
   // the zero entries after each half of both stages (no load writes them)
@@ -357,11 +413,15 @@ void conv_halo_kernel(ConvArgs a) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  halo_fetch<W, TN>(smem, src, npx, wave, lane, 0, zp);
+  if constexpr (VIN) halo_group_bases(a.gin, tl.slot, a.nx, 0, gb, gst);
+  halo_fetch<W, TN, VIN>(smem, src, npx, wave, lane, 0, zp, gb, gst);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   for (int c = 0; c < nch; ++c) {
-    if (c + 1 < nch) halo_fetch<W, TN>(smem + ((c + 1) & 1) * G::STAGE, src, npx, wave, lane, (c + 1) * 16, zp);
+    if (c + 1 < nch) {
+      if constexpr (VIN) halo_group_bases(a.gin, tl.slot, a.nx, (c + 1) * 16, gb, gst);
+      halo_fetch<W, TN, VIN>(smem + ((c + 1) & 1) * G::STAGE, src, npx, wave, lane, (c + 1) * 16, zp, gb, gst);
+    }
     halo_mma<W, TN>(smem + (c & 1) * G::STAGE, abase, zoff, edge, bbase, acc);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -369,7 +429,7 @@ void conv_halo_kernel(ConvArgs a) {
 
   // ---- epilogue: bias, activation, bf16 rounding, staged in LDS ----
   v4u skipv[NV];
-  if (!a.cols && !a.pool && a.add_mode) halo_skip<W, TN, BM>(a, tl, RI, 0, tid, skipv);
+  if (!a.cols && !a.pool && a.add_mode) halo_skip<W, TN, BM, VSKIP>(a, tl, RI, 0, tid, skipv, skip_e);
   {
     uint32_t ob[4][TN][8];
     halo_round<TN>(a, tl, lane, acc, ob);
@@ -450,8 +510,18 @@ int conv_halo_bn(int cout) { return cout <= 32 ? 32 : 64; }
 namespace {
 template <int W>
 hipError_t launch_halo_w(const ConvArgs& a, int bn, int tiles, hipStream_t s) {
-  if (bn == 32) hipLaunchKernelGGL((conv_halo_kernel<W, 1>), dim3((unsigned)tiles), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((conv_halo_kernel<W, 2>), dim3((unsigned)tiles), dim3(256), 0, s, a);
+  const dim3 grid((unsigned)tiles);
+  const int v = (a.gin.cache ? 1 : 0) | (a.gskip.cache ? 2 : 0);
+#define MURE_HALO_V(VV)                                                                       \
+  if (v == VV) {                                                                             \
+    if (bn == 32) hipLaunchKernelGGL((conv_halo_kernel<W, 1, VV>), grid, dim3(256), 0, s, a); \
+    else hipLaunchKernelGGL((conv_halo_kernel<W, 2, VV>), grid, dim3(256), 0, s, a);          \
+  }
+  MURE_HALO_V(0)
+  MURE_HALO_V(1)
+  MURE_HALO_V(2)
+  MURE_HALO_V(3)
+#undef MURE_HALO_V
   return hipGetLastError();
 }
 }  // namespace
@@ -462,6 +532,13 @@ hipError_t launch_conv_halo(const ConvArgs& a0, int nslots, hipStream_t s) {
       a0.out_f32 || a0.add_out_f32 || (a0.pool && a0.add_mode) || a0.vin.chmap)
     return hipErrorInvalidValue;
   if (a0.cols && (a0.in.mode != MODE_CACHE || a0.add_mode || a0.ncols <= 0)) return hipErrorInvalidValue;
+  // channel-group reads: pixel indices of the launch's rows stay below 2^31
+  if (a0.gin.cache && (a0.cols || !a0.gin.src || a0.gin.C != a0.C || a0.gin.P != a0.H * a0.W ||
+                       (int64_t)a0.nx * a0.gin.P >= INT32_MAX))
+    return hipErrorInvalidValue;
+  if (a0.gskip.cache && (a0.add_mode != 1 || !a0.gskip.src || a0.gskip.C != a0.Cout || a0.gskip.C % 8 ||
+                         a0.gskip.P != a0.H * a0.W))
+    return hipErrorInvalidValue;
   ConvArgs a = a0;
   if (a.cols) nslots = 1;
   const int TR = 512 / a.W;

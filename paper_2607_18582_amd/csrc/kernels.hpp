@@ -55,6 +55,31 @@ struct VirtualIn {
   int C = 0, HW = 0, T = 0;
 };
 
+// A bf16 tensor read in 8-channel groups: the first mutated node's output as
+// the halo kernel's input or fused shortcut, with only each slot's changed
+// groups materialised.  Group g of launch slot s at input row xi (relative to
+// the launch's first input), pixel p: when src[s * C / 8 + g] = e >= 0, side
+// plane e - g0 at element (xi * P + p) * 8; otherwise cache element
+// (xi * P + p) * C + 8 g (cache points at the launch's first input).
+struct GroupIn {
+  const void* cache = nullptr;           // nullptr: not in use
+  const int32_t* src = nullptr;          // [slots][C / 8]
+  const void* side = nullptr;            // [planes][nx][P][8]
+  int g0 = 0, C = 0, P = 0;
+};
+
+// Build the side planes of a GroupIn: plane e holds group ent[2e+1] of slot
+// ent[2e] through that slot's channel map (>= 0: cached channel, -1: zero,
+// <= -2: compact delta channel -2 - map, in delta row (slot - slot0) nx + xi).
+struct GroupPatchArgs {
+  const void* cache = nullptr;           // the launch's first input: [nx][P][C]
+  const int32_t* chmap = nullptr;        // [slots][C], indexed by ent's slot
+  const void* delta = nullptr;           // [(slots - slot0) * nx][P][T]
+  const int32_t* ent = nullptr;          // [n_ent][2]: (slot, group)
+  void* side = nullptr;                  // [n_ent][nx][P][8]
+  int n_ent = 0, nx = 0, P = 0, C = 0, T = 0, slot0 = 0;
+};
+
 // One gathered output column of the delta at the first mutated node: output
 // channel `c` of mutant slot `slot - col_slot0` (relative to the launch's
 // slot0).  A delta launch shares the cached input among all its columns and
@@ -90,6 +115,8 @@ struct ConvArgs {
   TensorArg skip;
   int Hs = 0, Ws = 0, Cs = 0;            // skip geometry
   int tile = 0;                          // tiled kernel's block shape (0 automatic)
+  // halo kernel only: input / identity shortcut read in 8-channel groups
+  GroupIn gin, gskip;
   // gathered-column delta (cols != nullptr): ncols columns instead of C_out
   // channels per slot; the input must be slot independent (prefix cache)
   const DeltaCol* cols = nullptr;
@@ -267,6 +294,7 @@ hipError_t launch_patch(const PatchArgs& a, hipStream_t s);
 hipError_t launch_kill(const KillArgs& a, hipStream_t s);
 hipError_t launch_labels(const LabelArgs& a, hipStream_t s);
 hipError_t launch_score(const ScoreArgs& a, int n_mutants, hipStream_t s);
+hipError_t launch_group_patch(const GroupPatchArgs& a, hipStream_t s);
 hipError_t launch_cow(const CowArgs* d_args, int n_copies, const DevRecord* d_recs,
                       const float* d_noise, int dtype, hipStream_t s);
 hipError_t launch_copy_rows(const TensorArg& src, void* dst, int64_t rows, int nx, int x0,

@@ -166,6 +166,11 @@ struct mure_ctx {
     int64_t vchmap = 0;                               // offset (int32) into chmapv: virtual maps
     int64_t cols = 0;                                 // offset (DeltaCol) into colv
     std::vector<int64_t> colbeg;                      // first column of each recompute slot (+1)
+    int64_t vgsrc = 0;                                // vhalo: offset (int32) into chmapv of the
+                                                      // [slots][C/8] side-plane table (-1: cache)
+    int64_t vgent = 0;                                // vhalo: offset (int32) into chmapv of the
+                                                      // (slot, group) entries, one per side plane
+    std::vector<int64_t> vgbeg;                       // vhalo: first entry of each slot (+1)
   };
   std::vector<GroupTabs> gtabs;
   std::map<int, int64_t> orig_w, orig_b;              // node -> offset of 1-entry original tables
@@ -177,6 +182,8 @@ struct mure_ctx {
   int64_t n_labels = 0;
   // run_mutants scratch
   DevBuf d_ws, d_kill, d_kills, d_masks;
+  DevBuf d_side;                                      // changed channel groups (vhalo clusters)
+  int64_t group_reads = 1;                            // option "group_reads"
   void* scratch = nullptr;                            // this GPU's scratch array (noalloc entry)
   // options
   int64_t max_ws_mb = 16384;
@@ -221,21 +228,6 @@ int64_t model_bytes(const Graph& g) {
   return b;
 }
 
-// The ADD node that reads convolution v as its first input when nothing else
-// reads v (conv_b of a residual block): the pair runs as one launch whose
-// epilogue adds the shortcut.  -1 if v is not such a convolution.
-int fused_add_of(const Graph& g, int v) {
-  const Node& n = g.nodes[v];
-  const int fam = node_family(g, v);
-  if (n.kind != K_CONV || n.maxpool || (fam != FAM_BIG && fam != FAM_HALO)) return -1;
-  int reader = -1, count = 0;
-  for (int j = v + 1; j < (int)g.nodes.size(); ++j)
-    for (int k = 0; k < g.nodes[j].n_in; ++k)
-      if (g.nodes[j].in[k] == v) { reader = j; ++count; }
-  if (count != 1 || g.nodes[reader].kind != K_ADD || g.nodes[reader].in[0] != v) return -1;
-  if (fam == FAM_HALO && reader == g.out()) return -1;   // the halo kernel stores bf16 only
-  return reader;
-}
 
 // Tensor reference of node p for the executor.
 struct Where {
@@ -253,6 +245,8 @@ struct Extra {
   int64_t exec_macs = -1;             // MACs the launch executes, when not slots * rows * node
   int64_t delta_channels = -1;        // channels a per-slot channel-list delta computes
   const VirtualIn* vin = nullptr;     // read the first mutated node's output virtually
+  const GroupIn* gin = nullptr;       // ... in 8-channel groups (halo kernel)
+  const GroupIn* gskip = nullptr;     // the fused ADD's shortcut, in 8-channel groups
   int fuse_add = -1;                  // ADD node fused into this convolution's epilogue
   Where skip{nullptr, MODE_BUF};      // that ADD's shortcut input
   const KillArgs* kill = nullptr;     // fuse the kill reduction when possible
@@ -382,6 +376,11 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
         if (fam != FAM_LDS) return ctx->fail(MURE_E_INVALID, "internal: virtual input to an im2col convolution");
         a.vin = *ex.vin;
       }
+      if (ex.gin || ex.gskip) {
+        if (fam != FAM_HALO) return ctx->fail(MURE_E_INVALID, "internal: channel-group read by a non-halo kernel");
+        if (ex.gin) a.gin = *ex.gin;
+        if (ex.gskip) a.gskip = *ex.gskip;
+      }
       if (ex.fuse_add >= 0) {
         const Node& an = g.nodes[ex.fuse_add];
         const Node& sn = g.nodes[an.in[1]];
@@ -414,7 +413,7 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
       const int64_t out_ch = (int64_t)n.H * n.W * (out_f32 ? 4 : es);       // one channel of a row
       const int64_t w_row = n.fan_in * es;                                  // one neuron's weights
       int64_t bytes;
-      const bool shared_in = ins[0].mode == MODE_CACHE && !ex.vin;
+      const bool shared_in = (ins[0].mode == MODE_CACHE && !ex.vin) || ex.gin;
       if (ex.cols) {
         bytes = nx * in_row + (int64_t)ex.ncols * (nx * out_ch + w_row);
       } else if (ex.ch_off) {
@@ -425,7 +424,7 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
                 (int64_t)nslots * nx * n.c_out * out_ch + (int64_t)nslots * n.c_out * w_row;
         if (ex.fuse_add >= 0) {
           const int64_t skip_row = g.nodes[g.nodes[ex.fuse_add].in[1]].out_elems() * es;
-          bytes += (ex.skip.mode == MODE_CACHE ? nx : (int64_t)nslots * nx) * skip_row;
+          bytes += (ex.skip.mode == MODE_CACHE || ex.gskip ? nx : (int64_t)nslots * nx) * skip_row;
         }
       }
       ctx->stats.kernel_bytes_algorithmic[fam] += (double)bytes;
@@ -544,6 +543,9 @@ static mure_status set_option_impl(mure_ctx* ctx, const char* name, int64_t valu
   } else if (n == "conv_tile") {
     if (value < 0 || value > 2) return ctx->fail(MURE_E_INVALID, "conv_tile must be 0, 1 or 2");
     ctx->conv_tile = value;
+  } else if (n == "group_reads") {
+    if (value != 0 && value != 1) return ctx->fail(MURE_E_INVALID, "group_reads must be 0 or 1");
+    ctx->group_reads = value;
   } else if (n == "kernel_timing") {
     if (value != 0 && value != 1) return ctx->fail(MURE_E_INVALID, "kernel_timing must be 0 or 1");
     ctx->kernel_timing = value;
@@ -757,6 +759,29 @@ static mure_status apply_mutants_impl(mure_ctx* ctx, int32_t n_mutants, const mu
       }
       gt.vchmap = (int64_t)chmaps.size();
       chmaps.insert(chmaps.end(), gr.vchmap.begin(), gr.vchmap.end());
+      // channel-group reads: a side plane per (slot, changed 8-channel group)
+      gt.vgbeg.assign(1, 0);
+      if (gr.vhalo) {
+        const int C = g.nodes[gr.mmi].c_out, G = C / 8;
+        std::vector<int32_t> src((size_t)gr.mutants.size() * G, -1), ent;
+        int32_t e = 0;
+        for (size_t s = 0; s < gr.mutants.size(); ++s) {
+          const int* row = &gr.vchmap[s * C];
+          for (int q = 0; q < G; ++q) {
+            bool changed = false;
+            for (int j = 0; j < 8; ++j) changed = changed || row[8 * q + j] != 8 * q + j;
+            if (!changed) continue;
+            src[s * G + q] = e++;
+            ent.push_back((int32_t)s);
+            ent.push_back(q);
+          }
+          gt.vgbeg.push_back(e);
+        }
+        gt.vgsrc = (int64_t)chmaps.size();
+        chmaps.insert(chmaps.end(), src.begin(), src.end());
+        gt.vgent = (int64_t)chmaps.size();
+        chmaps.insert(chmaps.end(), ent.begin(), ent.end());
+      }
     }
     // touched-channel lists of the recompute mutants (CSR, absolute offsets
     // into the list stored after every group's offsets)
@@ -1041,6 +1066,19 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
   const Placement& pl = cg.pl;
   const std::map<int, int>& fused_adds = cg.fused_adds;
   const int64_t nx = cg.nx, spc = cg.spc, cap_rows = cg.cap_rows;
+  // channel-group reads of mmi's output by its halo consumers (not with a
+  // caller's scratch array: the side planes live in a buffer of their own)
+  const Node& nmm = g.nodes[mmi];
+  const int64_t vP = (int64_t)nmm.H * nmm.W;
+  const bool vh = gr.vhalo && ctx->group_reads && ctx->fused && !ws && nx * vP < INT32_MAX;
+  if (vh) {
+    int64_t most = 0;
+    for (int cs0 = s_begin; cs0 < s_end; cs0 += (int)spc) {
+      const int cs1 = (int)std::min<int64_t>(s_end, cs0 + spc);
+      most = std::max<int64_t>(most, gt.vgbeg[cs1] - gt.vgbeg[cs0]);
+    }
+    HIPTRY(ctx->d_side.ensure((size_t)(most * nx * vP * 16)));
+  }
   if (ws) {
     if (cg.need_bytes > ws_bytes) return ctx->fail(MURE_E_NOMEM, "chunk workspace exceeds the scratch array");
   } else {
@@ -1085,7 +1123,7 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
         for (int k = 0; k < nm.n_in; ++k) ins.push_back(where(nm.in[k]));
         void* out = const_cast<void*>(where(mmi).p);
         const int rec_end = std::min(cs1, gr.n_recompute);
-        const int pa = gr.virt ? cs1 : gr.delta ? cs0 : std::max(cs0, gr.n_recompute);
+        const int pa = (gr.virt || vh) ? cs1 : gr.delta ? cs0 : std::max(cs0, gr.n_recompute);
         if (pa < cs1) {
           PatchArgs a;
           a.cache = mmi_cache;
@@ -1108,7 +1146,7 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
           Extra ex;
           int launch_slots = rec_end - cs0;
           if (gr.delta) {
-            if (gr.virt) ex.delta_T = gr.T;
+            if (gr.virt || vh) ex.delta_T = gr.T;
             ex.exec_macs = tl * per_ch * cnt;
             ex.delta_channels = tl;
             if (node_family(g, mmi) == FAM_VALU || node_family(g, mmi) == FAM_DW) {
@@ -1133,6 +1171,29 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
           }
         }
       }
+      // the changed 8-channel groups of every slot of the chunk, from the
+      // cache, the slot's channel map and the compact delta rows
+      GroupIn gin;
+      if (vh) {
+        const int64_t e0 = gt.vgbeg[cs0], e1 = gt.vgbeg[cs1];
+        const void* cache_x0 = static_cast<const char*>(mmi_cache) + x0 * vP * nm.C * 2;
+        if (e1 > e0) {
+          GroupPatchArgs gpa;
+          gpa.cache = cache_x0;
+          gpa.chmap = ctx->chmapv + gt.vchmap;
+          gpa.delta = where(mmi).p;
+          gpa.ent = ctx->chmapv + gt.vgent + 2 * e0;
+          gpa.side = ctx->d_side.p;
+          gpa.n_ent = (int)(e1 - e0); gpa.nx = cnt; gpa.P = (int)vP; gpa.C = nm.C; gpa.T = gr.T; gpa.slot0 = cs0;
+          HIPTRY(launch_group_patch(gpa, ctx->stream));
+          ctx->stats.launches++;
+          ctx->stats.group_planes += e1 - e0;
+        }
+        gin.cache = cache_x0;
+        gin.src = ctx->chmapv + gt.vgsrc + (int64_t)cs0 * (nm.C / 8);
+        gin.side = ctx->d_side.p;
+        gin.g0 = (int)e0; gin.C = nm.C; gin.P = (int)vP;
+      }
       VirtualIn vin;
       if (gr.virt) {
         vin.cache = mmi_cache;
@@ -1154,6 +1215,8 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
           Extra exf;
           exf.fuse_add = fa;
           exf.skip = where(g.nodes[fa].in[1]);
+          if (vh && g.nodes[fa].in[1] == mmi) exf.gskip = &gin;
+          if (vh && nd.n_in == 1 && nd.in[0] == mmi) exf.gin = &gin;
           if (fa == L) { exf.kill = nullptr; }
           done.insert(fa);
           mure_status st = exec_node(ctx, v, ins, const_cast<void*>(where(fa).p), MODE_BUF,
@@ -1167,6 +1230,7 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
         const float* const* bt = nd.weighted() ? reinterpret_cast<const float* const*>(tabs + gt.b.at(v) + cs0) : nullptr;
         Extra ex;
         if (v == L && ctx->fused) { ex.kill = &ka; ex.kill_fused = &fused; }
+        if (vh && nd.n_in == 1 && nd.in[0] == mmi) ex.gin = &gin;
         if (gr.virt && nd.n_in == 1 && nd.in[0] == mmi) {
           // the consumer of mmi: delta groups read every slot virtually; in
           // whole-node groups the recomputed slots read their own output rows
@@ -1258,6 +1322,7 @@ static mure_status run_mutants_impl(mure_ctx* ctx, uint64_t* kill_bits_dev, int6
     ~Restore() { c->kernel_timing = t; }
   } restore{ctx, timing};
   ctx->stats.launches = 0;
+  ctx->stats.group_planes = 0;
   ctx->stats.gemm_launches = 0;
   ctx->stats.ms_gemm = 0;
   ctx->stats.gemm_macs_algorithmic = 0;

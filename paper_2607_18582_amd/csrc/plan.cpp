@@ -189,6 +189,22 @@ int node_family(const Graph& g, int v) {
   return FAM_GEMM;
 }
 
+// The ADD node that reads convolution v as its first input when nothing else
+// reads v (conv_b of a residual block): the pair runs as one launch whose
+// epilogue adds the shortcut.  -1 if v is not such a convolution.
+int fused_add_of(const Graph& g, int v) {
+  const Node& n = g.nodes[v];
+  const int fam = node_family(g, v);
+  if (n.kind != K_CONV || n.maxpool || (fam != FAM_BIG && fam != FAM_HALO)) return -1;
+  int reader = -1, count = 0;
+  for (int j = v + 1; j < (int)g.nodes.size(); ++j)
+    for (int k = 0; k < g.nodes[j].n_in; ++k)
+      if (g.nodes[j].in[k] == v) { reader = j; ++count; }
+  if (count != 1 || g.nodes[reader].kind != K_ADD || g.nodes[reader].in[0] != v) return -1;
+  if (fam == FAM_HALO && reader == g.out()) return -1;   // the halo kernel stores bf16 only
+  return reader;
+}
+
 std::vector<int> boundary(const Graph& g, int mmi) {
   std::set<int> K;
   for (int j = mmi; j < (int)g.nodes.size(); ++j)
@@ -322,7 +338,27 @@ std::string build_plan(const Graph& g, int n_mutants, const std::vector<Record>&
           const int f = node_family(g, v);
           if (!(f == FAM_LDS || (f == FAM_DENSE && g.nodes[v].c_in <= 4096))) gr.virt = false;
         }
-    if (gr.virt) {
+    // channel-group reads (halo kernel): every consumer of mmi is a halo
+    // convolution reading it as its only input, or an identity-shortcut ADD
+    // fused into a halo convolution
+    if (!gr.virt && !vanilla && gr.mmi != g.out() && g.dtype == DT_BF16 && g.nodes[gr.mmi].c_out % 8 == 0 &&
+        (gr.delta || gr.n_recompute == 0)) {
+      bool ok = true, any = false;
+      for (int v = gr.mmi + 1; v < n && ok; ++v) {
+        const Node& nv = g.nodes[v];
+        for (int k = 0; k < nv.n_in; ++k) {
+          if (nv.in[k] != gr.mmi) continue;
+          if (k == 0 && nv.n_in == 1 && node_family(g, v) == FAM_HALO) {
+            any = true;
+          } else if (!(nv.kind == K_ADD && k == 1 && nv.shortcut == 0 && node_family(g, nv.in[0]) == FAM_HALO &&
+                       fused_add_of(g, nv.in[0]) == v)) {
+            ok = false;
+          }
+        }
+      }
+      gr.vhalo = ok && any;
+    }
+    if (gr.virt || gr.vhalo) {
       const int C = g.nodes[gr.mmi].c_out;
       gr.T = 0;
       if (gr.n_recompute > 0) {

@@ -163,7 +163,10 @@ struct Group {
                                 // (cache + compact delta rows); mmi is never materialised
   int T = 0;                    // channels per delta row (virt): max touched list (delta)
                                 // or C_out (whole-node recompute)
-  std::vector<int> vchmap;      // virt: [slot][C_out] channel map (-2-t = delta channel t)
+  std::vector<int> vchmap;      // virt, vhalo: [slot][C_out] channel map (-2-t = delta channel t)
+  bool vhalo = false;           // the halo kernel reads mmi's output in 8-channel groups:
+                                // each slot's changed groups materialised, the others
+                                // from the cache (needs the ADD fused, see fused_add_of)
 };
 
 struct Plan {
@@ -176,6 +179,10 @@ struct Plan {
   // ledger, per input
   int64_t macs_vanilla = 0, macs_memoized = 0, macs_algorithmic = 0, macs_executed = 0;
 };
+
+// The ADD node fused into convolution v's epilogue (v's only reader, reading
+// it as in[0]), or -1.
+int fused_add_of(const Graph& g, int v);
 
 // Memoization boundary K of a first mutated layer (Algorithm 1 / Section 4).
 std::vector<int> boundary(const Graph& g, int mmi);

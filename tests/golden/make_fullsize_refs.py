@@ -41,7 +41,7 @@ import workloads as W  # noqa: E402
 
 # name: (config, ratio index, mutants, spread inputs, smallest-margin inputs, screened prefix)
 SAMPLES = {
-    "resnet18w": ("resnet18w", 0, 6, 96, 32, 1024),
+    "resnet18w": ("resnet18w", 0, 6, 97, 32, 1024),
     "vgg_r0": ("vgg", 0, 16, 48, 16, 2048),
     "vgg_r1": ("vgg", 1, 16, 48, 16, 2048),
     "vgg_r2": ("vgg", 2, 16, 48, 16, 2048),

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) == set(B.EXPORTED)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.mure_version() == 4
+    assert lib.mure_version() == 5
 
 
 def _plan_ctx(model):

@@ -232,6 +232,23 @@ def test_fused_paths_equal_separate_kernels(cfg):
         assert np.array_equal(m1.get_logits(mid).cpu().numpy(), m2.get_logits(mid).cpu().numpy()), mid
 
 
+@pytest.mark.parametrize("cfg", ["resnet18w", "vgg"])
+def test_group_reads_equal_per_mutant_copies(cfg):
+    """The halo kernel reading the first mutated node's output (and a fused
+    identity shortcut) in 8-channel groups -- the cached groups shared, only
+    each mutant's changed groups copied -- gives exactly the results of a full
+    copy per mutant."""
+    wl = W.make_workload(cfg, n_inputs=70 if cfg == "resnet18w" else 130, n_mutants=12,
+                         ops=(W.GF, W.NEB, W.NAI, W.NS, W.WS))
+    m1, w1, k1, s1 = run_gpu(wl)
+    planes = m1.stats()["group_planes"]
+    m2, w2, k2, s2 = run_gpu(wl, group_reads=0)
+    assert planes > 0 and m2.stats()["group_planes"] == 0
+    assert np.array_equal(w1, w2) and np.array_equal(k1, k2) and s1 == s2
+    for mid in sample_mutants(m1, wl):
+        assert np.array_equal(m1.get_logits(mid).cpu().numpy(), m2.get_logits(mid).cpu().numpy()), mid
+
+
 def _fp32_cnn():
     """A small fp32 CNN whose convolutions take the LDS kernel's other
     instances and the fp32 im2col kernel:
