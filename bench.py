@@ -111,6 +111,15 @@ def read_traffic(kernel: str, config: str, n_inputs: int, n_mutants: int):
     return None
 
 
+# kernels of one family (the library times a family's launches together)
+FAMILY_KERNELS = {"lstm_kernel": ("lstm_kernel", "lstm_wide_kernel"),
+                  "dw_col_kernel": ("dw_col_kernel", "dw_full_kernel", "dw_list_kernel")}
+
+
+def _in_family(kernel: str, name: str) -> bool:
+    return any(k in name for k in FAMILY_KERNELS.get(kernel, (kernel,)))
+
+
 def _run_mutants_windows(rows):
     """Dispatch ids bracketing each run_mutants call: after run_original's
     label kernel, up to and including the score kernel."""
@@ -144,7 +153,7 @@ def summarize_pmc(fetch_csv: str, write_csv: str, kernel: str, args) -> str:
         wins = _run_mutants_windows(rows)
         for r in rows:
             d = int(r["Dispatch_Id"])
-            if kernel in r["Kernel_Name"] and any(a < d < b for a, b in wins):
+            if _in_family(kernel, r["Kernel_Name"]) and any(a < d < b for a, b in wins):
                 per.setdefault(d, {})[ctr] = float(r["Counter_Value"]) * 1024.0 * calib[ctr]
     ids = sorted(per)
     fetch = sum(per[d].get("FETCH_SIZE", 0.0) for d in ids)
@@ -183,7 +192,7 @@ def summarize_trace(trace_csv: str, stats_csv: str, kernel: str, args) -> str:
     trace = sorted(csv.DictReader(open(trace_csv)), key=lambda r: int(r["Dispatch_Id"]))
     wins = _run_mutants_windows(trace)[args.warmup:args.warmup + args.steps]
     durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6 for r in trace
-            if kernel in r["Kernel_Name"] and any(a < int(r["Dispatch_Id"]) < b for a, b in wins)]
+            if _in_family(kernel, r["Kernel_Name"]) and any(a < int(r["Dispatch_Id"]) < b for a, b in wins)]
     cmd = ("cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats --output-format csv "
            "-d <dir> -o kt -- python3 bench.py --config %s --steps %d --warmup %d"
            % (args.config, args.steps, args.warmup))
