@@ -61,12 +61,25 @@ __device__ __forceinline__ float tanhf_(float z) { return 2.f * sigmoidf_(2.f * 
 static __device__ __attribute__((aligned(16))) v4f g_lstm_zero[1] = {};
 __device__ __forceinline__ const float* lstm_zero() { return reinterpret_cast<const float*>(g_lstm_zero); }
 
+// Block b -> (slot, block of 64 input rows).  Block b runs on XCD b % 8; on
+// one XCD consecutive blocks take every slot of one row block in turn, so a
+// row block of a shared input (a prefix-cache tensor, read by every slot)
+// comes from HBM once and the other slots' reads hit that XCD's L2.  false:
+// padding of that order.
+__device__ __forceinline__ bool lstm_decode(const SeqArgs& a, int& sl, int& rb) {
+  const int b = (int)blockIdx.x, turn = b >> 3;
+  rb = (turn / a.nslots) * 8 + (b & 7);
+  sl = a.slot0 + turn % a.nslots;
+  return rb * 64 < a.nx;
+}
+
 template <int HT>                                      // H = 16 * HT units
 __global__ __launch_bounds__(256) void lstm_kernel(SeqArgs a) {
   extern __shared__ __attribute__((aligned(16))) float lsm[];
   constexpr int H = 16 * HT, NT = 4 * HT, NS = 4 * H + 16;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int sl = a.slot0 + (int)blockIdx.y;
+  int sl, rb;
+  if (!lstm_decode(a, sl, rb)) return;
   const int D = a.D, K = D + H + 1;
   const int KP = lstm_kpad(D, H), KA = lstm_ka(D, H);
   float* Ws = lsm;                                     // [KP][NS]
@@ -85,7 +98,7 @@ __global__ __launch_bounds__(256) void lstm_kernel(SeqArgs a) {
   }
   __syncthreads();
 
-  const int xi0 = (int)blockIdx.x * 64 + wave * 16;    // this wave's 16 rows
+  const int xi0 = rb * 64 + wave * 16;                 // this wave's 16 rows
   const float* __restrict__ X = reinterpret_cast<const float*>(a.in.p);
   float* __restrict__ Y = reinterpret_cast<float*>(a.out);
   float* A = As + wave * 16 * KA;
@@ -200,7 +213,8 @@ __global__ __launch_bounds__(256, 1) void lstm_wide_kernel(SeqArgs a) {
   typedef __attribute__((address_space(3))) void lds_void;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int NW = (int)blockDim.x / 64;                 // = H / 16
-  const int sl = a.slot0 + (int)blockIdx.y;
+  int sl, rb;
+  if (!lstm_decode(a, sl, rb)) return;
   const int D = a.D, H = a.H, K = D + H + 1, DS = D / 4;
   // LDS: two step tiles [KS][64][4]: [x_t, h_{t-1}, 1, zeros] of step t in
   // tile t % 2
@@ -221,7 +235,7 @@ __global__ __launch_bounds__(256, 1) void lstm_wide_kernel(SeqArgs a) {
     const int k = D + (r >> 8) * 4 + (r & 3);
     lsm[(b * KS + DS) * 256 + r] = k == D + H ? 1.f : 0.f;
   }
-  const int xi0 = (int)blockIdx.x * 64;
+  const int xi0 = rb * 64;
   const float* __restrict__ X = reinterpret_cast<const float*>(a.in.p);
   float* __restrict__ Y = reinterpret_cast<float*>(a.out);
   auto in_row = [&](int xi) {
@@ -324,7 +338,9 @@ hipError_t launch_embed(const SeqArgs& a, hipStream_t s) {
 hipError_t launch_lstm(const SeqArgs& a, hipStream_t s) {
   if (a.nslots <= 0 || a.nx <= 0) return hipSuccess;
   if (a.H % 16 || a.H < 16 || a.H > 64 || a.nslots > 65535) return hipErrorInvalidValue;
-  dim3 grid((unsigned)((a.nx + 63) / 64), (unsigned)a.nslots);
+  const int64_t nblk = ((int64_t)(a.nx + 63) / 64 + 7) / 8 * 8 * a.nslots;
+  if (nblk >= INT32_MAX) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)nblk);
   if (lstm_uses_wide(a.D, a.H)) {
     if (!lstm_wide_fits(a.D, a.H) || a.in.row_elems % 4) return hipErrorInvalidValue;
     const int ks = lstm_wide_ks(a.D, a.H);
