@@ -73,15 +73,21 @@ struct HaloTile {
 // When bands are parts of one image (H > TR) each XCD takes a contiguous run
 // of a slot's bands, so that the blocks running together on it share the
 // rows above and below their bands in its L2 (width 64 on resnet18w: 5.85 ->
-// 5.39 ms per launch); bands of whole images go round-robin.  false: t is
-// padding of that order.
+// 5.39 ms per launch); bands of whole images go round-robin.  When every slot
+// reads the same input (a prefix-cache tensor, or the cached groups of a
+// channel-group read), the slots of a (band, column block) take consecutive
+// turns instead of the slots coming one after another, so that the band is
+// fetched once per XCD.  false: t is padding of that order.
 template <int W, int TN>
 __device__ __forceinline__ bool halo_decode(const ConvArgs& a, int t, HaloTile& tl) {
   using G = HaloGeo<W, TN>;
   const int bgroups = (a.bands + 7) / 8;
   const int xcd = t & 7, turn = t >> 3, per_slot = bgroups * a.zblocks;
-  const int si = turn / per_slot, rem = turn % per_slot;
-  const int band = a.H > G::TR ? xcd * bgroups + rem / a.zblocks : (rem / a.zblocks) * 8 + xcd;
+  const bool slot_inner = a.in.mode == MODE_CACHE || a.gin.cache != nullptr;
+  const int si = slot_inner ? turn % a.halo_slots : turn / per_slot;
+  const int rem = slot_inner ? turn / a.halo_slots : turn % per_slot;
+  const int bi = rem / a.zblocks;
+  const int band = a.H > G::TR ? xcd * bgroups + bi : bi * 8 + xcd;
   if (band >= a.bands) return false;
   tl.slot = a.slot0 + si;
   tl.n0 = (rem % a.zblocks) * G::BN;
