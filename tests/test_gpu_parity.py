@@ -159,7 +159,7 @@ def test_weight_shuffle_operator():
                                 ops=(W.GF, W.NEB, W.NAI, W.NS, W.WS)))
 
 
-@pytest.mark.parametrize("cfg", ["lenet5", "vgg", "resnet20", "mobilenetv2", "lstm", "rnn_imdb"])
+@pytest.mark.parametrize("cfg", ["lenet5", "vgg", "resnet20", "mobilenetv2", "lstm", "rnn_imdb", "resnet18w"])
 def test_vanilla_mode_equals_memoized_bit_for_bit(cfg):
     """Theorem 1 on the GPU: running every mutant from the raw input gives
     exactly the memoized result -- kill bits, score and logits, bit for bit."""
