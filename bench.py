@@ -371,6 +371,13 @@ def main():
         "ms_run_mutants": ms_mut,
         "ms_run_original": float(np.median([s["ms_run_original"] for s in stats])),
         "ms_apply": float(np.median([s["ms_apply"] for s in stats])),
+        # where a step's device time goes: a2 apply, a3 the original forward,
+        # a4 the first mutated nodes, a5 + a6 the suffix layers and the kill /
+        # score reduction (run_mutants minus a4)
+        "time_split_ms": {"a2_apply": float(np.median([s["ms_apply"] for s in stats])),
+                          "a3_run_original": float(np.median([s["ms_run_original"] for s in stats])),
+                          "a4_first_mutated": float(np.median([s["ms_mmi"] for s in stats])),
+                          "a5_a6_suffix_and_kill": ms_mut - float(np.median([s["ms_mmi"] for s in stats]))},
         "mutation_score": [score["ms_num"], score["ms_den"]],
         "roofline": {**roof, "kernel": KERNELS[fam],
                      "traffic": tr["traffic_bytes_per_launch"] if tr else None,

@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define MURE_VERSION 5
+#define MURE_VERSION 6
 #define MURE_N_KERNELS 9   /* kernel families in mure_stats */
 /* Device scratch of mure_run_mutants_noalloc: a fixed array per GPU. */
 #define MURE_NOALLOC_SCRATCH_BYTES (256u << 20)
@@ -195,6 +195,10 @@ typedef struct {
    * halo convolutions that read that output in channel groups (option
    * "group_reads"); 0 when every consumer read per-mutant copies. */
   int64_t group_planes;
+  /* With option "kernel_timing" = 1: the part of ms_gemm spent computing the
+   * clusters' first mutated nodes (the deltas of Section 3's memoized
+   * execution), the rest being the suffix after them. */
+  double ms_mmi;
 } mure_stats;
 
 /* Version of this interface (MURE_VERSION). */

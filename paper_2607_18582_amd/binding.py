@@ -23,7 +23,7 @@ MURE_OK, MURE_E_INVALID, MURE_E_STATE, MURE_E_NOMEM, MURE_E_DEVICE, MURE_E_UNSUP
 STATUS_NAMES = {0: "MURE_OK", -1: "MURE_E_INVALID", -2: "MURE_E_STATE", -3: "MURE_E_NOMEM",
                 -4: "MURE_E_DEVICE", -5: "MURE_E_UNSUPPORTED"}
 MURE_F32, MURE_BF16 = 0, 1
-MURE_VERSION = 5
+MURE_VERSION = 6
 N_KERNELS = 9                                   # kernel families in mure_stats (MURE_N_KERNELS)
 OP_GAUSS_FUZZ, OP_EFFECT_BLOCK, OP_ACT_INVERSE, OP_NEURON_SWITCH, OP_WEIGHT_SHUFFLE = 0, 1, 2, 3, 4
 INPUT, DENSE, CONV2D, ADD, GAP, FLATTEN, DWCONV, EMBED, LSTM = 0, 1, 2, 3, 4, 5, 6, 7, 8
@@ -67,7 +67,7 @@ class mure_stats(C.Structure):
                 ("kernel_ms", C.c_double * N_KERNELS), ("kernel_macs_algorithmic", C.c_int64 * N_KERNELS),
                 ("kernel_bytes_algorithmic", C.c_double * N_KERNELS),
                 ("n_classes", C.c_int64), ("n_inputs", C.c_int64), ("n_mutants", C.c_int64),
-                ("group_planes", C.c_int64)]
+                ("group_planes", C.c_int64), ("ms_mmi", C.c_double)]
 
 
 def _pack(arrays, R: int, dtype):

@@ -196,6 +196,7 @@ struct mure_ctx {
   int64_t vanilla = 0;
   std::vector<hipEvent_t> tevents;                    // pairs around timed launches
   std::vector<int> tevent_family;                     // kernel family of each timed pair
+  std::vector<char> tevent_mmi;                       // ... and whether it computed a first mutated node
   size_t tevents_used = 0;
   mure_stats stats{};
 
@@ -250,6 +251,7 @@ struct Extra {
   int fuse_add = -1;                  // ADD node fused into this convolution's epilogue
   Where skip{nullptr, MODE_BUF};      // that ADD's shortcut input
   const KillArgs* kill = nullptr;     // fuse the kill reduction when possible
+  bool at_mmi = false;                // the launch computes a cluster's first mutated node
   bool* kill_fused = nullptr;
 };
 
@@ -400,6 +402,7 @@ mure_status exec_node(mure_ctx* ctx, int v, const std::vector<Where>& ins, void*
       if (ee != hipSuccess) return ctx->dev_fail(ee, "hipEventRecord");
       ctx->tevents_used += 2;
       ctx->tevent_family.push_back(fam);
+      ctx->tevent_mmi.push_back(ex.at_mmi ? 1 : 0);
       ctx->stats.gemm_launches++;
       ctx->stats.gemm_macs_algorithmic += alg_macs;
       ctx->stats.gemm_macs_executed += exec_macs;
@@ -1144,6 +1147,7 @@ static mure_status run_group(mure_ctx* ctx, int gi, int s_begin, int s_end, uint
           }
           const int64_t per_ch = nm.macs / nm.c_out;
           Extra ex;
+          ex.at_mmi = true;
           int launch_slots = rec_end - cs0;
           if (gr.delta) {
             if (gr.virt || vh) ex.delta_T = gr.T;
@@ -1323,6 +1327,7 @@ static mure_status run_mutants_impl(mure_ctx* ctx, uint64_t* kill_bits_dev, int6
   } restore{ctx, timing};
   ctx->stats.launches = 0;
   ctx->stats.group_planes = 0;
+  ctx->stats.ms_mmi = 0;
   ctx->stats.gemm_launches = 0;
   ctx->stats.ms_gemm = 0;
   ctx->stats.gemm_macs_algorithmic = 0;
@@ -1335,6 +1340,7 @@ static mure_status run_mutants_impl(mure_ctx* ctx, uint64_t* kill_bits_dev, int6
   }
   ctx->tevents_used = 0;
   ctx->tevent_family.clear();
+  ctx->tevent_mmi.clear();
   HIPTRY(hipEventRecord(ctx->ev0, ctx->stream));
   if (noalloc) {
     // zero fills as kernels (no memset nodes in work a caller may capture)
@@ -1366,9 +1372,11 @@ static mure_status run_mutants_impl(mure_ctx* ctx, uint64_t* kill_bits_dev, int6
     HIPTRY(hipEventElapsedTime(&t, ctx->tevents[i], ctx->tevents[i + 1]));
     ctx->stats.ms_gemm += t;
     ctx->stats.kernel_ms[ctx->tevent_family[i / 2]] += t;
+    if (ctx->tevent_mmi[i / 2]) ctx->stats.ms_mmi += t;
   }
   ctx->tevents_used = 0;
   ctx->tevent_family.clear();
+  ctx->tevent_mmi.clear();
   std::vector<int64_t> kills(M);
   std::vector<unsigned long long> masks(M * mw);
   unsigned long long nonfinite = 0;

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) == set(B.EXPORTED)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.mure_version() == 5
+    assert lib.mure_version() == 6
 
 
 def _plan_ctx(model):
