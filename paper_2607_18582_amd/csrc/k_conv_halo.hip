@@ -319,11 +319,11 @@ __device__ __forceinline__ void halo_skip(const ConvArgs& a, const HaloTile& tl,
       skipv[k] = *reinterpret_cast<const v4u*>(p);
       continue;
     }
+    // an identity shortcut read whole goes through the two-pass epilogue;
+    // what reaches here is option A
     const bf16_t* sp = reinterpret_cast<const bf16_t*>(a.skip.p) +
                        row_index(a.skip.mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0) * a.skip.row_elems;
-    if (a.add_mode == 1) {
-      skipv[k] = *reinterpret_cast<const v4u*>(sp + ((int64_t)y * W + x) * a.Cout + n);
-    } else {
+    {
       // option A: the skip subsampled by 2 and zero-padded in channels; with
       // the padding and C_s multiples of 8 a vector is wholly inside or out
       const int cs0 = n - (a.Cout - a.Cs) / 2;
@@ -373,6 +373,106 @@ __device__ __forceinline__ void halo_store_rows(const ConvArgs& a, const HaloTil
         val;
   }
 }
+// ---- epilogue in two passes for an identity shortcut ----
+// Pass P stores the 256 band pixels of M tiles 2P and 2P + 1 of every wave;
+// its local pixel ml is band pixel halo_pass_pixel(P, ml).  Pass 0's
+// shortcut rows are brought into the stage the last chunk left free by direct
+// loads issued with that chunk's MFMAs; pass 1's are loaded into registers
+// once pass 0 is staged, under pass 0's stores.
+__device__ __forceinline__ int halo_pass_pixel(int P, int ml) { return (ml >> 6) * 128 + P * 64 + (ml & 63); }
+
+// The shortcut row of input xi (relative to the launch).
+__device__ __forceinline__ const bf16_t* halo_skip_row(const ConvArgs& a, const HaloTile& tl, int xi) {
+  return reinterpret_cast<const bf16_t*>(a.skip.p) +
+         row_index(a.skip.mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0) * a.skip.row_elems;
+}
+
+// Pass 0's shortcut into F as [pixel ml][BN] (16-byte piece p = ml VPR + vc
+// at F + 16 p): wave w issues pieces 64 q + lane for q = w, w + 4, ...
+template <int W, int TN>
+__device__ __forceinline__ void halo_skip_dma(const ConvArgs& a, const HaloTile& tl, int RI, int wave, int lane,
+                                              unsigned char* F, const bf16_t* zp) {
+  using G = HaloGeo<W, TN>;
+#pragma unroll
+  for (int q = wave; q < 4 * G::VPR; q += 4) {
+    const int pc = q * 64 + lane, ml = pc / G::VPR, vc = pc % G::VPR;
+    const int n = tl.n0 + vc * 8;
+    int xi, y, x;
+    halo_pixel<W>(tl, RI, halo_pass_pixel(0, ml), xi, y, x);
+    const bf16_t* src = zp;
+    if (n < a.Cout && xi < a.nx) src = halo_skip_row(a, tl, xi) + ((int64_t)y * W + x) * a.Cout + n;
+    __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)(F + q * 1024), 16, 0, 0);
+  }
+}
+
+// Pass 1's shortcut vectors idx = tid + NT k (pixel ml = idx / VPR) into registers.
+template <int W, int TN>
+__device__ __forceinline__ void halo_skip_pass1(const ConvArgs& a, const HaloTile& tl, int RI, int tid,
+                                                v4u (&sk)[HaloGeo<W, TN>::VPR]) {
+  using G = HaloGeo<W, TN>;
+#pragma unroll
+  for (int k = 0; k < G::VPR; ++k) {
+    const int idx = tid + G::NT * k, ml = idx / G::VPR, n = tl.n0 + (idx % G::VPR) * 8;
+    int xi, y, x;
+    halo_pixel<W>(tl, RI, halo_pass_pixel(1, ml), xi, y, x);
+    sk[k] = v4u{0u, 0u, 0u, 0u};
+    if (n < a.Cout && xi < a.nx) sk[k] = *reinterpret_cast<const v4u*>(halo_skip_row(a, tl, xi) + ((int64_t)y * W + x) * a.Cout + n);
+  }
+}
+
+// Bias, activation and bf16 rounding of M tiles 2P and 2P + 1 of a wave's
+// accumulators (the other two stay in their registers until their pass), and
+// the rounded pixels into Os ([ml][OLD]).
+template <int W, int TN>
+__device__ __forceinline__ void halo_stage_pass(const ConvArgs& a, const HaloTile& tl, bf16_t* Os, int wave, int P,
+                                                int lane, const v16f (&acc)[4][TN]) {
+  using G = HaloGeo<W, TN>;
+  const int h = lane >> 5;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int nc = tl.n0 + j * 32 + (lane & 31);
+    const float bv = nc < a.Cout ? a.btab[tl.slot][nc] : 0.f;
+#pragma unroll
+    for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+      for (int e = 0; e < 16; e += 2) {
+        const int r = wave * 64 + ii * 32 + (e >> 2) * 8 + h * 4 + (e & 3);
+        const v16f& ac = acc[2 * P + ii][j];
+        const uint32_t v = f2bf2(act(ac[e] + bv, a.relu), act(ac[e + 1] + bv, a.relu));
+        Os[r * G::OLD + j * 32 + (lane & 31)] = (bf16_t)v;
+        Os[(r + 1) * G::OLD + j * 32 + (lane & 31)] = (bf16_t)(v >> 16);
+      }
+  }
+}
+
+// Pass P's output rows with the shortcut (from F for pass 0, sk for pass 1)
+// added in float32 before its activation.
+template <int W, int TN>
+__device__ __forceinline__ void halo_store_pass(const ConvArgs& a, const HaloTile& tl, int RI, int P, int tid,
+                                                const bf16_t* Os, const unsigned char* F,
+                                                const v4u (&sk)[HaloGeo<W, TN>::VPR]) {
+  using G = HaloGeo<W, TN>;
+#pragma unroll
+  for (int k = 0; k < G::VPR; ++k) {
+    const int idx = tid + G::NT * k, ml = idx / G::VPR, vc = idx % G::VPR;
+    const int n = tl.n0 + vc * 8;
+    if (n >= a.Cout) continue;
+    int xi, y, x;
+    halo_pixel<W>(tl, RI, halo_pass_pixel(P, ml), xi, y, x);
+    if (xi >= a.nx) continue;
+    v4u val = *reinterpret_cast<const v4u*>(&Os[ml * G::OLD + vc * 8]);
+    const v4u sv = P == 0 ? *reinterpret_cast<const v4u*>(F + idx * 16) : sk[k];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float t0 = act(bf2f((bf16_t)val[w]) + bf2f((bf16_t)sv[w]), a.add_relu);
+      const float t1 = act(bf2f((bf16_t)(val[w] >> 16)) + bf2f((bf16_t)(sv[w] >> 16)), a.add_relu);
+      val[w] = f2bf2(t0, t1);
+    }
+    const int64_t ro = row_index(a.out_mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0);
+    *reinterpret_cast<v4u*>(reinterpret_cast<bf16_t*>(a.out) + ro * a.out_row + ((int64_t)y * W + x) * a.Cout + n) =
+        val;
+  }
+}
 }  // namespace
 
 // Zero bytes that out-of-image halo pixels and columns past the last read.
@@ -399,6 +499,9 @@ void conv_halo_kernel(ConvArgs a) {
   const int npx = (G::TR / RI) * (RI + 2) * W;
   const bf16_t* const zp = reinterpret_cast<const bf16_t*>(g_halo_zero);
   const int nch = a.C / 16;
+  // an identity shortcut of the whole tile's rows: the two-pass epilogue
+  const bool split = !VSKIP && !a.cols && !a.pool && a.add_mode == 1;
+  static_assert(256 * G::OLD * 2 <= G::STAGE && 256 * G::BN * 2 <= G::STAGE, "a pass fits one stage");
 
   const bf16_t* src[G::QPW];
   halo_sources<W, TN, VIN>(a, tl, RI, npx, wave, lane, src);
@@ -427,24 +530,42 @@ void conv_halo_kernel(ConvArgs a) {
   halo_fetch<W, TN, VIN>(smem, src, npx, wave, lane, 0, zp, gb, gst);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  for (int c = 0; c < nch; ++c) {
-    if (c + 1 < nch) {
-      if constexpr (VIN) halo_group_bases(a.gin, tl.slot, a.nx, (c + 1) * 16, gb, gst);
-      halo_fetch<W, TN, VIN>(smem + ((c + 1) & 1) * G::STAGE, src, npx, wave, lane, (c + 1) * 16, zp, gb, gst);
-    }
+  for (int c = 0; c + 1 < nch; ++c) {
+    if constexpr (VIN) halo_group_bases(a.gin, tl.slot, a.nx, (c + 1) * 16, gb, gst);
+    halo_fetch<W, TN, VIN>(smem + ((c + 1) & 1) * G::STAGE, src, npx, wave, lane, (c + 1) * 16, zp, gb, gst);
     halo_mma<W, TN>(smem + (c & 1) * G::STAGE, abase, zoff, edge, bbase, acc);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
+  // the last chunk, outside the loop: its free stage receives pass 0's shortcut
+  if (split) halo_skip_dma<W, TN>(a, tl, RI, wave, lane, smem + (nch & 1) * G::STAGE, zp);
+  halo_mma<W, TN>(smem + ((nch - 1) & 1) * G::STAGE, abase, zoff, edge, bbase, acc);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
 
   // ---- epilogue: bias, activation, bf16 rounding, staged in LDS ----
-  v4u skipv[NV];
-  if (!a.cols && !a.pool && a.add_mode) halo_skip<W, TN, BM, VSKIP>(a, tl, RI, 0, tid, skipv, skip_e);
+  if (split) {
+    // two passes of 256 pixels through the last chunk's stage
+    bf16_t* Os = reinterpret_cast<bf16_t*>(smem + ((nch - 1) & 1) * G::STAGE);
+    const unsigned char* F = smem + (nch & 1) * G::STAGE;
+    halo_stage_pass<W, TN>(a, tl, Os, wave, 0, lane, acc);
+    v4u sk[VPR];                                         // pass 1's shortcut, under pass 0's stores
+    halo_skip_pass1<W, TN>(a, tl, RI, tid, sk);
+    __syncthreads();
+    halo_store_pass<W, TN>(a, tl, RI, 0, tid, Os, F, sk);
+    __syncthreads();
+    halo_stage_pass<W, TN>(a, tl, Os, wave, 1, lane, acc);
+    __syncthreads();
+    halo_store_pass<W, TN>(a, tl, RI, 1, tid, Os, F, sk);
+    return;
+  }
   {
     uint32_t ob[4][TN][8];
     halo_round<TN>(a, tl, lane, acc, ob);
     halo_stage<W, TN>(reinterpret_cast<bf16_t*>(smem), wave * 128, lane, ob);
   }
+  v4u skipv[NV];
+  if (!a.cols && !a.pool && a.add_mode) halo_skip<W, TN, BM, VSKIP>(a, tl, RI, 0, tid, skipv, skip_e);
   __syncthreads();
   const bf16_t* Os = reinterpret_cast<const bf16_t*>(smem);   // [BM][OLD]
   auto pixel = [&](int m, int& xi, int& y, int& x) { halo_pixel<W>(tl, RI, m, xi, y, x); };
