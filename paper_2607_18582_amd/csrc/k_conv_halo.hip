@@ -293,11 +293,11 @@ __device__ __forceinline__ void halo_pixel(const HaloTile& tl, int RI, int m, in
 }
 
 // A fused ADD's shortcut vectors for the output vectors idx = tid + NT k of
-// the pixels [m0, m0 + PB) (pixel idx / VPR, channels 8 (idx % VPR)),
-// requested before the staging so that their latency overlaps it.
-template <int W, int TN, int PB, bool VSKIP>
+// the pixels [m0, m0 + PB) (pixel idx / VPR, channels 8 (idx % VPR)): option
+// A, or (IDENT) an identity shortcut read whole.
+template <int W, int TN, int PB, bool IDENT>
 __device__ __forceinline__ void halo_skip(const ConvArgs& a, const HaloTile& tl, int RI, int m0, int tid,
-                                          v4u (&skipv)[PB * HaloGeo<W, TN>::VPR / HaloGeo<W, TN>::NT], int skip_e) {
+                                          v4u (&skipv)[PB * HaloGeo<W, TN>::VPR / HaloGeo<W, TN>::NT]) {
   using G = HaloGeo<W, TN>;
   constexpr int NV = PB * G::VPR / G::NT;
 #pragma unroll
@@ -307,35 +307,25 @@ __device__ __forceinline__ void halo_skip(const ConvArgs& a, const HaloTile& tl,
     halo_pixel<W>(tl, RI, m, xi, y, x);
     skipv[k] = v4u{0u, 0u, 0u, 0u};
     if (n >= a.Cout || xi >= a.nx) continue;
-    if constexpr (VSKIP) {
-      // identity shortcut read in channel groups; skip_e is the side plane of
-      // this thread's group (its n is the same for every k), looked up before
-      // the k loop
-      const GroupIn& gs = a.gskip;
-      const int e = skip_e;
-      const int64_t pix = (int64_t)xi * gs.P + y * W + x;
-      const bf16_t* p = e < 0 ? reinterpret_cast<const bf16_t*>(gs.cache) + pix * gs.C + n
-                              : reinterpret_cast<const bf16_t*>(gs.side) + (int64_t)(e - gs.g0) * a.nx * gs.P * 8 + pix * 8;
-      skipv[k] = *reinterpret_cast<const v4u*>(p);
-      continue;
+    if constexpr (IDENT) {
+      if (a.add_mode == 1) {
+        skipv[k] = *reinterpret_cast<const v4u*>(halo_skip_at<W, false>(a, tl, xi, y, x, n, -1));
+        continue;
+      }
     }
-    // an identity shortcut read whole goes through the two-pass epilogue;
-    // what reaches here is option A
+    // option A: the skip subsampled by 2 and zero-padded in channels; with the
+    // padding and C_s multiples of 8 a vector is wholly inside or out
     const bf16_t* sp = reinterpret_cast<const bf16_t*>(a.skip.p) +
                        row_index(a.skip.mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0) * a.skip.row_elems;
-    {
-      // option A: the skip subsampled by 2 and zero-padded in channels; with
-      // the padding and C_s multiples of 8 a vector is wholly inside or out
-      const int cs0 = n - (a.Cout - a.Cs) / 2;
-      const bf16_t* px = sp + ((int64_t)(2 * y) * a.Ws + 2 * x) * a.Cs;
-      if (((a.Cout - a.Cs) / 2) % 8 == 0 && a.Cs % 8 == 0) {
-        if (cs0 >= 0 && cs0 < a.Cs) skipv[k] = *reinterpret_cast<const v4u*>(px + cs0);
-      } else {
+    const int cs0 = n - (a.Cout - a.Cs) / 2;
+    const bf16_t* px = sp + ((int64_t)(2 * y) * a.Ws + 2 * x) * a.Cs;
+    if (((a.Cout - a.Cs) / 2) % 8 == 0 && a.Cs % 8 == 0) {
+      if (cs0 >= 0 && cs0 < a.Cs) skipv[k] = *reinterpret_cast<const v4u*>(px + cs0);
+    } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int cs = cs0 + e;
-          if (cs >= 0 && cs < a.Cs) skipv[k][e >> 1] |= (uint32_t)px[cs] << (16 * (e & 1));
-        }
+      for (int e = 0; e < 8; ++e) {
+        const int cs = cs0 + e;
+        if (cs >= 0 && cs < a.Cs) skipv[k][e >> 1] |= (uint32_t)px[cs] << (16 * (e & 1));
       }
     }
   }
@@ -381,17 +371,30 @@ __device__ __forceinline__ void halo_store_rows(const ConvArgs& a, const HaloTil
 // once pass 0 is staged, under pass 0's stores.
 __device__ __forceinline__ int halo_pass_pixel(int P, int ml) { return (ml >> 6) * 128 + P * 64 + (ml & 63); }
 
-// The shortcut row of input xi (relative to the launch).
-__device__ __forceinline__ const bf16_t* halo_skip_row(const ConvArgs& a, const HaloTile& tl, int xi) {
+// The identity shortcut's channels n .. n + 7 at output pixel (xi, y, x): from
+// whole rows, or (VSKIP) read in channel groups, from the shared cache or from
+// side plane e of the group (e < 0: unchanged, in the cache).  e is looked up
+// once per thread: its channels are the same at every pixel it handles.
+template <int W, bool VSKIP>
+__device__ __forceinline__ const bf16_t* halo_skip_at(const ConvArgs& a, const HaloTile& tl, int xi, int y, int x,
+                                                      int n, int e) {
+  if constexpr (VSKIP) {
+    const GroupIn& gs = a.gskip;
+    const int64_t pix = (int64_t)xi * gs.P + y * W + x;
+    return e < 0 ? reinterpret_cast<const bf16_t*>(gs.cache) + pix * gs.C + n
+                 : reinterpret_cast<const bf16_t*>(gs.side) + (int64_t)(e - gs.g0) * a.nx * gs.P * 8 + pix * 8;
+  }
   return reinterpret_cast<const bf16_t*>(a.skip.p) +
-         row_index(a.skip.mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0) * a.skip.row_elems;
+         row_index(a.skip.mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0) * a.skip.row_elems +
+         ((int64_t)y * W + x) * a.Cout + n;
 }
 
 // Pass 0's shortcut into F as [pixel ml][BN] (16-byte piece p = ml VPR + vc
-// at F + 16 p): wave w issues pieces 64 q + lane for q = w, w + 4, ...
-template <int W, int TN>
+// at F + 16 p): wave w issues pieces 64 q + lane for q = w, w + 4, ...; a
+// lane's vc is lane % VPR, the same as its thread's in the passes.
+template <int W, int TN, bool VSKIP>
 __device__ __forceinline__ void halo_skip_dma(const ConvArgs& a, const HaloTile& tl, int RI, int wave, int lane,
-                                              unsigned char* F, const bf16_t* zp) {
+                                              unsigned char* F, const bf16_t* zp, int skip_e) {
   using G = HaloGeo<W, TN>;
 #pragma unroll
   for (int q = wave; q < 4 * G::VPR; q += 4) {
@@ -400,15 +403,15 @@ __device__ __forceinline__ void halo_skip_dma(const ConvArgs& a, const HaloTile&
     int xi, y, x;
     halo_pixel<W>(tl, RI, halo_pass_pixel(0, ml), xi, y, x);
     const bf16_t* src = zp;
-    if (n < a.Cout && xi < a.nx) src = halo_skip_row(a, tl, xi) + ((int64_t)y * W + x) * a.Cout + n;
+    if (n < a.Cout && xi < a.nx) src = halo_skip_at<W, VSKIP>(a, tl, xi, y, x, n, skip_e);
     __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)(F + q * 1024), 16, 0, 0);
   }
 }
 
 // Pass 1's shortcut vectors idx = tid + NT k (pixel ml = idx / VPR) into registers.
-template <int W, int TN>
+template <int W, int TN, bool VSKIP>
 __device__ __forceinline__ void halo_skip_pass1(const ConvArgs& a, const HaloTile& tl, int RI, int tid,
-                                                v4u (&sk)[HaloGeo<W, TN>::VPR]) {
+                                                v4u (&sk)[HaloGeo<W, TN>::VPR], int skip_e) {
   using G = HaloGeo<W, TN>;
 #pragma unroll
   for (int k = 0; k < G::VPR; ++k) {
@@ -416,7 +419,7 @@ __device__ __forceinline__ void halo_skip_pass1(const ConvArgs& a, const HaloTil
     int xi, y, x;
     halo_pixel<W>(tl, RI, halo_pass_pixel(1, ml), xi, y, x);
     sk[k] = v4u{0u, 0u, 0u, 0u};
-    if (n < a.Cout && xi < a.nx) sk[k] = *reinterpret_cast<const v4u*>(halo_skip_row(a, tl, xi) + ((int64_t)y * W + x) * a.Cout + n);
+    if (n < a.Cout && xi < a.nx) sk[k] = *reinterpret_cast<const v4u*>(halo_skip_at<W, VSKIP>(a, tl, xi, y, x, n, skip_e));
   }
 }
 
@@ -500,7 +503,9 @@ void conv_halo_kernel(ConvArgs a) {
   const bf16_t* const zp = reinterpret_cast<const bf16_t*>(g_halo_zero);
   const int nch = a.C / 16;
   // an identity shortcut of the whole tile's rows: the two-pass epilogue
-  const bool split = !VSKIP && !a.cols && !a.pool && a.add_mode == 1;
+  // (not taken by inputs read in channel groups with a shortcut read whole:
+  // slower there, 4.27 against 4.15 ms per width-64 launch on resnet18w)
+  const bool split = (!VIN || VSKIP) && !a.cols && !a.pool && a.add_mode == 1;
   static_assert(256 * G::OLD * 2 <= G::STAGE && 256 * G::BN * 2 <= G::STAGE, "a pass fits one stage");
 
   const bf16_t* src[G::QPW];
@@ -538,7 +543,7 @@ void conv_halo_kernel(ConvArgs a) {
     __syncthreads();
   }
   // the last chunk, outside the loop: its free stage receives pass 0's shortcut
-  if (split) halo_skip_dma<W, TN>(a, tl, RI, wave, lane, smem + (nch & 1) * G::STAGE, zp);
+  if (split) halo_skip_dma<W, TN, VSKIP>(a, tl, RI, wave, lane, smem + (nch & 1) * G::STAGE, zp, skip_e);
   halo_mma<W, TN>(smem + ((nch - 1) & 1) * G::STAGE, abase, zoff, edge, bbase, acc);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
@@ -550,7 +555,7 @@ void conv_halo_kernel(ConvArgs a) {
     const unsigned char* F = smem + (nch & 1) * G::STAGE;
     halo_stage_pass<W, TN>(a, tl, Os, wave, 0, lane, acc);
     v4u sk[VPR];                                         // pass 1's shortcut, under pass 0's stores
-    halo_skip_pass1<W, TN>(a, tl, RI, tid, sk);
+    halo_skip_pass1<W, TN, VSKIP>(a, tl, RI, tid, sk, skip_e);
     __syncthreads();
     halo_store_pass<W, TN>(a, tl, RI, 0, tid, Os, F, sk);
     __syncthreads();
@@ -565,7 +570,7 @@ void conv_halo_kernel(ConvArgs a) {
     halo_stage<W, TN>(reinterpret_cast<bf16_t*>(smem), wave * 128, lane, ob);
   }
   v4u skipv[NV];
-  if (!a.cols && !a.pool && a.add_mode) halo_skip<W, TN, BM, VSKIP>(a, tl, RI, 0, tid, skipv, skip_e);
+  if (!a.cols && !a.pool && a.add_mode) halo_skip<W, TN, BM, VIN && !VSKIP>(a, tl, RI, 0, tid, skipv);
   __syncthreads();
   const bf16_t* Os = reinterpret_cast<const bf16_t*>(smem);   // [BM][OLD]
   auto pixel = [&](int m, int& xi, int& y, int& x) { halo_pixel<W>(tl, RI, m, xi, y, x); };
