@@ -292,13 +292,22 @@ def main():
         k, v = kv.split("=", 1)
         m.set_option(k, int(v))
 
+    walls = []                                         # host wall time of each call, per step
+
     def step():
         b0 = (batch[0] % n_batches) * N                # the next batch of the input set
         batch[0] += 1
+        t = [time.perf_counter()]
         m.load_model(md.nodes, md.in_hwc, md.dtype, md.weights, md.biases)
+        t.append(time.perf_counter())
         m.apply(wl.mutants)
+        t.append(time.perf_counter())
         m.run_original(xt[b0:b0 + N])
-        return m.run_mutants(kill)
+        t.append(time.perf_counter())
+        r = m.run_mutants(kill)
+        t.append(time.perf_counter())
+        walls.append(np.diff(t) * 1e3)
+        return r
 
     for _ in range(args.warmup):
         step()
@@ -378,6 +387,11 @@ def main():
                           "a3_run_original": float(np.median([s["ms_run_original"] for s in stats])),
                           "a4_first_mutated": float(np.median([s["ms_mmi"] for s in stats])),
                           "a5_a6_suffix_and_kill": ms_mut - float(np.median([s["ms_mmi"] for s in stats]))},
+        # the same step by host wall time around each call (each returns once
+        # its device work is done): a2 includes marshalling the records and
+        # staging their noise, which the device time above does not see
+        "wall_split_ms": dict(zip(("a1_load_model", "a2_apply_mutants", "a3_run_original", "a4_a6_run_mutants"),
+                                  np.median(walls[args.warmup:args.warmup + args.steps], axis=0).round(2).tolist())),
         "mutation_score": [score["ms_num"], score["ms_den"]],
         "roofline": {**roof, "kernel": KERNELS[fam],
                      "traffic": tr["traffic_bytes_per_launch"] if tr else None,

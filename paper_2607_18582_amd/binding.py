@@ -71,23 +71,29 @@ class mure_stats(C.Structure):
 
 
 def _pack(arrays, R: int, dtype):
-    """Pack the non-None entries of ``arrays`` (length R, or None) into one
-    contiguous pool; returns (pool, address of each record's entry or 0,
-    length of each record's entry or 0).  The per-record iteration runs in
-    C (map, itemgetter) rather than in Python loops."""
+    """Addresses and lengths of the non-None entries of ``arrays`` (length R,
+    or None) for the records' pointer fields; returns (the arrays to keep
+    alive while the call runs, address of each record's entry or 0, length of
+    each record's entry or 0).  Entries already of ``dtype`` and contiguous
+    are passed in place, without a copy: GF noise is fan-in long for every
+    record (hundreds of MB on the large models).  The per-record iteration
+    runs in C (map, itemgetter) rather than in Python loops."""
     addr = np.zeros(R, np.uint64)
     lens = np.zeros(R, np.int64)
     if arrays is None or len(arrays) == 0:
-        return np.zeros(1, dtype), addr, lens
+        return [], addr, lens
     idx = np.flatnonzero(np.fromiter(map(operator.is_not, arrays, itertools.repeat(None)), bool, R))
     if idx.size == 0:
-        return np.zeros(1, dtype), addr, lens
+        return [], addr, lens
     parts = operator.itemgetter(*idx.tolist())(arrays) if idx.size > 1 else (arrays[int(idx[0])],)
+    dt = np.dtype(dtype)
+    parts = [p if isinstance(p, np.ndarray) and p.dtype == dt and p.ndim == 1 and p.flags.c_contiguous
+             else np.ascontiguousarray(p, dt).reshape(-1) for p in parts]
     ln = np.fromiter(map(len, parts), np.int64, idx.size)
-    pool = np.concatenate(parts).astype(dtype, copy=False)
-    addr[idx] = np.where(ln > 0, pool.ctypes.data + pool.itemsize * (np.cumsum(ln) - ln), 0).astype(np.uint64)
+    ad = np.fromiter((p.__array_interface__["data"][0] for p in parts), np.uint64, idx.size)
+    addr[idx] = np.where(ln > 0, ad, 0).astype(np.uint64)
     lens[idx] = ln
-    return pool, addr, lens
+    return parts, addr, lens
 
 
 class MureError(RuntimeError):
@@ -227,8 +233,8 @@ class Mure:
         recs["layer"][:R] = layer
         recs["neuron"][:R] = neuron
         recs["partner"][:R] = partner
-        # per-record arrays (GF noise, WS permutation) are packed into one pool
-        # each and referenced by address and length; one Python pass per list
+        # per-record arrays (GF noise, WS permutation) are referenced by
+        # address and length, in place where their type allows
         pool, ppool = _pack(noise, R, np.float32), _pack(perm, R, np.int32)
         recs["noise"][:R], recs["noise_len"][:R] = pool[1], pool[2]
         wsr = ppool[2] > 0

@@ -12,6 +12,7 @@
 #include <set>
 #include <stdexcept>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "../../include/mure.h"
@@ -626,6 +627,46 @@ static mure_status load_model_impl(mure_ctx* ctx, const mure_layer* layers, int3
   return MURE_OK;
 }
 
+// A run of n 4-byte values at pool offset off, copied from src (zeros where
+// src is null).
+struct PoolSeg {
+  const void* src;
+  int64_t off, n;
+};
+
+// Fill the pool from its runs; a pool of 64 MB or more (GF noise is fan-in
+// long per record: 300 MB on resnet18w) is copied by up to 8 threads, each
+// taking a contiguous range of runs of about equal bytes.
+static void fill_pool(float* dst, const std::vector<PoolSeg>& segs, int64_t pool_n) {
+  auto run = [&](size_t a, size_t b) {
+    for (size_t i = a; i < b; ++i) {
+      const PoolSeg& q = segs[i];
+      if (q.src) std::memcpy(dst + q.off, q.src, (size_t)q.n * 4);
+      else std::memset(dst + q.off, 0, (size_t)q.n * 4);
+    }
+  };
+  const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
+  const int nt = pool_n * 4 >= (int64_t(64) << 20) ? (int)std::min(8u, hw) : 1;
+  if (nt <= 1 || segs.size() < 2) {
+    run(0, segs.size());
+    return;
+  }
+  const int64_t per = pool_n / nt + 1;
+  std::vector<std::thread> th;
+  size_t i0 = 0;
+  int64_t acc = 0;
+  for (size_t i = 0; i < segs.size() && (int)th.size() + 1 < nt; ++i) {
+    acc += segs[i].n;
+    if (acc >= per) {
+      th.emplace_back(run, i0, i + 1);
+      i0 = i + 1;
+      acc = 0;
+    }
+  }
+  run(i0, segs.size());
+  for (auto& t : th) t.join();
+}
+
 static mure_status apply_mutants_impl(mure_ctx* ctx, int32_t n_mutants, const mure_record* records,
                                int64_t n_records) {
   if (!ctx) return MURE_E_INVALID;
@@ -634,7 +675,10 @@ static mure_status apply_mutants_impl(mure_ctx* ctx, int32_t n_mutants, const mu
     return ctx->fail(MURE_E_INVALID, "bad mutant/record counts");
   const Graph& g = ctx->g;
   std::vector<Record> recs(n_records);
-  std::vector<float> noise;
+  // the per-record float pool (GF noise; WS permutation bits, then its
+  // scratch), copied straight from the callers' arrays into the staging block
+  std::vector<PoolSeg> segs;
+  int64_t pool_n = 0;
   for (int64_t r = 0; r < n_records; ++r) {
     const mure_record& x = records[r];
     Record& y = recs[r];
@@ -643,10 +687,12 @@ static mure_status apply_mutants_impl(mure_ctx* ctx, int32_t n_mutants, const mu
     if (x.op == OP_GF) {
       if (!x.noise || x.noise_len <= 0)
         return ctx->fail(MURE_E_INVALID, "record " + std::to_string(r) + ": Gaussian fuzz needs noise");
-      y.noise_off = (int64_t)noise.size();
+      y.noise_off = pool_n;
       y.noise_len = x.noise_len;
-      if (x.layer >= 0 && x.layer < (int)g.nodes.size() && x.noise_len == g.nodes[x.layer].fan_in)
-        noise.insert(noise.end(), x.noise, x.noise + x.noise_len);
+      if (x.layer >= 0 && x.layer < (int)g.nodes.size() && x.noise_len == g.nodes[x.layer].fan_in) {
+        segs.push_back(PoolSeg{x.noise, pool_n, x.noise_len});
+        pool_n += x.noise_len;
+      }
     } else if (x.op == OP_WS) {
       if (!x.perm || x.noise_len <= 0)
         return ctx->fail(MURE_E_INVALID, "record " + std::to_string(r) + ": weight shuffle needs a permutation");
@@ -659,14 +705,12 @@ static mure_status apply_mutants_impl(mure_ctx* ctx, int32_t n_mutants, const mu
             return ctx->fail(MURE_E_INVALID, "record " + std::to_string(r) + ": perm is not a permutation");
           seen[q] = 1;
         }
-        y.noise_off = (int64_t)noise.size();
-        for (int64_t k = 0; k < x.noise_len; ++k) {      // 4-byte integers in the float pool
-          float f;
-          std::memcpy(&f, &x.perm[k], 4);
-          noise.push_back(f);
-        }
-        y.scratch_off = (int64_t)noise.size();
-        noise.resize(noise.size() + (size_t)x.noise_len, 0.f);
+        y.noise_off = pool_n;                              // 4-byte integers in the float pool
+        segs.push_back(PoolSeg{x.perm, pool_n, x.noise_len});
+        pool_n += x.noise_len;
+        y.scratch_off = pool_n;
+        segs.push_back(PoolSeg{nullptr, pool_n, x.noise_len});
+        pool_n += x.noise_len;
       }
     }
   }
@@ -834,7 +878,7 @@ static mure_status apply_mutants_impl(mure_ctx* ctx, int32_t n_mutants, const mu
     const size_t o_cols = section(cols.size() * sizeof(DeltaCol));
     const size_t o_cargs = section(cargs.size() * sizeof(CowArgs));
     const size_t o_drecs = section(drecs.size() * sizeof(DevRecord));
-    const size_t o_noise = section(noise.size() * 4);
+    const size_t o_noise = section((size_t)pool_n * 4);
     HIPTRY(ctx->h_apply.ensure(std::max<size_t>(total, 256)));
     HIPTRY(ctx->d_apply.ensure(std::max<size_t>(total, 256)));
     char* h = static_cast<char*>(ctx->h_apply.p);
@@ -847,7 +891,7 @@ static mure_status apply_mutants_impl(mure_ctx* ctx, int32_t n_mutants, const mu
     put(o_cols, cols.data(), cols.size() * sizeof(DeltaCol));
     put(o_cargs, cargs.data(), cargs.size() * sizeof(CowArgs));
     put(o_drecs, drecs.data(), drecs.size() * sizeof(DevRecord));
-    put(o_noise, noise.data(), noise.size() * 4);
+    fill_pool(reinterpret_cast<float*>(h + o_noise), segs, pool_n);
     hipStream_t st = ctx->stream;
     char* d = ctx->d_apply.as<char>();
     if (total) HIPTRY(hipMemcpyAsync(d, h, total, hipMemcpyHostToDevice, st));

@@ -222,7 +222,9 @@ def test_record_parameter_packing():
     arrays = [np.array([1.5, -2.0], np.float32), None, np.arange(5, dtype=np.float64),
               np.zeros(0, np.float32), None, np.array([7.0], np.float32)]
     pool, addr, lens = B._pack(arrays, len(arrays), np.float32)
-    assert pool.dtype == np.float32 and pool.size == 8
+    assert all(p.dtype == np.float32 for p in pool) and sum(p.size for p in pool) == 8
+    # an entry already float32 and contiguous is passed in place
+    assert addr[0] == arrays[0].ctypes.data and addr[5] == arrays[5].ctypes.data
     assert lens.tolist() == [2, 0, 5, 0, 0, 1]
     assert addr[1] == 0 and addr[3] == 0 and addr[4] == 0
     for r, a in enumerate(arrays):
