@@ -263,42 +263,54 @@ __global__ __launch_bounds__(256) void cow_kernel(const CowArgs* args, const Dev
 }
 
 // ---------------------------------------------------------------- changed channel groups
-// Pixel-major: a thread takes one 8-channel group of one (input, pixel), so
-// the threads of a pixel read its whole cached row together; it then writes
-// that group for every entry (slot) of the launch that changed it.  The
+// A block stages a tile of GP_TILE pixel rows of the cache in LDS (one
+// coalesced read of each row), then writes the tile's 16-byte group vector of
+// every entry (slot, group): consecutive lanes take consecutive pixels of one
+// entry, so the side plane is written in whole runs.  A channel the entry
+// takes from another channel of the row (a switch) is read from the tile; one
+// it zeroes or recomputes comes from 0 or the compact delta rows.  The
 // entries' maps are staged in LDS (at most GROUP_PATCH_MAXE per launch).
 constexpr int GROUP_PATCH_MAXE = 256;
-__global__ __launch_bounds__(256) void group_patch_kernel(GroupPatchArgs a) {
+constexpr int GP_TILE_BYTES = 32768;                   // cached bytes per tile
+constexpr int GP_TILE_PAD = 16;                         // per row: spreads the rows over the banks
+__global__ __launch_bounds__(256) void group_patch_kernel(GroupPatchArgs a, int px_tile) {
   __shared__ int smap[GROUP_PATCH_MAXE][8];
   __shared__ int sgrp[GROUP_PATCH_MAXE], sslot[GROUP_PATCH_MAXE];
+  __shared__ __attribute__((aligned(16))) unsigned char tile[GP_TILE_BYTES + 256 * GP_TILE_PAD];
   for (int t = threadIdx.x; t < a.n_ent * 8; t += 256) {
     const int e = t >> 3, j = t & 7;
     const int slot = a.ent[2 * e], g = a.ent[2 * e + 1];
     smap[e][j] = a.chmap[(int64_t)slot * a.C + 8 * g + j];
     if (j == 0) { sgrp[e] = g; sslot[e] = slot; }
   }
-  __syncthreads();
-  const int G = a.C / 8, PPI = 256 / G;                 // pixels per block iteration
-  const int g = (int)threadIdx.x % G;
+  const int G = a.C / 8, RS = a.C * 2 + GP_TILE_PAD;   // row stride in the tile, bytes
   const int64_t npx = (int64_t)a.nx * a.P;
   const uint16_t* __restrict__ cache = reinterpret_cast<const uint16_t*>(a.cache);
   const uint16_t* __restrict__ delta = reinterpret_cast<const uint16_t*>(a.delta);
   v4u* side = reinterpret_cast<v4u*>(a.side);
-  if ((int)threadIdx.x >= PPI * G) return;
-  for (int64_t i = (int64_t)blockIdx.x * PPI + threadIdx.x / G; i < npx; i += (int64_t)gridDim.x * PPI) {
-    const v4u v0 = *reinterpret_cast<const v4u*>(cache + i * a.C + 8 * g);
-    for (int e = 0; e < a.n_ent; ++e) {
-      if (sgrp[e] != g) continue;
-      v4u v = v0;
+  for (int64_t i0 = (int64_t)blockIdx.x * px_tile; i0 < npx; i0 += (int64_t)gridDim.x * px_tile) {
+    const int npt = npx - i0 < px_tile ? (int)(npx - i0) : px_tile;
+    __syncthreads();                                    // the previous tile is consumed (and smap is staged)
+    for (int t = threadIdx.x; t < npt * G; t += 256) {
+      const int p = t / G, g = t % G;
+      *reinterpret_cast<v4u*>(tile + p * RS + g * 16) =
+          *reinterpret_cast<const v4u*>(cache + (i0 + p) * a.C + 8 * g);
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < a.n_ent * npt; t += 256) {
+      const int e = t / npt, p = t % npt;
+      const int g = sgrp[e];
+      const uint16_t* row = reinterpret_cast<const uint16_t*>(tile + p * RS);
+      v4u v = *reinterpret_cast<const v4u*>(row + 8 * g);
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int m = smap[e][j];
         if (m == 8 * g + j) continue;
-        const uint32_t x = m >= 0 ? cache[i * a.C + m]
-                         : m == -1 ? 0u : delta[((int64_t)(sslot[e] - a.slot0) * npx + i) * a.T + (-2 - m)];
+        const uint32_t x = m >= 0 ? row[m]
+                         : m == -1 ? 0u : delta[((int64_t)(sslot[e] - a.slot0) * npx + i0 + p) * a.T + (-2 - m)];
         v[j >> 1] = (v[j >> 1] & (0xffff0000u >> (16 * (j & 1)))) | (x << (16 * (j & 1)));
       }
-      side[(int64_t)e * npx + i] = v;
+      side[(int64_t)e * npx + i0 + p] = v;
     }
   }
 }
@@ -373,17 +385,18 @@ hipError_t launch_score(const ScoreArgs& a, int n_mutants, hipStream_t s) {
 
 hipError_t launch_group_patch(const GroupPatchArgs& a0, hipStream_t s) {
   if (a0.n_ent <= 0 || a0.nx <= 0) return hipSuccess;
-  if (a0.C % 8 || a0.C / 8 > 256 || a0.P <= 0) return hipErrorInvalidValue;
+  if (a0.C % 8 || a0.C * 2 > GP_TILE_BYTES || a0.P <= 0) return hipErrorInvalidValue;
   const int64_t npx = (int64_t)a0.nx * a0.P;
-  const int ppi = 256 / (a0.C / 8);
-  const unsigned gx = (unsigned)std::min<int64_t>((npx + ppi - 1) / ppi, 4096);
+  // pixels per tile: the cache rows that fit GP_TILE_BYTES, at most 256
+  const int px_tile = std::min(256, GP_TILE_BYTES / (a0.C * 2));
+  const unsigned gx = (unsigned)std::min<int64_t>((npx + px_tile - 1) / px_tile, 4096);
   // entries in pieces that fit the kernel's LDS table
   for (int e0 = 0; e0 < a0.n_ent; e0 += GROUP_PATCH_MAXE) {
     GroupPatchArgs a = a0;
     a.n_ent = std::min(GROUP_PATCH_MAXE, a0.n_ent - e0);
     a.ent = a0.ent + 2 * e0;
     a.side = reinterpret_cast<v4u*>(a0.side) + (int64_t)e0 * npx;
-    hipLaunchKernelGGL(group_patch_kernel, dim3(gx), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(group_patch_kernel, dim3(gx), dim3(256), 0, s, a, px_tile);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
