@@ -51,12 +51,12 @@ template <int W, int TN>
 struct HaloGeo {
   static constexpr int NT = 256, BM = 512, TR = BM / W, BN = 32 * TN;
   static constexpr int NPX = conv_halo_cap(W);          // halo pixels a stage holds
-  static constexpr int HSTR = (NPX + 1) * 16;           // bytes of one channel half: pixels, zero entry
-  static constexpr int HALO_B = 2 * HSTR;
+  static_assert(NPX % 32 == 0, "the halo is stored in blocks of 32 pixels");
+  static constexpr int NQ_HALO = NPX / 32;              // halo load instructions: a block of 32 pixels each
+  static constexpr int HZERO = NQ_HALO * 1024;          // the zero entries of the two halves
+  static constexpr int HALO_B = HZERO + 32;
   static constexpr int B_B = 9 * 2 * BN * 16;           // weights: [tap][half][column][8]
   static constexpr int STAGE = HALO_B + B_B;
-  static constexpr int NQH = (NPX + 63) / 64;           // load instructions per halo half
-  static constexpr int NQ_HALO = 2 * NQH;
   static constexpr int NQ = NQ_HALO + 9 * 2 * BN / 64;  // load instructions per chunk
   static constexpr int QPW = (NQ + 3) / 4;              // ... per wave
   static constexpr int OLD = BN + 8;                    // staged output row (bf16)
@@ -98,47 +98,59 @@ __device__ __forceinline__ bool halo_decode(const ConvArgs& a, int t, HaloTile& 
 }
 
 // The lane's sources for this wave's load instructions q = wave + 4 s of a
-// tile, at chunk 0 (nullptr: zeros).  q < NQ_HALO fills halo half q / NQH,
-// pixels 64 (q % NQH) + lane; the others fill 64 consecutive
-// [tap][half][column] weight entries.  VIN (input read in channel groups):
-// a halo source holds the pixel's index in the launch's rows plus one
-// instead of an address (0: zeros); the group's base comes per chunk.
+// tile.  q < NQ_HALO fills halo block q: pixels 32 q + (lane & 31), channel
+// half lane >> 5, so the two lanes of a pixel read the chunk's 32 bytes from
+// one cache line; hs.h[s] is the element offset of that pixel's half from
+// the tile's input base hs.in0 at chunk 0 (-1: zeros), or with VIN (input
+// read in channel groups) the pixel's index in the launch's rows (the
+// group's base comes per chunk).  The other instructions fill 64 consecutive
+// [tap][half][column] weight entries, contiguous in the chunk-major weight
+// layout; a lane reads the same column, output channel n of its slot's
+// weights, in every one of them, from hs.w (nullptr: zeros) plus a
+// per-instruction offset.
+template <int W, int TN>
+struct HaloSrc {
+  static constexpr int NH = (HaloGeo<W, TN>::NQ_HALO + 3) / 4;   // halo instructions per wave, at most
+  const bf16_t* in0;
+  int h[NH];
+  const bf16_t* w;
+};
+
 template <int W, int TN, bool VIN>
 __device__ __forceinline__ void halo_sources(const ConvArgs& a, const HaloTile& tl, int RI, int npx, int wave,
-                                             int lane, const bf16_t* (&src)[HaloGeo<W, TN>::QPW]) {
+                                             int lane, HaloSrc<W, TN>& hs) {
   using G = HaloGeo<W, TN>;
   const int ncol = a.cols ? a.ncols : a.Cout;
-  const bf16_t* in0 = reinterpret_cast<const bf16_t*>(a.in.p) +
-                      row_index(a.in.mode, (int64_t)tl.slot * a.nx + (tl.xi0 < a.nx ? tl.xi0 : 0), a.nx, a.x0) *
-                          a.in.row_elems;
+  hs.in0 = reinterpret_cast<const bf16_t*>(a.in.p) +
+           row_index(a.in.mode, (int64_t)tl.slot * a.nx + (tl.xi0 < a.nx ? tl.xi0 : 0), a.nx, a.x0) *
+               a.in.row_elems;
 #pragma unroll
-  for (int s = 0; s < G::QPW; ++s) {
+  for (int s = 0; s < HaloSrc<W, TN>::NH; ++s) {
     const int q = wave + 4 * s;
-    src[s] = nullptr;
-    if (q < G::NQ_HALO) {
-      const int hh = q / G::NQH, px = (q % G::NQH) * 64 + lane;
-      const int im = px / ((RI + 2) * W), rem = px % ((RI + 2) * W);
-      const int y = tl.y0 + rem / W - 1, x = rem % W;
-      if (px < npx && tl.xi0 + im < a.nx && (unsigned)y < (unsigned)a.H) {
-        if constexpr (VIN)
-          src[s] = reinterpret_cast<const bf16_t*>((uintptr_t)((tl.xi0 + im) * a.H * W + y * W + x + 1));
-        else
-          src[s] = in0 + im * a.in.row_elems + (y * W + x) * a.C + hh * 8;
-      }
-    } else if (q < G::NQ) {
-      const int e = (q - G::NQ_HALO) * 64 + lane;
-      const int tap = e / (2 * G::BN), hh = (e / G::BN) & 1, nc = tl.n0 + e % G::BN;
-      if (nc < ncol) {
-        const bf16_t* row;
-        if (a.cols) {
-          const DeltaCol cd = a.cols[nc];
-          row = reinterpret_cast<const bf16_t*>(a.wtab[a.slot0 + cd.slot - a.col_slot0]) + (int64_t)cd.c * a.K;
-        } else {
-          row = reinterpret_cast<const bf16_t*>(a.wtab[tl.slot]) + (int64_t)nc * a.K;
-        }
-        src[s] = row + tap * a.C + hh * 8;
-      }
+    const int hh = lane >> 5, px = q * 32 + (lane & 31);
+    const int im = px / ((RI + 2) * W), rem = px % ((RI + 2) * W);
+    const int y = tl.y0 + rem / W - 1, x = rem % W;
+    hs.h[s] = -1;
+    if (q < G::NQ_HALO && px < npx && tl.xi0 + im < a.nx && (unsigned)y < (unsigned)a.H)
+      hs.h[s] = VIN ? (tl.xi0 + im) * a.H * W + y * W + x
+                    : (int)(im * a.in.row_elems) + (y * W + x) * a.C + hh * 8;
+  }
+  // weights: column n0 + lane % BN of the tile; with BN = 32 the upper half
+  // wave reads the second channel half of each tap
+  const int nc = tl.n0 + lane % G::BN;
+  hs.w = nullptr;
+  if (nc < ncol) {
+    const void* w;
+    int n;
+    if (a.cols) {
+      const DeltaCol cd = a.cols[nc];
+      w = a.wtab[a.slot0 + cd.slot - a.col_slot0];
+      n = cd.c;
+    } else {
+      w = a.wtab[tl.slot];
+      n = nc;
     }
+    hs.w = reinterpret_cast<const bf16_t*>(w) + halo_w_index(n, 0, G::BN == 32 ? 8 * (lane >> 5) : 0, a.Cout);
   }
 }
 
@@ -161,65 +173,116 @@ __device__ __forceinline__ void halo_group_bases(const GroupIn& gi, int slot, in
   }
 }
 
-// Issue the loads of the chunk at channel c0 into the stage at st.  Lanes
-// past the halo load nothing.
+// Issue the loads of the chunk at channel c0 (weight entries wc on from
+// chunk 0's) into the stage at st.  Lanes past the halo load nothing.
 template <int W, int TN, bool VIN>
-__device__ __forceinline__ void halo_fetch(unsigned char* st, const bf16_t* const (&src)[HaloGeo<W, TN>::QPW],
-                                           int npx, int wave, int lane, int c0, const bf16_t* zp,
+__device__ __forceinline__ void halo_fetch(unsigned char* st, const HaloSrc<W, TN>& hs, int npx, int wave, int lane,
+                                           int c0, int wc, int Cout, const bf16_t* zp,
                                            const bf16_t* const (&gb)[2], const int (&gst)[2]) {
   using G = HaloGeo<W, TN>;
 #pragma unroll
   for (int s = 0; s < G::QPW; ++s) {
     const int q = wave + 4 * s;
     if (q >= G::NQ) continue;
-    const bool halo = q < G::NQ_HALO;
-    const int off = halo ? (q / G::NQH) * G::HSTR + (q % G::NQH) * 1024 : G::HALO_B + (q - G::NQ_HALO) * 1024;
-    if (!halo || (q % G::NQH) * 64 + lane < npx) {
-      const bf16_t* p;
-      if (VIN && halo) {
-        const int hh = q / G::NQH, pix = (int)(uintptr_t)src[s] - 1;
-        p = pix < 0 ? zp : gb[hh] + (int64_t)pix * gst[hh];
-      } else {
-        p = src[s] ? src[s] + c0 : zp;
+    if (q < G::NQ_HALO) {
+      if (q * 32 + (lane & 31) < npx) {
+        const int e = hs.h[s < HaloSrc<W, TN>::NH ? s : 0];
+        const bf16_t* p;
+        if constexpr (VIN) {
+          const int hh = lane >> 5;
+          p = e < 0 ? zp : gb[hh] + (int64_t)e * gst[hh];
+        } else {
+          p = e < 0 ? zp : hs.in0 + e + c0;
+        }
+        __builtin_amdgcn_global_load_lds((const void*)p, (lds_void*)(st + q * 1024), 16, 0, 0);
       }
-      __builtin_amdgcn_global_load_lds((const void*)p, (lds_void*)(st + off), 16, 0, 0);
+    } else {
+      // entries e = 64 (q - NQ_HALO) + lane: tap e / 2BN, half (e / BN) & 1
+      const int e0 = (q - G::NQ_HALO) * 64;
+      const int tap = e0 / (2 * G::BN), hu = G::BN == 64 ? (e0 / 64) & 1 : 0;
+      const bf16_t* p = hs.w ? hs.w + (int64_t)(tap * 2 + hu) * Cout * 8 + wc : zp;
+      __builtin_amdgcn_global_load_lds((const void*)p, (lds_void*)(st + G::HALO_B + (q - G::NQ_HALO) * 1024), 16,
+                                       0, 0);
     }
   }
 }
 
+// Byte offset in a stage of halo pixel p, channel half h: the halo is
+// stored in blocks of 32 pixels, [block][half][32][8].
+__device__ __forceinline__ int halo_addr(int p, int h) { return (p >> 5) * 1024 + h * 512 + (p & 31) * 16; }
+
 // Fragment bases: lane row (lane & 31) of M tile i is band pixel m, its 8 k
-// are channels 8 h of the chunk (h = lane >> 5).  abase[i] is the entry of
-// the pixel's column in the halo row above it; tap (dy, dx) adds the constant
-// ((dy + 1) W + dx) entries.  edge bit i: the pixel is in column 0, bit 4 + i:
-// in column W - 1.
+// are channels 8 h of the chunk (h = lane >> 5).  The tap (dy, dx) reads halo
+// pixel hp + (dy + 1) W + dx, where hp is the pixel's column in the halo row
+// above it.  A.r[i] is the entry of hp; for W >= 32 the rows below are whole
+// blocks further, for W <= 16 a row step stays in the block or moves to the
+// next one (halo_row_step).  A step of one column moves 16 bytes within a
+// block, or 528 across one (x = 31 | 32 at W = 64); cross bit i: the pixel is
+// the last of its block, bit 4 + i: the first.  edge bit i: the pixel is in
+// column 0, bit 4 + i: in column W - 1.
+template <int W>
+struct HaloA {
+  int r[4];
+  int zoff, edge, cross;
+};
+
+// halo_addr(p + k W) from a = halo_addr(p) (k = 1, 2), from the bits of a
+// that hold p % 32: the step leaves the block when p % 32 + k W >= 32.
+template <int W>
+__device__ __forceinline__ int halo_row_step(int a, int k) {
+  if constexpr (W >= 32) return a + k * (W / 32) * 1024;
+  const int d = k * W;                                   // pixels: 8, 16 or 32
+  if (d == 32) return a + 1024;
+  if (d == 16) return a + 256 + ((a & 256) << 1);        // bit 4 of p: 16 -> next block (+1024 - 256)
+  // d == 8: p % 32 >= 24 (bits 3 and 4 of p) -> next block (+1024 - 384)
+  return a + 128 + ((a & (a >> 1) & 128) << 2);
+}
 template <int W, int TN>
-__device__ __forceinline__ void halo_abase(int wave, int lane, int RI, int (&abase)[4], int& zoff, int& edge) {
+__device__ __forceinline__ void halo_abase(int wave, int lane, int RI, HaloA<W>& A) {
   using G = HaloGeo<W, TN>;
-  edge = 0;
+  const int h = lane >> 5;
+  A.edge = 0;
+  A.cross = 0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int m = wave * 128 + i * 32 + (lane & 31);
     const int row = m / W, x = m % W;
-    abase[i] = (lane >> 5) * G::HSTR + (((row / RI) * (RI + 2) + row % RI) * W + x) * 16;
-    edge |= (x == 0 ? 1 : 0) << i;
-    edge |= (x == W - 1 ? 1 : 0) << (4 + i);
+    const int hp = ((row / RI) * (RI + 2) + row % RI) * W + x;
+    A.r[i] = halo_addr(hp, h);
+    A.edge |= (x == 0 ? 1 : 0) << i;
+    A.edge |= (x == W - 1 ? 1 : 0) << (4 + i);
+    A.cross |= ((hp & 31) == 31 ? 1 : 0) << i;
+    A.cross |= ((hp & 31) == 0 ? 1 : 0) << (4 + i);
   }
-  zoff = (lane >> 5) * G::HSTR + G::NPX * 16;
+  A.zoff = G::HZERO + h * 16;
 }
 
 // The nine k-steps of the chunk staged at st (B: column j 32 + (lane & 31),
 // half h).
 template <int W, int TN>
-__device__ __forceinline__ void halo_mma(const unsigned char* st, const int (&abase)[4], int zoff, int edge,
-                                         int bbase, v16f (&acc)[4][TN]) {
+__device__ __forceinline__ void halo_mma(const unsigned char* st, const HaloA<W>& A, int bbase, v16f (&acc)[4][TN]) {
   using G = HaloGeo<W, TN>;
   v8bf fa[2][4], fb[2][TN];
   auto load = [&](int t, int p) {
-    const int dx = t % 3 - 1, toff = ((t / 3) * W + dx) * 16;
+    const int dy = t / 3, dx = t % 3 - 1;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      int off = abase[i] + toff;
-      if (dx != 0 && ((edge >> (i + (dx > 0 ? 4 : 0))) & 1)) off = zoff;
+      int off = A.r[i];
+      if (W < 32 && dy != 0) {
+        // recomputed at each use: kept, the row steps would hold 4-8 more registers
+        asm volatile("" : "+v"(off));
+        off = halo_row_step<W>(off, dy);
+      } else if (dy != 0) {
+        off = halo_row_step<W>(off, dy);
+      }
+      off += dx * 16;
+      // a column step crosses a block only inside a 64-pixel row; for
+      // W <= 32 the block edges are image edges, which read zeros
+      if constexpr (W == 64) {
+        if (dx > 0 && ((A.cross >> i) & 1)) off += 512;
+        if (dx < 0 && ((A.cross >> (4 + i)) & 1)) off -= 512;
+      }
+      if (dx != 0 && ((A.edge >> (i + (dx > 0 ? 4 : 0))) & 1)) off = A.zoff;
       fa[p][i] = *reinterpret_cast<const v8bf*>(st + off);
     }
 #pragma unroll
@@ -291,6 +354,10 @@ __device__ __forceinline__ void halo_pixel(const HaloTile& tl, int RI, int m, in
   xi = tl.xi0 + row / RI;
   y = tl.y0 + row % RI;
 }
+
+template <int W, bool VSKIP>
+__device__ __forceinline__ const bf16_t* halo_skip_at(const ConvArgs& a, const HaloTile& tl, int xi, int y, int x,
+                                                      int n, int e);
 
 // A fused ADD's shortcut vectors for the output vectors idx = tid + NT k of
 // the pixels [m0, m0 + PB) (pixel idx / VPR, channels 8 (idx % VPR)): option
@@ -508,8 +575,8 @@ void conv_halo_kernel(ConvArgs a) {
   const bool split = (!VIN || VSKIP) && !a.cols && !a.pool && a.add_mode == 1;
   static_assert(256 * G::OLD * 2 <= G::STAGE && 256 * G::BN * 2 <= G::STAGE, "a pass fits one stage");
 
-  const bf16_t* src[G::QPW];
-  halo_sources<W, TN, VIN>(a, tl, RI, npx, wave, lane, src);
+  HaloSrc<W, TN> hs;
+  halo_sources<W, TN, VIN>(a, tl, RI, npx, wave, lane, hs);
   const bf16_t* gb[2] = {nullptr, nullptr};
   int gst[2] = {0, 0};
   int skip_e = -1;
@@ -517,11 +584,12 @@ void conv_halo_kernel(ConvArgs a) {
     const int n = tl.n0 + (tid % VPR) * 8;            // the shortcut columns of this thread
     if (n < a.Cout) skip_e = a.gskip.src[tl.slot * (a.gskip.C / 8) + n / 8];
   }
-  int abase[4], zoff, edge;
-  halo_abase<W, TN>(wave, lane, RI, abase, zoff, edge);
-  // the zero entries after each half of both stages (no load writes them)
+  HaloA<W> A;
+  halo_abase<W, TN>(wave, lane, RI, A);
+  // the zero entries of both stages (no load writes them)
   if (tid < 4)
-    *reinterpret_cast<v4u*>(smem + (tid >> 1) * G::STAGE + (tid & 1) * G::HSTR + G::NPX * 16) = v4u{0u, 0u, 0u, 0u};
+    *reinterpret_cast<v4u*>(smem + (tid >> 1) * G::STAGE + G::HZERO + (tid & 1) * 16) = v4u{0u, 0u, 0u, 0u};
+  const int wstep = 9 * a.Cout;                          // chunk-major weight entries per input channel
   const int bbase = G::HALO_B + ((lane >> 5) * BN + (lane & 31)) * 16;
   v16f acc[4][TN];
 #pragma unroll
@@ -532,19 +600,20 @@ void conv_halo_kernel(ConvArgs a) {
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
   if constexpr (VIN) halo_group_bases(a.gin, tl.slot, a.nx, 0, gb, gst);
-  halo_fetch<W, TN, VIN>(smem, src, npx, wave, lane, 0, zp, gb, gst);
+  halo_fetch<W, TN, VIN>(smem, hs, npx, wave, lane, 0, 0, a.Cout, zp, gb, gst);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   for (int c = 0; c + 1 < nch; ++c) {
     if constexpr (VIN) halo_group_bases(a.gin, tl.slot, a.nx, (c + 1) * 16, gb, gst);
-    halo_fetch<W, TN, VIN>(smem + ((c + 1) & 1) * G::STAGE, src, npx, wave, lane, (c + 1) * 16, zp, gb, gst);
-    halo_mma<W, TN>(smem + (c & 1) * G::STAGE, abase, zoff, edge, bbase, acc);
+    halo_fetch<W, TN, VIN>(smem + ((c + 1) & 1) * G::STAGE, hs, npx, wave, lane, (c + 1) * 16,
+                           (c + 1) * 16 * wstep, a.Cout, zp, gb, gst);
+    halo_mma<W, TN>(smem + (c & 1) * G::STAGE, A, bbase, acc);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
   // the last chunk, outside the loop: its free stage receives pass 0's shortcut
   if (split) halo_skip_dma<W, TN, VSKIP>(a, tl, RI, wave, lane, smem + (nch & 1) * G::STAGE, zp, skip_e);
-  halo_mma<W, TN>(smem + ((nch - 1) & 1) * G::STAGE, abase, zoff, edge, bbase, acc);
+  halo_mma<W, TN>(smem + ((nch - 1) & 1) * G::STAGE, A, bbase, acc);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 

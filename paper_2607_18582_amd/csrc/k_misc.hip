@@ -215,7 +215,8 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
 // ---------------------------------------------------------------- copy-on-write mutation
 // One block per (mutant, layer) copy: copy the original parameters, then
 // apply that mutant's records on this layer in order.  Weight (neuron n, k)
-// is element n rs + k ks of the layer's array.
+// is element n rs + k ks of the layer's array, or for chunk-major halo
+// weights halo_w_index(n, k / C_in, k % C_in, C_out).
 template <typename T>
 __global__ __launch_bounds__(256) void cow_kernel(const CowArgs* args, const DevRecord* recs,
                                                   const float* noise) {
@@ -226,33 +227,40 @@ __global__ __launch_bounds__(256) void cow_kernel(const CowArgs* args, const Dev
   for (int64_t i = threadIdx.x; i < n; i += blockDim.x) wd[i] = ws[i];
   for (int i = threadIdx.x; i < c.c_out; i += blockDim.x) c.b_dst[i] = c.b_src[i];
   __syncthreads();
+  // element k (k = tap C_in + ci for a convolution) of neuron nr's weights
+  auto at = [&](int nr, int64_t k) -> T& {
+    if (c.halo_c > 0) return wd[halo_w_index(nr, (int)(k / c.halo_c), (int)(k % c.halo_c), c.c_out)];
+    return wd[(int64_t)nr * c.rs + k * c.ks];
+  };
   for (int ri = c.rec0; ri < c.rec1; ++ri) {
     const DevRecord r = recs[ri];
-    T* row = wd + (int64_t)r.neuron * c.rs;
-    const int64_t ks = c.ks;
     if (r.op == 0) {                      // Gaussian fuzz: float32 add, then round
       const float* eps = noise + r.noise_off;
-      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x)
-        row[k * ks] = from_f<T>(to_f<T>(row[k * ks]) + eps[k]);
+      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) {
+        T& w = at(r.neuron, k);
+        w = from_f<T>(to_f<T>(w) + eps[k]);
+      }
     } else if (r.op == 1) {               // effect block
-      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) row[k * ks] = T(0);
+      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) at(r.neuron, k) = T(0);
       if (threadIdx.x == 0) c.b_dst[r.neuron] = 0.f;
     } else if (r.op == 2) {               // activation inverse (exact sign flip)
       for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) {
-        if constexpr (sizeof(T) == 2) row[k * ks] = (T)(row[k * ks] ^ 0x8000u);
-        else row[k * ks] = -row[k * ks];
+        T& w = at(r.neuron, k);
+        if constexpr (sizeof(T) == 2) w = (T)(w ^ 0x8000u);
+        else w = -w;
       }
       if (threadIdx.x == 0) c.b_dst[r.neuron] = -c.b_dst[r.neuron];
     } else if (r.op == 4) {               // weight shuffle: row[k] <- old row[perm[k]]
       float* scratch = const_cast<float*>(noise) + r.scratch_off;
       const int32_t* perm = reinterpret_cast<const int32_t*>(noise + r.noise_off);
-      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) scratch[k] = to_f<T>(row[k * ks]);
+      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) scratch[k] = to_f<T>(at(r.neuron, k));
       __syncthreads();
-      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) row[k * ks] = from_f<T>(scratch[perm[k]]);
+      for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) at(r.neuron, k) = from_f<T>(scratch[perm[k]]);
     } else {                              // neuron switch
-      T* other = wd + (int64_t)r.partner * c.rs;
       for (int64_t k = threadIdx.x; k < c.fan_in; k += blockDim.x) {
-        const T t = row[k * ks]; row[k * ks] = other[k * ks]; other[k * ks] = t;
+        T& u = at(r.neuron, k);
+        T& v = at(r.partner, k);
+        const T t = u; u = v; v = t;
       }
       if (threadIdx.x == 0) {
         const float t = c.b_dst[r.neuron]; c.b_dst[r.neuron] = c.b_dst[r.partner]; c.b_dst[r.partner] = t;

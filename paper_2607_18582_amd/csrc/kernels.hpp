@@ -36,6 +36,15 @@ inline DivU32 make_divu32(uint32_t d) {
   return v;
 }
 
+// Weights of a convolution the halo kernel computes (bf16 3x3, C_in % 16 ==
+// 0) are kept chunk-major, [C_in / 16][tap][half][C_out][8], instead of
+// [C_out][kh][kw][C_in]: the weight tile of one 16-channel chunk is then 18
+// contiguous runs of C_out x 16 bytes.  Index of weight (output channel n,
+// tap = ky kw + kx, input channel ci).
+__host__ __device__ inline int64_t halo_w_index(int n, int tap, int ci, int Cout) {
+  return ((((int64_t)(ci >> 4) * 9 + tap) * 2 + ((ci >> 3) & 1)) * Cout + n) * 8 + (ci & 7);
+}
+
 struct TensorArg {
   const void* p = nullptr;
   int mode = MODE_BUF;
@@ -273,6 +282,7 @@ struct CowArgs {                           // one copy-on-write parameter copy
   const float* b_src; float* b_dst;
   int c_out; int64_t fan_in;
   int64_t rs, ks;                          // element strides of a neuron's row and of k (EMBED: 1, c_out)
+  int halo_c;                              // > 0: chunk-major halo weights with this C_in (rs, ks unused)
   int rec0, rec1;                          // records [rec0, rec1) in the device record table
 };
 

@@ -610,6 +610,18 @@ static mure_status load_model_impl(mure_ctx* ctx, const mure_layer* layers, int3
             std::memcpy(&t[(size_t)((v * e.c_out + d) * es)], src + (size_t)((d * e.c_in + v) * es), (size_t)es);
         HIPTRY(hipMemcpyAsync(ctx->d_w[i]->p, t.data(), wb, hipMemcpyHostToDevice, ctx->stream));
         HIPTRY(hipStreamSynchronize(ctx->stream));
+      } else if (node_family(g, i) == FAM_HALO) {
+        // chunk-major for the halo kernel (bf16): KRSC weight (n, tap, ci)
+        // moves to halo_w_index(n, tap, ci, C_out)
+        const Node& cv = g.nodes[i];
+        std::vector<uint16_t> t((size_t)cv.n_weights());
+        const uint16_t* src = static_cast<const uint16_t*>(weights[i]);
+        for (int n = 0; n < cv.c_out; ++n)
+          for (int tap = 0; tap < 9; ++tap)
+            for (int ci = 0; ci < cv.inC; ++ci)
+              t[(size_t)halo_w_index(n, tap, ci, cv.c_out)] = src[((size_t)n * 9 + tap) * cv.inC + ci];
+        HIPTRY(hipMemcpyAsync(ctx->d_w[i]->p, t.data(), wb, hipMemcpyHostToDevice, ctx->stream));
+        HIPTRY(hipStreamSynchronize(ctx->stream));
       } else {
         HIPTRY(hipMemcpyAsync(ctx->d_w[i]->p, weights[i], wb, hipMemcpyHostToDevice, ctx->stream));
       }
@@ -759,6 +771,7 @@ static mure_status apply_mutants_impl(mure_ctx* ctx, int32_t n_mutants, const mu
       const bool tok_major = g.nodes[cc.layer].kind == K_EMBED;      // stored [V][D]
       a.rs = tok_major ? 1 : a.fan_in;
       a.ks = tok_major ? a.c_out : 1;
+      a.halo_c = node_family(g, cc.layer) == FAM_HALO ? g.nodes[cc.layer].inC : 0;
       a.rec0 = (int)drecs.size();
       for (int r : cc.records) {
         DevRecord d;
