@@ -4,8 +4,8 @@
 // Block tile: 128 GEMM rows (output pixels of (slot, input) rows, pool-window
 // major when pooling) x BN output channels, k in chunks of 64.  The im2col
 // gather moves 16-byte vectors -- 8 consecutive input channels of one filter
-// tap -- guided by a per-block table of the taps; the next chunk's global
-// loads are issued before the current chunk's MFMAs (register prefetch).
+// tap.  The next chunk's global loads are issued before the current chunk's
+// MFMAs (register prefetch).
 // Reduction order: k = (dy, dx, c_in), c_in fastest, in increasing steps of
 // 32 with zero padding, for every launch of a node.
 #include "dev.hpp"
@@ -25,21 +25,26 @@ static __device__ __attribute__((aligned(16))) v4u g_zero_page[16] = {};
 // tables, which the compiler cannot place in an address space by itself)
 typedef __attribute__((address_space(1))) const v4u gv4u;
 
-// G: 16-byte vectors (8 input channels each) per filter tap in a thread's
-// half chunk of 32 k -- 4 when C_in % 32 == 0, 2 when C_in % 16 == 0, else 1.
-// The tap of each group is the same for the whole wavefront, so its index
-// math runs once per wave on the scalar unit and each row needs one bounds
-// check and one address per group.
+// LINE (C_in % 64 == 0): a chunk of 64 k is 64 channels of one tap, a whole
+// 128-byte line of each row's input pixel.  A thread gathers vector tid % 8
+// of rows tid / 8 + (THREADS / 8) r, so a load instruction reads eight whole
+// lines instead of 16 bytes from each of 64; the chunk's tap is the same for
+// every lane.  Otherwise a thread gathers one row's half chunk of 32 k, in
+// groups of G 16-byte vectors of one tap -- G = 4 when C_in % 32 == 0, 2 when
+// C_in % 16 == 0, else 1 -- whose tap is the same for the whole wavefront;
+// with 16-32 channels consecutive rows' vectors are neighbours in memory.
 //
-// The 128-row tiles are compiled for three (BN = 128: 138 VGPRs instead of
-// 172) and five (BN = 64: 92 instead of 116) resident waves per SIMD, without
-// spills; their LDS (37 and 28 KB per block) admits that many blocks.
-template <int BM, int BN, int WAVES_M, int WAVES_N, int G>
-__global__ __launch_bounds__(64 * WAVES_M * WAVES_N, BM == 128 && BN == 128 ? 3 : BM == 128 && BN == 64 ? 5 : 1)
+// The 128-row tiles are compiled for three (BN = 128) and five (BN = 64; four
+// with LINE, whose four rows per thread need more registers) resident waves
+// per SIMD, without spills; their LDS (37 and 28 KB per block) admits that
+// many blocks.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int G, bool LINE>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N, BM == 128 && BN == 128 ? 3 : BM == 128 && BN == 64 ? (LINE ? 4 : 5) : 1)
 void conv_big_kernel(ConvArgs a) {
   constexpr int THREADS = 64 * WAVES_M * WAVES_N;
   constexpr int BK = BIG_BK, LD = BIG_LD;
-  constexpr int ROWS_PER_THREAD = BM * 2 / THREADS;   // A rows gathered by each thread (2 per row)
+  constexpr int LPR = LINE ? 8 : 2;                     // threads per A row
+  constexpr int ROWS_PER_THREAD = BM * LPR / THREADS;   // A rows gathered by each thread
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int TM = WM / 16, TN = WN / 16;
   constexpr int BVEC = BN * BK / 8;                    // 16-byte vectors of a B chunk
@@ -60,12 +65,12 @@ void conv_big_kernel(ConvArgs a) {
   const int ncol = a.cols ? a.ncols : a.Cout;
   const bf16_t* const zp = reinterpret_cast<const bf16_t*>(g_zero_page);
 
-  // the A rows this thread gathers: rows arow + RSTEP*r, k half ahalf (a wave
-  // covers 64 consecutive rows of one half, so its 16-byte LDS stores hit
-  // distinct banks)
-  constexpr int RSTEP = THREADS / 2;
-  const int arow = tid % RSTEP;
-  const int ahalf = __builtin_amdgcn_readfirstlane(tid / RSTEP);   // wave-uniform
+  // the A rows this thread gathers: rows arow + RSTEP r; LINE: vector av of
+  // each, else k half av (a wave covers 64 consecutive rows of one half, so
+  // its 16-byte LDS stores hit distinct banks)
+  constexpr int RSTEP = THREADS / LPR;
+  const int arow = LINE ? tid / 8 : tid % RSTEP;
+  const int av = LINE ? tid % 8 : __builtin_amdgcn_readfirstlane(tid / RSTEP);
   bool mvalid[ROWS_PER_THREAD];
   int iy0[ROWS_PER_THREAD], ix0[ROWS_PER_THREAD];
   const bf16_t* inrow[ROWS_PER_THREAD];
@@ -113,24 +118,39 @@ void conv_big_kernel(ConvArgs a) {
   }
   __syncthreads();
 
-  v4u ra[ROWS_PER_THREAD][4], rb[BPT];
+  constexpr int VPT = LINE ? 1 : 4;                    // 16-byte vectors per row per thread
+  v4u ra[ROWS_PER_THREAD][VPT], rb[BPT];
   auto load_chunk = [&](int kc) {
-#pragma unroll
-    for (int jg = 0; jg < 4; jg += G) {
-      // k of this group (wave-uniform): tap t, first channel ci
-      const int k = kc + ahalf * 32 + jg * 8;
-      int t, ci, dy, dx;
-      divmodu(a.dC, (uint32_t)k, t, ci);
+    if constexpr (LINE) {
+      // the chunk's tap t (wave-uniform) and this thread's channels ci
+      int t, c0, dy, dx;
+      divmodu(a.dC, (uint32_t)kc, t, c0);
       divmodu(a.dKW, (uint32_t)t, dy, dx);
-      const int off = (dy * a.W + dx) * a.C + ci;
-      if (k >= a.K) dy = -(1 << 20);                 // past the end: every row reads zeros
+      const int off = (dy * a.W + dx) * a.C + c0 + av * 8;
 #pragma unroll
       for (int r = 0; r < ROWS_PER_THREAD; ++r) {
         const int iy = iy0[r] + dy, ix = ix0[r] + dx;
         const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
-        const v4u* src = reinterpret_cast<const v4u*>(ok ? inrow[r] + off : zp);
+        ra[r][0] = *reinterpret_cast<const v4u*>(ok ? inrow[r] + off : zp);
+      }
+    } else {
 #pragma unroll
-        for (int g = 0; g < G; ++g) ra[r][jg + g] = src[g];
+      for (int jg = 0; jg < 4; jg += G) {
+        // k of this group (wave-uniform): tap t, first channel ci
+        const int k = kc + av * 32 + jg * 8;
+        int t, ci, dy, dx;
+        divmodu(a.dC, (uint32_t)k, t, ci);
+        divmodu(a.dKW, (uint32_t)t, dy, dx);
+        const int off = (dy * a.W + dx) * a.C + ci;
+        if (k >= a.K) dy = -(1 << 20);               // past the end: every row reads zeros
+#pragma unroll
+        for (int r = 0; r < ROWS_PER_THREAD; ++r) {
+          const int iy = iy0[r] + dy, ix = ix0[r] + dx;
+          const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+          const v4u* src = reinterpret_cast<const v4u*>(ok ? inrow[r] + off : zp);
+#pragma unroll
+          for (int g = 0; g < G; ++g) ra[r][jg + g] = src[g];
+        }
       }
     }
 #pragma unroll
@@ -145,8 +165,8 @@ void conv_big_kernel(ConvArgs a) {
 #pragma unroll
     for (int r = 0; r < ROWS_PER_THREAD; ++r)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        *reinterpret_cast<v4u*>(&As[(arow + RSTEP * r) * LD + (ahalf * 4 + j) * 8]) = ra[r][j];
+      for (int j = 0; j < VPT; ++j)
+        *reinterpret_cast<v4u*>(&As[(arow + RSTEP * r) * LD + (LINE ? av : av * 4 + j) * 8]) = ra[r][j];
 #pragma unroll
     for (int j = 0; j < BPT; ++j) {
       const int i = tid + j * THREADS;
@@ -322,21 +342,21 @@ void conv_big_kernel(ConvArgs a) {
 
 int conv_big_bn(int cout) { return cout <= 16 ? 16 : cout <= 32 ? 32 : cout <= 64 ? 64 : 128; }
 
-template <int G>
+template <int G, bool LINE>
 static hipError_t launch_big(const ConvArgs& a, dim3 grid, int bm, int bn, hipStream_t s) {
   if (bm == 128) {
     switch (bn) {
-      case 16: hipLaunchKernelGGL((conv_big_kernel<128, 16, 4, 1, G>), grid, dim3(256), 0, s, a); break;
-      case 32: hipLaunchKernelGGL((conv_big_kernel<128, 32, 4, 1, G>), grid, dim3(256), 0, s, a); break;
-      case 64: hipLaunchKernelGGL((conv_big_kernel<128, 64, 4, 1, G>), grid, dim3(256), 0, s, a); break;
-      default: hipLaunchKernelGGL((conv_big_kernel<128, 128, 2, 2, G>), grid, dim3(256), 0, s, a); break;
+      case 16: hipLaunchKernelGGL((conv_big_kernel<128, 16, 4, 1, G, LINE>), grid, dim3(256), 0, s, a); break;
+      case 32: hipLaunchKernelGGL((conv_big_kernel<128, 32, 4, 1, G, LINE>), grid, dim3(256), 0, s, a); break;
+      case 64: hipLaunchKernelGGL((conv_big_kernel<128, 64, 4, 1, G, LINE>), grid, dim3(256), 0, s, a); break;
+      default: hipLaunchKernelGGL((conv_big_kernel<128, 128, 2, 2, G, LINE>), grid, dim3(256), 0, s, a); break;
     }
   } else {
     switch (bn) {
-      case 16: hipLaunchKernelGGL((conv_big_kernel<256, 16, 8, 1, G>), grid, dim3(512), 0, s, a); break;
-      case 32: hipLaunchKernelGGL((conv_big_kernel<256, 32, 8, 1, G>), grid, dim3(512), 0, s, a); break;
-      case 64: hipLaunchKernelGGL((conv_big_kernel<256, 64, 4, 2, G>), grid, dim3(512), 0, s, a); break;
-      default: hipLaunchKernelGGL((conv_big_kernel<256, 128, 4, 2, G>), grid, dim3(512), 0, s, a); break;
+      case 16: hipLaunchKernelGGL((conv_big_kernel<256, 16, 8, 1, G, LINE>), grid, dim3(512), 0, s, a); break;
+      case 32: hipLaunchKernelGGL((conv_big_kernel<256, 32, 8, 1, G, LINE>), grid, dim3(512), 0, s, a); break;
+      case 64: hipLaunchKernelGGL((conv_big_kernel<256, 64, 4, 2, G, LINE>), grid, dim3(512), 0, s, a); break;
+      default: hipLaunchKernelGGL((conv_big_kernel<256, 128, 4, 2, G, LINE>), grid, dim3(512), 0, s, a); break;
     }
   }
   return hipGetLastError();
@@ -361,9 +381,10 @@ hipError_t launch_conv_big(const ConvArgs& a0, int nslots, hipStream_t s) {
   a.dPq = make_divu32((uint32_t)std::max(1, a.P / 4));
   a.dC = make_divu32((uint32_t)a.C);
   a.dKW = make_divu32((uint32_t)a.kw);
-  if (a.C % 32 == 0) return launch_big<4>(a, grid, bm, bn, s);
-  if (a.C % 16 == 0) return launch_big<2>(a, grid, bm, bn, s);
-  return launch_big<1>(a, grid, bm, bn, s);
+  if (a.C % 64 == 0) return launch_big<4, true>(a, grid, bm, bn, s);
+  if (a.C % 32 == 0) return launch_big<4, false>(a, grid, bm, bn, s);
+  if (a.C % 16 == 0) return launch_big<2, false>(a, grid, bm, bn, s);
+  return launch_big<1, false>(a, grid, bm, bn, s);
 }
 
 }  // namespace mure
