@@ -10,25 +10,28 @@
 //
 // The input channels go in chunks of 16.  Per chunk the block stages in LDS
 // (a) the band's input rows plus the row above and below each packed image's
-// rows (the halo, zero outside the image), W pixels a row, stored as two
-// halves of 8 channels, [half][halo pixel][8]: every input element crosses
-// the memory pipeline once per block and chunk instead of once per tap as an
-// im2col gather would; and (b) the chunk's weights for the tile's columns,
-// [tap][half][column][8].  One MFMA k-step of 16 is one tap of the chunk, so a
-// chunk is nine k-steps, and the A fragment of a tap is the lane's halo entry
-// at a constant offset: the operand reads take immediate offsets.  A tap that
-// would read column -1 or W reads a zero entry kept after each half instead
-// (a per-lane select), so the halo has no border columns.  Both fragments of a
-// k-step are 32 consecutive 16-byte entries per half wave (32 pixels of whole
-// image rows), which ds_read_b128 serves without bank conflicts.  Within a
-// chunk the fragments of tap t + 1 are read before the MFMAs of tap t are
-// issued.
+// rows (the halo, zero outside the image), W pixels a row, in blocks of 32
+// pixels with the two 8-channel halves of each block side by side,
+// [block][half][32][8]: every input element crosses the memory pipeline once
+// per block and chunk instead of once per tap as an im2col gather would; and
+// (b) the chunk's weights for the tile's columns, [tap][half][column][8].
+// One MFMA k-step of 16 is one tap of the chunk, so a chunk is nine k-steps,
+// and the A fragment of a tap is the lane's halo entry of the pixel shifted
+// by (dy, dx).  A tap that would read column -1 or W reads a zero block
+// instead (a per-lane select), so the halo has no border columns.  Both
+// fragments of a k-step are 32 consecutive pixels or columns per half wave,
+// which ds_read_b128 serves without bank conflicts.  Within a chunk the
+// fragments of tap t + 1 are read before the MFMAs of tap t are issued.
 //
 // The stages are fetched with direct global-to-LDS loads (16 bytes per lane,
 // landing at consecutive LDS addresses per instruction), so staging takes no
-// registers; they are double-buffered: the loads of chunk c + 1 are issued
-// before the MFMAs of chunk c and waited for after them, one barrier per
-// chunk.
+// registers.  A load instruction fetches one halo block -- the two lanes of
+// a pixel read the chunk's 32 bytes of one cache line -- or 1 KB of weights,
+// contiguous in the chunk-major weight layout (halo_w_index): an address
+// unit that serves about one cache line per two clocks then moves 32 or 128
+// bytes per line instead of 16.  The stages are double-buffered: the loads
+// of chunk c + 1 are issued before the MFMAs of chunk c and waited for after
+// them, one barrier per chunk.
 //
 // One tile per block.  The epilogue (bias, activation, bf16 rounding) stages
 // the tile in LDS and stores whole output rows as 16-byte vectors, with a
@@ -53,8 +56,8 @@ struct HaloGeo {
   static constexpr int NPX = conv_halo_cap(W);          // halo pixels a stage holds
   static_assert(NPX % 32 == 0, "the halo is stored in blocks of 32 pixels");
   static constexpr int NQ_HALO = NPX / 32;              // halo load instructions: a block of 32 pixels each
-  static constexpr int HZERO = NQ_HALO * 1024;          // the zero entries of the two halves
-  static constexpr int HALO_B = HZERO + 32;
+  static constexpr int HZERO = NQ_HALO * 1024;          // a zero block: [half][32][8]
+  static constexpr int HALO_B = HZERO + 1024;
   static constexpr int B_B = 9 * 2 * BN * 16;           // weights: [tap][half][column][8]
   static constexpr int STAGE = HALO_B + B_B;
   static constexpr int NQ = NQ_HALO + 9 * 2 * BN / 64;  // load instructions per chunk
@@ -219,11 +222,14 @@ __device__ __forceinline__ int halo_addr(int p, int h) { return (p >> 5) * 1024 
 // next one (halo_row_step).  A step of one column moves 16 bytes within a
 // block, or 528 across one (x = 31 | 32 at W = 64); cross bit i: the pixel is
 // the last of its block, bit 4 + i: the first.  edge bit i: the pixel is in
-// column 0, bit 4 + i: in column W - 1.
+// column 0, bit 4 + i: in column W - 1.  A tap that would read column -1 or
+// W reads the zero block instead, at the offset it would have had in its own
+// block: the half wave's 32 lanes then still hit 32 distinct 16-byte slots
+// (one shared zero entry cost a bank conflict on every such read).
 template <int W>
 struct HaloA {
   int r[4];
-  int zoff, edge, cross;
+  int edge, cross;
 };
 
 // halo_addr(p + k W) from a = halo_addr(p) (k = 1, 2), from the bits of a
@@ -239,7 +245,6 @@ __device__ __forceinline__ int halo_row_step(int a, int k) {
 }
 template <int W, int TN>
 __device__ __forceinline__ void halo_abase(int wave, int lane, int RI, HaloA<W>& A) {
-  using G = HaloGeo<W, TN>;
   const int h = lane >> 5;
   A.edge = 0;
   A.cross = 0;
@@ -254,7 +259,6 @@ __device__ __forceinline__ void halo_abase(int wave, int lane, int RI, HaloA<W>&
     A.cross |= ((hp & 31) == 31 ? 1 : 0) << i;
     A.cross |= ((hp & 31) == 0 ? 1 : 0) << (4 + i);
   }
-  A.zoff = G::HZERO + h * 16;
 }
 
 // The nine k-steps of the chunk staged at st (B: column j 32 + (lane & 31),
@@ -282,7 +286,7 @@ __device__ __forceinline__ void halo_mma(const unsigned char* st, const HaloA<W>
         if (dx > 0 && ((A.cross >> i) & 1)) off += 512;
         if (dx < 0 && ((A.cross >> (4 + i)) & 1)) off -= 512;
       }
-      if (dx != 0 && ((A.edge >> (i + (dx > 0 ? 4 : 0))) & 1)) off = A.zoff;
+      if (dx != 0 && ((A.edge >> (i + (dx > 0 ? 4 : 0))) & 1)) off = G::HZERO | (off & 1023);
       fa[p][i] = *reinterpret_cast<const v8bf*>(st + off);
     }
 #pragma unroll
@@ -548,7 +552,7 @@ __device__ __forceinline__ void halo_store_pass(const ConvArgs& a, const HaloTil
 // Zero bytes that out-of-image halo pixels and columns past the last read.
 static __device__ __attribute__((aligned(16))) v4u g_halo_zero[4] = {};
 
-// Two blocks per CU (at most 78 KB of LDS each).
+// Two blocks per CU (at most 80 KB of LDS each).
 // V bit 0: the input is read in channel groups (a.gin); bit 1: the identity
 // shortcut is (a.gskip).
 template <int W, int TN, int V>
@@ -574,6 +578,7 @@ void conv_halo_kernel(ConvArgs a) {
   // slower there, 4.27 against 4.15 ms per width-64 launch on resnet18w)
   const bool split = (!VIN || VSKIP) && !a.cols && !a.pool && a.add_mode == 1;
   static_assert(256 * G::OLD * 2 <= G::STAGE && 256 * G::BN * 2 <= G::STAGE, "a pass fits one stage");
+  static_assert(G::STAGE % 1024 == 0 && G::HZERO % 1024 == 0, "stages and zero blocks are 1024-byte aligned");
 
   HaloSrc<W, TN> hs;
   halo_sources<W, TN, VIN>(a, tl, RI, npx, wave, lane, hs);
@@ -586,9 +591,9 @@ void conv_halo_kernel(ConvArgs a) {
   }
   HaloA<W> A;
   halo_abase<W, TN>(wave, lane, RI, A);
-  // the zero entries of both stages (no load writes them)
-  if (tid < 4)
-    *reinterpret_cast<v4u*>(smem + (tid >> 1) * G::STAGE + G::HZERO + (tid & 1) * 16) = v4u{0u, 0u, 0u, 0u};
+  // the zero blocks of both stages (no load writes them)
+  if (tid < 128)
+    *reinterpret_cast<v4u*>(smem + (tid >> 6) * G::STAGE + G::HZERO + (tid & 63) * 16) = v4u{0u, 0u, 0u, 0u};
   const int wstep = 9 * a.Cout;                          // chunk-major weight entries per input channel
   const int bbase = G::HALO_B + ((lane >> 5) * BN + (lane & 31)) * 16;
   v16f acc[4][TN];
