@@ -49,6 +49,11 @@ __device__ __forceinline__ int64_t row_index(int mode, int64_t r, int nx, int x0
   return mode == MODE_BUF ? r : (int64_t)x0 + (r % nx);
 }
 
+// the same for chunk row (slot, xi) with 0 <= xi < nx, without the modulo
+__device__ __forceinline__ int64_t row_at(int mode, int slot, int xi, int nx, int x0) {
+  return mode == MODE_BUF ? (int64_t)slot * nx + xi : (int64_t)x0 + xi;
+}
+
 // store a node output element (the network output is kept in float32)
 template <typename T>
 __device__ __forceinline__ void store_out(void* out, int out_f32, int64_t i, float v) {

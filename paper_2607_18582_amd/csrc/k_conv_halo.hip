@@ -77,16 +77,18 @@ struct HaloTile {
 // of a slot's bands, so that the blocks running together on it share the
 // rows above and below their bands in its L2 (width 64 on resnet18w: 5.85 ->
 // 5.39 ms per launch); bands of whole images go round-robin.  When every slot
-// reads the same input (a prefix-cache tensor, or the cached groups of a
-// channel-group read), the slots of a (band, column block) take consecutive
-// turns instead of the slots coming one after another, so that the band is
-// fetched once per XCD.  false: t is padding of that order.
+// reads the same input or shortcut (a prefix-cache tensor, or the cached
+// groups of a channel-group read), the slots of a (band, column block) take
+// consecutive turns instead of the slots coming one after another, so that
+// the band is fetched once per XCD (slot after slot, a cached shortcut was
+// streamed from HBM once per slot: 13 GB instead of 7.8 per width-64
+// launch).  false: t is padding of that order.
 template <int W, int TN>
 __device__ __forceinline__ bool halo_decode(const ConvArgs& a, int t, HaloTile& tl) {
   using G = HaloGeo<W, TN>;
   const int bgroups = (a.bands + 7) / 8;
   const int xcd = t & 7, turn = t >> 3, per_slot = bgroups * a.zblocks;
-  const bool slot_inner = a.in.mode == MODE_CACHE || a.gin.cache != nullptr;
+  const bool slot_inner = a.in.mode == MODE_CACHE || a.gin.cache != nullptr || a.gskip.cache != nullptr;
   const int si = slot_inner ? turn % a.halo_slots : turn / per_slot;
   const int rem = slot_inner ? turn / a.halo_slots : turn % per_slot;
   const int bi = rem / a.zblocks;
@@ -125,7 +127,7 @@ __device__ __forceinline__ void halo_sources(const ConvArgs& a, const HaloTile& 
   using G = HaloGeo<W, TN>;
   const int ncol = a.cols ? a.ncols : a.Cout;
   hs.in0 = reinterpret_cast<const bf16_t*>(a.in.p) +
-           row_index(a.in.mode, (int64_t)tl.slot * a.nx + (tl.xi0 < a.nx ? tl.xi0 : 0), a.nx, a.x0) *
+           row_at(a.in.mode, tl.slot, tl.xi0 < a.nx ? tl.xi0 : 0, a.nx, a.x0) *
                a.in.row_elems;
 #pragma unroll
   for (int s = 0; s < HaloSrc<W, TN>::NH; ++s) {
@@ -350,13 +352,14 @@ __device__ __forceinline__ void halo_stage(bf16_t* Os, int r0, int lane, const u
       }
 }
 
-// band pixel m -> (input xi, image row y, column x)
+// band pixel m -> (input xi, image row y, column x); a band's images are RI
+// = 2^rsh rows each (RI = H or 512 / W, both powers of two)
 template <int W>
-__device__ __forceinline__ void halo_pixel(const HaloTile& tl, int RI, int m, int& xi, int& y, int& x) {
+__device__ __forceinline__ void halo_pixel(const HaloTile& tl, int rsh, int m, int& xi, int& y, int& x) {
   const int row = m / W;
   x = m % W;
-  xi = tl.xi0 + row / RI;
-  y = tl.y0 + row % RI;
+  xi = tl.xi0 + (row >> rsh);
+  y = tl.y0 + (row & ((1 << rsh) - 1));
 }
 
 template <int W, bool VSKIP>
@@ -367,7 +370,7 @@ __device__ __forceinline__ const bf16_t* halo_skip_at(const ConvArgs& a, const H
 // the pixels [m0, m0 + PB) (pixel idx / VPR, channels 8 (idx % VPR)): option
 // A, or (IDENT) an identity shortcut read whole.
 template <int W, int TN, int PB, bool IDENT>
-__device__ __forceinline__ void halo_skip(const ConvArgs& a, const HaloTile& tl, int RI, int m0, int tid,
+__device__ __forceinline__ void halo_skip(const ConvArgs& a, const HaloTile& tl, int rsh, int m0, int tid,
                                           v4u (&skipv)[PB * HaloGeo<W, TN>::VPR / HaloGeo<W, TN>::NT]) {
   using G = HaloGeo<W, TN>;
   constexpr int NV = PB * G::VPR / G::NT;
@@ -375,7 +378,7 @@ __device__ __forceinline__ void halo_skip(const ConvArgs& a, const HaloTile& tl,
   for (int k = 0; k < NV; ++k) {
     const int idx = tid + G::NT * k, m = m0 + idx / G::VPR, n = tl.n0 + (idx % G::VPR) * 8;
     int xi, y, x;
-    halo_pixel<W>(tl, RI, m, xi, y, x);
+    halo_pixel<W>(tl, rsh, m, xi, y, x);
     skipv[k] = v4u{0u, 0u, 0u, 0u};
     if (n >= a.Cout || xi >= a.nx) continue;
     if constexpr (IDENT) {
@@ -387,7 +390,7 @@ __device__ __forceinline__ void halo_skip(const ConvArgs& a, const HaloTile& tl,
     // option A: the skip subsampled by 2 and zero-padded in channels; with the
     // padding and C_s multiples of 8 a vector is wholly inside or out
     const bf16_t* sp = reinterpret_cast<const bf16_t*>(a.skip.p) +
-                       row_index(a.skip.mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0) * a.skip.row_elems;
+                       row_at(a.skip.mode, tl.slot, xi, a.nx, a.x0) * a.skip.row_elems;
     const int cs0 = n - (a.Cout - a.Cs) / 2;
     const bf16_t* px = sp + ((int64_t)(2 * y) * a.Ws + 2 * x) * a.Cs;
     if (((a.Cout - a.Cs) / 2) % 8 == 0 && a.Cs % 8 == 0) {
@@ -406,7 +409,7 @@ __device__ __forceinline__ void halo_skip(const ConvArgs& a, const HaloTile& tl,
 // m - m0), with the ADD's shortcut (add_mode 1 or 2) added in float32 before
 // its activation: thread tid stores the vectors idx = tid + NT k.
 template <int W, int TN, int PB>
-__device__ __forceinline__ void halo_store_rows(const ConvArgs& a, const HaloTile& tl, int RI, int m0, int tid,
+__device__ __forceinline__ void halo_store_rows(const ConvArgs& a, const HaloTile& tl, int rsh, int m0, int tid,
                                                 const bf16_t* Os, int add_mode,
                                                 const v4u (&skipv)[PB * HaloGeo<W, TN>::VPR / HaloGeo<W, TN>::NT]) {
   using G = HaloGeo<W, TN>;
@@ -417,7 +420,7 @@ __device__ __forceinline__ void halo_store_rows(const ConvArgs& a, const HaloTil
     const int n = tl.n0 + vc * 8;
     if (n >= a.Cout) continue;
     int xi, y, x;
-    halo_pixel<W>(tl, RI, m0 + ml, xi, y, x);
+    halo_pixel<W>(tl, rsh, m0 + ml, xi, y, x);
     if (xi >= a.nx) continue;
     v4u val = *reinterpret_cast<const v4u*>(&Os[ml * G::OLD + vc * 8]);
     if (add_mode) {
@@ -429,7 +432,7 @@ __device__ __forceinline__ void halo_store_rows(const ConvArgs& a, const HaloTil
         val[w] = f2bf2(t0, t1);
       }
     }
-    const int64_t ro = row_index(a.out_mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0);
+    const int64_t ro = row_at(a.out_mode, tl.slot, xi, a.nx, a.x0);
     *reinterpret_cast<v4u*>(reinterpret_cast<bf16_t*>(a.out) + ro * a.out_row + ((int64_t)y * W + x) * a.Cout + n) =
         val;
   }
@@ -456,7 +459,7 @@ __device__ __forceinline__ const bf16_t* halo_skip_at(const ConvArgs& a, const H
                  : reinterpret_cast<const bf16_t*>(gs.side) + (int64_t)(e - gs.g0) * a.nx * gs.P * 8 + pix * 8;
   }
   return reinterpret_cast<const bf16_t*>(a.skip.p) +
-         row_index(a.skip.mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0) * a.skip.row_elems +
+         row_at(a.skip.mode, tl.slot, xi, a.nx, a.x0) * a.skip.row_elems +
          ((int64_t)y * W + x) * a.Cout + n;
 }
 
@@ -464,7 +467,7 @@ __device__ __forceinline__ const bf16_t* halo_skip_at(const ConvArgs& a, const H
 // at F + 16 p): wave w issues pieces 64 q + lane for q = w, w + 4, ...; a
 // lane's vc is lane % VPR, the same as its thread's in the passes.
 template <int W, int TN, bool VSKIP>
-__device__ __forceinline__ void halo_skip_dma(const ConvArgs& a, const HaloTile& tl, int RI, int wave, int lane,
+__device__ __forceinline__ void halo_skip_dma(const ConvArgs& a, const HaloTile& tl, int rsh, int wave, int lane,
                                               unsigned char* F, const bf16_t* zp, int skip_e) {
   using G = HaloGeo<W, TN>;
 #pragma unroll
@@ -472,7 +475,7 @@ __device__ __forceinline__ void halo_skip_dma(const ConvArgs& a, const HaloTile&
     const int pc = q * 64 + lane, ml = pc / G::VPR, vc = pc % G::VPR;
     const int n = tl.n0 + vc * 8;
     int xi, y, x;
-    halo_pixel<W>(tl, RI, halo_pass_pixel(0, ml), xi, y, x);
+    halo_pixel<W>(tl, rsh, halo_pass_pixel(0, ml), xi, y, x);
     const bf16_t* src = zp;
     if (n < a.Cout && xi < a.nx) src = halo_skip_at<W, VSKIP>(a, tl, xi, y, x, n, skip_e);
     __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)(F + q * 1024), 16, 0, 0);
@@ -481,14 +484,14 @@ __device__ __forceinline__ void halo_skip_dma(const ConvArgs& a, const HaloTile&
 
 // Pass 1's shortcut vectors idx = tid + NT k (pixel ml = idx / VPR) into registers.
 template <int W, int TN, bool VSKIP>
-__device__ __forceinline__ void halo_skip_pass1(const ConvArgs& a, const HaloTile& tl, int RI, int tid,
+__device__ __forceinline__ void halo_skip_pass1(const ConvArgs& a, const HaloTile& tl, int rsh, int tid,
                                                 v4u (&sk)[HaloGeo<W, TN>::VPR], int skip_e) {
   using G = HaloGeo<W, TN>;
 #pragma unroll
   for (int k = 0; k < G::VPR; ++k) {
     const int idx = tid + G::NT * k, ml = idx / G::VPR, n = tl.n0 + (idx % G::VPR) * 8;
     int xi, y, x;
-    halo_pixel<W>(tl, RI, halo_pass_pixel(1, ml), xi, y, x);
+    halo_pixel<W>(tl, rsh, halo_pass_pixel(1, ml), xi, y, x);
     sk[k] = v4u{0u, 0u, 0u, 0u};
     if (n < a.Cout && xi < a.nx) sk[k] = *reinterpret_cast<const v4u*>(halo_skip_at<W, VSKIP>(a, tl, xi, y, x, n, skip_e));
   }
@@ -522,7 +525,7 @@ __device__ __forceinline__ void halo_stage_pass(const ConvArgs& a, const HaloTil
 // Pass P's output rows with the shortcut (from F for pass 0, sk for pass 1)
 // added in float32 before its activation.
 template <int W, int TN>
-__device__ __forceinline__ void halo_store_pass(const ConvArgs& a, const HaloTile& tl, int RI, int P, int tid,
+__device__ __forceinline__ void halo_store_pass(const ConvArgs& a, const HaloTile& tl, int rsh, int P, int tid,
                                                 const bf16_t* Os, const unsigned char* F,
                                                 const v4u (&sk)[HaloGeo<W, TN>::VPR]) {
   using G = HaloGeo<W, TN>;
@@ -532,7 +535,7 @@ __device__ __forceinline__ void halo_store_pass(const ConvArgs& a, const HaloTil
     const int n = tl.n0 + vc * 8;
     if (n >= a.Cout) continue;
     int xi, y, x;
-    halo_pixel<W>(tl, RI, halo_pass_pixel(P, ml), xi, y, x);
+    halo_pixel<W>(tl, rsh, halo_pass_pixel(P, ml), xi, y, x);
     if (xi >= a.nx) continue;
     v4u val = *reinterpret_cast<const v4u*>(&Os[ml * G::OLD + vc * 8]);
     const v4u sv = P == 0 ? *reinterpret_cast<const v4u*>(F + idx * 16) : sk[k];
@@ -542,7 +545,7 @@ __device__ __forceinline__ void halo_store_pass(const ConvArgs& a, const HaloTil
       const float t1 = act(bf2f((bf16_t)(val[w] >> 16)) + bf2f((bf16_t)(sv[w] >> 16)), a.add_relu);
       val[w] = f2bf2(t0, t1);
     }
-    const int64_t ro = row_index(a.out_mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0);
+    const int64_t ro = row_at(a.out_mode, tl.slot, xi, a.nx, a.x0);
     *reinterpret_cast<v4u*>(reinterpret_cast<bf16_t*>(a.out) + ro * a.out_row + ((int64_t)y * W + x) * a.Cout + n) =
         val;
   }
@@ -570,6 +573,7 @@ void conv_halo_kernel(ConvArgs a) {
   if (!halo_decode<W, TN>(a, (int)blockIdx.x, tl)) return;   // padding of the order (whole block)
   const int ncol = a.cols ? a.ncols : a.Cout;
   const int RI = a.H < G::TR ? a.H : G::TR;
+  const int rsh = 31 - __builtin_clz((unsigned)RI);
   const int npx = (G::TR / RI) * (RI + 2) * W;
   const bf16_t* const zp = reinterpret_cast<const bf16_t*>(g_halo_zero);
   const int nch = a.C / 16;
@@ -617,7 +621,7 @@ void conv_halo_kernel(ConvArgs a) {
     __syncthreads();
   }
   // the last chunk, outside the loop: its free stage receives pass 0's shortcut
-  if (split) halo_skip_dma<W, TN, VSKIP>(a, tl, RI, wave, lane, smem + (nch & 1) * G::STAGE, zp, skip_e);
+  if (split) halo_skip_dma<W, TN, VSKIP>(a, tl, rsh, wave, lane, smem + (nch & 1) * G::STAGE, zp, skip_e);
   halo_mma<W, TN>(smem + ((nch - 1) & 1) * G::STAGE, A, bbase, acc);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
@@ -629,13 +633,13 @@ void conv_halo_kernel(ConvArgs a) {
     const unsigned char* F = smem + (nch & 1) * G::STAGE;
     halo_stage_pass<W, TN>(a, tl, Os, wave, 0, lane, acc);
     v4u sk[VPR];                                         // pass 1's shortcut, under pass 0's stores
-    halo_skip_pass1<W, TN, VSKIP>(a, tl, RI, tid, sk, skip_e);
+    halo_skip_pass1<W, TN, VSKIP>(a, tl, rsh, tid, sk, skip_e);
     __syncthreads();
-    halo_store_pass<W, TN>(a, tl, RI, 0, tid, Os, F, sk);
+    halo_store_pass<W, TN>(a, tl, rsh, 0, tid, Os, F, sk);
     __syncthreads();
     halo_stage_pass<W, TN>(a, tl, Os, wave, 1, lane, acc);
     __syncthreads();
-    halo_store_pass<W, TN>(a, tl, RI, 1, tid, Os, F, sk);
+    halo_store_pass<W, TN>(a, tl, rsh, 1, tid, Os, F, sk);
     return;
   }
   {
@@ -644,10 +648,10 @@ void conv_halo_kernel(ConvArgs a) {
     halo_stage<W, TN>(reinterpret_cast<bf16_t*>(smem), wave * 128, lane, ob);
   }
   v4u skipv[NV];
-  if (!a.cols && !a.pool && a.add_mode) halo_skip<W, TN, BM, VIN && !VSKIP>(a, tl, RI, 0, tid, skipv);
+  if (!a.cols && !a.pool && a.add_mode) halo_skip<W, TN, BM, VIN && !VSKIP>(a, tl, rsh, 0, tid, skipv);
   __syncthreads();
   const bf16_t* Os = reinterpret_cast<const bf16_t*>(smem);   // [BM][OLD]
-  auto pixel = [&](int m, int& xi, int& y, int& x) { halo_pixel<W>(tl, RI, m, xi, y, x); };
+  auto pixel = [&](int m, int& xi, int& y, int& x) { halo_pixel<W>(tl, rsh, m, xi, y, x); };
   if (a.cols) {
     // gathered columns: each column has its own slot and channel
     const int PX = a.pool ? BM / 4 : BM;
@@ -674,7 +678,7 @@ void conv_halo_kernel(ConvArgs a) {
       const int ostride = a.delta_T > 0 ? a.delta_T : a.Cout;
       const int n = a.delta_T > 0 ? cd.t : cd.c;
       const int Wo = a.pool ? W / 2 : W;
-      const int64_t ro = row_index(a.out_mode, (int64_t)os * a.nx + xi, a.nx, a.x0);
+      const int64_t ro = row_at(a.out_mode, os, xi, a.nx, a.x0);
       reinterpret_cast<bf16_t*>(a.out)[ro * a.out_row + ((int64_t)y * Wo + x) * ostride + n] = f2bf(v);
     }
     return;
@@ -706,13 +710,13 @@ void conv_halo_kernel(ConvArgs a) {
         }
         o[w] = r;
       }
-      const int64_t ro = row_index(a.out_mode, (int64_t)tl.slot * a.nx + xi, a.nx, a.x0);
+      const int64_t ro = row_at(a.out_mode, tl.slot, xi, a.nx, a.x0);
       *reinterpret_cast<v4u*>(reinterpret_cast<bf16_t*>(a.out) + ro * a.out_row +
                               ((int64_t)(y >> 1) * (W / 2) + (x >> 1)) * a.Cout + n) = o;
     }
     return;
   }
-  halo_store_rows<W, TN, BM>(a, tl, RI, 0, tid, Os, a.add_mode, skipv);
+  halo_store_rows<W, TN, BM>(a, tl, rsh, 0, tid, Os, a.add_mode, skipv);
 }
 
 int conv_halo_bn(int cout) { return cout <= 32 ? 32 : 64; }
