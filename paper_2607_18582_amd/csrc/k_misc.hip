@@ -7,6 +7,54 @@ namespace mure {
 // ---------------------------------------------------------------- ADD
 // out = ReLU?(float(a) + float(s')) with s' = s, or for option A
 // s'[y][x][c] = s[2y][2x][c - before] inside the copied channel range, else 0.
+//
+// Vector form: one 16-byte vector (VEC channels of one pixel) per item, with
+// multiply-high divisors for the row / pixel / channel-vector decode.  Needs
+// C % VEC == 0 and, for option A, a channel offset and C_s that are whole
+// vectors (a vector of the shortcut is then wholly inside or outside).
+template <typename T>
+__global__ __launch_bounds__(256) void add_vec_kernel(AddArgs a, int total_v, DivU32 dper, DivU32 dnx,
+                                                      DivU32 dcv, DivU32 dw) {
+  constexpr int VEC = 16 / sizeof(T);
+  const int64_t per = (int64_t)a.H * a.W * a.C;
+  const int before = (a.C - a.Cs) / 2;
+  for (int i = (int)(blockIdx.x * 256 + threadIdx.x); i < total_v; i += (int)(gridDim.x * 256)) {
+    int r, e, sl, xi;
+    divmodu(dper, (uint32_t)i, r, e);                // e = pixel * (C / VEC) + cv
+    divmodu(dnx, (uint32_t)r, sl, xi);
+    const T* ap = reinterpret_cast<const T*>(a.a.p) + row_at(a.a.mode, sl, xi, a.nx, a.x0) * a.a.row_elems;
+    const T* sp = reinterpret_cast<const T*>(a.s.p) + row_at(a.s.mode, sl, xi, a.nx, a.x0) * a.s.row_elems;
+    const v4u av = *reinterpret_cast<const v4u*>(ap + (int64_t)e * VEC);
+    v4u sv = v4u{0u, 0u, 0u, 0u};
+    if (a.shortcut == 0) {
+      sv = *reinterpret_cast<const v4u*>(sp + (int64_t)e * VEC);
+    } else {
+      int pix, cv, y, x;
+      divmodu(dcv, (uint32_t)e, pix, cv);
+      divmodu(dw, (uint32_t)pix, y, x);
+      const int cs = cv * VEC - before;
+      if (cs >= 0 && cs < a.Cs) sv = *reinterpret_cast<const v4u*>(sp + ((int64_t)(2 * y) * a.Ws + 2 * x) * a.Cs + cs);
+    }
+    T x8[VEC], s8[VEC];
+    __builtin_memcpy(x8, &av, 16);
+    __builtin_memcpy(s8, &sv, 16);
+    T* const op = reinterpret_cast<T*>(a.out);
+    const int64_t o = row_at(a.out_mode, sl, xi, a.nx, a.x0) * per + (int64_t)e * VEC;
+    if (a.out_f32) {
+      float* const of = reinterpret_cast<float*>(a.out) + o;
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) of[j] = act(to_f<T>(x8[j]) + to_f<T>(s8[j]), a.relu);
+    } else {
+      T o8[VEC];
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) o8[j] = from_f<T>(act(to_f<T>(x8[j]) + to_f<T>(s8[j]), a.relu));
+      v4u ov;
+      __builtin_memcpy(&ov, o8, 16);
+      *reinterpret_cast<v4u*>(op + o) = ov;
+    }
+  }
+}
+
 template <typename T>
 __global__ void add_kernel(AddArgs a) {
   const int64_t per = (int64_t)a.H * a.W * a.C;
@@ -344,6 +392,21 @@ static unsigned grid_for(int64_t total, int block = 256) {
 hipError_t launch_add(const AddArgs& a, int dtype, hipStream_t s) {
   const int64_t total = a.rows * a.H * a.W * a.C;
   if (total == 0) return hipSuccess;
+  const int vec = dtype == 0 ? 4 : 8;
+  const int64_t per_v = (int64_t)a.H * a.W * a.C / vec;
+  const bool vec_ok = a.C % vec == 0 && total / vec < (1 << 30) && a.rows < (1 << 30) && a.a.row_elems % vec == 0 &&
+                      a.s.row_elems % vec == 0 &&
+                      (a.shortcut == 0 || (((a.C - a.Cs) / 2) % vec == 0 && a.Cs % vec == 0));
+  if (vec_ok) {
+    const int total_v = (int)(total / vec);
+    const DivU32 dper = make_divu32((uint32_t)per_v), dnx = make_divu32((uint32_t)std::max(1, a.nx));
+    const DivU32 dcv = make_divu32((uint32_t)(a.C / vec)), dw = make_divu32((uint32_t)std::max(1, a.W));
+    if (dtype == 0)
+      hipLaunchKernelGGL(add_vec_kernel<float>, dim3(grid_for(total_v)), dim3(256), 0, s, a, total_v, dper, dnx, dcv, dw);
+    else
+      hipLaunchKernelGGL(add_vec_kernel<bf16_t>, dim3(grid_for(total_v)), dim3(256), 0, s, a, total_v, dper, dnx, dcv, dw);
+    return hipGetLastError();
+  }
   if (dtype == 0) hipLaunchKernelGGL(add_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s, a);
   else hipLaunchKernelGGL(add_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s, a);
   return hipGetLastError();
