@@ -135,6 +135,7 @@ struct ConvArgs {
   // band (XCD-aware order)
   DivU32 dP, dPq, dWp, dWc, dHW, dC, dKW, dImg;
   int bands = 0, zblocks = 1, halo_slots = 1;
+  int big_gx = 1, big_gz = 1, big_tiles = 0;            // conv_big: row tiles, column blocks, all tiles
 };
 
 // DENSE on MFMA: out[r][n] = sum_k in[r][k] * W[n][k] + b[n] (k in increasing
