@@ -110,15 +110,21 @@ __global__ void gap_kernel(GapArgs a) {
 // Node mmi of an effect-block / switch mutant: the original's output with
 // channel c taken from original channel chmap[c] (-1: zero).  Bitwise copy.
 // A block copies `rows` consecutive inputs of one slot: a contiguous span of
-// the cache and of the chunk buffer.  16-byte vectors whose channels the map
-// keeps in place are copied whole, the others element by element.
+// the cache and of the chunk buffer.  The span goes through LDS in tiles of
+// whole pixels (one coalesced 16-byte load per vector); 16-byte vectors
+// whose channels the map keeps in place are copied whole, the others
+// gathered element by element from the staged pixel (gathered from global
+// memory, two bytes a load, they had cost most of the kernel's time).
 constexpr int PATCH_MAXC = 4096;
+constexpr int PATCH_TILE_B = 32768;                     // staged bytes per tile
 
 template <typename E>
 __global__ __launch_bounds__(256) void patch_kernel(PatchArgs a, int rows, DivU32 dcv, DivU32 dc) {
   constexpr int VEC = 16 / sizeof(E);
+  constexpr int TV_MAX = PATCH_TILE_B / 16;             // vectors per tile, at most
   __shared__ int map[PATCH_MAXC];
   __shared__ unsigned char keep[PATCH_MAXC / VEC];
+  __shared__ __attribute__((aligned(16))) v4u tile[TV_MAX];
   const int tid = threadIdx.x;
   const int sl = (int)blockIdx.y;
   const int32_t* cm = a.chmap + (int64_t)(a.chmap_slot0 + sl) * a.C;
@@ -141,36 +147,47 @@ __global__ __launch_bounds__(256) void patch_kernel(PatchArgs a, int rows, DivU3
   const int per = a.P * a.C;
   const E* src = reinterpret_cast<const E*>(a.cache) + ((int64_t)a.x0 + xi0) * per;
   E* dst = reinterpret_cast<E*>(a.out) + ((int64_t)(a.slot0 + sl) * a.nx + xi0) * per;
-  if (vec) {
-    // PB vectors per thread and batch: all loads, then all stores, so a
-    // batch waits once for its loads (and the previous batch's stores)
-    constexpr int PB = 8;
+  if (vec && CV <= TV_MAX) {
+    constexpr int PB = TV_MAX / 256;                    // vectors per thread and tile
+    const int TV = TV_MAX / CV * CV;                    // a tile holds whole pixels
     const int nv = nr * (per / VEC);
-    for (int v0 = tid; v0 < nv; v0 += 256 * PB) {
-      v4u o[PB];
+    const E* const te = reinterpret_cast<const E*>(tile);
+    for (int t0 = 0; t0 < nv; t0 += TV) {
+      const int tn = min(TV, nv - t0);
+      // the tile's cached vectors, all loads first
+      v4u ld[PB];
 #pragma unroll
       for (int u = 0; u < PB; ++u) {
-        const int v = v0 + 256 * u;
-        if (v >= nv) continue;
-        const int cv = (int)(v - divu(dcv, (uint32_t)v) * CV);
+        const int v = tid + 256 * u;
+        if (v < tn) ld[u] = reinterpret_cast<const v4u*>(src)[t0 + v];
+      }
+#pragma unroll
+      for (int u = 0; u < PB; ++u) {
+        const int v = tid + 256 * u;
+        if (v < tn) tile[v] = ld[u];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < PB; ++u) {
+        const int v = tid + 256 * u;
+        if (v >= tn) continue;
+        const int cv = (int)((uint32_t)v - divu(dcv, (uint32_t)v) * (uint32_t)CV);
+        v4u o;
         if (keep[cv]) {
-          o[u] = reinterpret_cast<const v4u*>(src)[v];
+          o = tile[v];
         } else {
-          const int e0 = v * VEC, pix0 = e0 - cv * VEC;
+          const int pix0 = (v - cv) * VEC;              // the pixel's first element in the tile
           E t[VEC];
 #pragma unroll
           for (int j = 0; j < VEC; ++j) {
             const int m = map[cv * VEC + j];
-            t[j] = m < 0 ? E(0) : src[pix0 + m];
+            t[j] = m < 0 ? E(0) : te[pix0 + m];
           }
-          __builtin_memcpy(&o[u], t, 16);
+          __builtin_memcpy(&o, t, 16);
         }
+        reinterpret_cast<v4u*>(dst)[t0 + v] = o;
       }
-#pragma unroll
-      for (int u = 0; u < PB; ++u) {
-        const int v = v0 + 256 * u;
-        if (v < nv) reinterpret_cast<v4u*>(dst)[v] = o[u];
-      }
+      __syncthreads();                                  // the tile is read before the next one lands
     }
   } else {
     const int ne = nr * per;
