@@ -286,6 +286,23 @@ def test_fp32_cnn_lds_instances_and_im2col():
         assert np.array_equal(m1.get_logits(mid).cpu().numpy(), m2.get_logits(mid).cpu().numpy()), mid
 
 
+@pytest.mark.parametrize("shortcut", ["optionA", "proj"])
+def test_fp32_tiny_resnet_unfused_adds(shortcut):
+    """Parity on a small fp32 residual net whose mutants start at every
+    convolution: a cluster whose first mutated node is a block's second
+    convolution runs its ADD unfused (the 4-lane vector ADD on the identity
+    block; the element ADD where option A's channel offset is not a whole
+    vector), and memoized equals vanilla bit for bit."""
+    model = W.tiny_resnet("f32", shortcut=shortcut)
+    x = W.make_inputs(model, 300, "uniform")
+    mu = W.make_mutants(model, 40, 1, "layer_first", variant=5, ops=(W.GF, W.NEB, W.NAI, W.NS, W.WS))
+    wl = W.Workload("tiny_resnet_" + shortcut, model, x, mu)
+    _parity(wl)
+    m1, w1, k1, s1 = run_gpu(wl)
+    m2, w2, k2, s2 = run_gpu(wl, vanilla=1)
+    assert np.array_equal(w1, w2) and np.array_equal(k1, k2) and s1 == s2
+
+
 def test_reapply_in_one_context_matches_fresh_contexts():
     """One context, three mutant sets in turn (larger, smaller with fewer
     inputs, the first again): each run equals a fresh context's bit for bit,
