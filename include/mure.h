@@ -300,7 +300,7 @@ mure_status mure_mutant_plan(const mure_ctx* ctx, int32_t mutant_id, int32_t* mm
 mure_status mure_get_stats(const mure_ctx* ctx, mure_stats* out);
 
 /* Tuning and testing knobs (name, integer value).  Known names:
- *   "max_workspace_mb"  cap on per-chunk activation buffers (default 16384)
+ *   "max_workspace_mb"  cap on per-chunk activation buffers (default 65536)
  *   "max_device_mb"     cap on the device memory of the model, the mutants'
  *                       copy-on-write layers and the prefix cache (0 = none,
  *                       the default): apply_mutants and run_original refuse a

@@ -187,7 +187,7 @@ struct mure_ctx {
   int64_t group_reads = 1;                            // option "group_reads"
   void* scratch = nullptr;                            // this GPU's scratch array (noalloc entry)
   // options
-  int64_t max_ws_mb = 16384;
+  int64_t max_ws_mb = 65536;
   int64_t max_device_mb = 0;                          // 0: no cap on model + copies + prefix cache
   int64_t cow_bytes = 0;                              // copy-on-write pool of the applied mutants
   int64_t chunk_inputs = 0;
