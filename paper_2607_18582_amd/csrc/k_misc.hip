@@ -289,7 +289,16 @@ __global__ __launch_bounds__(256) void cow_kernel(const CowArgs* args, const Dev
   const T* ws = reinterpret_cast<const T*>(c.w_src);
   T* wd = reinterpret_cast<T*>(c.w_dst);
   const int64_t n = (int64_t)c.c_out * c.fan_in;
-  for (int64_t i = threadIdx.x; i < n; i += blockDim.x) wd[i] = ws[i];
+  // the copy in 16-byte vectors when both arrays allow it (the pool's
+  // copies are 256-byte aligned; the originals are device allocations)
+  const int64_t nb = n * (int64_t)sizeof(T);
+  if (nb % 16 == 0 && ((uintptr_t)ws | (uintptr_t)wd) % 16 == 0) {
+    const v4u* vs = reinterpret_cast<const v4u*>(ws);
+    v4u* vd = reinterpret_cast<v4u*>(wd);
+    for (int64_t i = threadIdx.x; i < nb / 16; i += blockDim.x) vd[i] = vs[i];
+  } else {
+    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) wd[i] = ws[i];
+  }
   for (int i = threadIdx.x; i < c.c_out; i += blockDim.x) c.b_dst[i] = c.b_src[i];
   __syncthreads();
   // element k (k = tap C_in + ci for a convolution) of neuron nr's weights
