@@ -241,6 +241,8 @@ def main():
     ap.add_argument("--summarize-trace", nargs=2, metavar=("TRACE_CSV", "STATS_CSV"),
                     help="print the kernel-trace summary of a rocprofv3 run and exit")
     ap.add_argument("--kernel", default="conv_lds_kernel", help="kernel the summaries follow")
+    ap.add_argument("--no-measured-peaks", action="store_true",
+                    help="skip the STREAM copy and MFMA-loop ceilings measured after the timed steps")
     args = ap.parse_args()
     cfgd = W.CONFIGS[args.config]
     n_all = args.inputs or cfgd["n_inputs"]
@@ -432,6 +434,18 @@ def main():
                               "ms_run_mutants_vanilla": float(np.median([s["ms_run_mutants"] for s in vstats])),
                               "same_score": [vscore["ms_num"], vscore["ms_den"]] == [score["ms_num"], score["ms_den"]],
                               "macs_vanilla": vstats[-1]["macs_executed"]}
+    if not args.no_measured_peaks:
+        # the ceilings this card sustains (a STREAM copy, a register-only MFMA
+        # loop), measured after the timed steps; the fractions above are
+        # against the vendor's figures, these against the measured ones
+        from paper_2607_18582_amd.peaks import measure_peaks
+        mp = measure_peaks(0)
+        line["measured_peaks"] = {k: round(v, 2) for k, v in mp.items()}
+        meas = {"hbm": mp["hbm_copy_gbs"],
+                "mfma": mp["mfma_bf16_tflops"] if md.dtype == "bf16" else mp["mfma_f32_tflops"]}
+        mpk = meas.get(roof["bound"])
+        line["roofline"]["measured_peak"] = mpk
+        line["roofline"]["frac_of_measured"] = roof["achieved"] / mpk if mpk else None
     if not args.no_cpu_baseline:
         # about 10 s of oracle work on the host cores
         om, oi = ORACLE_SAMPLE[args.config]

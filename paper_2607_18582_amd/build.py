@@ -1,9 +1,12 @@
-"""Build libmure.so (the C-ABI library) for gfx950 with hipcc, in-tree.
+"""Build libmure.so (the C-ABI library) and libmure_peaks.so (the measured
+copy and MFMA ceilings, ``include/mure_peaks.h``) for gfx950 with hipcc,
+in-tree.
 
     python -m paper_2607_18582_amd.build        # or build() from Python
 
-Every HIP source is compiled with packed-FP32 instructions disabled and the
-objects are linked into ``paper_2607_18582_amd/libmure.so``.
+Every HIP source is compiled with packed-FP32 instructions disabled; the
+objects of ``csrc/`` are linked into ``paper_2607_18582_amd/libmure.so`` and
+those of ``peaks/`` into ``paper_2607_18582_amd/libmure_peaks.so``.
 """
 from __future__ import annotations
 
@@ -18,6 +21,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libmure.so")
+PEAKS = os.path.join(HERE, "peaks")
+PEAKS_LIB = os.path.join(HERE, "libmure_peaks.so")
 ARCH = "gfx950"
 
 COMMON = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}",
@@ -33,8 +38,8 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def sources():
-    return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC)
+def sources(d: str = CSRC):
+    return sorted(os.path.join(d, f) for f in os.listdir(d)
                   if f.endswith((".hip", ".cpp")))
 
 
@@ -52,19 +57,24 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = True) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    srcs = sources()
-    with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        objs = list(ex.map(_compile, srcs))
-    tmp = LIB + ".tmp"
+def _link(objs, lib: str, verbose: bool) -> None:
+    tmp = lib + ".tmp"
     cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
     if verbose:
-        print(f"built {LIB}")
+        print(f"built {lib}")
+
+
+def build(verbose: bool = True) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    srcs, psrcs = sources(), sources(PEAKS)
+    with ThreadPoolExecutor(max_workers=min(8, len(srcs) + len(psrcs))) as ex:
+        objs = list(ex.map(_compile, srcs + psrcs))
+    _link(objs[:len(srcs)], LIB, verbose)
+    _link(objs[len(srcs):], PEAKS_LIB, verbose)
     return LIB
 
 
