@@ -111,6 +111,27 @@ def read_traffic(kernel: str, config: str, n_inputs: int, n_mutants: int):
     return None
 
 
+def counters_path(kernel: str, config: str) -> str:
+    return os.path.join(PROFILES, f"{kernel}_{config}_mfma_counters.md")
+
+
+def read_counters(kernel: str, config: str, n_inputs: int, n_mutants: int):
+    """MFMA busy share and clock of ``kernel`` from its committed counter
+    summary, or None (no summary for this workload, or the library changed
+    since the counters were taken)."""
+    try:
+        with open(counters_path(kernel, config)) as f:
+            for ln in f:
+                if ln.startswith('{"kernel"'):
+                    d = json.loads(ln)
+                    if (d["source_hash"] == library_source_hash() and d["n_inputs"] == n_inputs
+                            and d["n_mutants"] == n_mutants):
+                        return d
+    except OSError:
+        pass
+    return None
+
+
 # kernels of one family (the library times a family's launches together)
 FAMILY_KERNELS = {"lstm_kernel": ("lstm_kernel", "lstm_wide_kernel"),
                   "dw_col_kernel": ("dw_col_kernel", "dw_full_kernel", "dw_list_kernel")}
@@ -182,6 +203,65 @@ def summarize_pmc(fetch_csv: str, write_csv: str, kernel: str, args) -> str:
     return "\n".join(out)
 
 
+def summarize_counters(csv_path: str, kernel: str, args) -> str:
+    """Markdown summary of one rocprofv3 --pmc run of the MFMA counters
+    (SQ_INSTS_VALU_MFMA_MOPS_<dtype>, SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE)
+    over ``bench.py --steps 1 --warmup 0``: per launch of ``kernel`` inside
+    run_mutants, the MFMA flops the hardware executed (512 per MOP), the core
+    clock (GRBM_GUI_ACTIVE is summed over the XCDs: per XCD it counts the
+    cycles of the dispatch), and the share of SIMD cycles with the matrix core
+    busy (busy cycles summed over the SIMDs / (cycles x SIMDs))."""
+    import csv
+    rows = sorted(csv.DictReader(open(csv_path)), key=lambda r: int(r["Dispatch_Id"]))
+    wins = _run_mutants_windows(rows)
+    per, dur = {}, {}
+    for r in rows:
+        d = int(r["Dispatch_Id"])
+        if _in_family(kernel, r["Kernel_Name"]) and any(a < d < b for a, b in wins):
+            per.setdefault(d, {})
+            per[d][r["Counter_Name"]] = per[d].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+            dur[d] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+    ids = sorted(per)
+    names = sorted({c for d in ids for c in per[d]})
+    mops = [c for c in names if c.startswith("SQ_INSTS_VALU_MFMA_MOPS_")]
+    simds, xcds = args.simds, args.xcds
+    cmd = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 240 rocprofv3 --pmc %s --output-format csv "
+           "-d <dir> -o pmc -- python3 bench.py --config %s --steps 1 --warmup 0 --no-cpu-baseline --gain 0 "
+           "--no-measured-peaks" % (" ".join(names), args.config))
+    out = [f"# MFMA counters of {kernel}, {args.config}", "",
+           "Commands, from the repository root:", "", "```", cmd,
+           "python3 bench.py --summarize-counters <counter_collection.csv> --kernel %s --config %s"
+           % (kernel, args.config), "```", "",
+           f"Per run_mutants launch of `{kernel}` ({len(ids)} launches; times are those of the counter "
+           "run, whose dispatches are serialized and slower than in the kernel trace). Executed MFMA flops "
+           f"= 512 x the MOPS counter; cycles = GRBM_GUI_ACTIVE / {xcds} XCDs; clock = cycles / "
+           f"duration; MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (cycles x {simds} SIMDs).", "",
+           "| dispatch | " + " | ".join(names) + " | ms | clock GHz | MFMA flops | MFMA busy |",
+           "|---" * (len(names) + 5) + "|"]
+    tot = {c: 0.0 for c in names}
+    for d in ids:
+        v = per[d]
+        for c in names:
+            tot[c] += v.get(c, 0.0)
+        fl = 512.0 * sum(v.get(c, 0.0) for c in mops)
+        cyc = v.get("GRBM_GUI_ACTIVE", 0.0) / xcds
+        busy = v.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (cyc * simds) if cyc else 0.0
+        ghz = cyc / dur[d] / 1e9 if dur[d] > 0 else 0.0
+        out.append(f"| {d} | " + " | ".join(f"{v.get(c, 0.0):.4g}" for c in names) +
+                   f" | {dur[d] * 1e3:.3f} | {ghz:.2f} | {fl:.4g} | {busy:.3f} |")
+    n = max(len(ids), 1)
+    fl = 512.0 * sum(tot[c] for c in mops) / n
+    cyc = tot.get("GRBM_GUI_ACTIVE", 0.0) / xcds
+    secs = sum(dur.values())
+    rec = {"kernel": kernel, "config": args.config, "n_inputs": args.n_inputs_resolved,
+           "n_mutants": args.n_mutants_resolved, "launches": len(ids), "mfma_flops_per_launch": fl,
+           "mfma_busy": tot.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (cyc * simds) if cyc else 0.0,
+           "cycles_per_launch": cyc / n, "mean_clock_ghz": cyc / secs / 1e9 if secs > 0 else 0.0,
+           "ms_per_launch_counter_run": secs * 1e3 / n, "source_hash": library_source_hash()}
+    out += ["", "All launches together:", "", "```json", json.dumps(rec), "```", ""]
+    return "\n".join(out)
+
+
 def summarize_trace(trace_csv: str, stats_csv: str, kernel: str, args) -> str:
     """Markdown summary of ``rocprofv3 --kernel-trace --stats`` over a default
     bench run: per-kernel totals, and the average duration of ``kernel``'s
@@ -240,6 +320,10 @@ def main():
                     help="print the HBM traffic summary of two rocprofv3 --pmc runs and exit")
     ap.add_argument("--summarize-trace", nargs=2, metavar=("TRACE_CSV", "STATS_CSV"),
                     help="print the kernel-trace summary of a rocprofv3 run and exit")
+    ap.add_argument("--summarize-counters", metavar="COUNTER_CSV",
+                    help="print the MFMA counter summary of a rocprofv3 --pmc run and exit")
+    ap.add_argument("--simds", type=int, default=1024, help="SIMDs of the GPU (counter summaries)")
+    ap.add_argument("--xcds", type=int, default=8, help="XCDs of the GPU (counter summaries)")
     ap.add_argument("--kernel", default="conv_lds_kernel", help="kernel the summaries follow")
     ap.add_argument("--no-measured-peaks", action="store_true",
                     help="skip the STREAM copy and MFMA-loop ceilings measured after the timed steps")
@@ -247,11 +331,13 @@ def main():
     cfgd = W.CONFIGS[args.config]
     n_all = args.inputs or cfgd["n_inputs"]
     ips = min(args.inputs_per_step or INPUTS_PER_STEP.get(args.config, n_all), n_all)
-    if args.summarize_pmc or args.summarize_trace:
+    if args.summarize_pmc or args.summarize_trace or args.summarize_counters:
         args.n_inputs_resolved = ips
         args.n_mutants_resolved = args.mutants or cfgd["n_mutants"]
         if args.summarize_pmc:
             print(summarize_pmc(*args.summarize_pmc, args.kernel, args), end="")
+        elif args.summarize_counters:
+            print(summarize_counters(args.summarize_counters, args.kernel, args), end="")
         else:
             print(summarize_trace(*args.summarize_trace, args.kernel, args), end="")
         return
@@ -355,6 +441,7 @@ def main():
     all_flops = 2.0 * st["gemm_macs_algorithmic"]
     all_achieved = all_flops / (ms_gemm * 1e-3) / 1e12 if ms_gemm > 0 else 0.0
     tr = read_traffic(KERNEL_NAMES[fam], args.config, N, M)
+    mc = read_counters(KERNEL_NAMES[fam], args.config, N, M)
     # every kernel family that ran: time, launches and its own roofline
     families = {}
     for f in range(len(KERNEL_NAMES)):
@@ -399,6 +486,13 @@ def main():
                      "traffic": tr["traffic_bytes_per_launch"] if tr else None,
                      "traffic_source": os.path.relpath(traffic_path(KERNEL_NAMES[fam], args.config), ROOT)
                      if tr else None,
+                     # the hardware's view from the committed MFMA counter run: the
+                     # share of SIMD cycles with the matrix core busy, at the clock
+                     # the card ran (the vendor peak assumes 2.4 GHz)
+                     "mfma_counters": {"busy": mc["mfma_busy"], "clock_ghz": mc["mean_clock_ghz"],
+                                       "executed_flops_per_launch": mc["mfma_flops_per_launch"],
+                                       "source": os.path.relpath(counters_path(KERNEL_NAMES[fam], args.config), ROOT)}
+                     if mc else None,
                      "launches": launches, "avg_launch_ms": ms_k / max(launches, 1),
                      "alg_flops_per_launch": alg_flops / max(launches, 1),
                      "alg_bytes_per_launch": alg_bytes / max(launches, 1),
