@@ -1,5 +1,5 @@
 """GPU parity at the workloads' full sizes, in the launch configuration the
-benchmark uses (default options: whole input set per chunk, 16 GB workspace).
+benchmark uses (default options: whole input set per chunk, the 64 GB workspace).
 
 The GPU runs the whole workload.  The oracle's results for a sample of
 (mutant, input) pairs -- at least two mutants of every first-mutated layer
