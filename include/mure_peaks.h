@@ -27,14 +27,16 @@ extern "C" {
 
 /* STREAM copy: dst[i] = src[i] for the `bytes` bytes of two device buffers
  * (16-byte aligned, `bytes` a positive multiple of 16, not overlapping),
- * repeated `reps` times (1..1000) after one untimed launch.  *gbs receives
- * the best launch's rate, counting 2 * bytes (read and write) per launch, in
- * GB/s (1e9 bytes per second).  The caller owns both buffers. */
+ * in eight variants of the copy kernel (4 or 8 vectors in flight per thread,
+ * plain or non-temporal stores, 8 or 32 blocks per CU), each repeated `reps`
+ * times (1..1000) after one untimed launch.  *gbs receives the best launch's
+ * rate, counting 2 * bytes (read and write) per launch, in GB/s (1e9 bytes
+ * per second).  The caller owns both buffers. */
 int mure_peak_copy(const void* src, void* dst, int64_t bytes, int reps, void* stream, double* gbs);
 
 /* MFMA loop: `blocks` workgroups (1..65536) of 4 wavefronts, each wavefront
- * running `iters` rounds (1..10^7) of 4 independent accumulator chains of
- * v_mfma_f32_32x32x16_bf16 (dtype 1) or v_mfma_f32_16x16x4_f32 (dtype 0),
+ * running `iters` rounds (1..10^7) of independent accumulator chains: 4 of
+ * v_mfma_f32_32x32x16_bf16 (dtype 1) or 8 of v_mfma_f32_16x16x4_f32 (dtype 0),
  * repeated `reps` times (1..100) after one untimed launch.  Every lane then
  * stores the sum of its accumulators into `sink` (device, blocks * 256
  * floats, owned by the caller), so no work can be removed.  *tflops

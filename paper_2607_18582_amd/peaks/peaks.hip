@@ -14,22 +14,25 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
-constexpr int COPY_UNROLL = 4;   // 16-byte vectors in flight per thread
-
-// dst = src over n 16-byte vectors; a block covers 1,024 consecutive vectors
-// per round (four loads issued before the four stores), rounds grid-strided.
+// dst = src over n 16-byte vectors; a block covers 256 U consecutive vectors
+// per round (U loads issued before the U stores), rounds grid-strided; NT:
+// non-temporal stores (no allocation in the caches for the written lines).
+template <int U, bool NT>
 __global__ __launch_bounds__(256) void peak_copy_kernel(const v4u* __restrict__ src, v4u* __restrict__ dst,
                                                         int64_t n) {
-  const int64_t stride = (int64_t)gridDim.x * 256 * COPY_UNROLL;
-  for (int64_t i = (int64_t)blockIdx.x * 256 * COPY_UNROLL + threadIdx.x; i < n; i += stride) {
-    v4u v[COPY_UNROLL];
-    if (i + (COPY_UNROLL - 1) * 256 < n) {
+  const int64_t stride = (int64_t)gridDim.x * 256 * U;
+  for (int64_t i = (int64_t)blockIdx.x * 256 * U + threadIdx.x; i < n; i += stride) {
+    v4u v[U];
+    if (i + (U - 1) * 256 < n) {
 #pragma unroll
-      for (int u = 0; u < COPY_UNROLL; ++u) v[u] = src[i + u * 256];
+      for (int u = 0; u < U; ++u) v[u] = src[i + u * 256];
 #pragma unroll
-      for (int u = 0; u < COPY_UNROLL; ++u) dst[i + u * 256] = v[u];
+      for (int u = 0; u < U; ++u) {
+        if constexpr (NT) __builtin_nontemporal_store(v[u], dst + i + u * 256);
+        else dst[i + u * 256] = v[u];
+      }
     } else {
-      for (int u = 0; u < COPY_UNROLL && i + u * 256 < n; ++u) dst[i + u * 256] = src[i + u * 256];
+      for (int u = 0; u < U && i + u * 256 < n; ++u) dst[i + u * 256] = src[i + u * 256];
     }
   }
 }
@@ -123,15 +126,33 @@ extern "C" int mure_peak_copy(const void* src, void* dst, int64_t bytes, int rep
   if ((s0 | d0) % 16) return -1;
   if (s0 < d0 + (uint64_t)bytes && d0 < s0 + (uint64_t)bytes) return -1;   // overlapping
   const int64_t n = bytes / 16;
-  const int64_t want = (n + 256 * COPY_UNROLL - 1) / (256 * COPY_UNROLL);
-  const unsigned grid = (unsigned)std::min<int64_t>(want, 256 * 16);      // 16 blocks per CU at most
   hipStream_t s = (hipStream_t)stream;
-  double ms = 0.0;
-  const int st = time_best(s, reps, [&] {
-    hipLaunchKernelGGL(peak_copy_kernel, dim3(grid), dim3(256), 0, s, (const v4u*)src, (v4u*)dst, n);
-  }, &ms);
-  if (st) return st;
-  *gbs = ms > 0.0 ? 2.0 * (double)bytes / (ms * 1e-3) / 1e9 : 0.0;
+  int dev = 0, cus = 256;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_status(e);
+  // the best of eight variants: 4 or 8 vectors in flight per thread, plain or
+  // non-temporal stores, 8 or 32 blocks per CU (fewer when the copy is small)
+  double best = 0.0;
+  for (int variant = 0; variant < 8; ++variant) {
+    const int u = variant & 1 ? 8 : 4;
+    const bool nt = (variant >> 1) & 1;
+    const int per_cu = variant & 4 ? 32 : 8;
+    const int64_t want = (n + 256 * u - 1) / (256 * u);
+    const unsigned grid = (unsigned)std::max<int64_t>(1, std::min<int64_t>(want, (int64_t)cus * per_cu));
+    double ms = 0.0;
+    const int st = time_best(s, reps, [&] {
+      const v4u* sv = (const v4u*)src;
+      v4u* dv = (v4u*)dst;
+      if (u == 4 && !nt) hipLaunchKernelGGL((peak_copy_kernel<4, false>), dim3(grid), dim3(256), 0, s, sv, dv, n);
+      else if (u == 4) hipLaunchKernelGGL((peak_copy_kernel<4, true>), dim3(grid), dim3(256), 0, s, sv, dv, n);
+      else if (!nt) hipLaunchKernelGGL((peak_copy_kernel<8, false>), dim3(grid), dim3(256), 0, s, sv, dv, n);
+      else hipLaunchKernelGGL((peak_copy_kernel<8, true>), dim3(grid), dim3(256), 0, s, sv, dv, n);
+    }, &ms);
+    if (st) return st;
+    if (ms > 0.0) best = std::max(best, 2.0 * (double)bytes / (ms * 1e-3) / 1e9);
+  }
+  *gbs = best;
   return 0;
 }
 
